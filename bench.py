@@ -1,0 +1,241 @@
+#!/usr/bin/env python3
+"""Benchmark of the Parason accounting/reward hot path on one MI355X.
+
+One step = one parason_run over the whole resident batch: segment plan, tag
+scan of every token, per-row grammar automaton, group normalisation and the
+reward of Definition 3.1.  The default workload is the large one: 89,000
+prompts x 8 rollouts, rows of 25,150-75,450 tokens (mean 50.3k, the hard rows
+of Table 5): 3.58e10 int32 tokens, 143 GB, resident in HBM before timing.
+
+Prints one JSON line (rank 0, N = 1).  `value` is tokens per second of the
+whole step.  `roofline` is for the dominant kernel (the token scan), timed with
+HIP events recorded around its launch on the run's stream; its achieved rate
+uses algorithmic bytes (4 B per token + 12 B per row of starts and lengths).
+`cpu_baseline` times the CPU oracle (single-threaded C) on a bounded sample of
+the same rows.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "scan_segments_large_traffic.json")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """hipEvent_t pairs through the HIP runtime (the stream is the run's stream)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self):
+        e = ctypes.c_void_p()
+        rc = self.hip.hipEventCreate(ctypes.byref(e))
+        if rc != 0:
+            raise RuntimeError("hipEventCreate failed: %d" % rc)
+        return e
+
+    def elapsed_ms(self, a, b):
+        self.hip.hipEventSynchronize(b)
+        ms = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b)
+        if rc != 0:
+            raise RuntimeError("hipEventElapsedTime failed: %d" % rc)
+        return float(ms.value)
+
+
+def cpu_baseline(tokens_d, starts_h, lengths_h, correct_h, tag_ids, coef, budget_s=12.0):
+    """Time the CPU oracle on the first groups of the batch (copied to the host
+    outside the timed region), sized for about budget_s seconds of CPU work."""
+    import numpy as np
+
+    from oracle import oracle as O
+
+    G = 8
+
+    def sample(n_groups):
+        n = n_groups * G
+        lo, hi = int(starts_h[0]), int(starts_h[n - 1] + lengths_h[n - 1])
+        toks = tokens_d[lo:hi].cpu().numpy()
+        return toks, (starts_h[:n] - lo).astype(np.int64), lengths_h[:n].copy(), correct_h[:n].copy()
+
+    def timed(toks, st, ln, co):
+        t0 = time.perf_counter()
+        rows = O.eval_rows(toks, st, ln, tag_ids)
+        O.group_reward(rows, co, G, coef["alpha"], coef["beta_subtask"], coef["beta_trial"], coef["rho"],
+                       coef["rho_clip"])
+        return time.perf_counter() - t0
+
+    probe = sample(4)
+    dt = timed(*probe)
+    rate = probe[0].size / max(dt, 1e-6)
+    want = budget_s * rate
+    per_group = probe[0].size / 4
+    n_groups = int(max(4, min(len(starts_h) // G, want / per_group)))
+    toks, st, ln, co = sample(n_groups)
+    dt = timed(toks, st, ln, co)
+    return {
+        "value": toks.size / dt,
+        "unit": "tokens/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": "first %d groups (%d rows, %d tokens) of the same workload, copied to the host; %.1f s "
+                  "single-threaded" % (n_groups, n_groups * G, toks.size, dt),
+        "rows_per_s": n_groups * G / dt,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="large", choices=["tiny", "small", "typical", "large", "ragged"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(groups shard across GPUs with no exchange; see the design notes). Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_24658_amd import parason as PX
+    from paper_2608_24658_amd.synth import synth as S
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    G = S.GROUP_SIZE
+    coef = dict(alpha=0.1, beta_subtask=0.0, beta_trial=0.1, rho=0.5, rho_clip=0.25)
+
+    P = S.make_params(args.workload)
+    n = S.n_rows_of(args.workload)
+    log("generating %s: %d rows" % (args.workload, n))
+    t0 = time.time()
+    tokens, starts, lengths, correct = S.device_batch(P, n, device=dev)
+    torch.cuda.synchronize()
+    n_tok = int(tokens.numel())
+    log("generated %d tokens (%.1f GB) in %.1f s" % (n_tok, n_tok * 4 / 1e9, time.time() - t0))
+
+    px = PX.Parason(S.CONTIGUOUS_TAGS, group_size=G, **coef)
+    out = px.alloc_outputs(n, dev)
+    ws = px.alloc_workspace(n, n_tok, dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    hev = HipEvents()
+    ev = [hev.create(), hev.create()]
+    c_ev = (ctypes.c_void_p * 2)(ev[0], ev[1])
+
+    def step(timed_scan):
+        rc = px.run_timed_raw(tokens.data_ptr(), starts.data_ptr(), lengths.data_ptr(), correct.data_ptr(), n, out,
+                              ws.data_ptr(), ws.numel(), stream, c_ev if timed_scan else None)
+        if rc != PX.OK:
+            raise PX.ParasonError(rc, "parason_run")
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+
+    # whole-step timing
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(False)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_per_step = dt * 1e3 / args.steps
+
+    # the dominant kernel, timed with HIP events around its launch
+    scan_ms = []
+    for _ in range(args.steps):
+        step(True)
+        scan_ms.append(hev.elapsed_ms(ev[0], ev[1]))
+    torch.cuda.synchronize()
+    scan_avg = float(np.mean(scan_ms))
+
+    # sanity of the last step
+    fl = out["flags"].cpu().numpy().view(np.uint32)
+    n_valid = int(np.sum(fl & PX.FLAG_VALID))
+    alg_bytes = 4.0 * n_tok + 12.0 * n
+    achieved = alg_bytes / (scan_avg * 1e-3) / 1e9
+    traffic = None
+    if os.path.exists(PROFILE_TRAFFIC):
+        try:
+            tr = json.load(open(PROFILE_TRAFFIC))
+            if tr.get("workload") == args.workload and tr.get("kernel_source_sha") == kernel_sha():
+                traffic = tr.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+
+    res = {
+        "metric": "hot-path throughput (items/s) + achieved % of HBM or MFMA roofline, 1×MI355X",
+        "value": n_tok / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic (seeded generator shaped like the paper's rollouts; no dataset or model)",
+        "config": {
+            "workload": "%s: %d groups x %d rollouts, %d rows, %d tokens (%.1f GB int32)"
+                        % (args.workload, n // G, G, n, n_tok, n_tok * 4 / 1e9),
+            "rows": n,
+            "tokens": n_tok,
+            "group_size": G,
+            "tag_ids": "contiguous (V-12 .. V-1, V = 151936)",
+            "parallelism": "single GPU",
+        },
+        "rows_per_s": n / (ms_per_step * 1e-3),
+        "valid_rows": n_valid,
+        "roofline": {
+            "kernel": "scan_segments",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "kernel_ms": scan_avg,
+            "algorithmic_bytes": alg_bytes,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample")
+        res["cpu_baseline"] = cpu_baseline(tokens, starts.cpu().numpy(), lengths.cpu().numpy(),
+                                           correct.cpu().numpy(), S.CONTIGUOUS_TAGS, coef, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+def kernel_sha():
+    import hashlib
+
+    h = hashlib.sha256()
+    for p in ("paper_2608_24658_amd/csrc/parason_kernels.h", "paper_2608_24658_amd/csrc/parason.hip"):
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    return h.hexdigest()[:16]
+
+
+if __name__ == "__main__":
+    main()

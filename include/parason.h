@@ -1,0 +1,163 @@
+/*
+ * parason.h -- C-ABI of the MI355X (gfx950) hot path of Parason:
+ * parallel-trajectory accounting and the Parallelism-Aware GRPO reward.
+ *
+ * For every generated token stream (a rollout) of a batch grouped G rollouts
+ * per prompt, the library
+ *   1. checks the stream against the grammar of the figure "Context-Free
+ *      Grammar for Parason" (Sec. 3.2),
+ *   2. computes its total tokens L_total and its model latency T_i, the length
+ *      of the longest generation path, where each <Parallel> block contributes
+ *      its longest branch (Sec. 4, "Evaluation"; T_i and L_latency in Sec. 3.3),
+ *   3. counts the tokens placed in Subtask and in Trial branches (R_subtask and
+ *      R_trial of Sec. 3.3),
+ *   4. normalises latency and the two ratios within each group of G and
+ *      evaluates the reward of Definition 3.1 ("Parallel RL Reward", Sec. 3.3)
+ *      with the shaping function f the identity.
+ *
+ * Readings of points the paper leaves open (all implemented identically by the
+ * test oracle):
+ *   - each tag is one reserved token id; every other id is Text;
+ *   - every token costs 1 on the path that emits it, tags included;
+ *   - <Parallel> and its outline are on the enclosing path:
+ *       lat(P) = 1 + |<Outlines> ... </Outlines>| + max_k lat(thread k) + 1,
+ *       lat(thread) = 2 + lat(its body);
+ *   - a token is a Subtask (Trial) token when its innermost enclosing <Thread>
+ *     pairs with a Subtask (Trial) entry; thread k pairs with entry k; surplus
+ *     threads are untyped and the row gets PARASON_FLAG_COUNT_MISMATCH;
+ *   - free Text may follow </think> and counts sequentially; nothing may
+ *     precede <think>;
+ *   - an invalid or truncated stream is sequential (latency = total, no branch
+ *     tokens, no blocks, depth 0); first_error_pos is the length of its longest
+ *     prefix that is a prefix of some valid stream;
+ *   - mu and sigma are over the G rollouts of one prompt, population form;
+ *     z = 0 when all G values are equal (decided exactly) or sigma is 0;
+ *   - the reward is evaluated in IEEE double precision in a fixed order with no
+ *     fused multiply-add, then stored as float.
+ *
+ * Threading: a handle is immutable after parason_create; parason_run may be
+ * called concurrently on different streams with different workspaces.
+ * No function throws; every error is a negative status.
+ */
+#ifndef PARASON_H
+#define PARASON_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------- */
+#define PARASON_OK 0
+#define PARASON_ERR_NULL (-1)      /* a required pointer argument is NULL */
+#define PARASON_ERR_SIZE (-2)      /* negative or too large n_traj / total_tokens */
+#define PARASON_ERR_GROUP (-3)     /* group_size < 1 or n_traj % group_size != 0 */
+#define PARASON_ERR_WORKSPACE (-4) /* workspace smaller than parason_workspace_size */
+#define PARASON_ERR_TAGS (-5)      /* a tag id is negative or two tag ids are equal */
+#define PARASON_ERR_PARAM (-6)     /* a reward parameter is not finite */
+#define PARASON_ERR_ALIGN (-7)     /* tokens not 4-byte aligned or workspace not 256-byte aligned */
+#define PARASON_ERR_HIP (-8)       /* a HIP call or kernel launch failed */
+#define PARASON_ERR_DEVICE (-9)    /* the current device is not gfx950 or cannot be queried */
+
+/* ---- per-row flag bits (parason_outputs.flags) ------------------------- */
+#define PARASON_FLAG_VALID (1u << 0)          /* the stream is in the language */
+#define PARASON_FLAG_TRUNCATED (1u << 1)      /* invalid only because it ends early */
+#define PARASON_FLAG_COUNT_MISMATCH (1u << 2) /* valid; some block has #threads != #entries */
+#define PARASON_FLAG_TRIGGERED (1u << 3)      /* valid and holds >= 1 <Parallel> block (Table 4) */
+/* The row was not evaluated; its integer outputs are 0, its reward (and the
+ * rewards of its whole group) are NaN: */
+#define PARASON_FLAG_DEPTH_LIMIT (1u << 8)    /* nesting or entry count beyond the slow path's store */
+#define PARASON_FLAG_WS_OVERFLOW (1u << 9)    /* the rows need more workspace than was passed */
+#define PARASON_FLAG_BAD_ROW (1u << 10)       /* negative start or length */
+
+/* ---- configuration flag bits (parason_config.flags) -------------------- */
+/* An invalid stream keeps the caller's correctness bit (default: an invalid
+ * stream counts as incorrect, reward -1). */
+#define PARASON_CFG_INVALID_KEEPS_CORRECTNESS (1u << 0)
+
+/* Maximum nesting depth and number of outline entries of open blocks that the
+ * library evaluates; a row beyond either is flagged PARASON_FLAG_DEPTH_LIMIT.
+ * (A row needs at least 6 tokens per nesting level.) */
+#define PARASON_MAX_DEPTH (1 << 20)
+#define PARASON_MAX_OPEN_ENTRIES (1 << 24)
+
+typedef struct parason_config {
+    /* Token ids of the tags, in this order:
+     *   <think> </think> <Parallel> </Parallel> <Outlines> </Outlines>
+     *   <Subtask> </Subtask> <Trial> </Trial> <Thread> </Thread>
+     * (the terminals of the grammar, Sec. 3.2).  Distinct and >= 0. */
+    int32_t tag_ids[12];
+    /* G: rollouts per prompt; rows [g*G, (g+1)*G) form group g (8 in Sec. 4). */
+    int32_t group_size;
+    /* Reward coefficients of Definition 3.1: alpha (latency penalty),
+     * beta_subtask, beta_trial (parallelism incentives), rho and rho_clip
+     * (clipped acceleration reward).  Must be finite. */
+    double alpha, beta_subtask, beta_trial, rho, rho_clip;
+    uint32_t flags; /* PARASON_CFG_* */
+} parason_config;
+
+/* Caller-owned device arrays of n_traj elements each.  All are required except
+ * r_subtask, r_trial and eta, which may be NULL. */
+typedef struct parason_outputs {
+    int32_t *total;           /* L_total = length of the row */
+    int32_t *latency;         /* T_i = L_latency (longest generation path) */
+    int32_t *n_subtask;       /* tokens in Subtask branches */
+    int32_t *n_trial;         /* tokens in Trial branches */
+    int32_t *n_blocks;        /* number of <Parallel> blocks */
+    int32_t *max_depth;       /* deepest <Parallel> nesting (1 = top level) */
+    int32_t *first_error_pos; /* -1 if valid, else longest viable prefix length */
+    uint32_t *flags;          /* PARASON_FLAG_* */
+    float *reward;            /* R_i of Definition 3.1 */
+    float *r_subtask;         /* optional: n_subtask / total (0 if total == 0) */
+    float *r_trial;           /* optional: n_trial / total */
+    float *eta;               /* optional: eta(s) = 1 - latency / total */
+} parason_outputs;
+
+typedef struct parason_handle parason_handle;
+
+/* Validate *cfg and create a handle (host memory only; the current HIP device
+ * must be a gfx950 GPU).  On success *out receives the handle. */
+int parason_create(const parason_config *cfg, parason_handle **out);
+
+/* Bytes of device workspace parason_run needs for n_traj rows whose lengths
+ * add up to at most total_tokens. */
+int parason_workspace_size(const parason_handle *h, int64_t n_traj, int64_t total_tokens, size_t *bytes);
+
+/* Evaluate a batch, asynchronously on `stream` (a hipStream_t; NULL is the
+ * default stream).  Device pointers:
+ *   tokens   int32 token ids; row i is tokens[starts[i] .. starts[i]+lengths[i]).
+ *            Rows may be in any order, may leave gaps (a padded [B, Lmax]
+ *            layout is starts[i] = i*Lmax) and may overlap.  4-byte aligned.
+ *   starts   int64[n_traj], element offsets into tokens
+ *   lengths  int32[n_traj]
+ *   correct  uint8[n_traj], nonzero = the final answer is correct
+ *   out      per-row outputs (the struct itself is host memory)
+ *   workspace, workspace_bytes: scratch from the caller, 256-byte aligned, at
+ *            least parason_workspace_size(h, n_traj, sum of lengths) bytes; its
+ *            contents need no initialisation and are meaningless afterwards.
+ * Host-side argument errors return a negative status before any launch.
+ * Device-side problems (bad rows, workspace too small for the actual lengths)
+ * are reported per row in out->flags.  Nothing is synchronised inside. */
+int parason_run(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                const uint8_t *correct, int64_t n_traj, const parason_outputs *out, void *workspace,
+                size_t workspace_bytes, void *stream);
+
+/* parason_run, plus hipEventRecord of scan_events[0] on `stream` just before
+ * the token-scan kernel (the one whose HBM traffic bounds the path) and of
+ * scan_events[1] just after it.  scan_events holds two hipEvent_t created by
+ * the caller; a NULL array records nothing.  For measurement. */
+int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                      const uint8_t *correct, int64_t n_traj, const parason_outputs *out, void *workspace,
+                      size_t workspace_bytes, void *stream, void *const *scan_events);
+
+void parason_destroy(parason_handle *h);
+
+/* Static description of a status code. */
+const char *parason_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PARASON_H */

@@ -1,0 +1,272 @@
+/*
+ * parason.hip -- C-ABI of the Parason accounting/reward path for gfx950.
+ * The kernels are in parason_kernels.h; this file validates arguments, lays
+ * out the caller's workspace and enqueues the launches on the caller's stream.
+ */
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstring>
+#include <new>
+
+#include "parason.h"
+#include "parason_kernels.h"
+
+struct parason_handle {
+    parason_config cfg;
+    pk::TagMatch tm;
+};
+
+namespace {
+
+constexpr size_t ALIGN = 256;
+constexpr int SCAN_BLOCK = 256;         /* threads per scan block (4 waves) */
+constexpr int SCAN_BLOCKS_PER_CU = 4;   /* persistent grid: 16 waves per CU (106 VGPRs: 4 waves per SIMD) */
+constexpr int64_t MAX_SEGMENTS = (int64_t)1 << 40;
+
+size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+/* Byte offsets of the workspace sections for n rows. */
+struct Layout {
+    size_t seg_off, tile_sum, tile_off, counters, deep_rows, deep_frames, deep_bits, seg_count, events;
+    size_t fixed;  /* bytes before the per-segment sections */
+    int64_t n_tiles;
+};
+
+Layout layout_for(int64_t n)
+{
+    Layout L;
+    L.n_tiles = n > 0 ? (n + pk::PLAN_TILE - 1) / pk::PLAN_TILE : 1;
+    size_t o = 0;
+    L.seg_off = o;
+    o = align_up(o + (size_t)(n + 1) * sizeof(int64_t));
+    L.tile_sum = o;
+    o = align_up(o + (size_t)L.n_tiles * sizeof(int64_t));
+    L.tile_off = o;
+    o = align_up(o + (size_t)L.n_tiles * sizeof(int64_t));
+    L.counters = o;
+    o = align_up(o + 4 * sizeof(int32_t));
+    L.deep_rows = o;
+    o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    L.deep_frames = o;
+    o = align_up(o + (size_t)pk::DEEP_FRAMES * pk::FRAME_WORDS * sizeof(int32_t));
+    L.deep_bits = o;
+    o = align_up(o + (size_t)(pk::DEEP_ENTRY_BITS / 32) * sizeof(uint32_t));
+    L.fixed = o;
+    L.seg_count = o;
+    L.events = 0; /* depends on the capacity */
+    return L;
+}
+
+constexpr size_t PER_SEGMENT = sizeof(int32_t) + (size_t)pk::EV_CAP * sizeof(uint32_t);
+
+/* Segments a workspace of `bytes` can hold for n rows. */
+int64_t capacity_for(int64_t n, size_t bytes)
+{
+    Layout L = layout_for(n);
+    if (bytes < L.fixed + 2 * ALIGN) return 0;
+    int64_t cap = (int64_t)((bytes - L.fixed - 2 * ALIGN) / PER_SEGMENT);
+    return cap < MAX_SEGMENTS ? cap : MAX_SEGMENTS;
+}
+
+/* Upper bound of the number of segments of rows whose lengths add up to total. */
+int64_t segment_bound(int64_t n, int64_t total)
+{
+    /* a row of len tokens covers at most (len + 6) / 4 + 1 vectors */
+    return (total + 7 * n) / (4 * pk::SEG_VEC) + 2 * n + 1;
+}
+
+int cu_count()
+{
+    static std::atomic<int> cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return -1;
+    if (dev >= 0 && dev < 64) {
+        int c = cached[dev].load(std::memory_order_relaxed);
+        if (c > 0) return c;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return -1;
+    if (dev >= 0 && dev < 64) cached[dev].store(cus, std::memory_order_relaxed);
+    return cus;
+}
+
+bool is_finite(double x) { return std::isfinite(x); }
+
+}  // namespace
+
+extern "C" {
+
+const char *parason_strerror(int status)
+{
+    switch (status) {
+    case PARASON_OK: return "ok";
+    case PARASON_ERR_NULL: return "a required pointer argument is NULL";
+    case PARASON_ERR_SIZE: return "negative or too large size argument";
+    case PARASON_ERR_GROUP: return "group_size < 1 or n_traj is not a multiple of group_size";
+    case PARASON_ERR_WORKSPACE: return "workspace smaller than parason_workspace_size";
+    case PARASON_ERR_TAGS: return "tag ids must be distinct and non-negative";
+    case PARASON_ERR_PARAM: return "a reward parameter is not finite";
+    case PARASON_ERR_ALIGN: return "tokens must be 4-byte aligned and the workspace 256-byte aligned";
+    case PARASON_ERR_HIP: return "a HIP call or kernel launch failed";
+    case PARASON_ERR_DEVICE: return "no usable HIP device";
+    default: return "unknown status";
+    }
+}
+
+int parason_create(const parason_config *cfg, parason_handle **out)
+{
+    if (!cfg || !out) return PARASON_ERR_NULL;
+    *out = nullptr;
+    if (cfg->group_size < 1) return PARASON_ERR_GROUP;
+    for (int i = 0; i < 12; ++i) {
+        if (cfg->tag_ids[i] < 0) return PARASON_ERR_TAGS;
+        for (int j = 0; j < i; ++j)
+            if (cfg->tag_ids[i] == cfg->tag_ids[j]) return PARASON_ERR_TAGS;
+    }
+    if (!is_finite(cfg->alpha) || !is_finite(cfg->beta_subtask) || !is_finite(cfg->beta_trial) || !is_finite(cfg->rho) ||
+        !is_finite(cfg->rho_clip))
+        return PARASON_ERR_PARAM;
+
+    parason_handle *h = new (std::nothrow) parason_handle;
+    if (!h) return PARASON_ERR_NULL;
+    h->cfg = *cfg;
+    std::memset(&h->tm, 0, sizeof(h->tm));
+    int32_t lo = cfg->tag_ids[0], hi = cfg->tag_ids[0];
+    for (int i = 0; i < 12; ++i) {
+        h->tm.ids[i] = cfg->tag_ids[i];
+        lo = cfg->tag_ids[i] < lo ? cfg->tag_ids[i] : lo;
+        hi = cfg->tag_ids[i] > hi ? cfg->tag_ids[i] : hi;
+    }
+    /* twelve distinct ids spanning 12 values: a permutation of [lo, lo + 12) */
+    h->tm.contiguous = (int64_t)hi - (int64_t)lo == 11;
+    h->tm.base = lo;
+    if (h->tm.contiguous) {
+        for (int i = 0; i < 12; ++i) {
+            uint32_t o = (uint32_t)(cfg->tag_ids[i] - lo), c = (uint32_t)(i + 1);
+            if (o < 8) h->tm.lut_lo |= c << (4 * o);
+            else h->tm.lut_hi |= c << (4 * (o - 8));
+        }
+    }
+    *out = h;
+    return PARASON_OK;
+}
+
+void parason_destroy(parason_handle *h) { delete h; }
+
+int parason_workspace_size(const parason_handle *h, int64_t n_traj, int64_t total_tokens, size_t *bytes)
+{
+    if (!h || !bytes) return PARASON_ERR_NULL;
+    if (n_traj < 0 || total_tokens < 0 || n_traj > INT32_MAX) return PARASON_ERR_SIZE;
+    int64_t segs = segment_bound(n_traj, total_tokens);
+    if (segs > MAX_SEGMENTS) return PARASON_ERR_SIZE;
+    Layout L = layout_for(n_traj);
+    *bytes = L.fixed + 2 * ALIGN + (size_t)segs * PER_SEGMENT;
+    return PARASON_OK;
+}
+
+int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                      const uint8_t *correct, int64_t n_traj, const parason_outputs *out, void *workspace,
+                      size_t workspace_bytes, void *stream_ptr, void *const *scan_events)
+{
+    if (!h || !out) return PARASON_ERR_NULL;
+    if (n_traj < 0 || n_traj > INT32_MAX) return PARASON_ERR_SIZE;
+    const int32_t G = h->cfg.group_size;
+    if (n_traj % G != 0) return PARASON_ERR_GROUP;
+    if (n_traj == 0) return PARASON_OK;
+    if (!tokens || !starts || !lengths || !correct || !workspace) return PARASON_ERR_NULL;
+    if (!out->total || !out->latency || !out->n_subtask || !out->n_trial || !out->n_blocks || !out->max_depth ||
+        !out->first_error_pos || !out->flags || !out->reward)
+        return PARASON_ERR_NULL;
+    if (((uintptr_t)tokens & 3u) != 0 || ((uintptr_t)workspace & (ALIGN - 1)) != 0) return PARASON_ERR_ALIGN;
+    const int64_t cap = capacity_for(n_traj, workspace_bytes);
+    if (cap < 1) return PARASON_ERR_WORKSPACE;
+
+    const int cus = cu_count();
+    if (cus <= 0) return PARASON_ERR_DEVICE;
+    hipStream_t stream = (hipStream_t)stream_ptr;
+
+    /* The scan reads 16-byte vectors on the 16-byte grid below `tokens`. */
+    const int64_t mis = (int64_t)(((uintptr_t)tokens & 15u) >> 2);
+    const int32_t *tok_base = tokens - mis;
+
+    Layout L = layout_for(n_traj);
+    char *ws = (char *)workspace;
+    int64_t *seg_off = (int64_t *)(ws + L.seg_off);
+    int64_t *tile_sum = (int64_t *)(ws + L.tile_sum);
+    int64_t *tile_off = (int64_t *)(ws + L.tile_off);
+    int32_t *counters = (int32_t *)(ws + L.counters);
+    int32_t *deep_rows = (int32_t *)(ws + L.deep_rows);
+    int32_t *deep_frames = (int32_t *)(ws + L.deep_frames);
+    uint32_t *deep_bits = (uint32_t *)(ws + L.deep_bits);
+    int32_t *seg_count = (int32_t *)(ws + L.seg_count);
+    uint32_t *events = (uint32_t *)(ws + align_up(L.seg_count + (size_t)cap * sizeof(int32_t)));
+
+    const unsigned tiles = (unsigned)L.n_tiles;
+    pk::plan_tiles<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_sum);
+    pk::plan_top<<<dim3(1), dim3(1024), 0, stream>>>(tile_sum, L.n_tiles, tile_off, seg_off, n_traj, counters);
+    pk::plan_rows<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_off,
+                                                                        seg_off);
+
+    const unsigned scan_blocks = (unsigned)(cus * SCAN_BLOCKS_PER_CU);
+    if (scan_events && hipEventRecord((hipEvent_t)scan_events[0], stream) != hipSuccess) return PARASON_ERR_HIP;
+    if (h->tm.contiguous)
+        pk::scan_segments<true><<<dim3(scan_blocks), dim3(SCAN_BLOCK), 0, stream>>>(
+            tok_base, mis, starts, lengths, n_traj, seg_off, cap, seg_count, events, h->tm);
+    else
+        pk::scan_segments<false><<<dim3(scan_blocks), dim3(SCAN_BLOCK), 0, stream>>>(
+            tok_base, mis, starts, lengths, n_traj, seg_off, cap, seg_count, events, h->tm);
+    if (scan_events && hipEventRecord((hipEvent_t)scan_events[1], stream) != hipSuccess) return PARASON_ERR_HIP;
+
+    pk::RowArgs ra;
+    ra.tok_base = tok_base;
+    ra.mis = mis;
+    ra.starts = starts;
+    ra.lengths = lengths;
+    ra.n = n_traj;
+    ra.seg_off = seg_off;
+    ra.seg_cap = cap;
+    ra.seg_count = seg_count;
+    ra.events = events;
+    ra.tm = h->tm;
+    ra.out = pk::RowOut{out->total, out->latency, out->n_subtask, out->n_trial, out->n_blocks, out->max_depth,
+                        out->first_error_pos, out->flags};
+    const unsigned row_blocks = (unsigned)((n_traj + 63) / 64);
+    pk::rows_fast<<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, counters, deep_rows);
+    pk::rows_deep<<<dim3(1), dim3(64), 0, stream>>>(ra, counters, deep_rows, deep_frames, deep_bits);
+
+    pk::RewardArgs rw;
+    rw.total = out->total;
+    rw.latency = out->latency;
+    rw.n_subtask = out->n_subtask;
+    rw.n_trial = out->n_trial;
+    rw.flags = out->flags;
+    rw.correct = correct;
+    rw.n_groups = n_traj / G;
+    rw.G = G;
+    rw.alpha = h->cfg.alpha;
+    rw.beta_s = h->cfg.beta_subtask;
+    rw.beta_r = h->cfg.beta_trial;
+    rw.rho = h->cfg.rho;
+    rw.rho_clip = h->cfg.rho_clip;
+    rw.cfg_flags = h->cfg.flags;
+    rw.reward = out->reward;
+    rw.r_subtask = out->r_subtask;
+    rw.r_trial = out->r_trial;
+    rw.eta = out->eta;
+    const unsigned reward_blocks = (unsigned)((rw.n_groups + 255) / 256);
+    pk::group_reward<<<dim3(reward_blocks), dim3(256), 0, stream>>>(rw);
+
+    return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
+}
+
+int parason_run(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                const uint8_t *correct, int64_t n_traj, const parason_outputs *out, void *workspace,
+                size_t workspace_bytes, void *stream)
+{
+    return parason_run_timed(h, tokens, starts, lengths, correct, n_traj, out, workspace, workspace_bytes, stream,
+                             nullptr);
+}
+
+}  // extern "C"

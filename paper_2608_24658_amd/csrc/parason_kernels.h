@@ -1,0 +1,851 @@
+/*
+ * parason_kernels.h -- gfx950 kernels of the Parason accounting/reward path.
+ *
+ * Data flow of one parason_run (all on the caller's stream):
+ *
+ *   plan_tiles / plan_top / plan_rows
+ *        Each row is cut into segments of SEG_VEC 16-byte vectors (4096
+ *        tokens), aligned to the 16-byte grid of the token buffer.  A three
+ *        pass exclusive scan gives seg_off[i] (first segment of row i) and the
+ *        segment count seg_off[n].
+ *   scan_segments  (HBM-bound; one wave per segment, persistent grid)
+ *        Streams every token once with 16-byte loads, tests it against the
+ *        twelve tag ids and compacts the rare tag tokens with wave ballots into
+ *        a per-segment event list (position in segment << 4 | class).  Tags are
+ *        about 0.1-1% of tokens.  A segment holding more than EV_CAP tags keeps
+ *        only its count; the row kernel re-reads its tokens.
+ *   rows_fast      (one thread per row)
+ *        Runs the grammar's pushdown automaton over the row's events; Text runs
+ *        are the gaps between event positions.  Produces the integer outputs.
+ *        Frames of open blocks live in LDS (FAST_DEPTH per row, 64 outline
+ *        entries per block); a row that needs more is handed to rows_deep.
+ *   rows_deep      (one thread, only rows handed over)
+ *        The same automaton with frames and entry types in global workspace.
+ *   group_reward   (one thread per group of G rows)
+ *        Statistics and Definition 3.1 in IEEE double, fixed order.
+ *
+ * Paper references: grammar -- figure "Context-Free Grammar for Parason"
+ * (Sec. 3.2); latency -- Sec. 4 "Evaluation"; ratios, eta and the reward --
+ * Sec. 3.3, Definition 3.1.
+ */
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "parason.h"
+
+namespace pk {
+
+constexpr int WAVE = 64;
+constexpr int SEG_VEC = 1024;            /* 16-byte vectors per segment */
+constexpr int SEG_TOK = 4 * SEG_VEC;     /* tokens per segment */
+constexpr int LOADS = SEG_VEC / WAVE;    /* vector loads per lane per segment */
+constexpr int EV_CAP = 128;              /* events stored per segment */
+constexpr int PLAN_TILE = 4096;          /* rows per plan tile */
+constexpr int PLAN_THREADS = 256;
+constexpr int ROWS_PER_THREAD = PLAN_TILE / PLAN_THREADS;
+constexpr int FAST_DEPTH = 8;            /* LDS frames per row (depth <= FAST_DEPTH + 1) */
+constexpr int FAST_ENTRIES = 64;         /* entries per open block on the fast path */
+constexpr int FRAME_WORDS = 8;
+constexpr int64_t DEEP_FRAMES = PARASON_MAX_DEPTH;
+constexpr int64_t DEEP_ENTRY_BITS = PARASON_MAX_OPEN_ENTRIES;
+
+/* Token classes: 0 = Text, 1..12 = tags in tag_ids order. */
+enum : uint32_t {
+    C_TEXT = 0, C_THINK, C_END_THINK, C_PAR, C_END_PAR, C_OUT, C_END_OUT,
+    C_SUB, C_END_SUB, C_TRI, C_END_TRI, C_THR, C_END_THR
+};
+
+/* Branch type of the innermost enclosing thread. */
+enum : uint32_t { T_MAIN = 0, T_SUB = 1, T_TRI = 2 };
+
+struct TagMatch {
+    int32_t ids[12];
+    int32_t base;     /* contiguous case: smallest id */
+    uint32_t lut_lo;  /* contiguous case: class of id base+o in nibble o (o < 8) */
+    uint32_t lut_hi;  /* nibbles for o = 8..11 */
+    int32_t contiguous;
+};
+
+__device__ __forceinline__ uint32_t classify(const TagMatch &tm, int32_t t, bool contig)
+{
+    if (contig) {
+        uint32_t o = (uint32_t)t - (uint32_t)tm.base;
+        if (o >= 12u) return C_TEXT;
+        return o < 8u ? (tm.lut_lo >> (4u * o)) & 15u : (tm.lut_hi >> (4u * (o - 8u))) & 15u;
+    }
+    uint32_t c = C_TEXT;
+#pragma unroll
+    for (int k = 0; k < 12; ++k) c = (t == tm.ids[k]) ? (uint32_t)(k + 1) : c;
+    return c;
+}
+
+__device__ __forceinline__ int64_t row_segments(int64_t start, int32_t len, int64_t mis)
+{
+    if (start < 0 || len <= 0) return 0;
+    int64_t g = start + mis;
+    int64_t nvec = ((g + (int64_t)len - 1) >> 2) - (g >> 2) + 1;
+    return (nvec + SEG_VEC - 1) / SEG_VEC;
+}
+
+__device__ __forceinline__ int64_t uniform64(int64_t x)
+{
+    uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+/* Inclusive prefix sum over the 64 lanes of a wave. */
+__device__ __forceinline__ int64_t wave_inclusive_scan(int64_t v)
+{
+    const int lane = threadIdx.x & (WAVE - 1);
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) {
+        int64_t o = __shfl_up(v, d, WAVE);
+        if (lane >= d) v += o;
+    }
+    return v;
+}
+
+/* ------------------------------------------------------------------ plan */
+
+/* tile_sum[b] = number of segments of rows [b*PLAN_TILE, (b+1)*PLAN_TILE). */
+__global__ void __launch_bounds__(PLAN_THREADS) plan_tiles(const int64_t *__restrict__ starts,
+                                                           const int32_t *__restrict__ lengths, int64_t n,
+                                                           int64_t mis, int64_t *__restrict__ tile_sum)
+{
+    __shared__ int64_t part[PLAN_THREADS / WAVE];
+    int64_t r0 = (int64_t)blockIdx.x * PLAN_TILE;
+    int64_t s = 0;
+    for (int j = 0; j < ROWS_PER_THREAD; ++j) {
+        int64_t r = r0 + (int64_t)j * PLAN_THREADS + threadIdx.x; /* coalesced */
+        if (r < n) s += row_segments(starts[r], lengths[r], mis);
+    }
+    s = wave_inclusive_scan(s);
+    if ((threadIdx.x & (WAVE - 1)) == WAVE - 1) part[threadIdx.x / WAVE] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int64_t t = 0;
+        for (int w = 0; w < PLAN_THREADS / WAVE; ++w) t += part[w];
+        tile_sum[blockIdx.x] = t;
+    }
+}
+
+/* tile_off = exclusive scan of tile_sum; seg_off[n] = total; clears counters. */
+__global__ void __launch_bounds__(1024) plan_top(const int64_t *__restrict__ tile_sum, int64_t n_tiles,
+                                                 int64_t *__restrict__ tile_off, int64_t *__restrict__ seg_off,
+                                                 int64_t n, int32_t *__restrict__ counters)
+{
+    __shared__ int64_t part[1024 / WAVE];
+    __shared__ int64_t carry_s;
+    if (threadIdx.x == 0) carry_s = 0;
+    if (threadIdx.x < 4) counters[threadIdx.x] = 0;
+    __syncthreads();
+    for (int64_t base = 0; base < n_tiles; base += 1024) {
+        int64_t i = base + threadIdx.x;
+        int64_t v = i < n_tiles ? tile_sum[i] : 0;
+        int64_t inc = wave_inclusive_scan(v);
+        if ((threadIdx.x & (WAVE - 1)) == WAVE - 1) part[threadIdx.x / WAVE] = inc;
+        __syncthreads();
+        int64_t before = carry_s;
+        for (int w = 0; w < (int)(threadIdx.x / WAVE); ++w) before += part[w];
+        if (i < n_tiles) tile_off[i] = before + inc - v;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int64_t t = 0;
+            for (int w = 0; w < 1024 / WAVE; ++w) t += part[w];
+            carry_s += t;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) seg_off[n] = carry_s;
+}
+
+/* seg_off[i] = first segment of row i. */
+__global__ void __launch_bounds__(PLAN_THREADS) plan_rows(const int64_t *__restrict__ starts,
+                                                          const int32_t *__restrict__ lengths, int64_t n,
+                                                          int64_t mis, const int64_t *__restrict__ tile_off,
+                                                          int64_t *__restrict__ seg_off)
+{
+    __shared__ int64_t part[PLAN_THREADS / WAVE];
+    /* thread t owns the ROWS_PER_THREAD consecutive rows starting at r0 + t*ROWS_PER_THREAD */
+    int64_t r0 = (int64_t)blockIdx.x * PLAN_TILE + (int64_t)threadIdx.x * ROWS_PER_THREAD;
+    int64_t cnt[ROWS_PER_THREAD];
+    int64_t s = 0;
+#pragma unroll
+    for (int j = 0; j < ROWS_PER_THREAD; ++j) {
+        int64_t r = r0 + j;
+        cnt[j] = r < n ? row_segments(starts[r], lengths[r], mis) : 0;
+        s += cnt[j];
+    }
+    int64_t inc = wave_inclusive_scan(s);
+    if ((threadIdx.x & (WAVE - 1)) == WAVE - 1) part[threadIdx.x / WAVE] = inc;
+    __syncthreads();
+    int64_t off = tile_off[blockIdx.x] + inc - s;
+    for (int w = 0; w < (int)(threadIdx.x / WAVE); ++w) off += part[w];
+#pragma unroll
+    for (int j = 0; j < ROWS_PER_THREAD; ++j) {
+        int64_t r = r0 + j;
+        if (r < n) seg_off[r] = off;
+        off += cnt[j];
+    }
+}
+
+/* ------------------------------------------------------------------ scan */
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+/* 16-byte streaming load (each token is read exactly once). */
+__device__ __forceinline__ int4 load_vec(const int4 *p)
+{
+    v4i v = __builtin_nontemporal_load(reinterpret_cast<const v4i *>(p));
+    return make_int4(v.x, v.y, v.z, v.w);
+}
+
+/* One wave per segment; waves take contiguous ranges of segment ids. */
+template <bool CONTIG>
+__global__ void __launch_bounds__(256) scan_segments(const int32_t *__restrict__ tok_base, int64_t mis,
+                                                     const int64_t *__restrict__ starts,
+                                                     const int32_t *__restrict__ lengths, int64_t n,
+                                                     const int64_t *__restrict__ seg_off, int64_t seg_cap,
+                                                     int32_t *__restrict__ seg_count, uint32_t *__restrict__ events,
+                                                     TagMatch tm)
+{
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int64_t wave = uniform64((int64_t)blockIdx.x * (blockDim.x / WAVE) + (threadIdx.x / WAVE));
+    const int64_t n_waves = (int64_t)gridDim.x * (blockDim.x / WAVE);
+    const int64_t S = seg_off[n];
+    if (S > seg_cap) return; /* the row kernel reports PARASON_FLAG_WS_OVERFLOW */
+    /* S < 2^40 and n_waves < 2^20 (checked on the host), so S * wave fits */
+    const int64_t s_begin = uniform64(S * wave / n_waves);
+    const int64_t s_end = uniform64(S * (wave + 1) / n_waves);
+    if (s_begin >= s_end) return;
+
+    /* the row holding s_begin: seg_off[row] <= s_begin < seg_off[row + 1] */
+    int64_t lo = 0, hi = n;
+    while (hi - lo > 1) {
+        int64_t mid = (lo + hi) >> 1;
+        if (seg_off[mid] <= s_begin) lo = mid; else hi = mid;
+    }
+    int64_t row = uniform64(lo);
+    int64_t row_first = uniform64(seg_off[row]);
+    int64_t row_next = uniform64(seg_off[row + 1]);
+    int64_t g = 0, vrow0 = 0, vend = 0;
+    int32_t len = 0;
+    bool row_loaded = false;
+
+    for (int64_t s = s_begin; s < s_end; ++s) {
+        while (row_next <= s) {
+            ++row;
+            row_first = row_next;
+            row_next = uniform64(seg_off[row + 1]);
+            row_loaded = false;
+        }
+        if (!row_loaded) {
+            g = uniform64(starts[row] + mis);
+            len = __builtin_amdgcn_readfirstlane(lengths[row]);
+            vrow0 = g >> 2;
+            vend = (g + (int64_t)len + 3) >> 2;
+            row_loaded = true;
+        }
+        const int64_t v0 = vrow0 + (s - row_first) * SEG_VEC;
+        const int64_t v1 = min(v0 + (int64_t)SEG_VEC, vend);
+        const int4 *src = reinterpret_cast<const int4 *>(tok_base);
+
+        int4 x[LOADS];
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            int64_t v = v0 + i * WAVE + lane;
+            if (v < v1) x[i] = load_vec(src + v);
+            else x[i] = make_int4(-1, -1, -1, -1);
+        }
+
+        uint32_t cnt = 0; /* wave-uniform */
+        uint32_t *ev = events + s * EV_CAP;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const int64_t v = v0 + i * WAVE + lane;
+            /* elements 4v+j with g <= 4v+j < g+len belong to the row */
+            const int64_t lo_j = g - 4 * v, hi_j = g + (int64_t)len - 4 * v;
+            const int32_t t[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
+            uint32_t cls[4];
+            uint32_t m = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                cls[j] = classify(tm, t[j], CONTIG);
+                bool in = (j >= lo_j) && (j < hi_j) && (v < v1);
+                m |= (cls[j] != 0 && in) ? (1u << j) : 0u;
+            }
+            const uint64_t any = __ballot(m != 0);
+            if (any == 0) continue;
+            const uint64_t b0 = __ballot(m & 1u), b1 = __ballot(m & 2u), b2 = __ballot(m & 4u), b3 = __ballot(m & 8u);
+            uint32_t pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b0 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b0, 0u));
+            pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b1 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b1, pre));
+            pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b2 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b2, pre));
+            pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b3 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b3, pre));
+            if (m) {
+                uint32_t idx = cnt + pre;
+                const uint32_t local = (uint32_t)(4 * (v - v0));
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (m & (1u << j)) {
+                        if (idx < (uint32_t)EV_CAP) ev[idx] = ((local + (uint32_t)j) << 4) | cls[j];
+                        ++idx;
+                    }
+                }
+            }
+            cnt += (uint32_t)(__popcll(b0) + __popcll(b1) + __popcll(b2) + __popcll(b3));
+        }
+        if (lane == 0) seg_count[s] = (int32_t)cnt;
+    }
+}
+
+/* ------------------------------------------------------------------ automaton */
+
+/* The open block on top of the stack (kept in registers). */
+struct Top {
+    int32_t saved_acc;  /* latency of the enclosing body when <Parallel> came */
+    int32_t block_main; /* <Parallel> + outline tokens so far */
+    int32_t max_w;      /* longest finished thread */
+    int32_t n_e;        /* outline entries */
+    int32_t k;          /* threads so far */
+    uint32_t saved_ctx; /* branch type of the enclosing context */
+    uint64_t ent;       /* fast store: entry-type bits; deep store: first bit index */
+};
+
+/* Fast store: FAST_DEPTH frames per thread in LDS, entry types as a 64-bit mask. */
+struct LdsStore {
+    int32_t *lds; /* [FAST_DEPTH][FRAME_WORDS][blockDim] */
+    int tid, nt;
+    __device__ int32_t &at(int d, int f) { return lds[(d * FRAME_WORDS + f) * nt + tid]; }
+    __device__ bool push(const Top &t, int d)
+    {
+        if (d > FAST_DEPTH) return false;
+        at(d - 1, 0) = t.saved_acc;
+        at(d - 1, 1) = t.block_main;
+        at(d - 1, 2) = t.max_w;
+        at(d - 1, 3) = t.n_e;
+        at(d - 1, 4) = t.k;
+        at(d - 1, 5) = (int32_t)t.saved_ctx;
+        at(d - 1, 6) = (int32_t)(uint32_t)t.ent;
+        at(d - 1, 7) = (int32_t)(uint32_t)(t.ent >> 32);
+        return true;
+    }
+    __device__ void pop(Top &t, int d)
+    {
+        t.saved_acc = at(d - 1, 0);
+        t.block_main = at(d - 1, 1);
+        t.max_w = at(d - 1, 2);
+        t.n_e = at(d - 1, 3);
+        t.k = at(d - 1, 4);
+        t.saved_ctx = (uint32_t)at(d - 1, 5);
+        t.ent = (uint64_t)(uint32_t)at(d - 1, 6) | ((uint64_t)(uint32_t)at(d - 1, 7) << 32);
+    }
+    __device__ void begin_block(Top &t) { t.ent = 0; }
+    __device__ void end_block(const Top &) {}
+    __device__ bool add_entry(Top &t, bool trial)
+    {
+        if (t.n_e >= FAST_ENTRIES) return false;
+        if (trial) t.ent |= (uint64_t)1 << t.n_e;
+        return true;
+    }
+    __device__ uint32_t entry_type(const Top &t, int32_t k) { return ((t.ent >> k) & 1u) ? T_TRI : T_SUB; }
+};
+
+/* Deep store: frames and entry bits in global workspace (single thread). */
+struct GlobalStore {
+    int32_t *frames;  /* [DEEP_FRAMES][FRAME_WORDS] */
+    uint32_t *bits;   /* DEEP_ENTRY_BITS bits */
+    int64_t esp;      /* next free entry bit */
+    __device__ bool push(const Top &t, int d)
+    {
+        if ((int64_t)d > DEEP_FRAMES) return false;
+        int32_t *f = frames + (int64_t)(d - 1) * FRAME_WORDS;
+        f[0] = t.saved_acc;
+        f[1] = t.block_main;
+        f[2] = t.max_w;
+        f[3] = t.n_e;
+        f[4] = t.k;
+        f[5] = (int32_t)t.saved_ctx;
+        f[6] = (int32_t)(uint32_t)t.ent;
+        f[7] = (int32_t)(uint32_t)(t.ent >> 32);
+        return true;
+    }
+    __device__ void pop(Top &t, int d)
+    {
+        const int32_t *f = frames + (int64_t)(d - 1) * FRAME_WORDS;
+        t.saved_acc = f[0];
+        t.block_main = f[1];
+        t.max_w = f[2];
+        t.n_e = f[3];
+        t.k = f[4];
+        t.saved_ctx = (uint32_t)f[5];
+        t.ent = (uint64_t)(uint32_t)f[6] | ((uint64_t)(uint32_t)f[7] << 32);
+    }
+    __device__ void begin_block(Top &t) { t.ent = (uint64_t)esp; }
+    __device__ void end_block(const Top &t) { esp = (int64_t)t.ent; }
+    __device__ bool add_entry(Top &t, bool trial)
+    {
+        int64_t b = (int64_t)t.ent + t.n_e;
+        if (b >= DEEP_ENTRY_BITS) return false;
+        uint32_t w = bits[b >> 5], m = 1u << (b & 31);
+        bits[b >> 5] = trial ? (w | m) : (w & ~m);
+        esp = b + 1;
+        return true;
+    }
+    __device__ uint32_t entry_type(const Top &t, int32_t k)
+    {
+        int64_t b = (int64_t)t.ent + k;
+        return ((bits[b >> 5] >> (b & 31)) & 1u) ? T_TRI : T_SUB;
+    }
+};
+
+enum : uint32_t { S_START, S_BODY, S_P_OPEN, S_O_OPEN, S_ENTRY, S_E_DONE, S_O_DONE, S_W_DONE, S_TRAIL };
+
+/* Pushdown automaton of the grammar, fed with tag events in position order.
+ * Text runs are the gaps between consecutive event positions. */
+template <class Store>
+struct Automaton {
+    Store st;
+    int32_t prev;      /* position of the last token consumed */
+    uint32_t state;
+    int32_t acc;       /* latency of the current body (main or thread) */
+    int32_t depth, n_blocks, max_depth;
+    int32_t n_sub, n_tri;
+    uint32_t ctx;      /* innermost enclosing thread's branch type */
+    uint32_t open_tag; /* class of the open entry tag */
+    int32_t entry_len; /* Text tokens of the open entry */
+    int32_t err;       /* first error position, -1 while none */
+    bool mismatch;
+    bool overflow;     /* the store ran out: hand the row to the slow path */
+    Top top;
+
+    __device__ void init()
+    {
+        prev = -1;
+        state = S_START;
+        acc = 0;
+        depth = n_blocks = max_depth = 0;
+        n_sub = n_tri = 0;
+        ctx = T_MAIN;
+        open_tag = 0;
+        entry_len = 0;
+        err = -1;
+        mismatch = false;
+        overflow = false;
+    }
+
+    __device__ void attribute(int32_t n)
+    {
+        n_sub += ctx == T_SUB ? n : 0;
+        n_tri += ctx == T_TRI ? n : 0;
+    }
+
+    /* n > 0 Text tokens at prev+1 .. prev+n.  Returns false on error. */
+    __device__ bool text(int32_t n)
+    {
+        switch (state) {
+        case S_BODY:
+            acc += n;
+            attribute(n);
+            break;
+        case S_ENTRY:
+            top.block_main += n;
+            entry_len += n;
+            attribute(n);
+            break;
+        case S_TRAIL:
+            acc += n;
+            break;
+        default:
+            err = prev + 1;
+            return false;
+        }
+        prev += n;
+        return true;
+    }
+
+    __device__ bool fail(int32_t p)
+    {
+        err = p;
+        return false;
+    }
+
+    __device__ void open_thread()
+    {
+        uint32_t t = top.k < top.n_e ? st.entry_type(top, top.k) : T_MAIN;
+        ctx = t;
+        acc = 1;
+        attribute(1);
+        state = S_BODY;
+    }
+
+    /* The tag of class c at position p (prev == p - 1).  False on error or
+     * store overflow. */
+    __device__ bool tag(int32_t p, uint32_t c)
+    {
+        switch (state) {
+        case S_START:
+            if (c != C_THINK) return fail(p);
+            acc = 1;
+            state = S_BODY;
+            break;
+        case S_BODY:
+            if (c == C_PAR) {
+                if (depth >= 1 && !st.push(top, depth)) {
+                    overflow = true;
+                    return false;
+                }
+                top.saved_acc = acc;
+                top.block_main = 1;
+                top.max_w = 0;
+                top.n_e = 0;
+                top.k = 0;
+                top.saved_ctx = ctx;
+                st.begin_block(top);
+                depth += 1;
+                n_blocks += 1;
+                max_depth = max(max_depth, depth);
+                attribute(1);
+                state = S_P_OPEN;
+            } else if (c == C_END_THINK && depth == 0) {
+                acc += 1;
+                state = S_TRAIL;
+            } else if (c == C_END_THR && depth > 0) {
+                acc += 1;
+                attribute(1);
+                top.max_w = max(top.max_w, acc);
+                top.k += 1;
+                ctx = top.saved_ctx;
+                state = S_W_DONE;
+            } else {
+                return fail(p);
+            }
+            break;
+        case S_P_OPEN:
+            if (c != C_OUT) return fail(p);
+            top.block_main += 1;
+            attribute(1);
+            state = S_O_OPEN;
+            break;
+        case S_O_OPEN:
+        case S_E_DONE:
+            if (c == C_SUB || c == C_TRI) {
+                top.block_main += 1;
+                attribute(1);
+                open_tag = c;
+                entry_len = 0;
+                state = S_ENTRY;
+            } else if (c == C_END_OUT && state == S_E_DONE) {
+                top.block_main += 1;
+                attribute(1);
+                state = S_O_DONE;
+            } else {
+                return fail(p);
+            }
+            break;
+        case S_ENTRY:
+            if (entry_len == 0 || c != open_tag + 1) return fail(p);
+            if (!st.add_entry(top, open_tag == C_TRI)) {
+                overflow = true;
+                return false;
+            }
+            top.n_e += 1;
+            top.block_main += 1;
+            attribute(1);
+            state = S_E_DONE;
+            break;
+        case S_O_DONE:
+        case S_W_DONE:
+            if (c == C_THR) {
+                open_thread();
+            } else if (c == C_END_PAR && state == S_W_DONE) {
+                if (top.k != top.n_e) mismatch = true;
+                attribute(1);
+                int32_t lat = top.block_main + top.max_w + 1;
+                acc = top.saved_acc + lat;
+                st.end_block(top);
+                depth -= 1;
+                if (depth >= 1) st.pop(top, depth);
+                state = S_BODY;
+            } else {
+                return fail(p);
+            }
+            break;
+        default: /* S_TRAIL: only Text may follow </think> */
+            return fail(p);
+        }
+        prev = p;
+        return true;
+    }
+
+    __device__ bool event(int32_t p, uint32_t c)
+    {
+        int32_t gap = p - prev - 1;
+        if (gap > 0 && !text(gap)) return false;
+        return tag(p, c);
+    }
+
+    /* End of the row (no error or overflow so far). */
+    __device__ void finish(int32_t len)
+    {
+        int32_t gap = len - prev - 1;
+        if (gap > 0 && !text(gap)) return;
+        if (state != S_TRAIL) err = len;
+    }
+};
+
+struct RowOut {
+    int32_t *total, *latency, *n_subtask, *n_trial, *n_blocks, *max_depth, *first_error_pos;
+    uint32_t *flags;
+};
+
+__device__ __forceinline__ void write_row(const RowOut &o, int64_t r, int32_t total, int32_t lat, int32_t ns,
+                                          int32_t nt, int32_t nb, int32_t md, int32_t fe, uint32_t fl)
+{
+    o.total[r] = total;
+    o.latency[r] = lat;
+    o.n_subtask[r] = ns;
+    o.n_trial[r] = nt;
+    o.n_blocks[r] = nb;
+    o.max_depth[r] = md;
+    o.first_error_pos[r] = fe;
+    o.flags[r] = fl;
+}
+
+template <class Store>
+__device__ __forceinline__ void write_result(const RowOut &o, int64_t r, int32_t len, const Automaton<Store> &A)
+{
+    if (A.err < 0) {
+        uint32_t fl = PARASON_FLAG_VALID;
+        if (A.mismatch) fl |= PARASON_FLAG_COUNT_MISMATCH;
+        if (A.n_blocks > 0) fl |= PARASON_FLAG_TRIGGERED;
+        write_row(o, r, len, A.acc, A.n_sub, A.n_tri, A.n_blocks, A.max_depth, -1, fl);
+    } else {
+        write_row(o, r, len, len, 0, 0, 0, 0, A.err, A.err == len ? PARASON_FLAG_TRUNCATED : 0u);
+    }
+}
+
+struct RowArgs {
+    const int32_t *tok_base;
+    int64_t mis;
+    const int64_t *starts;
+    const int32_t *lengths;
+    int64_t n;
+    const int64_t *seg_off;
+    int64_t seg_cap;
+    const int32_t *seg_count;
+    const uint32_t *events;
+    TagMatch tm;
+    RowOut out;
+};
+
+/* Feed row r's events to A.  Returns false when A stopped early.
+ * A segment whose events were not stored (more than EV_CAP tags) is classified
+ * again token by token.  Both sources feed the same single call of A.event:
+ * with two inlined copies of the automaton (one per source) the gfx950 build
+ * returned wrong results for dense segments although the same source is
+ * correct when compiled for the CPU. */
+template <class Store>
+__device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, Automaton<Store> &A)
+{
+    const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
+    const int64_t vrow0 = g >> 2, vend = (g + (int64_t)len + 3) >> 2;
+    for (int64_t s = s0; s < s1; ++s) {
+        const int64_t v0 = vrow0 + (s - s0) * SEG_VEC;
+        const int64_t base = 4 * v0 - g;
+        const int32_t cnt = a.seg_count[s];
+        const bool dense = cnt > EV_CAP;
+        const uint32_t *ev = a.events + s * EV_CAP;
+        const int64_t q_end = 4 * min(v0 + (int64_t)SEG_VEC, vend);
+        int64_t q = 4 * v0;
+        int32_t e = 0;
+        for (;;) {
+            int32_t p = 0;
+            uint32_t c = 0;
+            if (!dense) {
+                if (e >= cnt) break;
+                uint32_t w = ev[e++];
+                p = (int32_t)(base + (w >> 4));
+                c = w & 15u;
+            } else {
+                while (q < q_end) {
+                    const int32_t t = a.tok_base[q];
+                    const int64_t pp = q - g;
+                    ++q;
+                    if (pp < 0 || pp >= len) continue;
+                    c = classify(a.tm, t, a.tm.contiguous != 0);
+                    if (c) {
+                        p = (int32_t)pp;
+                        break;
+                    }
+                }
+                if (c == 0) break;
+            }
+            if (!A.event(p, c)) return false;
+        }
+    }
+    return true;
+}
+
+/* One thread per row. */
+__global__ void __launch_bounds__(64) rows_fast(RowArgs a, int32_t *__restrict__ counters,
+                                                int32_t *__restrict__ deep_rows)
+{
+    __shared__ int32_t lds[FAST_DEPTH * FRAME_WORDS * 64];
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= a.n) return;
+    const int64_t start = a.starts[r];
+    const int32_t len = a.lengths[r];
+    if (start < 0 || len < 0) {
+        write_row(a.out, r, 0, 0, 0, 0, 0, 0, 0, PARASON_FLAG_BAD_ROW);
+        return;
+    }
+    if (a.seg_off[a.n] > a.seg_cap) {
+        write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
+        return;
+    }
+    Automaton<LdsStore> A;
+    A.st.lds = lds;
+    A.st.tid = threadIdx.x;
+    A.st.nt = blockDim.x;
+    A.init();
+    if (drive_row(a, r, start + a.mis, len, A)) A.finish(len);
+    if (A.overflow) {
+        int32_t slot = atomicAdd(&counters[0], 1);
+        deep_rows[slot] = (int32_t)r;
+        return; /* rows_deep writes this row */
+    }
+    write_result(a.out, r, len, A);
+}
+
+/* Rows whose nesting or entry count exceeded the fast store, one after the
+ * other, on a single thread with frames in global workspace. */
+__global__ void __launch_bounds__(64) rows_deep(RowArgs a, const int32_t *__restrict__ counters,
+                                                const int32_t *__restrict__ deep_rows, int32_t *__restrict__ frames,
+                                                uint32_t *__restrict__ bits)
+{
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    const int32_t n_deep = counters[0];
+    for (int32_t i = 0; i < n_deep; ++i) {
+        const int64_t r = deep_rows[i];
+        const int32_t len = a.lengths[r];
+        Automaton<GlobalStore> A;
+        A.st.frames = frames;
+        A.st.bits = bits;
+        A.st.esp = 0;
+        A.init();
+        if (drive_row(a, r, a.starts[r] + a.mis, len, A)) A.finish(len);
+        if (A.overflow)
+            write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_DEPTH_LIMIT);
+        else
+            write_result(a.out, r, len, A);
+    }
+}
+
+/* ------------------------------------------------------------------ reward */
+
+struct RewardArgs {
+    const int32_t *total, *latency, *n_subtask, *n_trial;
+    const uint32_t *flags;
+    const uint8_t *correct;
+    int64_t n_groups;
+    int32_t G;
+    double alpha, beta_s, beta_r, rho, rho_clip;
+    uint32_t cfg_flags;
+    float *reward, *r_subtask, *r_trial, *eta;
+};
+
+constexpr uint32_t NOT_EVALUATED = PARASON_FLAG_DEPTH_LIMIT | PARASON_FLAG_WS_OVERFLOW | PARASON_FLAG_BAD_ROW;
+
+__device__ __forceinline__ double ratio(int32_t n, int32_t total)
+{
+    return total > 0 ? __ddiv_rn((double)n, (double)total) : 0.0;
+}
+
+/* Do all rows of the group have the same ratio n/total?  Exact (cross-multiplied). */
+__device__ __forceinline__ bool same_ratio(const int32_t *nn, const int32_t *tt, int64_t r0, int32_t G)
+{
+    int64_t n0 = tt[r0] > 0 ? nn[r0] : 0, d0 = tt[r0] > 0 ? tt[r0] : 1;
+    for (int32_t i = 1; i < G; ++i) {
+        int64_t ni = tt[r0 + i] > 0 ? nn[r0 + i] : 0, di = tt[r0 + i] > 0 ? tt[r0 + i] : 1;
+        if (ni * d0 != n0 * di) return false;
+    }
+    return true;
+}
+
+/* mean and population standard deviation of x over the group, by index order */
+struct Moments {
+    double mu, sigma;
+};
+
+template <class F>
+__device__ __forceinline__ Moments moments(F x, int32_t G)
+{
+    double s = 0.0;
+    for (int32_t i = 0; i < G; ++i) s = __dadd_rn(s, x(i));
+    double mu = __ddiv_rn(s, (double)G);
+    double ss = 0.0;
+    for (int32_t i = 0; i < G; ++i) {
+        double d = __dsub_rn(x(i), mu);
+        ss = __dadd_rn(ss, __dmul_rn(d, d));
+    }
+    return Moments{mu, __dsqrt_rn(__ddiv_rn(ss, (double)G))};
+}
+
+__device__ __forceinline__ double zscore(double x, Moments m, bool all_equal)
+{
+    return (all_equal || m.sigma == 0.0) ? 0.0 : __ddiv_rn(__dsub_rn(x, m.mu), m.sigma);
+}
+
+__global__ void __launch_bounds__(256) group_reward(RewardArgs a)
+{
+    const int64_t grp = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (grp >= a.n_groups) return;
+    const int32_t G = a.G;
+    const int64_t r0 = grp * G;
+
+    bool evaluated = true;
+    bool lat_equal = true;
+    for (int32_t i = 0; i < G; ++i) {
+        evaluated = evaluated && !(a.flags[r0 + i] & NOT_EVALUATED);
+        lat_equal = lat_equal && a.latency[r0 + i] == a.latency[r0];
+    }
+    if (!evaluated) {
+        const float nan = __int_as_float(0x7fc00000);
+        for (int32_t i = 0; i < G; ++i) {
+            a.reward[r0 + i] = nan;
+            if (a.r_subtask) a.r_subtask[r0 + i] = nan;
+            if (a.r_trial) a.r_trial[r0 + i] = nan;
+            if (a.eta) a.eta[r0 + i] = nan;
+        }
+        return;
+    }
+    const bool sub_equal = same_ratio(a.n_subtask, a.total, r0, G);
+    const bool tri_equal = same_ratio(a.n_trial, a.total, r0, G);
+    auto xT = [&](int32_t i) { return (double)a.latency[r0 + i]; };
+    auto xs = [&](int32_t i) { return ratio(a.n_subtask[r0 + i], a.total[r0 + i]); };
+    auto xr = [&](int32_t i) { return ratio(a.n_trial[r0 + i], a.total[r0 + i]); };
+    const Moments mT = moments(xT, G), ms = moments(xs, G), mr = moments(xr, G);
+
+    for (int32_t i = 0; i < G; ++i) {
+        const int64_t r = r0 + i;
+        const int32_t tot = a.total[r];
+        const double e = tot > 0 ? __dsub_rn(1.0, __ddiv_rn((double)a.latency[r], (double)tot)) : 0.0;
+        const bool valid = (a.flags[r] & PARASON_FLAG_VALID) != 0;
+        const bool c = a.correct[r] != 0 && (valid || (a.cfg_flags & PARASON_CFG_INVALID_KEEPS_CORRECTNESS));
+        const double accel = __dmul_rn(a.rho, e);
+        const double clipped = accel < a.rho_clip ? accel : a.rho_clip;
+        double inner = __dsub_rn(1.0, __dmul_rn(a.alpha, zscore(xT(i), mT, lat_equal)));
+        inner = __dadd_rn(inner, __dmul_rn(a.beta_s, zscore(xs(i), ms, sub_equal)));
+        inner = __dadd_rn(inner, __dmul_rn(a.beta_r, zscore(xr(i), mr, tri_equal)));
+        inner = __dadd_rn(inner, clipped);
+        const double R = __dadd_rn(-1.0, __dmul_rn(__dmul_rn(2.0, c ? 1.0 : 0.0), inner));
+        a.reward[r] = (float)R;
+        if (a.r_subtask) a.r_subtask[r] = (float)xs(i);
+        if (a.r_trial) a.r_trial[r] = (float)xr(i);
+        if (a.eta) a.eta[r] = (float)e;
+    }
+}
+
+} /* namespace pk */

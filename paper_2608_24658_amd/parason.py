@@ -1,0 +1,220 @@
+"""Python binding of libparason.so (argument marshalling only).
+
+Every step of the path runs in the HIP kernels behind the C-ABI declared in
+``include/parason.h``; this module turns torch tensors into device pointers and
+passes torch's current HIP stream.  It raises if the library is missing: there
+is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libparason.so")
+
+OK = 0
+ERR_NULL, ERR_SIZE, ERR_GROUP, ERR_WORKSPACE, ERR_TAGS, ERR_PARAM, ERR_ALIGN, ERR_HIP, ERR_DEVICE = range(-1, -10, -1)
+
+FLAG_VALID = 1 << 0
+FLAG_TRUNCATED = 1 << 1
+FLAG_COUNT_MISMATCH = 1 << 2
+FLAG_TRIGGERED = 1 << 3
+FLAG_DEPTH_LIMIT = 1 << 8
+FLAG_WS_OVERFLOW = 1 << 9
+FLAG_BAD_ROW = 1 << 10
+
+CFG_INVALID_KEEPS_CORRECTNESS = 1 << 0
+
+MAX_DEPTH = 1 << 20
+MAX_OPEN_ENTRIES = 1 << 24
+
+EXPORTED = ("parason_create", "parason_workspace_size", "parason_run", "parason_run_timed", "parason_destroy",
+            "parason_strerror")
+
+
+class Config(ctypes.Structure):
+    _fields_ = [
+        ("tag_ids", ctypes.c_int32 * 12),
+        ("group_size", ctypes.c_int32),
+        ("alpha", ctypes.c_double),
+        ("beta_subtask", ctypes.c_double),
+        ("beta_trial", ctypes.c_double),
+        ("rho", ctypes.c_double),
+        ("rho_clip", ctypes.c_double),
+        ("flags", ctypes.c_uint32),
+    ]
+
+
+class Outputs(ctypes.Structure):
+    _fields_ = [
+        ("total", ctypes.c_void_p),
+        ("latency", ctypes.c_void_p),
+        ("n_subtask", ctypes.c_void_p),
+        ("n_trial", ctypes.c_void_p),
+        ("n_blocks", ctypes.c_void_p),
+        ("max_depth", ctypes.c_void_p),
+        ("first_error_pos", ctypes.c_void_p),
+        ("flags", ctypes.c_void_p),
+        ("reward", ctypes.c_void_p),
+        ("r_subtask", ctypes.c_void_p),
+        ("r_trial", ctypes.c_void_p),
+        ("eta", ctypes.c_void_p),
+    ]
+
+
+INT_FIELDS = ("total", "latency", "n_subtask", "n_trial", "n_blocks", "max_depth", "first_error_pos")
+FLOAT_FIELDS = ("reward", "r_subtask", "r_trial", "eta")
+
+_lib = None
+
+
+class ParasonError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s failed: %s (%d)" % (what, strerror(status), status))
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                "libparason.so is not built (%s); run __graft_entry__.build() -- there is no fallback" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        L.parason_create.restype = ctypes.c_int
+        L.parason_create.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(ctypes.c_void_p)]
+        L.parason_workspace_size.restype = ctypes.c_int
+        L.parason_workspace_size.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]
+        L.parason_run.restype = ctypes.c_int
+        L.parason_run.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+            ctypes.POINTER(Outputs), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+        ]
+        L.parason_run_timed.restype = ctypes.c_int
+        L.parason_run_timed.argtypes = L.parason_run.argtypes + [ctypes.c_void_p]
+        L.parason_destroy.restype = None
+        L.parason_destroy.argtypes = [ctypes.c_void_p]
+        L.parason_strerror.restype = ctypes.c_char_p
+        L.parason_strerror.argtypes = [ctypes.c_int]
+        _lib = L
+    return _lib
+
+
+def strerror(status: int) -> str:
+    return lib().parason_strerror(status).decode()
+
+
+def make_config(tag_ids, group_size=8, alpha=0.1, beta_subtask=0.0, beta_trial=0.1, rho=0.5, rho_clip=0.25,
+                flags=0) -> Config:
+    c = Config()
+    ids = [int(t) for t in tag_ids]
+    if len(ids) != 12:
+        raise ValueError("tag_ids must have 12 entries")
+    for i, t in enumerate(ids):
+        c.tag_ids[i] = t
+    c.group_size = int(group_size)
+    c.alpha, c.beta_subtask, c.beta_trial = float(alpha), float(beta_subtask), float(beta_trial)
+    c.rho, c.rho_clip = float(rho), float(rho_clip)
+    c.flags = int(flags)
+    return c
+
+
+class Parason:
+    """Handle of the C-ABI (immutable configuration)."""
+
+    def __init__(self, tag_ids, group_size=8, alpha=0.1, beta_subtask=0.0, beta_trial=0.1, rho=0.5,
+                 rho_clip=0.25, flags=0):
+        self.config = make_config(tag_ids, group_size, alpha, beta_subtask, beta_trial, rho, rho_clip, flags)
+        h = ctypes.c_void_p()
+        rc = lib().parason_create(ctypes.byref(self.config), ctypes.byref(h))
+        if rc != OK:
+            raise ParasonError(rc, "parason_create")
+        self._h = h
+
+    @property
+    def group_size(self) -> int:
+        return self.config.group_size
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().parason_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace_size(self, n_traj: int, total_tokens: int) -> int:
+        b = ctypes.c_size_t()
+        rc = lib().parason_workspace_size(self._h, int(n_traj), int(total_tokens), ctypes.byref(b))
+        if rc != OK:
+            raise ParasonError(rc, "parason_workspace_size")
+        return b.value
+
+    def alloc_outputs(self, n_traj: int, device, derived: bool = True) -> dict:
+        import torch
+
+        out = {k: torch.empty(n_traj, dtype=torch.int32, device=device) for k in INT_FIELDS}
+        out["flags"] = torch.empty(n_traj, dtype=torch.int32, device=device)  # uint32 bits
+        out["reward"] = torch.empty(n_traj, dtype=torch.float32, device=device)
+        if derived:
+            for k in ("r_subtask", "r_trial", "eta"):
+                out[k] = torch.empty(n_traj, dtype=torch.float32, device=device)
+        return out
+
+    def alloc_workspace(self, n_traj: int, total_tokens: int, device):
+        import torch
+
+        return torch.empty(self.workspace_size(n_traj, total_tokens), dtype=torch.uint8, device=device)
+
+    def run_raw(self, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, n_traj, out: dict, ws_ptr, ws_bytes,
+                stream) -> int:
+        """Direct C-ABI call with raw device pointers; returns the status."""
+        o = Outputs()
+        for k in INT_FIELDS + ("flags", "reward"):
+            setattr(o, k, out[k].data_ptr())
+        for k in ("r_subtask", "r_trial", "eta"):
+            setattr(o, k, out[k].data_ptr() if k in out and out[k] is not None else None)
+        return lib().parason_run(self._h, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, int(n_traj),
+                                 ctypes.byref(o), ws_ptr, int(ws_bytes), stream)
+
+    def run_timed_raw(self, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, n_traj, out: dict, ws_ptr, ws_bytes,
+                      stream, scan_events) -> int:
+        """parason_run_timed: scan_events is a ctypes array of two hipEvent_t (or None)."""
+        o = Outputs()
+        for k in INT_FIELDS + ("flags", "reward"):
+            setattr(o, k, out[k].data_ptr())
+        for k in ("r_subtask", "r_trial", "eta"):
+            setattr(o, k, out[k].data_ptr() if k in out and out[k] is not None else None)
+        ev = ctypes.cast(scan_events, ctypes.c_void_p) if scan_events is not None else None
+        return lib().parason_run_timed(self._h, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, int(n_traj),
+                                       ctypes.byref(o), ws_ptr, int(ws_bytes), stream, ev)
+
+    def run(self, tokens, starts, lengths, correct, out: dict | None = None, workspace=None, total_tokens=None,
+            derived: bool = True) -> dict:
+        """Evaluate a batch of rows held in device tensors (asynchronous on the
+        current stream).  tokens int32, starts int64, lengths int32, correct uint8."""
+        import torch
+
+        n = int(starts.numel())
+        for t, dt in ((tokens, torch.int32), (starts, torch.int64), (lengths, torch.int32), (correct, torch.uint8)):
+            if t.dtype != dt or not t.is_cuda or not t.is_contiguous():
+                raise TypeError("expected contiguous %s device tensors" % dt)
+        if lengths.numel() != n or correct.numel() != n:
+            raise ValueError("starts, lengths and correct must have the same length")
+        if out is None:
+            out = self.alloc_outputs(n, tokens.device, derived)
+        if workspace is None:
+            if total_tokens is None:
+                total_tokens = int(lengths.to(torch.int64).clamp_min(0).sum().item()) if n else 0
+            workspace = self.alloc_workspace(n, total_tokens, tokens.device)
+        stream = torch.cuda.current_stream(tokens.device).cuda_stream
+        tok_ptr = tokens.data_ptr() if tokens.numel() else starts.data_ptr()
+        rc = self.run_raw(tok_ptr, starts.data_ptr(), lengths.data_ptr(), correct.data_ptr(), n, out,
+                          workspace.data_ptr(), workspace.numel(), stream)
+        if rc != OK:
+            raise ParasonError(rc, "parason_run")
+        return out

@@ -1,0 +1,80 @@
+"""Shared helpers of the GPU parity tests: run the HIP path through the C-ABI
+and compare with the CPU oracle on the same inputs.
+
+Tolerances: every integer output (total, latency, branch tokens, blocks, depth,
+first error position, flags) must be bit-exact.  Both sides evaluate the reward
+in IEEE double in the same order; the GPU rounds it once to float, so
+|R_gpu - R_oracle| <= 2^-24 |R| for correctly rounded double arithmetic.  The
+test bound is 2^-23 * max(1, |R|) (one float ulp at |R| = 1); the same bound
+holds for R_subtask, R_trial and eta.
+"""
+import sys
+
+import numpy as np
+
+from oracle import oracle as O
+from paper_2608_24658_amd import parason as PX
+
+TOL = 2.0 ** -23
+
+DEFAULT_COEF = dict(alpha=0.1, beta_subtask=0.0, beta_trial=0.1, rho=0.5, rho_clip=0.25)
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(a, dtype, device):
+    import torch
+
+    return torch.as_tensor(np.ascontiguousarray(a)).to(device=device, dtype=dtype)
+
+
+def oracle_expect(tokens, starts, lengths, correct, tag_ids, G=8, coef=DEFAULT_COEF, cfg_flags=0):
+    rows = O.eval_rows(tokens, starts, lengths, tag_ids)
+    R, rs, rt, eta = O.group_reward(rows, correct, G, coef["alpha"], coef["beta_subtask"], coef["beta_trial"],
+                                    coef["rho"], coef["rho_clip"], cfg_flags)
+    return rows, R, rs, rt, eta
+
+
+def fetch(out):
+    res = {k: v.cpu().numpy() for k, v in out.items()}
+    res["flags"] = res["flags"].view(np.uint32)
+    return res
+
+
+def compare(got, rows, R, rs, rt, eta, idx=None, what=""):
+    """Compare GPU outputs `got` (dict of numpy arrays) with the oracle's rows
+    `rows` and float64 values; idx selects the GPU rows the oracle rows belong to."""
+    sel = (lambda a: a) if idx is None else (lambda a: a[idx])
+    for k in PX.INT_FIELDS:
+        g = sel(got[k])
+        if not np.array_equal(g, rows[k]):
+            bad = np.nonzero(g != rows[k])[0]
+            raise AssertionError("%s %s differs at %d rows, first %d: gpu %d oracle %d" % (
+                what, k, bad.size, bad[0], g[bad[0]], rows[k][bad[0]]))
+    g = sel(got["flags"])
+    if not np.array_equal(g, rows["flags"]):
+        bad = np.nonzero(g != rows["flags"])[0]
+        raise AssertionError("%s flags differ at %d rows, first %d: gpu %x oracle %x" % (
+            what, bad.size, bad[0], g[bad[0]], rows["flags"][bad[0]]))
+    for name, ref in (("reward", R), ("r_subtask", rs), ("r_trial", rt), ("eta", eta)):
+        if name not in got:
+            continue
+        v = sel(got[name]).astype(np.float64)
+        err = np.abs(v - ref)
+        lim = TOL * np.maximum(1.0, np.abs(ref))
+        if not np.all(err <= lim):
+            i = int(np.argmax(err - lim))
+            raise AssertionError("%s %s row %d: gpu %.9g oracle %.17g" % (what, name, i, v[i], ref[i]))
+    n_exact = int(np.sum(sel(got["reward"]) == R.astype(np.float32)))
+    return n_exact
+
+
+def run_gpu(px, tokens_d, starts_d, lengths_d, correct_d, ws_total=None):
+    import torch
+
+    out = px.run(tokens_d, starts_d, lengths_d, correct_d, total_tokens=ws_total)
+    torch.cuda.synchronize()
+    return fetch(out)

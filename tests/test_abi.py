@@ -1,0 +1,110 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function the
+header declares, and rejects bad arguments on the host before any launch.
+
+Every parason_run call here fails a host-side check before the first HIP call,
+so these tests are safe on a GPU machine too (no kernel ever sees the fake
+pointers)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_24658_amd import parason as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "parason.h")
+TAGS = list(range(151924, 151936))
+FAKE = 0x100000  # never dereferenced: each call below fails a host check first
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(parason_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_function():
+    names = declared_functions()
+    assert set(names) == set(P.EXPORTED)
+    L = P.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_strerror_covers_codes():
+    for rc in range(0, -10, -1):
+        assert P.strerror(rc) != "unknown status"
+    assert P.strerror(-99) == "unknown status"
+
+
+def _create(cfg):
+    h = ctypes.c_void_p()
+    rc = P.lib().parason_create(ctypes.byref(cfg), ctypes.byref(h))
+    if rc == P.OK:
+        P.lib().parason_destroy(h)
+    return rc
+
+
+def test_create_validates_config():
+    assert _create(P.make_config(TAGS)) == P.OK
+    assert _create(P.make_config(TAGS[:11] + [TAGS[0]])) == P.ERR_TAGS
+    assert _create(P.make_config([-1] + TAGS[1:])) == P.ERR_TAGS
+    assert _create(P.make_config(TAGS, group_size=0)) == P.ERR_GROUP
+    assert _create(P.make_config(TAGS, alpha=float("nan"))) == P.ERR_PARAM
+    assert _create(P.make_config(TAGS, rho_clip=float("inf"))) == P.ERR_PARAM
+    h = ctypes.c_void_p()
+    assert P.lib().parason_create(None, ctypes.byref(h)) == P.ERR_NULL
+    with pytest.raises(P.ParasonError):
+        P.Parason(TAGS, group_size=-3)
+
+
+def test_workspace_size_validates_and_grows():
+    px = P.Parason(TAGS)
+    a = px.workspace_size(8, 1000)
+    b = px.workspace_size(8, 10 ** 6)
+    c = px.workspace_size(800, 10 ** 6)
+    assert 0 < a < b < c
+    with pytest.raises(P.ParasonError):
+        px.workspace_size(-1, 10)
+    with pytest.raises(P.ParasonError):
+        px.workspace_size(8, -10)
+    sz = ctypes.c_size_t()
+    assert P.lib().parason_workspace_size(None, 8, 10, ctypes.byref(sz)) == P.ERR_NULL
+
+
+class _FakeOut(dict):
+    def __init__(self):
+        class T:
+            def __init__(self, p):
+                self.p = p
+
+            def data_ptr(self):
+                return self.p
+
+        super().__init__({k: T(FAKE) for k in P.INT_FIELDS + ("flags", "reward")})
+
+
+def test_run_rejects_bad_arguments_before_launch():
+    px = P.Parason(TAGS, group_size=8)
+    out = _FakeOut()
+    ws = px.workspace_size(16, 1000)
+    run = px.run_raw
+    # n_traj not a multiple of G
+    assert run(FAKE, FAKE, FAKE, FAKE, 12, out, FAKE, ws, None) == P.ERR_GROUP
+    assert run(FAKE, FAKE, FAKE, FAKE, -8, out, FAKE, ws, None) == P.ERR_SIZE
+    # n_traj == 0 is a no-op
+    assert run(0, 0, 0, 0, 0, out, 0, 0, None) == P.OK
+    # NULL inputs
+    assert run(0, FAKE, FAKE, FAKE, 16, out, FAKE, ws, None) == P.ERR_NULL
+    assert run(FAKE, FAKE, FAKE, 0, 16, out, FAKE, ws, None) == P.ERR_NULL
+    assert run(FAKE, FAKE, FAKE, FAKE, 16, out, 0, ws, None) == P.ERR_NULL
+    bad = dict(out)
+    bad["reward"] = type(out["reward"])(0)
+    assert run(FAKE, FAKE, FAKE, FAKE, 16, bad, FAKE, ws, None) == P.ERR_NULL
+    # alignment: tokens must be 4-byte aligned, the workspace 256-byte aligned
+    assert run(FAKE + 2, FAKE, FAKE, FAKE, 16, out, FAKE, ws, None) == P.ERR_ALIGN
+    assert run(FAKE, FAKE, FAKE, FAKE, 16, out, FAKE + 64, ws, None) == P.ERR_ALIGN
+    # workspace too small
+    assert run(FAKE, FAKE, FAKE, FAKE, 16, out, FAKE, 1024, None) == P.ERR_WORKSPACE
+    assert P.lib().parason_run(None, FAKE, FAKE, FAKE, FAKE, 16, None, FAKE, ws, None) == P.ERR_NULL

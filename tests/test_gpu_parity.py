@@ -1,0 +1,257 @@
+"""GPU parity: the HIP path (through the C-ABI) against the CPU oracle.
+
+Inputs are the seeded synthetic workloads (generated on the device and
+regenerated bit-identically by the host mirror) and hand-built adversarial
+batches.  Integer outputs must be bit-exact; float outputs within the bound
+stated in gpu_util.
+"""
+import numpy as np
+import pytest
+
+import grammar_pins as GP
+from gpu_util import DEFAULT_COEF, compare, fetch, log, oracle_expect, run_gpu, to_dev
+from oracle import oracle as O
+from paper_2608_24658_amd import parason as PX
+from paper_2608_24658_amd.synth import synth as S
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+G = S.GROUP_SIZE
+TAGS = S.CONTIGUOUS_TAGS
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def px_for(tags=TAGS, **kw):
+    coef = dict(DEFAULT_COEF)
+    coef.update(kw)
+    return PX.Parason(tags, group_size=G, **coef), coef
+
+
+@pytest.mark.parametrize("workload", ["tiny", "small", "ragged", "typical"])
+def test_workload_parity(dev, workload):
+    log("case workload=%s" % workload)
+    P = S.make_params(workload)
+    n = S.n_rows_of(workload)
+    tok_d, st_d, ln_d, co_d = S.device_batch(P, n, device=dev)
+    tok_h, st_h, ln_h, co_h = S.host_batch(P, n)
+    assert np.array_equal(st_d.cpu().numpy(), st_h) and np.array_equal(ln_d.cpu().numpy(), ln_h)
+    assert np.array_equal(co_d.cpu().numpy(), co_h)
+    assert np.array_equal(tok_d.cpu().numpy(), tok_h), "device generator differs from the host mirror"
+    px, coef = px_for()
+    got = run_gpu(px, tok_d, st_d, ln_d, co_d)
+    rows, R, rs, rt, eta = oracle_expect(tok_h, st_h, ln_h, co_h, TAGS, G, coef)
+    n_exact = compare(got, rows, R, rs, rt, eta, what=workload)
+    log("%s: %d rows, %d tokens, %d/%d rewards bit-exact" % (workload, n, tok_h.size, n_exact, n))
+
+
+def test_scattered_tag_ids(dev):
+    log("case scattered tags")
+    P = S.make_params("small", tag_ids=S.SCATTERED_TAGS)
+    n = S.n_rows_of("small")
+    tok_d, st_d, ln_d, co_d = S.device_batch(P, n, device=dev)
+    tok_h, st_h, ln_h, co_h = S.host_batch(P, n)
+    assert np.array_equal(tok_d.cpu().numpy(), tok_h)
+    px, coef = px_for(S.SCATTERED_TAGS, alpha=0.0, beta_subtask=0.05, beta_trial=0.0)
+    got = run_gpu(px, tok_d, st_d, ln_d, co_d)
+    compare(got, *oracle_expect(tok_h, st_h, ln_h, co_h, S.SCATTERED_TAGS, G, coef), what="scattered")
+
+
+def pack(streams, tags, text_ids=None):
+    """Class strings -> packed tokens, starts, lengths (rows padded to a multiple of G)."""
+    rng = np.random.default_rng(len(streams))
+    toks = []
+    for s in streams:
+        t = np.array(GP.to_tokens(s, tags), dtype=np.int32) if len(s) else np.zeros(0, np.int32)
+        text = rng.integers(0, 150000, size=t.size).astype(np.int32)
+        text = np.where(np.isin(text, tags), 7, text)
+        is_text = np.array([c == GP.TEXT for c in s], dtype=bool) if len(s) else np.zeros(0, bool)
+        toks.append(np.where(is_text, text, t))
+    while len(toks) % G:
+        toks.append(np.array(GP.to_tokens(GP.parse_names("think t3 /think"), tags), np.int32))
+    lengths = np.array([t.size for t in toks], np.int32)
+    starts = np.zeros(len(toks), np.int64)
+    starts[1:] = np.cumsum(lengths[:-1])
+    tokens = np.concatenate(toks) if lengths.sum() else np.zeros(0, np.int32)
+    return tokens, starts, lengths
+
+
+def deep_stream(depth, kind=GP.SUB):
+    close = GP.END_SUB if kind == GP.SUB else GP.END_TRI
+    s = [GP.THINK]
+    for _ in range(depth):
+        s += [GP.PAR, GP.OUT, kind, GP.TEXT, close, GP.END_OUT, GP.THR, GP.TEXT]
+    for _ in range(depth):
+        s += [GP.END_THR, GP.END_PAR]
+    return s + [GP.END_THINK]
+
+
+def fanout_stream(k, n_threads=None, trial_every=3):
+    s = [GP.THINK, GP.TEXT, GP.PAR, GP.OUT]
+    for i in range(k):
+        if i % trial_every == 0:
+            s += [GP.TRI, GP.TEXT, GP.END_TRI]
+        else:
+            s += [GP.SUB, GP.TEXT, GP.TEXT, GP.END_SUB]
+    s += [GP.END_OUT]
+    for i in range(k if n_threads is None else n_threads):
+        s += [GP.THR] + [GP.TEXT] * (i % 5) + [GP.END_THR]
+    return s + [GP.END_PAR, GP.END_THINK]
+
+
+def adversarial_streams():
+    rng = np.random.default_rng(11)
+    streams = []
+    # every valid string up to length 14 plus mutations/truncations of some
+    valid = [list(s) for s in GP.enumerate_valid(16)]
+    streams += valid[::3]
+    for s in valid[::7]:
+        i = int(rng.integers(0, len(s)))
+        streams.append(s[:i] + [int(rng.integers(0, 13))] + s[i + 1:])
+        streams.append(s[: int(rng.integers(0, len(s) + 1))])
+    # empty rows, single tokens
+    streams += [[], [GP.THINK], [GP.TEXT], [GP.END_THINK]]
+    # nesting: fast-path limit is 9 levels, then the deep path
+    streams += [deep_stream(d) for d in (1, 2, 8, 9, 10, 40, 1000)]
+    streams.append(deep_stream(300, GP.TRI)[:-5])  # truncated deep
+    # fan-out beyond the 64 entries of the fast path, with a thread-count mismatch
+    streams += [fanout_stream(64), fanout_stream(65), fanout_stream(200, 150), fanout_stream(70, 90)]
+    # dense: tags everywhere (segments overflow their event capacity)
+    dense = [GP.THINK]
+    for _ in range(2500):
+        dense += [GP.PAR, GP.OUT, GP.TRI, GP.TEXT, GP.END_TRI, GP.END_OUT, GP.THR, GP.END_THR, GP.THR, GP.TEXT,
+                  GP.END_THR, GP.END_PAR]
+    streams.append(dense + [GP.END_THINK, GP.TEXT])
+    streams.append(dense[:-3] + [GP.END_THINK])  # invalid deep inside a dense row
+    # long text with tags straddling segment boundaries
+    long = [GP.THINK] + [GP.TEXT] * 4094 + [GP.PAR, GP.OUT, GP.SUB, GP.TEXT, GP.END_SUB, GP.SUB, GP.TEXT, GP.END_SUB,
+                                           GP.END_OUT, GP.THR] + [GP.TEXT] * 9000 + [GP.END_THR, GP.THR, GP.END_THR,
+                                                                                      GP.END_PAR, GP.END_THINK]
+    streams.append(long)
+    streams.append(long[:4097] + [GP.TEXT] + long[4097:])  # misplaced text
+    # the repaired Figure 3
+    import json
+    import os
+
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "fig3_repaired.json")))
+    streams.append(GP.parse_names(g["stream"]))
+    return streams
+
+
+@pytest.mark.parametrize("tags", ["contiguous", "scattered"])
+def test_adversarial_streams(dev, tags):
+    log("case adversarial tags=%s" % tags)
+    tag_ids = TAGS if tags == "contiguous" else S.SCATTERED_TAGS
+    tokens, starts, lengths = pack(adversarial_streams(), tag_ids)
+    n = lengths.size
+    correct = (np.arange(n) % 3 != 0).astype(np.uint8)
+    px, coef = px_for(tag_ids)
+    got = run_gpu(px, to_dev(tokens, torch.int32, dev), to_dev(starts, torch.int64, dev),
+                  to_dev(lengths, torch.int32, dev), to_dev(correct, torch.uint8, dev))
+    compare(got, *oracle_expect(tokens, starts, lengths, correct, tag_ids, G, coef), what="adversarial")
+    assert int(np.sum(got["max_depth"] == 1000)) == 1
+    log("adversarial: %d rows ok" % n)
+
+
+def test_layouts_misaligned_padded_overlapping_reversed(dev):
+    log("case layouts")
+    P = S.make_params("small")
+    tok_h, st_h, ln_h, co_h = S.host_batch(P, 64)
+    px, coef = px_for()
+    expect = oracle_expect(tok_h, st_h, ln_h, co_h, TAGS, G, coef)
+    # misaligned base pointer: tokens start 1, 2, 3 elements past a 16-byte boundary
+    for shift in (1, 2, 3):
+        buf = np.concatenate([np.full(shift, 5, np.int32), tok_h])
+        d = to_dev(buf, torch.int32, dev)[shift:]
+        got = run_gpu(px, d, to_dev(st_h, torch.int64, dev), to_dev(ln_h, torch.int32, dev),
+                      to_dev(co_h, torch.uint8, dev))
+        compare(got, *expect, what="shift %d" % shift)
+    # padded [B, Lmax] layout with odd Lmax (rows start at every alignment)
+    lmax = int(ln_h.max()) + 3
+    padded = np.full((64, lmax), 11, np.int32)
+    for i in range(64):
+        padded[i, : ln_h[i]] = tok_h[st_h[i]: st_h[i] + ln_h[i]]
+    starts_p = (np.arange(64) * lmax).astype(np.int64)
+    got = run_gpu(px, to_dev(padded.ravel(), torch.int32, dev), to_dev(starts_p, torch.int64, dev),
+                  to_dev(ln_h, torch.int32, dev), to_dev(co_h, torch.uint8, dev))
+    compare(got, *expect, what="padded")
+    # rows in reverse order
+    perm = np.arange(64)[::-1].copy()
+    got = run_gpu(px, to_dev(tok_h, torch.int32, dev), to_dev(st_h[perm], torch.int64, dev),
+                  to_dev(ln_h[perm], torch.int32, dev), to_dev(co_h[perm], torch.uint8, dev))
+    rows, R, rs, rt, eta = oracle_expect(tok_h, st_h[perm], ln_h[perm], co_h[perm], TAGS, G, coef)
+    compare(got, rows, R, rs, rt, eta, what="reversed")
+    # overlapping rows: every row is the same stream, plus prefixes of it
+    st_o = np.zeros(64, np.int64)
+    ln_o = np.array([ln_h[0] - (i % 5) * 7 for i in range(64)], np.int32)
+    got = run_gpu(px, to_dev(tok_h, torch.int32, dev), to_dev(st_o, torch.int64, dev),
+                  to_dev(ln_o, torch.int32, dev), to_dev(co_h, torch.uint8, dev))
+    compare(got, *oracle_expect(tok_h, st_o, ln_o, co_h, TAGS, G, coef), what="overlapping")
+
+
+def test_bad_rows_and_workspace_overflow(dev):
+    log("case bad rows / overflow")
+    P = S.make_params("small")
+    tok_h, st_h, ln_h, co_h = S.host_batch(P, 32)
+    px, coef = px_for()
+    ln_bad = ln_h.copy()
+    ln_bad[9] = -5
+    got = run_gpu(px, to_dev(tok_h, torch.int32, dev), to_dev(st_h, torch.int64, dev),
+                  to_dev(ln_bad, torch.int32, dev), to_dev(co_h, torch.uint8, dev))
+    assert got["flags"][9] == PX.FLAG_BAD_ROW
+    assert np.all(np.isnan(got["reward"][8:16]))
+    keep = np.r_[0:8, 16:32]
+    compare({k: v[keep] for k, v in got.items()},
+            *oracle_expect(tok_h, st_h[keep], ln_h[keep], co_h[keep], TAGS, G, coef), what="bad-row rest")
+    # a workspace sized for no tokens at all, for rows of 4-10 segments each
+    Pt = S.make_params("typical")
+    tok_t, st_t, ln_t, co_t = S.host_batch(Pt, 32)
+    got = run_gpu(px, to_dev(tok_t, torch.int32, dev), to_dev(st_t, torch.int64, dev),
+                  to_dev(ln_t, torch.int32, dev), to_dev(co_t, torch.uint8, dev), ws_total=0)
+    assert np.all(got["flags"] == PX.FLAG_WS_OVERFLOW)
+    assert np.all(np.isnan(got["reward"]))
+
+
+def test_config_flag_and_coefficients(dev):
+    log("case cfg flags")
+    P = S.make_params("ragged")
+    n = S.n_rows_of("ragged")
+    tok_h, st_h, ln_h, co_h = S.host_batch(P, n)
+    for coef_over, fl in ((dict(alpha=0.0, beta_subtask=0.1, beta_trial=0.0, rho=2.0, rho_clip=0.1), 0),
+                          (dict(alpha=0.3, beta_subtask=0.025, beta_trial=0.05, rho=0.0, rho_clip=0.0),
+                           PX.CFG_INVALID_KEEPS_CORRECTNESS)):
+        px, coef = px_for(flags=fl, **coef_over)
+        got = run_gpu(px, to_dev(tok_h, torch.int32, dev), to_dev(st_h, torch.int64, dev),
+                      to_dev(ln_h, torch.int32, dev), to_dev(co_h, torch.uint8, dev))
+        compare(got, *oracle_expect(tok_h, st_h, ln_h, co_h, TAGS, G, coef, fl), what="cfg %s" % fl)
+
+
+def test_group_sizes(dev):
+    log("case group sizes")
+    P = S.make_params("tiny", groups=15)
+    n = 120
+    tok_h, st_h, ln_h, co_h = S.host_batch(P, n)
+    for g in (1, 3, 5, 120):
+        px = PX.Parason(TAGS, group_size=g, **DEFAULT_COEF)
+        got = run_gpu(px, to_dev(tok_h, torch.int32, dev), to_dev(st_h, torch.int64, dev),
+                      to_dev(ln_h, torch.int32, dev), to_dev(co_h, torch.uint8, dev))
+        compare(got, *oracle_expect(tok_h, st_h, ln_h, co_h, TAGS, g, DEFAULT_COEF), what="G=%d" % g)
+
+
+def test_repeatable(dev):
+    log("case repeatable")
+    P = S.make_params("small")
+    n = S.n_rows_of("small")
+    tok_d, st_d, ln_d, co_d = S.device_batch(P, n, device=dev)
+    px, _ = px_for()
+    a = run_gpu(px, tok_d, st_d, ln_d, co_d)
+    b = run_gpu(px, tok_d, st_d, ln_d, co_d)
+    for k in a:
+        assert np.array_equal(a[k].view(np.uint32) if a[k].dtype == np.float32 else a[k],
+                              b[k].view(np.uint32) if b[k].dtype == np.float32 else b[k]), k
