@@ -109,6 +109,8 @@ def main():
     ap.add_argument("--workload", default="large", choices=["tiny", "small", "typical", "large", "ragged"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain device-to-device copy of 4 GiB (HBM counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -119,6 +121,16 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.calibrate_copy:
+        # known traffic: 4 GiB read + 4 GiB written per copy
+        x = torch.ones(1 << 30, dtype=torch.int32, device="cuda:0")
+        y = torch.empty_like(x)
+        for _ in range(3):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "copy", "bytes_read": 4 << 30, "bytes_written": 4 << 30, "launches": 3}))
+        return
 
     from paper_2608_24658_amd import parason as PX
     from paper_2608_24658_amd.synth import synth as S
