@@ -22,7 +22,10 @@ namespace {
 
 constexpr size_t ALIGN = 256;
 constexpr int SCAN_BLOCK = 256;         /* threads per scan block (4 waves) */
-constexpr int SCAN_BLOCKS_PER_CU = 4;   /* persistent grid: 16 waves per CU (106 VGPRs: 4 waves per SIMD) */
+#ifndef PARASON_SCAN_BLOCKS_PER_CU
+#define PARASON_SCAN_BLOCKS_PER_CU 4
+#endif
+constexpr int SCAN_BLOCKS_PER_CU = PARASON_SCAN_BLOCKS_PER_CU; /* persistent grid of 4-wave blocks */
 constexpr int64_t MAX_SEGMENTS = (int64_t)1 << 40;
 
 size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }

@@ -37,7 +37,13 @@
 namespace pk {
 
 constexpr int WAVE = 64;
-constexpr int SEG_VEC = 1024;            /* 16-byte vectors per segment */
+#ifndef PARASON_SEG_VEC
+#define PARASON_SEG_VEC 512
+#endif
+#ifndef PARASON_SCAN_WAVES_PER_SIMD
+#define PARASON_SCAN_WAVES_PER_SIMD 4
+#endif
+constexpr int SEG_VEC = PARASON_SEG_VEC; /* 16-byte vectors per segment (2048 tokens) */
 constexpr int SEG_TOK = 4 * SEG_VEC;     /* tokens per segment */
 constexpr int LOADS = SEG_VEC / WAVE;    /* vector loads per lane per segment */
 constexpr int EV_CAP = 128;              /* events stored per segment */
@@ -80,11 +86,18 @@ __device__ __forceinline__ uint32_t classify(const TagMatch &tm, int32_t t, bool
     return c;
 }
 
+/* First 16-byte vector of a row's segments: the 128-byte line (8 vectors) that
+ * holds its first token, so every wave-wide load covers whole L2 lines. */
+__device__ __forceinline__ int64_t row_first_vec(int64_t g) { return (g >> 5) << 3; }
+
+/* One past the last vector holding a token of the row. */
+__device__ __forceinline__ int64_t row_end_vec(int64_t g, int32_t len) { return (g + (int64_t)len + 3) >> 2; }
+
 __device__ __forceinline__ int64_t row_segments(int64_t start, int32_t len, int64_t mis)
 {
     if (start < 0 || len <= 0) return 0;
     int64_t g = start + mis;
-    int64_t nvec = ((g + (int64_t)len - 1) >> 2) - (g >> 2) + 1;
+    int64_t nvec = row_end_vec(g, len) - row_first_vec(g);
     return (nvec + SEG_VEC - 1) / SEG_VEC;
 }
 
@@ -202,14 +215,149 @@ __device__ __forceinline__ int4 load_vec(const int4 *p)
     return make_int4(v.x, v.y, v.z, v.w);
 }
 
-/* One wave per segment; waves take contiguous ranges of segment ids. */
+__device__ __forceinline__ bool is_tag(const TagMatch &tm, int32_t t, bool contig)
+{
+    if (contig) return (uint32_t)t - (uint32_t)tm.base < 12u;
+    bool h = false;
+#pragma unroll
+    for (int k = 0; k < 12; ++k) h = h || (t == tm.ids[k]);
+    return h;
+}
+
+__device__ __forceinline__ uint32_t lane_bit(uint64_t mask, int lane) { return (uint32_t)(mask >> lane) & 1u; }
+
+/* Tags of the LOADS vectors x[i] (vector v0 + i*WAVE + lane of this lane) go to
+ * the segment's event list ev in position order; cnt counts all of them.  EDGE:
+ * the segment holds the first or last vector of its row, so only segment
+ * positions q = 4*(i*WAVE + lane) + j with q_lo <= q < q_hi belong to the row. */
+template <bool CONTIG, bool EDGE>
+__device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_lo, int32_t q_hi,
+                                             uint32_t *__restrict__ ev, uint32_t &cnt, const TagMatch &tm, int lane)
+{
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+        const int32_t t[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
+        const int32_t q0 = 4 * (i * WAVE + lane);
+        uint64_t b[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            bool hit = is_tag(tm, t[j], CONTIG);
+            if (EDGE) hit = hit && q0 + j >= q_lo && q0 + j < q_hi;
+            b[j] = __ballot(hit);
+        }
+        if ((b[0] | b[1] | b[2] | b[3]) == 0) continue; /* wave-uniform: most vectors hold no tag */
+        uint32_t pre = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b[j], pre));
+        const uint32_t mine = lane_bit(b[0], lane) | lane_bit(b[1], lane) << 1 | lane_bit(b[2], lane) << 2 |
+                              lane_bit(b[3], lane) << 3;
+        if (mine) {
+            uint32_t idx = cnt + pre;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (mine & (1u << j)) {
+                    if (idx < (uint32_t)EV_CAP) ev[idx] = ((uint32_t)(q0 + j) << 4) | classify(tm, t[j], CONTIG);
+                    ++idx;
+                }
+            }
+        }
+        cnt += (uint32_t)(__popcll(b[0]) + __popcll(b[1]) + __popcll(b[2]) + __popcll(b[3]));
+    }
+}
+
+/* A segment as the scan wave sees it (all fields wave-uniform). */
+struct SegView {
+    int64_t s;          /* segment id */
+    int64_t v0, v1;     /* its vectors [v0, v1) */
+    int32_t q_lo, q_hi; /* segment positions that belong to the row */
+    bool edge;          /* holds the first or the last vector of the row */
+};
+
+/* Walks a wave's contiguous range of segment ids, row by row. */
+struct SegCursor {
+    const int64_t *seg_off;
+    const int64_t *starts;
+    const int32_t *lengths;
+    int64_t mis;
+    int64_t row, row_first, row_next;
+    int64_t g, vrow0, vend;
+    int32_t len;
+    bool loaded;
+
+    __device__ void seek(int64_t s, int64_t n)
+    {
+        /* the row holding s: seg_off[row] <= s < seg_off[row + 1] */
+        int64_t lo = 0, hi = n;
+        while (hi - lo > 1) {
+            int64_t mid = (lo + hi) >> 1;
+            if (seg_off[mid] <= s) lo = mid; else hi = mid;
+        }
+        row = uniform64(lo);
+        row_first = uniform64(seg_off[row]);
+        row_next = uniform64(seg_off[row + 1]);
+        loaded = false;
+    }
+
+    __device__ SegView view(int64_t s)
+    {
+        while (row_next <= s) {
+            ++row;
+            row_first = row_next;
+            row_next = uniform64(seg_off[row + 1]);
+            loaded = false;
+        }
+        if (!loaded) {
+            g = uniform64(starts[row] + mis);
+            len = __builtin_amdgcn_readfirstlane(lengths[row]);
+            vrow0 = row_first_vec(g);
+            vend = row_end_vec(g, len);
+            loaded = true;
+        }
+        SegView w;
+        w.s = s;
+        w.v0 = vrow0 + (s - row_first) * SEG_VEC;
+        w.v1 = min(w.v0 + (int64_t)SEG_VEC, vend);
+        w.edge = w.v0 == vrow0 || w.v1 == vend;
+        /* row positions g .. g+len-1 relative to the segment's first element */
+        const int64_t lo = g - 4 * w.v0, hi = g + (int64_t)len - 4 * w.v0;
+        w.q_lo = (int32_t)max((int64_t)0, lo);
+        w.q_hi = (int32_t)min((int64_t)4 * (w.v1 - w.v0), hi);
+        return w;
+    }
+};
+
+__device__ __forceinline__ void issue_loads(int4 (&x)[LOADS], const int4 *src, const SegView &w, int lane)
+{
+    const int4 *p = src + w.v0 + lane;
+    if (!w.edge) {
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) x[i] = load_vec(p + i * WAVE);
+    } else {
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i)
+            x[i] = (w.v0 + i * WAVE + lane < w.v1) ? load_vec(p + i * WAVE) : make_int4(-1, -1, -1, -1);
+    }
+}
+
 template <bool CONTIG>
-__global__ void __launch_bounds__(256) scan_segments(const int32_t *__restrict__ tok_base, int64_t mis,
-                                                     const int64_t *__restrict__ starts,
-                                                     const int32_t *__restrict__ lengths, int64_t n,
-                                                     const int64_t *__restrict__ seg_off, int64_t seg_cap,
-                                                     int32_t *__restrict__ seg_count, uint32_t *__restrict__ events,
-                                                     TagMatch tm)
+__device__ __forceinline__ void finish_segment(const int4 (&x)[LOADS], const SegView &w, uint32_t *__restrict__ events,
+                                               int32_t *__restrict__ seg_count, const TagMatch &tm, int lane)
+{
+    uint32_t cnt = 0; /* wave-uniform */
+    uint32_t *ev = events + w.s * EV_CAP;
+    if (!w.edge) scan_vectors<CONTIG, false>(x, 0, SEG_TOK, ev, cnt, tm, lane);
+    else scan_vectors<CONTIG, true>(x, w.q_lo, w.q_hi, ev, cnt, tm, lane);
+    if (lane == 0) seg_count[w.s] = (int32_t)cnt;
+}
+
+/* One wave per segment; waves take contiguous ranges of segment ids.  The
+ * loads of the next segment are in flight while the current one is scanned. */
+template <bool CONTIG>
+__global__ void __launch_bounds__(256, PARASON_SCAN_WAVES_PER_SIMD) scan_segments(
+    const int32_t *__restrict__ tok_base, int64_t mis, const int64_t *__restrict__ starts,
+    const int32_t *__restrict__ lengths, int64_t n, const int64_t *__restrict__ seg_off, int64_t seg_cap,
+    int32_t *__restrict__ seg_count, uint32_t *__restrict__ events, TagMatch tm)
 {
     const int lane = threadIdx.x & (WAVE - 1);
     const int64_t wave = uniform64((int64_t)blockIdx.x * (blockDim.x / WAVE) + (threadIdx.x / WAVE));
@@ -221,82 +369,32 @@ __global__ void __launch_bounds__(256) scan_segments(const int32_t *__restrict__
     const int64_t s_end = uniform64(S * (wave + 1) / n_waves);
     if (s_begin >= s_end) return;
 
-    /* the row holding s_begin: seg_off[row] <= s_begin < seg_off[row + 1] */
-    int64_t lo = 0, hi = n;
-    while (hi - lo > 1) {
-        int64_t mid = (lo + hi) >> 1;
-        if (seg_off[mid] <= s_begin) lo = mid; else hi = mid;
-    }
-    int64_t row = uniform64(lo);
-    int64_t row_first = uniform64(seg_off[row]);
-    int64_t row_next = uniform64(seg_off[row + 1]);
-    int64_t g = 0, vrow0 = 0, vend = 0;
-    int32_t len = 0;
-    bool row_loaded = false;
+    const int4 *src = reinterpret_cast<const int4 *>(tok_base);
+    SegCursor cur;
+    cur.seg_off = seg_off;
+    cur.starts = starts;
+    cur.lengths = lengths;
+    cur.mis = mis;
+    cur.seek(s_begin, n);
 
-    for (int64_t s = s_begin; s < s_end; ++s) {
-        while (row_next <= s) {
-            ++row;
-            row_first = row_next;
-            row_next = uniform64(seg_off[row + 1]);
-            row_loaded = false;
+    int4 xa[LOADS], xb[LOADS];
+    SegView a = cur.view(s_begin), b;
+    issue_loads(xa, src, a, lane);
+    for (int64_t s = s_begin;; s += 2) {
+        const bool has_b = s + 1 < s_end;
+        if (has_b) {
+            b = cur.view(s + 1);
+            issue_loads(xb, src, b, lane);
         }
-        if (!row_loaded) {
-            g = uniform64(starts[row] + mis);
-            len = __builtin_amdgcn_readfirstlane(lengths[row]);
-            vrow0 = g >> 2;
-            vend = (g + (int64_t)len + 3) >> 2;
-            row_loaded = true;
+        finish_segment<CONTIG>(xa, a, events, seg_count, tm, lane);
+        if (!has_b) break;
+        const bool has_c = s + 2 < s_end;
+        if (has_c) {
+            a = cur.view(s + 2);
+            issue_loads(xa, src, a, lane);
         }
-        const int64_t v0 = vrow0 + (s - row_first) * SEG_VEC;
-        const int64_t v1 = min(v0 + (int64_t)SEG_VEC, vend);
-        const int4 *src = reinterpret_cast<const int4 *>(tok_base);
-
-        int4 x[LOADS];
-#pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            int64_t v = v0 + i * WAVE + lane;
-            if (v < v1) x[i] = load_vec(src + v);
-            else x[i] = make_int4(-1, -1, -1, -1);
-        }
-
-        uint32_t cnt = 0; /* wave-uniform */
-        uint32_t *ev = events + s * EV_CAP;
-#pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            const int64_t v = v0 + i * WAVE + lane;
-            /* elements 4v+j with g <= 4v+j < g+len belong to the row */
-            const int64_t lo_j = g - 4 * v, hi_j = g + (int64_t)len - 4 * v;
-            const int32_t t[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
-            uint32_t cls[4];
-            uint32_t m = 0;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                cls[j] = classify(tm, t[j], CONTIG);
-                bool in = (j >= lo_j) && (j < hi_j) && (v < v1);
-                m |= (cls[j] != 0 && in) ? (1u << j) : 0u;
-            }
-            const uint64_t any = __ballot(m != 0);
-            if (any == 0) continue;
-            const uint64_t b0 = __ballot(m & 1u), b1 = __ballot(m & 2u), b2 = __ballot(m & 4u), b3 = __ballot(m & 8u);
-            uint32_t pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b0 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b0, 0u));
-            pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b1 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b1, pre));
-            pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b2 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b2, pre));
-            pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b3 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b3, pre));
-            if (m) {
-                uint32_t idx = cnt + pre;
-                const uint32_t local = (uint32_t)(4 * (v - v0));
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (m & (1u << j)) {
-                        if (idx < (uint32_t)EV_CAP) ev[idx] = ((local + (uint32_t)j) << 4) | cls[j];
-                        ++idx;
-                    }
-                }
-            }
-            cnt += (uint32_t)(__popcll(b0) + __popcll(b1) + __popcll(b2) + __popcll(b3));
-        }
-        if (lane == 0) seg_count[s] = (int32_t)cnt;
+        finish_segment<CONTIG>(xb, b, events, seg_count, tm, lane);
+        if (!has_c) break;
     }
 }
 
@@ -650,7 +748,7 @@ template <class Store>
 __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, Automaton<Store> &A)
 {
     const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
-    const int64_t vrow0 = g >> 2, vend = (g + (int64_t)len + 3) >> 2;
+    const int64_t vrow0 = row_first_vec(g), vend = row_end_vec(g, len);
     for (int64_t s = s0; s < s1; ++s) {
         const int64_t v0 = vrow0 + (s - s0) * SEG_VEC;
         const int64_t base = 4 * v0 - g;
