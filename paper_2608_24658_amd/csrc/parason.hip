@@ -21,7 +21,6 @@ struct parason_handle {
 namespace {
 
 constexpr size_t ALIGN = 256;
-constexpr int SCAN_BLOCK = 256;         /* threads per scan block (4 waves) */
 #ifndef PARASON_SCAN_BLOCKS_PER_CU
 #define PARASON_SCAN_BLOCKS_PER_CU 4
 #endif
@@ -32,7 +31,7 @@ size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 /* Byte offsets of the workspace sections for n rows. */
 struct Layout {
-    size_t seg_off, tile_sum, tile_off, counters, deep_rows, deep_frames, deep_bits, seg_count, events;
+    size_t seg_off, tile_sum, tile_off, counters, done, deep_rows, deep_frames, deep_bits, seg_count, events;
     size_t fixed;  /* bytes before the per-segment sections */
     int64_t n_tiles;
 };
@@ -50,6 +49,8 @@ Layout layout_for(int64_t n)
     o = align_up(o + (size_t)L.n_tiles * sizeof(int64_t));
     L.counters = o;
     o = align_up(o + 4 * sizeof(int32_t));
+    L.done = o;
+    o = align_up(o + (size_t)(n > 0 ? n : 1));
     L.deep_rows = o;
     o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
     L.deep_frames = o;
@@ -200,6 +201,7 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     int64_t *tile_sum = (int64_t *)(ws + L.tile_sum);
     int64_t *tile_off = (int64_t *)(ws + L.tile_off);
     int32_t *counters = (int32_t *)(ws + L.counters);
+    uint8_t *done = (uint8_t *)(ws + L.done);
     int32_t *deep_rows = (int32_t *)(ws + L.deep_rows);
     int32_t *deep_frames = (int32_t *)(ws + L.deep_frames);
     uint32_t *deep_bits = (uint32_t *)(ws + L.deep_bits);
@@ -210,16 +212,29 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     pk::plan_tiles<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_sum);
     pk::plan_top<<<dim3(1), dim3(1024), 0, stream>>>(tile_sum, L.n_tiles, tile_off, seg_off, n_traj, counters);
     pk::plan_rows<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_off,
-                                                                        seg_off);
+                                                                        seg_off, done);
 
+    const pk::RowOut row_out{out->total,    out->latency,   out->n_subtask,       out->n_trial,
+                             out->n_blocks, out->max_depth, out->first_error_pos, out->flags};
+    pk::ScanArgs sa;
+    sa.tok_base = tok_base;
+    sa.mis = mis;
+    sa.starts = starts;
+    sa.lengths = lengths;
+    sa.n = n_traj;
+    sa.seg_off = seg_off;
+    sa.seg_cap = cap;
+    sa.seg_count = seg_count;
+    sa.events = events;
+    sa.done = done;
+    sa.tm = h->tm;
+    sa.out = row_out;
     const unsigned scan_blocks = (unsigned)(cus * SCAN_BLOCKS_PER_CU);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[0], stream) != hipSuccess) return PARASON_ERR_HIP;
     if (h->tm.contiguous)
-        pk::scan_segments<true><<<dim3(scan_blocks), dim3(SCAN_BLOCK), 0, stream>>>(
-            tok_base, mis, starts, lengths, n_traj, seg_off, cap, seg_count, events, h->tm);
+        pk::scan_rows<true><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
     else
-        pk::scan_segments<false><<<dim3(scan_blocks), dim3(SCAN_BLOCK), 0, stream>>>(
-            tok_base, mis, starts, lengths, n_traj, seg_off, cap, seg_count, events, h->tm);
+        pk::scan_rows<false><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[1], stream) != hipSuccess) return PARASON_ERR_HIP;
 
     pk::RowArgs ra;
@@ -233,10 +248,9 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.seg_count = seg_count;
     ra.events = events;
     ra.tm = h->tm;
-    ra.out = pk::RowOut{out->total, out->latency, out->n_subtask, out->n_trial, out->n_blocks, out->max_depth,
-                        out->first_error_pos, out->flags};
+    ra.out = row_out;
     const unsigned row_blocks = (unsigned)((n_traj + 63) / 64);
-    pk::rows_fast<<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, counters, deep_rows);
+    pk::rows_fast<<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, done, counters, deep_rows);
     pk::rows_deep<<<dim3(1), dim3(64), 0, stream>>>(ra, counters, deep_rows, deep_frames, deep_bits);
 
     pk::RewardArgs rw;

@@ -4,24 +4,26 @@
  * Data flow of one parason_run (all on the caller's stream):
  *
  *   plan_tiles / plan_top / plan_rows
- *        Each row is cut into segments of SEG_VEC 16-byte vectors (4096
- *        tokens), aligned to the 16-byte grid of the token buffer.  A three
- *        pass exclusive scan gives seg_off[i] (first segment of row i) and the
- *        segment count seg_off[n].
- *   scan_segments  (HBM-bound; one wave per segment, persistent grid)
+ *        Each row is cut into segments of SEG_VEC 16-byte vectors, starting at
+ *        the 128-byte line that holds its first token.  A three-pass exclusive
+ *        scan gives seg_off[i] (first segment of row i) and the segment count
+ *        seg_off[n]; done[i] is cleared.
+ *   scan_rows  (HBM-bound; one wave per segment, persistent grid)
  *        Streams every token once with 16-byte loads, tests it against the
- *        twelve tag ids and compacts the rare tag tokens with wave ballots into
- *        a per-segment event list (position in segment << 4 | class).  Tags are
- *        about 0.1-1% of tokens.  A segment holding more than EV_CAP tags keeps
- *        only its count; the row kernel re-reads its tokens.
- *   rows_fast      (one thread per row)
- *        Runs the grammar's pushdown automaton over the row's events; Text runs
- *        are the gaps between event positions.  Produces the integer outputs.
- *        Frames of open blocks live in LDS (FAST_DEPTH per row, 64 outline
+ *        twelve tag ids with a wave ballot and compacts the rare tags (about
+ *        0.1-1% of tokens) in position order.  A row whose segments all fall in
+ *        one wave's range keeps its events in that wave's LDS buffer, and the
+ *        wave runs the grammar's pushdown automaton over them as soon as the
+ *        row's last segment is scanned (done[i] = 1).  Other rows leave their
+ *        events in per-segment global slots.
+ *   rows_fast  (one thread per row not done)
+ *        The same automaton over the global slots; a segment holding more than
+ *        EV_CAP tags, or marked dense by the scan, is classified again token by
+ *        token.  Frames of open blocks in LDS (FAST_DEPTH per row, 64 outline
  *        entries per block); a row that needs more is handed to rows_deep.
- *   rows_deep      (one thread, only rows handed over)
+ *   rows_deep  (one thread, only rows handed over)
  *        The same automaton with frames and entry types in global workspace.
- *   group_reward   (one thread per group of G rows)
+ *   group_reward  (one thread per group of G rows)
  *        Statistics and Definition 3.1 in IEEE double, fixed order.
  *
  * Paper references: grammar -- figure "Context-Free Grammar for Parason"
@@ -174,11 +176,11 @@ __global__ void __launch_bounds__(1024) plan_top(const int64_t *__restrict__ til
     if (threadIdx.x == 0) seg_off[n] = carry_s;
 }
 
-/* seg_off[i] = first segment of row i. */
+/* seg_off[i] = first segment of row i; done[i] = 0 (no row evaluated yet). */
 __global__ void __launch_bounds__(PLAN_THREADS) plan_rows(const int64_t *__restrict__ starts,
                                                           const int32_t *__restrict__ lengths, int64_t n,
                                                           int64_t mis, const int64_t *__restrict__ tile_off,
-                                                          int64_t *__restrict__ seg_off)
+                                                          int64_t *__restrict__ seg_off, uint8_t *__restrict__ done)
 {
     __shared__ int64_t part[PLAN_THREADS / WAVE];
     /* thread t owns the ROWS_PER_THREAD consecutive rows starting at r0 + t*ROWS_PER_THREAD */
@@ -199,202 +201,11 @@ __global__ void __launch_bounds__(PLAN_THREADS) plan_rows(const int64_t *__restr
 #pragma unroll
     for (int j = 0; j < ROWS_PER_THREAD; ++j) {
         int64_t r = r0 + j;
-        if (r < n) seg_off[r] = off;
+        if (r < n) {
+            seg_off[r] = off;
+            done[r] = 0;
+        }
         off += cnt[j];
-    }
-}
-
-/* ------------------------------------------------------------------ scan */
-
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-/* 16-byte streaming load (each token is read exactly once). */
-__device__ __forceinline__ int4 load_vec(const int4 *p)
-{
-    v4i v = __builtin_nontemporal_load(reinterpret_cast<const v4i *>(p));
-    return make_int4(v.x, v.y, v.z, v.w);
-}
-
-__device__ __forceinline__ bool is_tag(const TagMatch &tm, int32_t t, bool contig)
-{
-    if (contig) return (uint32_t)t - (uint32_t)tm.base < 12u;
-    bool h = false;
-#pragma unroll
-    for (int k = 0; k < 12; ++k) h = h || (t == tm.ids[k]);
-    return h;
-}
-
-__device__ __forceinline__ uint32_t lane_bit(uint64_t mask, int lane) { return (uint32_t)(mask >> lane) & 1u; }
-
-/* Tags of the LOADS vectors x[i] (vector v0 + i*WAVE + lane of this lane) go to
- * the segment's event list ev in position order; cnt counts all of them.  EDGE:
- * the segment holds the first or last vector of its row, so only segment
- * positions q = 4*(i*WAVE + lane) + j with q_lo <= q < q_hi belong to the row. */
-template <bool CONTIG, bool EDGE>
-__device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_lo, int32_t q_hi,
-                                             uint32_t *__restrict__ ev, uint32_t &cnt, const TagMatch &tm, int lane)
-{
-#pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-        const int32_t t[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
-        const int32_t q0 = 4 * (i * WAVE + lane);
-        uint64_t b[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            bool hit = is_tag(tm, t[j], CONTIG);
-            if (EDGE) hit = hit && q0 + j >= q_lo && q0 + j < q_hi;
-            b[j] = __ballot(hit);
-        }
-        if ((b[0] | b[1] | b[2] | b[3]) == 0) continue; /* wave-uniform: most vectors hold no tag */
-        uint32_t pre = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b[j], pre));
-        const uint32_t mine = lane_bit(b[0], lane) | lane_bit(b[1], lane) << 1 | lane_bit(b[2], lane) << 2 |
-                              lane_bit(b[3], lane) << 3;
-        if (mine) {
-            uint32_t idx = cnt + pre;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (mine & (1u << j)) {
-                    if (idx < (uint32_t)EV_CAP) ev[idx] = ((uint32_t)(q0 + j) << 4) | classify(tm, t[j], CONTIG);
-                    ++idx;
-                }
-            }
-        }
-        cnt += (uint32_t)(__popcll(b[0]) + __popcll(b[1]) + __popcll(b[2]) + __popcll(b[3]));
-    }
-}
-
-/* A segment as the scan wave sees it (all fields wave-uniform). */
-struct SegView {
-    int64_t s;          /* segment id */
-    int64_t v0, v1;     /* its vectors [v0, v1) */
-    int32_t q_lo, q_hi; /* segment positions that belong to the row */
-    bool edge;          /* holds the first or the last vector of the row */
-};
-
-/* Walks a wave's contiguous range of segment ids, row by row. */
-struct SegCursor {
-    const int64_t *seg_off;
-    const int64_t *starts;
-    const int32_t *lengths;
-    int64_t mis;
-    int64_t row, row_first, row_next;
-    int64_t g, vrow0, vend;
-    int32_t len;
-    bool loaded;
-
-    __device__ void seek(int64_t s, int64_t n)
-    {
-        /* the row holding s: seg_off[row] <= s < seg_off[row + 1] */
-        int64_t lo = 0, hi = n;
-        while (hi - lo > 1) {
-            int64_t mid = (lo + hi) >> 1;
-            if (seg_off[mid] <= s) lo = mid; else hi = mid;
-        }
-        row = uniform64(lo);
-        row_first = uniform64(seg_off[row]);
-        row_next = uniform64(seg_off[row + 1]);
-        loaded = false;
-    }
-
-    __device__ SegView view(int64_t s)
-    {
-        while (row_next <= s) {
-            ++row;
-            row_first = row_next;
-            row_next = uniform64(seg_off[row + 1]);
-            loaded = false;
-        }
-        if (!loaded) {
-            g = uniform64(starts[row] + mis);
-            len = __builtin_amdgcn_readfirstlane(lengths[row]);
-            vrow0 = row_first_vec(g);
-            vend = row_end_vec(g, len);
-            loaded = true;
-        }
-        SegView w;
-        w.s = s;
-        w.v0 = vrow0 + (s - row_first) * SEG_VEC;
-        w.v1 = min(w.v0 + (int64_t)SEG_VEC, vend);
-        w.edge = w.v0 == vrow0 || w.v1 == vend;
-        /* row positions g .. g+len-1 relative to the segment's first element */
-        const int64_t lo = g - 4 * w.v0, hi = g + (int64_t)len - 4 * w.v0;
-        w.q_lo = (int32_t)max((int64_t)0, lo);
-        w.q_hi = (int32_t)min((int64_t)4 * (w.v1 - w.v0), hi);
-        return w;
-    }
-};
-
-__device__ __forceinline__ void issue_loads(int4 (&x)[LOADS], const int4 *src, const SegView &w, int lane)
-{
-    const int4 *p = src + w.v0 + lane;
-    if (!w.edge) {
-#pragma unroll
-        for (int i = 0; i < LOADS; ++i) x[i] = load_vec(p + i * WAVE);
-    } else {
-#pragma unroll
-        for (int i = 0; i < LOADS; ++i)
-            x[i] = (w.v0 + i * WAVE + lane < w.v1) ? load_vec(p + i * WAVE) : make_int4(-1, -1, -1, -1);
-    }
-}
-
-template <bool CONTIG>
-__device__ __forceinline__ void finish_segment(const int4 (&x)[LOADS], const SegView &w, uint32_t *__restrict__ events,
-                                               int32_t *__restrict__ seg_count, const TagMatch &tm, int lane)
-{
-    uint32_t cnt = 0; /* wave-uniform */
-    uint32_t *ev = events + w.s * EV_CAP;
-    if (!w.edge) scan_vectors<CONTIG, false>(x, 0, SEG_TOK, ev, cnt, tm, lane);
-    else scan_vectors<CONTIG, true>(x, w.q_lo, w.q_hi, ev, cnt, tm, lane);
-    if (lane == 0) seg_count[w.s] = (int32_t)cnt;
-}
-
-/* One wave per segment; waves take contiguous ranges of segment ids.  The
- * loads of the next segment are in flight while the current one is scanned. */
-template <bool CONTIG>
-__global__ void __launch_bounds__(256, PARASON_SCAN_WAVES_PER_SIMD) scan_segments(
-    const int32_t *__restrict__ tok_base, int64_t mis, const int64_t *__restrict__ starts,
-    const int32_t *__restrict__ lengths, int64_t n, const int64_t *__restrict__ seg_off, int64_t seg_cap,
-    int32_t *__restrict__ seg_count, uint32_t *__restrict__ events, TagMatch tm)
-{
-    const int lane = threadIdx.x & (WAVE - 1);
-    const int64_t wave = uniform64((int64_t)blockIdx.x * (blockDim.x / WAVE) + (threadIdx.x / WAVE));
-    const int64_t n_waves = (int64_t)gridDim.x * (blockDim.x / WAVE);
-    const int64_t S = seg_off[n];
-    if (S > seg_cap) return; /* the row kernel reports PARASON_FLAG_WS_OVERFLOW */
-    /* S < 2^40 and n_waves < 2^20 (checked on the host), so S * wave fits */
-    const int64_t s_begin = uniform64(S * wave / n_waves);
-    const int64_t s_end = uniform64(S * (wave + 1) / n_waves);
-    if (s_begin >= s_end) return;
-
-    const int4 *src = reinterpret_cast<const int4 *>(tok_base);
-    SegCursor cur;
-    cur.seg_off = seg_off;
-    cur.starts = starts;
-    cur.lengths = lengths;
-    cur.mis = mis;
-    cur.seek(s_begin, n);
-
-    int4 xa[LOADS], xb[LOADS];
-    SegView a = cur.view(s_begin), b;
-    issue_loads(xa, src, a, lane);
-    for (int64_t s = s_begin;; s += 2) {
-        const bool has_b = s + 1 < s_end;
-        if (has_b) {
-            b = cur.view(s + 1);
-            issue_loads(xb, src, b, lane);
-        }
-        finish_segment<CONTIG>(xa, a, events, seg_count, tm, lane);
-        if (!has_b) break;
-        const bool has_c = s + 2 < s_end;
-        if (has_c) {
-            a = cur.view(s + 2);
-            issue_loads(xa, src, a, lane);
-        }
-        finish_segment<CONTIG>(xb, b, events, seg_count, tm, lane);
-        if (!has_c) break;
     }
 }
 
@@ -438,6 +249,46 @@ struct LdsStore {
         t.k = at(d - 1, 4);
         t.saved_ctx = (uint32_t)at(d - 1, 5);
         t.ent = (uint64_t)(uint32_t)at(d - 1, 6) | ((uint64_t)(uint32_t)at(d - 1, 7) << 32);
+    }
+    __device__ void begin_block(Top &t) { t.ent = 0; }
+    __device__ void end_block(const Top &) {}
+    __device__ bool add_entry(Top &t, bool trial)
+    {
+        if (t.n_e >= FAST_ENTRIES) return false;
+        if (trial) t.ent |= (uint64_t)1 << t.n_e;
+        return true;
+    }
+    __device__ uint32_t entry_type(const Top &t, int32_t k) { return ((t.ent >> k) & 1u) ? T_TRI : T_SUB; }
+};
+
+/* Wave store: one automaton per wave running in uniform control flow (its
+ * values live in scalar registers); FAST_DEPTH frames in the wave's LDS. */
+struct WaveStore {
+    int32_t *lds; /* [FAST_DEPTH][FRAME_WORDS] of this wave */
+    __device__ int32_t get(int d, int f) { return __builtin_amdgcn_readfirstlane(lds[d * FRAME_WORDS + f]); }
+    __device__ bool push(const Top &t, int d)
+    {
+        if (d > FAST_DEPTH) return false;
+        int32_t *f = lds + (d - 1) * FRAME_WORDS;
+        f[0] = t.saved_acc;
+        f[1] = t.block_main;
+        f[2] = t.max_w;
+        f[3] = t.n_e;
+        f[4] = t.k;
+        f[5] = (int32_t)t.saved_ctx;
+        f[6] = (int32_t)(uint32_t)t.ent;
+        f[7] = (int32_t)(uint32_t)(t.ent >> 32);
+        return true;
+    }
+    __device__ void pop(Top &t, int d)
+    {
+        t.saved_acc = get(d - 1, 0);
+        t.block_main = get(d - 1, 1);
+        t.max_w = get(d - 1, 2);
+        t.n_e = get(d - 1, 3);
+        t.k = get(d - 1, 4);
+        t.saved_ctx = (uint32_t)get(d - 1, 5);
+        t.ent = (uint64_t)(uint32_t)get(d - 1, 6) | ((uint64_t)(uint32_t)get(d - 1, 7) << 32);
     }
     __device__ void begin_block(Top &t) { t.ent = 0; }
     __device__ void end_block(const Top &) {}
@@ -786,13 +637,15 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, A
     return true;
 }
 
-/* One thread per row. */
-__global__ void __launch_bounds__(64) rows_fast(RowArgs a, int32_t *__restrict__ counters,
-                                                int32_t *__restrict__ deep_rows)
+/* One thread per row the scan did not evaluate (rows split between two scan
+ * waves, rows whose events did not fit the wave's LDS buffer, rows without
+ * segments). */
+__global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__restrict__ done,
+                                                int32_t *__restrict__ counters, int32_t *__restrict__ deep_rows)
 {
     __shared__ int32_t lds[FAST_DEPTH * FRAME_WORDS * 64];
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= a.n) return;
+    if (r >= a.n || done[r]) return;
     const int64_t start = a.starts[r];
     const int32_t len = a.lengths[r];
     if (start < 0 || len < 0) {
@@ -838,6 +691,298 @@ __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const int32_t *__rest
             write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_DEPTH_LIMIT);
         else
             write_result(a.out, r, len, A);
+    }
+}
+
+/* ------------------------------------------------------------------ scan */
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+/* 16-byte streaming load (each token is read exactly once). */
+__device__ __forceinline__ int4 load_vec(const int4 *p)
+{
+    v4i v = __builtin_nontemporal_load(reinterpret_cast<const v4i *>(p));
+    return make_int4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ bool is_tag(const TagMatch &tm, int32_t t, bool contig)
+{
+    if (contig) return (uint32_t)t - (uint32_t)tm.base < 12u;
+    bool h = false;
+#pragma unroll
+    for (int k = 0; k < 12; ++k) h = h || (t == tm.ids[k]);
+    return h;
+}
+
+__device__ __forceinline__ uint32_t lane_bit(uint64_t mask, int lane) { return (uint32_t)(mask >> lane) & 1u; }
+
+/* Tags of the LOADS vectors x[i] (vector v0 + i*WAVE + lane of this lane) are
+ * appended to dst[0 .. cap) in position order as (q + bias) << 4 | class, where
+ * q = 4*(i*WAVE + lane) + j is the position in the segment; cnt counts all of
+ * them, stored or not.  EDGE: the segment holds the first or last vector of its
+ * row, so only positions q_lo <= q < q_hi belong to the row. */
+template <bool CONTIG, bool EDGE>
+__device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_lo, int32_t q_hi,
+                                             uint32_t *__restrict__ dst, uint32_t cap, int32_t bias, uint32_t &cnt,
+                                             const TagMatch &tm, int lane)
+{
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+        const int32_t t[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
+        const int32_t q0 = 4 * (i * WAVE + lane);
+        uint64_t b[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            bool hit = is_tag(tm, t[j], CONTIG);
+            if (EDGE) hit = hit && q0 + j >= q_lo && q0 + j < q_hi;
+            b[j] = __ballot(hit);
+        }
+        if ((b[0] | b[1] | b[2] | b[3]) == 0) continue; /* wave-uniform: most vectors hold no tag */
+        uint32_t pre = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b[j], pre));
+        const uint32_t mine = lane_bit(b[0], lane) | lane_bit(b[1], lane) << 1 | lane_bit(b[2], lane) << 2 |
+                              lane_bit(b[3], lane) << 3;
+        if (mine) {
+            uint32_t idx = cnt + pre;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (mine & (1u << j)) {
+                    if (idx < cap) dst[idx] = ((uint32_t)(q0 + j + bias) << 4) | classify(tm, t[j], CONTIG);
+                    ++idx;
+                }
+            }
+        }
+        cnt += (uint32_t)(__popcll(b[0]) + __popcll(b[1]) + __popcll(b[2]) + __popcll(b[3]));
+    }
+}
+
+/* A segment as the scan wave sees it (all fields wave-uniform). */
+struct SegView {
+    int64_t s;                  /* segment id */
+    int64_t row, first, last;   /* its row and the row's first and last segment */
+    int64_t v0, v1;             /* its vectors [v0, v1) */
+    int64_t g;                  /* row start on the element grid of tok_base */
+    int32_t len;
+    int32_t q_lo, q_hi;         /* segment positions that belong to the row */
+    bool edge;                  /* holds the first or the last vector of the row */
+    bool owned;                 /* every segment of the row is in this wave's range */
+};
+
+/* Walks a wave's contiguous range of segment ids, row by row. */
+struct SegCursor {
+    const int64_t *seg_off;
+    const int64_t *starts;
+    const int32_t *lengths;
+    int64_t mis, s_begin, s_end;
+    int64_t row, row_first, row_next;
+    int64_t g, vrow0, vend;
+    int32_t len;
+    bool loaded;
+
+    __device__ void seek(int64_t s, int64_t n)
+    {
+        /* the row holding s: seg_off[row] <= s < seg_off[row + 1] */
+        int64_t lo = 0, hi = n;
+        while (hi - lo > 1) {
+            int64_t mid = (lo + hi) >> 1;
+            if (seg_off[mid] <= s) lo = mid; else hi = mid;
+        }
+        row = uniform64(lo);
+        row_first = uniform64(seg_off[row]);
+        row_next = uniform64(seg_off[row + 1]);
+        loaded = false;
+    }
+
+    __device__ SegView view(int64_t s)
+    {
+        while (row_next <= s) {
+            ++row;
+            row_first = row_next;
+            row_next = uniform64(seg_off[row + 1]);
+            loaded = false;
+        }
+        if (!loaded) {
+            g = uniform64(starts[row] + mis);
+            len = __builtin_amdgcn_readfirstlane(lengths[row]);
+            vrow0 = row_first_vec(g);
+            vend = row_end_vec(g, len);
+            loaded = true;
+        }
+        SegView w;
+        w.s = s;
+        w.row = row;
+        w.first = row_first;
+        w.last = row_next - 1;
+        w.g = g;
+        w.len = len;
+        w.v0 = vrow0 + (s - row_first) * SEG_VEC;
+        w.v1 = min(w.v0 + (int64_t)SEG_VEC, vend);
+        w.edge = w.v0 == vrow0 || w.v1 == vend;
+        /* row positions g .. g+len-1 relative to the segment's first element */
+        const int64_t lo = g - 4 * w.v0, hi = g + (int64_t)len - 4 * w.v0;
+        w.q_lo = (int32_t)max((int64_t)0, lo);
+        w.q_hi = (int32_t)min((int64_t)4 * (w.v1 - w.v0), hi);
+        /* LDS events hold (position << 4 | class) in 32 bits */
+        w.owned = row_first >= s_begin && row_next <= s_end && len < (1 << 27);
+        return w;
+    }
+};
+
+__device__ __forceinline__ void issue_loads(int4 (&x)[LOADS], const int4 *src, const SegView &w, int lane)
+{
+    const int4 *p = src + w.v0 + lane;
+    if (!w.edge) {
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) x[i] = load_vec(p + i * WAVE);
+    } else {
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i)
+            x[i] = (w.v0 + i * WAVE + lane < w.v1) ? load_vec(p + i * WAVE) : make_int4(-1, -1, -1, -1);
+    }
+}
+
+/* seg_count[s] = DENSE for s in [a, b): the row kernel classifies those
+ * segments' tokens again. */
+constexpr int32_t DENSE = EV_CAP + 1;
+
+__device__ __forceinline__ void mark_dense(int32_t *seg_count, int64_t a, int64_t b, int lane)
+{
+    for (int64_t s = a + lane; s < b; s += WAVE) seg_count[s] = DENSE;
+}
+
+struct ScanArgs {
+    const int32_t *tok_base;
+    int64_t mis;
+    const int64_t *starts;
+    const int32_t *lengths;
+    int64_t n;
+    const int64_t *seg_off;
+    int64_t seg_cap;
+    int32_t *seg_count;
+    uint32_t *events;
+    uint8_t *done;
+    TagMatch tm;
+    RowOut out;
+};
+
+/* Row being collected by a scan wave, in processing order. */
+struct RowCollect {
+    uint32_t lcnt; /* events in the wave's LDS buffer */
+    bool global;   /* events go to the segments' global slots; the row kernel evaluates the row */
+};
+
+constexpr int EVL = 1024;                 /* LDS events per wave */
+constexpr int SCAN_WAVES = 4;             /* waves per scan block */
+
+/* The whole of row `row` is in the wave's LDS buffer lev[0 .. lcnt): run the
+ * automaton in uniform control flow (scalar registers) and write the row's
+ * outputs.  The scan kernel has exactly one call site of it. */
+__device__ __forceinline__ void evaluate_row(const ScanArgs &a, int64_t row, int64_t first, int64_t last, int32_t len,
+                                          uint32_t lcnt, uint32_t *lev, int32_t *lfr, int lane)
+{
+    Automaton<WaveStore> A;
+    A.st.lds = lfr;
+    A.init();
+    bool ok = true;
+    for (uint32_t c0 = 0; ok && c0 < lcnt; c0 += WAVE) {
+        const uint32_t mine = c0 + lane < lcnt ? lev[c0 + lane] : 0u;
+        const uint32_t m = min((uint32_t)WAVE, lcnt - c0);
+        for (uint32_t j = 0; j < m; ++j) {
+            const uint32_t e = (uint32_t)__builtin_amdgcn_readlane((int)mine, (int)j);
+            if (!A.event((int32_t)(e >> 4), e & 15u)) {
+                ok = false;
+                break;
+            }
+        }
+    }
+    if (ok) A.finish(len);
+    if (A.overflow) {
+        /* nesting beyond the wave's frames: the row kernel takes the row */
+        mark_dense(a.seg_count, first, last + 1, lane);
+        return;
+    }
+    if (lane == 0) {
+        write_result(a.out, row, len, A);
+        a.done[row] = 1;
+    }
+}
+
+/* Scan one segment whose loads are in x.  A row owned by the wave collects
+ * its events in the wave's LDS buffer and is evaluated by the wave as soon as
+ * its last segment is scanned; any other row leaves its events in the global
+ * per-segment slots for rows_fast. */
+template <bool CONTIG>
+__device__ __forceinline__ void finish_segment(const ScanArgs &a, const int4 (&x)[LOADS], const SegView &w,
+                                               RowCollect &rc, uint32_t *lev, int32_t *lfr, int lane)
+{
+    if (w.s == w.first) {
+        rc.lcnt = 0;
+        rc.global = !w.owned;
+    }
+    uint32_t cnt = 0; /* wave-uniform */
+    if (!rc.global) {
+        const int32_t bias = (int32_t)(4 * w.v0 - w.g); /* row position of segment position 0 */
+        const uint32_t cap = (uint32_t)EVL - rc.lcnt;
+        if (!w.edge) scan_vectors<CONTIG, false>(x, 0, SEG_TOK, lev + rc.lcnt, cap, bias, cnt, a.tm, lane);
+        else scan_vectors<CONTIG, true>(x, w.q_lo, w.q_hi, lev + rc.lcnt, cap, bias, cnt, a.tm, lane);
+        if (cnt > cap) {
+            /* the row's events overflow the LDS buffer: its segments so far are
+             * classified again by the row kernel, the rest use global slots */
+            mark_dense(a.seg_count, w.first, w.s + 1, lane);
+            rc.global = true;
+        } else {
+            rc.lcnt += cnt;
+        }
+    } else {
+        if (!w.edge) scan_vectors<CONTIG, false>(x, 0, SEG_TOK, a.events + w.s * EV_CAP, EV_CAP, 0, cnt, a.tm, lane);
+        else scan_vectors<CONTIG, true>(x, w.q_lo, w.q_hi, a.events + w.s * EV_CAP, EV_CAP, 0, cnt, a.tm, lane);
+        if (lane == 0) a.seg_count[w.s] = (int32_t)cnt;
+    }
+    if (w.s != w.last || rc.global) return;
+    evaluate_row(a, w.row, w.first, w.last, w.len, rc.lcnt, lev, lfr, lane);
+}
+
+/* One wave per segment; waves take contiguous ranges of segment ids.  Other
+ * waves of the CU keep HBM busy while a wave compacts a segment or evaluates a
+ * row. */
+template <bool CONTIG>
+__global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD) scan_rows(ScanArgs a)
+{
+    __shared__ uint32_t lds_ev[SCAN_WAVES][EVL];
+    __shared__ int32_t lds_fr[SCAN_WAVES][FAST_DEPTH * FRAME_WORDS];
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int wib = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
+    const int64_t wave = uniform64((int64_t)blockIdx.x * SCAN_WAVES + wib);
+    const int64_t n_waves = (int64_t)gridDim.x * SCAN_WAVES;
+    const int64_t S = a.seg_off[a.n];
+    if (S > a.seg_cap) return; /* the row kernel reports PARASON_FLAG_WS_OVERFLOW */
+    /* S < 2^40 and n_waves < 2^20 (checked on the host), so S * wave fits */
+    const int64_t s_begin = uniform64(S * wave / n_waves);
+    const int64_t s_end = uniform64(S * (wave + 1) / n_waves);
+    if (s_begin >= s_end) return;
+
+    const int4 *src = reinterpret_cast<const int4 *>(a.tok_base);
+    SegCursor cur;
+    cur.seg_off = a.seg_off;
+    cur.starts = a.starts;
+    cur.lengths = a.lengths;
+    cur.mis = a.mis;
+    cur.s_begin = s_begin;
+    cur.s_end = s_end;
+    cur.seek(s_begin, a.n);
+    uint32_t *lev = lds_ev[wib];
+    int32_t *lfr = lds_fr[wib];
+
+    RowCollect rc;
+    rc.lcnt = 0;
+    rc.global = true; /* a row already begun in the previous wave's range */
+    for (int64_t s = s_begin; s < s_end; ++s) {
+        const SegView w = cur.view(s);
+        int4 x[LOADS];
+        issue_loads(x, src, w, lane);
+        finish_segment<CONTIG>(a, x, w, rc, lev, lfr, lane);
     }
 }
 
