@@ -31,7 +31,7 @@ size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 /* Byte offsets of the workspace sections for n rows. */
 struct Layout {
-    size_t seg_off, tile_sum, tile_off, counters, done, deep_rows, deep_frames, deep_bits, seg_count, events;
+    size_t seg_off, tile_sum, tile_off, counters, mode, deep_rows, deep_frames, deep_bits, seg_count, events;
     size_t fixed;  /* bytes before the per-segment sections */
     int64_t n_tiles;
 };
@@ -49,7 +49,7 @@ Layout layout_for(int64_t n)
     o = align_up(o + (size_t)L.n_tiles * sizeof(int64_t));
     L.counters = o;
     o = align_up(o + 4 * sizeof(int32_t));
-    L.done = o;
+    L.mode = o;
     o = align_up(o + (size_t)(n > 0 ? n : 1));
     L.deep_rows = o;
     o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
@@ -201,7 +201,7 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     int64_t *tile_sum = (int64_t *)(ws + L.tile_sum);
     int64_t *tile_off = (int64_t *)(ws + L.tile_off);
     int32_t *counters = (int32_t *)(ws + L.counters);
-    uint8_t *done = (uint8_t *)(ws + L.done);
+    uint8_t *mode = (uint8_t *)(ws + L.mode);
     int32_t *deep_rows = (int32_t *)(ws + L.deep_rows);
     int32_t *deep_frames = (int32_t *)(ws + L.deep_frames);
     uint32_t *deep_bits = (uint32_t *)(ws + L.deep_bits);
@@ -212,7 +212,7 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     pk::plan_tiles<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_sum);
     pk::plan_top<<<dim3(1), dim3(1024), 0, stream>>>(tile_sum, L.n_tiles, tile_off, seg_off, n_traj, counters);
     pk::plan_rows<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_off,
-                                                                        seg_off, done);
+                                                                        seg_off, mode);
 
     const pk::RowOut row_out{out->total,    out->latency,   out->n_subtask,       out->n_trial,
                              out->n_blocks, out->max_depth, out->first_error_pos, out->flags};
@@ -226,9 +226,8 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     sa.seg_cap = cap;
     sa.seg_count = seg_count;
     sa.events = events;
-    sa.done = done;
+    sa.mode = mode;
     sa.tm = h->tm;
-    sa.out = row_out;
     const unsigned scan_blocks = (unsigned)(cus * SCAN_BLOCKS_PER_CU);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[0], stream) != hipSuccess) return PARASON_ERR_HIP;
     if (h->tm.contiguous)
@@ -250,8 +249,8 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.tm = h->tm;
     ra.out = row_out;
     const unsigned row_blocks = (unsigned)((n_traj + 63) / 64);
-    pk::rows_fast<<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, done, counters, deep_rows);
-    pk::rows_deep<<<dim3(1), dim3(64), 0, stream>>>(ra, counters, deep_rows, deep_frames, deep_bits);
+    pk::rows_fast<<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows);
+    pk::rows_deep<<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);
 
     pk::RewardArgs rw;
     rw.total = out->total;

@@ -7,20 +7,20 @@
  *        Each row is cut into segments of SEG_VEC 16-byte vectors, starting at
  *        the 128-byte line that holds its first token.  A three-pass exclusive
  *        scan gives seg_off[i] (first segment of row i) and the segment count
- *        seg_off[n]; done[i] is cleared.
+ *        seg_off[n]; mode[i] is cleared.
  *   scan_rows  (HBM-bound; one wave per segment, persistent grid)
  *        Streams every token once with 16-byte loads, tests it against the
  *        twelve tag ids with a wave ballot and compacts the rare tags (about
  *        0.1-1% of tokens) in position order.  A row whose segments all fall in
- *        one wave's range keeps its events in that wave's LDS buffer, and the
- *        wave runs the grammar's pushdown automaton over them as soon as the
- *        row's last segment is scanned (done[i] = 1).  Other rows leave their
- *        events in per-segment global slots.
- *   rows_fast  (one thread per row not done)
- *        The same automaton over the global slots; a segment holding more than
- *        EV_CAP tags, or marked dense by the scan, is classified again token by
- *        token.  Frames of open blocks in LDS (FAST_DEPTH per row, 64 outline
- *        entries per block); a row that needs more is handed to rows_deep.
+ *        one wave's range collects its events in that wave's LDS buffer and is
+ *        written out, coalesced, as one compact list (mode[i] = 1).  Other rows
+ *        leave their events in per-segment global slots (mode[i] = 0).
+ *   rows_fast  (one thread per row)
+ *        The grammar's pushdown automaton over the row's events; Text runs are
+ *        the gaps between event positions.  A segment holding more than EV_CAP
+ *        tags, or marked DENSE by the scan, is classified again token by token.
+ *        Frames of open blocks in LDS (FAST_DEPTH per row, 64 outline entries
+ *        per block); a row that needs more is handed to rows_deep.
  *   rows_deep  (one thread, only rows handed over)
  *        The same automaton with frames and entry types in global workspace.
  *   group_reward  (one thread per group of G rows)
@@ -52,7 +52,10 @@ constexpr int EV_CAP = 128;              /* events stored per segment */
 constexpr int PLAN_TILE = 4096;          /* rows per plan tile */
 constexpr int PLAN_THREADS = 256;
 constexpr int ROWS_PER_THREAD = PLAN_TILE / PLAN_THREADS;
-constexpr int FAST_DEPTH = 8;            /* LDS frames per row (depth <= FAST_DEPTH + 1) */
+#ifndef PARASON_FAST_DEPTH
+#define PARASON_FAST_DEPTH 8
+#endif
+constexpr int FAST_DEPTH = PARASON_FAST_DEPTH; /* LDS frames per row (depth <= FAST_DEPTH + 1) */
 constexpr int FAST_ENTRIES = 64;         /* entries per open block on the fast path */
 constexpr int FRAME_WORDS = 8;
 constexpr int64_t DEEP_FRAMES = PARASON_MAX_DEPTH;
@@ -176,11 +179,11 @@ __global__ void __launch_bounds__(1024) plan_top(const int64_t *__restrict__ til
     if (threadIdx.x == 0) seg_off[n] = carry_s;
 }
 
-/* seg_off[i] = first segment of row i; done[i] = 0 (no row evaluated yet). */
+/* seg_off[i] = first segment of row i; mode[i] = 0 (events in per-segment slots). */
 __global__ void __launch_bounds__(PLAN_THREADS) plan_rows(const int64_t *__restrict__ starts,
                                                           const int32_t *__restrict__ lengths, int64_t n,
                                                           int64_t mis, const int64_t *__restrict__ tile_off,
-                                                          int64_t *__restrict__ seg_off, uint8_t *__restrict__ done)
+                                                          int64_t *__restrict__ seg_off, uint8_t *__restrict__ mode)
 {
     __shared__ int64_t part[PLAN_THREADS / WAVE];
     /* thread t owns the ROWS_PER_THREAD consecutive rows starting at r0 + t*ROWS_PER_THREAD */
@@ -203,7 +206,7 @@ __global__ void __launch_bounds__(PLAN_THREADS) plan_rows(const int64_t *__restr
         int64_t r = r0 + j;
         if (r < n) {
             seg_off[r] = off;
-            done[r] = 0;
+            mode[r] = 0;
         }
         off += cnt[j];
     }
@@ -249,46 +252,6 @@ struct LdsStore {
         t.k = at(d - 1, 4);
         t.saved_ctx = (uint32_t)at(d - 1, 5);
         t.ent = (uint64_t)(uint32_t)at(d - 1, 6) | ((uint64_t)(uint32_t)at(d - 1, 7) << 32);
-    }
-    __device__ void begin_block(Top &t) { t.ent = 0; }
-    __device__ void end_block(const Top &) {}
-    __device__ bool add_entry(Top &t, bool trial)
-    {
-        if (t.n_e >= FAST_ENTRIES) return false;
-        if (trial) t.ent |= (uint64_t)1 << t.n_e;
-        return true;
-    }
-    __device__ uint32_t entry_type(const Top &t, int32_t k) { return ((t.ent >> k) & 1u) ? T_TRI : T_SUB; }
-};
-
-/* Wave store: one automaton per wave running in uniform control flow (its
- * values live in scalar registers); FAST_DEPTH frames in the wave's LDS. */
-struct WaveStore {
-    int32_t *lds; /* [FAST_DEPTH][FRAME_WORDS] of this wave */
-    __device__ int32_t get(int d, int f) { return __builtin_amdgcn_readfirstlane(lds[d * FRAME_WORDS + f]); }
-    __device__ bool push(const Top &t, int d)
-    {
-        if (d > FAST_DEPTH) return false;
-        int32_t *f = lds + (d - 1) * FRAME_WORDS;
-        f[0] = t.saved_acc;
-        f[1] = t.block_main;
-        f[2] = t.max_w;
-        f[3] = t.n_e;
-        f[4] = t.k;
-        f[5] = (int32_t)t.saved_ctx;
-        f[6] = (int32_t)(uint32_t)t.ent;
-        f[7] = (int32_t)(uint32_t)(t.ent >> 32);
-        return true;
-    }
-    __device__ void pop(Top &t, int d)
-    {
-        t.saved_acc = get(d - 1, 0);
-        t.block_main = get(d - 1, 1);
-        t.max_w = get(d - 1, 2);
-        t.n_e = get(d - 1, 3);
-        t.k = get(d - 1, 4);
-        t.saved_ctx = (uint32_t)get(d - 1, 5);
-        t.ent = (uint64_t)(uint32_t)get(d - 1, 6) | ((uint64_t)(uint32_t)get(d - 1, 7) << 32);
     }
     __device__ void begin_block(Top &t) { t.ent = 0; }
     __device__ void end_block(const Top &) {}
@@ -590,34 +553,48 @@ struct RowArgs {
 };
 
 /* Feed row r's events to A.  Returns false when A stopped early.
- * A segment whose events were not stored (more than EV_CAP tags) is classified
- * again token by token.  Both sources feed the same single call of A.event:
- * with two inlined copies of the automaton (one per source) the gfx950 build
- * returned wrong results for dense segments although the same source is
- * correct when compiled for the CPU. */
+ *
+ * Three sources, all feeding the one call of A.event below: a compact list
+ * (the scan collected the whole row: events[first*EV_CAP ..], row positions,
+ * count in seg_count[first]), or per segment its stored events (segment
+ * positions) or, for a segment holding more than EV_CAP tags or marked DENSE,
+ * its tokens classified again one by one.  With two inlined copies of the
+ * automaton (one per source) the gfx950 build returned wrong results for dense
+ * segments although the same source is correct when compiled for the CPU, so
+ * the sources are merged into one fetch loop. */
 template <class Store>
-__device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, Automaton<Store> &A)
+__device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, bool compact, Automaton<Store> &A)
 {
     const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
     const int64_t vrow0 = row_first_vec(g), vend = row_end_vec(g, len);
-    for (int64_t s = s0; s < s1; ++s) {
-        const int64_t v0 = vrow0 + (s - s0) * SEG_VEC;
-        const int64_t base = 4 * v0 - g;
-        const int32_t cnt = a.seg_count[s];
-        const bool dense = cnt > EV_CAP;
-        const uint32_t *ev = a.events + s * EV_CAP;
-        const int64_t q_end = 4 * min(v0 + (int64_t)SEG_VEC, vend);
-        int64_t q = 4 * v0;
-        int32_t e = 0;
+    int64_t s = s0;              /* next segment to open */
+    const uint32_t *ev = nullptr;
+    int32_t e = 0, cnt = 0;      /* stored-event cursor */
+    int64_t base = 0;            /* row position of stored position 0 */
+    bool dense = false;
+    int64_t q = 0, q_end = 0;    /* dense cursor (element index on the token grid) */
+    uint4 quad = make_uint4(0u, 0u, 0u, 0u);
+    if (compact) {
+        ev = a.events + s0 * EV_CAP;
+        cnt = a.seg_count[s0];
+        s = s1;
+    }
+    for (;;) {
+        int32_t p = 0;
+        uint32_t c = 0;
         for (;;) {
-            int32_t p = 0;
-            uint32_t c = 0;
-            if (!dense) {
-                if (e >= cnt) break;
-                uint32_t w = ev[e++];
+            if (!dense && e < cnt) {
+                /* stored lists start 512-byte aligned and their slots are
+                 * multiples of 4 events: read them 16 bytes at a time */
+                if ((e & 3) == 0) quad = *reinterpret_cast<const uint4 *>(ev + e);
+                const uint32_t k = (uint32_t)e & 3u;
+                const uint32_t w = k == 0 ? quad.x : k == 1 ? quad.y : k == 2 ? quad.z : quad.w;
+                ++e;
                 p = (int32_t)(base + (w >> 4));
                 c = w & 15u;
-            } else {
+                break;
+            }
+            if (dense) {
                 while (q < q_end) {
                     const int32_t t = a.tok_base[q];
                     const int64_t pp = q - g;
@@ -629,23 +606,40 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, A
                         break;
                     }
                 }
-                if (c == 0) break;
+                if (c) break;
+                dense = false;
             }
-            if (!A.event(p, c)) return false;
+            if (s >= s1) break;
+            /* open segment s */
+            const int64_t v0 = vrow0 + (s - s0) * SEG_VEC;
+            const int32_t n_s = a.seg_count[s];
+            base = 4 * v0 - g;
+            e = 0;
+            if (n_s <= EV_CAP) {
+                ev = a.events + s * EV_CAP;
+                cnt = n_s;
+            } else {
+                cnt = 0;
+                dense = true;
+                q = 4 * v0;
+                q_end = 4 * min(v0 + (int64_t)SEG_VEC, vend);
+            }
+            ++s;
         }
+        if (c == 0) break; /* no more events */
+        if (!A.event(p, c)) return false;
     }
     return true;
 }
 
-/* One thread per row the scan did not evaluate (rows split between two scan
- * waves, rows whose events did not fit the wave's LDS buffer, rows without
- * segments). */
-__global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__restrict__ done,
+/* One thread per row.  mode[r] == 1: the scan left the row's events as one
+ * compact list; 0: per-segment slots. */
+__global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__restrict__ mode,
                                                 int32_t *__restrict__ counters, int32_t *__restrict__ deep_rows)
 {
     __shared__ int32_t lds[FAST_DEPTH * FRAME_WORDS * 64];
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= a.n || done[r]) return;
+    if (r >= a.n) return;
     const int64_t start = a.starts[r];
     const int32_t len = a.lengths[r];
     if (start < 0 || len < 0) {
@@ -661,7 +655,7 @@ __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__rest
     A.st.tid = threadIdx.x;
     A.st.nt = blockDim.x;
     A.init();
-    if (drive_row(a, r, start + a.mis, len, A)) A.finish(len);
+    if (drive_row(a, r, start + a.mis, len, mode[r] == 1, A)) A.finish(len);
     if (A.overflow) {
         int32_t slot = atomicAdd(&counters[0], 1);
         deep_rows[slot] = (int32_t)r;
@@ -672,7 +666,8 @@ __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__rest
 
 /* Rows whose nesting or entry count exceeded the fast store, one after the
  * other, on a single thread with frames in global workspace. */
-__global__ void __launch_bounds__(64) rows_deep(RowArgs a, const int32_t *__restrict__ counters,
+__global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__restrict__ mode,
+                                                const int32_t *__restrict__ counters,
                                                 const int32_t *__restrict__ deep_rows, int32_t *__restrict__ frames,
                                                 uint32_t *__restrict__ bits)
 {
@@ -686,7 +681,7 @@ __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const int32_t *__rest
         A.st.bits = bits;
         A.st.esp = 0;
         A.init();
-        if (drive_row(a, r, a.starts[r] + a.mis, len, A)) A.finish(len);
+        if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
         if (A.overflow)
             write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_DEPTH_LIMIT);
         else
@@ -862,9 +857,8 @@ struct ScanArgs {
     int64_t seg_cap;
     int32_t *seg_count;
     uint32_t *events;
-    uint8_t *done;
+    uint8_t *mode;
     TagMatch tm;
-    RowOut out;
 };
 
 /* Row being collected by a scan wave, in processing order. */
@@ -876,46 +870,32 @@ struct RowCollect {
 constexpr int EVL = 1024;                 /* LDS events per wave */
 constexpr int SCAN_WAVES = 4;             /* waves per scan block */
 
-/* The whole of row `row` is in the wave's LDS buffer lev[0 .. lcnt): run the
- * automaton in uniform control flow (scalar registers) and write the row's
- * outputs.  The scan kernel has exactly one call site of it. */
-__device__ __forceinline__ void evaluate_row(const ScanArgs &a, int64_t row, int64_t first, int64_t last, int32_t len,
-                                          uint32_t lcnt, uint32_t *lev, int32_t *lfr, int lane)
+/* The whole of row `row` is in the wave's LDS buffer lev[0 .. lcnt): copy it,
+ * coalesced, to the row's own slot range events[first*EV_CAP ..] as one
+ * compact list for the row kernel (mode 1).  A list longer than the row's
+ * slots makes the row kernel classify its segments again. */
+__device__ __forceinline__ void flush_row(const ScanArgs &a, int64_t row, int64_t first, int64_t last, uint32_t lcnt,
+                                          const uint32_t *lev, int lane)
 {
-    Automaton<WaveStore> A;
-    A.st.lds = lfr;
-    A.init();
-    bool ok = true;
-    for (uint32_t c0 = 0; ok && c0 < lcnt; c0 += WAVE) {
-        const uint32_t mine = c0 + lane < lcnt ? lev[c0 + lane] : 0u;
-        const uint32_t m = min((uint32_t)WAVE, lcnt - c0);
-        for (uint32_t j = 0; j < m; ++j) {
-            const uint32_t e = (uint32_t)__builtin_amdgcn_readlane((int)mine, (int)j);
-            if (!A.event((int32_t)(e >> 4), e & 15u)) {
-                ok = false;
-                break;
-            }
-        }
-    }
-    if (ok) A.finish(len);
-    if (A.overflow) {
-        /* nesting beyond the wave's frames: the row kernel takes the row */
+    if ((int64_t)lcnt > (last - first + 1) * EV_CAP) {
         mark_dense(a.seg_count, first, last + 1, lane);
         return;
     }
+    uint32_t *dst = a.events + first * EV_CAP;
+    for (uint32_t i = lane; i < lcnt; i += WAVE) dst[i] = lev[i];
     if (lane == 0) {
-        write_result(a.out, row, len, A);
-        a.done[row] = 1;
+        a.seg_count[first] = (int32_t)lcnt;
+        a.mode[row] = 1;
     }
 }
 
 /* Scan one segment whose loads are in x.  A row owned by the wave collects
- * its events in the wave's LDS buffer and is evaluated by the wave as soon as
- * its last segment is scanned; any other row leaves its events in the global
- * per-segment slots for rows_fast. */
+ * its events in the wave's LDS buffer; any other row leaves its events in the
+ * global per-segment slots for rows_fast.  Returns true when this segment
+ * completes a row whose events are all in the LDS buffer (rc.lcnt of them). */
 template <bool CONTIG>
-__device__ __forceinline__ void finish_segment(const ScanArgs &a, const int4 (&x)[LOADS], const SegView &w,
-                                               RowCollect &rc, uint32_t *lev, int32_t *lfr, int lane)
+__device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&x)[LOADS], const SegView &w,
+                                                RowCollect &rc, uint32_t *lev, int lane)
 {
     if (w.s == w.first) {
         rc.lcnt = 0;
@@ -940,18 +920,16 @@ __device__ __forceinline__ void finish_segment(const ScanArgs &a, const int4 (&x
         else scan_vectors<CONTIG, true>(x, w.q_lo, w.q_hi, a.events + w.s * EV_CAP, EV_CAP, 0, cnt, a.tm, lane);
         if (lane == 0) a.seg_count[w.s] = (int32_t)cnt;
     }
-    if (w.s != w.last || rc.global) return;
-    evaluate_row(a, w.row, w.first, w.last, w.len, rc.lcnt, lev, lfr, lane);
+    return w.s == w.last && !rc.global;
 }
 
-/* One wave per segment; waves take contiguous ranges of segment ids.  Other
- * waves of the CU keep HBM busy while a wave compacts a segment or evaluates a
- * row. */
+/* One wave per segment; waves take contiguous ranges of segment ids.  A wave
+ * issues the loads of its next segment as soon as the current one is
+ * compacted, before it flushes a finished row's events. */
 template <bool CONTIG>
 __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD) scan_rows(ScanArgs a)
 {
     __shared__ uint32_t lds_ev[SCAN_WAVES][EVL];
-    __shared__ int32_t lds_fr[SCAN_WAVES][FAST_DEPTH * FRAME_WORDS];
     const int lane = threadIdx.x & (WAVE - 1);
     const int wib = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
     const int64_t wave = uniform64((int64_t)blockIdx.x * SCAN_WAVES + wib);
@@ -973,16 +951,22 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
     cur.s_end = s_end;
     cur.seek(s_begin, a.n);
     uint32_t *lev = lds_ev[wib];
-    int32_t *lfr = lds_fr[wib];
 
     RowCollect rc;
     rc.lcnt = 0;
     rc.global = true; /* a row already begun in the previous wave's range */
+    SegView w = cur.view(s_begin);
+    int4 x[LOADS];
+    issue_loads(x, src, w, lane);
     for (int64_t s = s_begin; s < s_end; ++s) {
-        const SegView w = cur.view(s);
-        int4 x[LOADS];
-        issue_loads(x, src, w, lane);
-        finish_segment<CONTIG>(a, x, w, rc, lev, lfr, lane);
+        const bool row_in_lds = collect_segment<CONTIG>(a, x, w, rc, lev, lane);
+        const int64_t row = w.row, first = w.first, last = w.last;
+        /* the next segment's loads fly while a finished row's automaton runs */
+        if (s + 1 < s_end) {
+            w = cur.view(s + 1);
+            issue_loads(x, src, w, lane);
+        }
+        if (row_in_lds) flush_row(a, row, first, last, rc.lcnt, lev, lane);
     }
 }
 
