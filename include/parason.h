@@ -76,6 +76,37 @@ extern "C" {
 /* An invalid stream keeps the caller's correctness bit (default: an invalid
  * stream counts as incorrect, reward -1). */
 #define PARASON_CFG_INVALID_KEEPS_CORRECTNESS (1u << 0)
+/* mu and sigma over the whole batch instead of each group of G rows (the
+ * alternative reading of the normalisation population).  A batch holding any
+ * row that was not evaluated gets NaN rewards throughout. */
+#define PARASON_CFG_BATCH_STATS (1u << 1)
+
+/* ---- batch metrics (parason_outputs.metrics, doubles) ------------------- */
+/* As the paper reports them: trigger ratio = share of rows with >= 1
+ * <Parallel> block (Table 4); acceleration = total tokens / longest-path
+ * tokens (Tables 4 and 5); mean latency tokens (Tables 2 and 4); saved tokens
+ * = generated - latency (Table 5).  Counts are exact; sums of token counts
+ * are exact below 2^53. */
+#define PARASON_METRIC_ROWS 0
+#define PARASON_METRIC_VALID 1
+#define PARASON_METRIC_TRIGGERED 2
+#define PARASON_METRIC_CORRECT 3
+#define PARASON_METRIC_TRUNCATED 4
+#define PARASON_METRIC_COUNT_MISMATCH 5
+#define PARASON_METRIC_SUM_TOTAL 6
+#define PARASON_METRIC_SUM_LATENCY 7
+#define PARASON_METRIC_SUM_SUBTASK 8
+#define PARASON_METRIC_SUM_TRIAL 9
+#define PARASON_METRIC_TRIGGER_RATIO 10
+#define PARASON_METRIC_ACCELERATION 11
+#define PARASON_METRIC_MEAN_LATENCY 12
+#define PARASON_METRIC_MEAN_TOTAL 13
+#define PARASON_METRIC_MEAN_SAVED 14
+#define PARASON_METRIC_SUBTASK_SHARE 15
+#define PARASON_METRIC_TRIAL_SHARE 16
+#define PARASON_METRIC_ACCURACY 17
+#define PARASON_METRIC_MEAN_REWARD 18
+#define PARASON_METRIC_COUNT 19
 
 /* Maximum nesting depth and number of outline entries of open blocks that the
  * library evaluates; a row beyond either is flagged PARASON_FLAG_DEPTH_LIMIT.
@@ -99,7 +130,7 @@ typedef struct parason_config {
 } parason_config;
 
 /* Caller-owned device arrays of n_traj elements each.  All are required except
- * r_subtask, r_trial and eta, which may be NULL. */
+ * r_subtask, r_trial, eta and metrics, which may be NULL. */
 typedef struct parason_outputs {
     int32_t *total;           /* L_total = length of the row */
     int32_t *latency;         /* T_i = L_latency (longest generation path) */
@@ -113,6 +144,8 @@ typedef struct parason_outputs {
     float *r_subtask;         /* optional: n_subtask / total (0 if total == 0) */
     float *r_trial;           /* optional: n_trial / total */
     float *eta;               /* optional: eta(s) = 1 - latency / total */
+    double *metrics;          /* optional: PARASON_METRIC_COUNT batch metrics (mean reward
+                                 over the stored float rewards) */
 } parason_outputs;
 
 typedef struct parason_handle parason_handle;

@@ -41,6 +41,14 @@ F_COUNT_MISMATCH = 1 << 2
 F_TRIGGERED = 1 << 3
 
 CFG_INVALID_KEEPS_CORRECTNESS = 1 << 0
+CFG_BATCH_STATS = 1 << 1
+
+METRICS = (
+    "rows", "valid", "triggered", "correct", "truncated", "count_mismatch",
+    "sum_total", "sum_latency", "sum_subtask", "sum_trial",
+    "trigger_ratio", "acceleration", "mean_latency", "mean_total", "mean_saved",
+    "subtask_share", "trial_share", "accuracy", "mean_reward",
+)
 
 TAG_NAMES = (
     "<think>", "</think>", "<Parallel>", "</Parallel>", "<Outlines>", "</Outlines>",
@@ -80,6 +88,9 @@ def lib():
             ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
             ctypes.c_void_p, ctypes.c_void_p,
         ]
+        L.oracle_batch_metrics.restype = ctypes.c_int
+        L.oracle_batch_metrics.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                           ctypes.c_void_p]
         _lib = L
     return _lib
 
@@ -118,7 +129,15 @@ def eval_stream(stream, tag_ids) -> np.void:
 
 def group_reward(rows: np.ndarray, correct, group_size: int, alpha: float, beta_subtask: float,
                  beta_trial: float, rho: float, rho_clip: float, cfg_flags: int = 0):
-    """Reward of Definition 3.1 per row, plus R_subtask, R_trial and eta (all float64)."""
+    """Reward of Definition 3.1 per row, plus R_subtask, R_trial and eta (all float64).
+
+    With CFG_BATCH_STATS in cfg_flags, mu and sigma are taken over the whole
+    batch (the batch is one normalisation group) instead of each G rows."""
+    if cfg_flags & CFG_BATCH_STATS:
+        group_size = len(rows)
+        if group_size == 0:
+            z = np.zeros(0)
+            return z, z, z, z
     rows = np.ascontiguousarray(rows, dtype=ROW_DTYPE)
     correct = np.ascontiguousarray(correct, dtype=np.uint8)
     n = rows.shape[0]
@@ -136,3 +155,19 @@ def group_reward(rows: np.ndarray, correct, group_size: int, alpha: float, beta_
     if rc != 0:
         raise ValueError("oracle_group_reward failed: %d (n_rows %% group_size must be 0)" % rc)
     return reward, r_sub, r_tri, eta
+
+
+def batch_metrics(rows: np.ndarray, correct, reward) -> dict:
+    """Batch metrics of Tables 2, 4 and 5 (see oracle_batch_metrics)."""
+    rows = np.ascontiguousarray(rows, dtype=ROW_DTYPE)
+    correct = np.ascontiguousarray(correct, dtype=np.uint8)
+    reward = np.ascontiguousarray(reward, dtype=np.float64)
+    m = np.zeros(len(METRICS), np.float64)
+    n = rows.shape[0]
+    if n == 0:
+        rows = np.zeros(1, dtype=ROW_DTYPE)
+        correct = np.zeros(1, np.uint8)
+        reward = np.zeros(1)
+    rc = lib().oracle_batch_metrics(_ptr(rows), _ptr(correct), _ptr(reward), n, _ptr(m))
+    assert rc == 0
+    return dict(zip(METRICS, m.tolist()))

@@ -465,3 +465,66 @@ int oracle_group_reward(const oracle_row_t *rows, const uint8_t *correct, int64_
     free(buf);
     return 0;
 }
+
+/* ---------------------------------------------------------------------------
+ * Batch metrics, as the paper reports them (Table 2, 4 and 5):
+ *   trigger ratio      = share of samples with at least one <Parallel> block
+ *                        (Table 4 caption);
+ *   acceleration ratio = total tokens / longest-path tokens (Table 4 caption;
+ *                        Table 5: generated / latency tokens);
+ *   token latency      = mean longest-path tokens (Tables 2, 4);
+ *   saved tokens       = generated - latency tokens (Table 5);
+ * plus accuracy, validity and branch-token shares.  Index order is the
+ * interface contract (PARASON_METRIC_* in the C-ABI).
+ * ------------------------------------------------------------------------- */
+enum {
+    M_ROWS = 0, M_VALID, M_TRIGGERED, M_CORRECT, M_TRUNCATED, M_MISMATCH,
+    M_SUM_TOTAL, M_SUM_LATENCY, M_SUM_SUBTASK, M_SUM_TRIAL,
+    M_TRIGGER_RATIO, M_ACCELERATION, M_MEAN_LATENCY, M_MEAN_TOTAL, M_MEAN_SAVED,
+    M_SUBTASK_SHARE, M_TRIAL_SHARE, M_ACCURACY, M_MEAN_REWARD, M_COUNT
+};
+
+int oracle_batch_metrics(const oracle_row_t *rows, const uint8_t *correct, const double *reward, int64_t n,
+                         double *m)
+{
+    int64_t valid = 0, trig = 0, corr = 0, trunc = 0, mism = 0;
+    int64_t st = 0, sl = 0, ss = 0, sr = 0;
+    double rsum = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+        valid += (rows[i].flags & F_VALID) != 0;
+        trig += (rows[i].flags & F_TRIGGERED) != 0;
+        trunc += (rows[i].flags & F_TRUNCATED) != 0;
+        mism += (rows[i].flags & F_COUNT_MISMATCH) != 0;
+        corr += correct[i] != 0;
+        st += rows[i].total;
+        sl += rows[i].latency;
+        ss += rows[i].n_subtask;
+        sr += rows[i].n_trial;
+        rsum = rsum + reward[i];
+    }
+    for (int k = 0; k < M_COUNT; ++k) m[k] = 0.0;
+    m[M_ROWS] = (double)n;
+    m[M_VALID] = (double)valid;
+    m[M_TRIGGERED] = (double)trig;
+    m[M_CORRECT] = (double)corr;
+    m[M_TRUNCATED] = (double)trunc;
+    m[M_MISMATCH] = (double)mism;
+    m[M_SUM_TOTAL] = (double)st;
+    m[M_SUM_LATENCY] = (double)sl;
+    m[M_SUM_SUBTASK] = (double)ss;
+    m[M_SUM_TRIAL] = (double)sr;
+    if (n > 0) {
+        m[M_TRIGGER_RATIO] = (double)trig / (double)n;
+        m[M_MEAN_LATENCY] = (double)sl / (double)n;
+        m[M_MEAN_TOTAL] = (double)st / (double)n;
+        m[M_MEAN_SAVED] = (double)(st - sl) / (double)n;
+        m[M_ACCURACY] = (double)corr / (double)n;
+        m[M_MEAN_REWARD] = rsum / (double)n;
+    }
+    if (sl > 0) m[M_ACCELERATION] = (double)st / (double)sl;
+    if (st > 0) {
+        m[M_SUBTASK_SHARE] = (double)ss / (double)st;
+        m[M_TRIAL_SHARE] = (double)sr / (double)st;
+    }
+    return 0;
+}

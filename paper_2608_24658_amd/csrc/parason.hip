@@ -32,6 +32,7 @@ size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 /* Byte offsets of the workspace sections for n rows. */
 struct Layout {
     size_t seg_off, tile_sum, tile_off, counters, mode, deep_rows, deep_frames, deep_bits, seg_count, events;
+    size_t red_d, red_i, stats;
     size_t fixed;  /* bytes before the per-segment sections */
     int64_t n_tiles;
 };
@@ -57,6 +58,13 @@ Layout layout_for(int64_t n)
     o = align_up(o + (size_t)pk::DEEP_FRAMES * pk::FRAME_WORDS * sizeof(int32_t));
     L.deep_bits = o;
     o = align_up(o + (size_t)(pk::DEEP_ENTRY_BITS / 32) * sizeof(uint32_t));
+    /* partial sums of the batch reductions (one record per 4096 rows) */
+    L.red_d = o;
+    o = align_up(o + (size_t)L.n_tiles * 3 * sizeof(double));
+    L.red_i = o;
+    o = align_up(o + (size_t)L.n_tiles * pk::NMI * sizeof(int64_t));
+    L.stats = o;
+    o = align_up(o + sizeof(pk::BatchStats));
     L.fixed = o;
     L.seg_count = o;
     L.events = 0; /* depends on the capacity */
@@ -206,6 +214,9 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     int32_t *deep_frames = (int32_t *)(ws + L.deep_frames);
     uint32_t *deep_bits = (uint32_t *)(ws + L.deep_bits);
     int32_t *seg_count = (int32_t *)(ws + L.seg_count);
+    double *red_d = (double *)(ws + L.red_d);
+    int64_t *red_i = (int64_t *)(ws + L.red_i);
+    pk::BatchStats *stats = (pk::BatchStats *)(ws + L.stats);
     uint32_t *events = (uint32_t *)(ws + align_up(L.seg_count + (size_t)cap * sizeof(int32_t)));
 
     const unsigned tiles = (unsigned)L.n_tiles;
@@ -271,8 +282,26 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     rw.r_subtask = out->r_subtask;
     rw.r_trial = out->r_trial;
     rw.eta = out->eta;
-    const unsigned reward_blocks = (unsigned)((rw.n_groups + 255) / 256);
-    pk::group_reward<<<dim3(reward_blocks), dim3(256), 0, stream>>>(rw);
+    rw.batch = nullptr;
+    rw.n = n_traj;
+    if (h->cfg.flags & PARASON_CFG_BATCH_STATS) {
+        pk::StatsArgs st{out->total, out->latency, out->n_subtask, out->n_trial, out->flags, n_traj, red_d, red_i, stats};
+        pk::batch_stats_tiles<1><<<dim3(tiles), dim3(pk::RED_THREADS), 0, stream>>>(st);
+        pk::batch_stats_final<1><<<dim3(1), dim3(pk::RED_THREADS), 0, stream>>>(st, L.n_tiles);
+        pk::batch_stats_tiles<2><<<dim3(tiles), dim3(pk::RED_THREADS), 0, stream>>>(st);
+        pk::batch_stats_final<2><<<dim3(1), dim3(pk::RED_THREADS), 0, stream>>>(st, L.n_tiles);
+        rw.batch = stats;
+        pk::batch_reward<<<dim3((unsigned)((n_traj + 255) / 256)), dim3(256), 0, stream>>>(rw);
+    } else {
+        const unsigned reward_blocks = (unsigned)((rw.n_groups + 255) / 256);
+        pk::group_reward<<<dim3(reward_blocks), dim3(256), 0, stream>>>(rw);
+    }
+    if (out->metrics) {
+        pk::MetricsArgs ma{out->total, out->latency, out->n_subtask, out->n_trial, out->flags, correct,
+                           out->reward, n_traj, red_i, red_d, out->metrics};
+        pk::metrics_tiles<<<dim3(tiles), dim3(pk::RED_THREADS), 0, stream>>>(ma);
+        pk::metrics_final<<<dim3(1), dim3(pk::RED_THREADS), 0, stream>>>(ma, L.n_tiles);
+    }
 
     return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
 }

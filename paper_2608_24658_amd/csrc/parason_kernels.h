@@ -972,12 +972,22 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
 
 /* ------------------------------------------------------------------ reward */
 
+/* Batch-wide statistics (PARASON_CFG_BATCH_STATS), in workspace. */
+struct BatchStats {
+    double mu[3];    /* latency, Subtask ratio, Trial ratio */
+    double sigma[3];
+    int32_t all_equal[3];
+    int32_t not_evaluated; /* rows flagged not evaluated */
+};
+
 struct RewardArgs {
     const int32_t *total, *latency, *n_subtask, *n_trial;
     const uint32_t *flags;
     const uint8_t *correct;
     int64_t n_groups;
     int32_t G;
+    const BatchStats *batch; /* non-null: one normalisation group = the whole batch */
+    int64_t n;
     double alpha, beta_s, beta_r, rho, rho_clip;
     uint32_t cfg_flags;
     float *reward, *r_subtask, *r_trial, *eta;
@@ -1025,6 +1035,36 @@ __device__ __forceinline__ double zscore(double x, Moments m, bool all_equal)
     return (all_equal || m.sigma == 0.0) ? 0.0 : __ddiv_rn(__dsub_rn(x, m.mu), m.sigma);
 }
 
+__device__ __forceinline__ void write_reward(const RewardArgs &a, int64_t r, double zT, double zs, double zr, double xs,
+                                             double xr)
+{
+    const int32_t tot = a.total[r];
+    const double e = tot > 0 ? __dsub_rn(1.0, __ddiv_rn((double)a.latency[r], (double)tot)) : 0.0;
+    const bool valid = (a.flags[r] & PARASON_FLAG_VALID) != 0;
+    const bool c = a.correct[r] != 0 && (valid || (a.cfg_flags & PARASON_CFG_INVALID_KEEPS_CORRECTNESS));
+    const double accel = __dmul_rn(a.rho, e);
+    const double clipped = accel < a.rho_clip ? accel : a.rho_clip;
+    double inner = __dsub_rn(1.0, __dmul_rn(a.alpha, zT));
+    inner = __dadd_rn(inner, __dmul_rn(a.beta_s, zs));
+    inner = __dadd_rn(inner, __dmul_rn(a.beta_r, zr));
+    inner = __dadd_rn(inner, clipped);
+    const double R = __dadd_rn(-1.0, __dmul_rn(__dmul_rn(2.0, c ? 1.0 : 0.0), inner));
+    a.reward[r] = (float)R;
+    if (a.r_subtask) a.r_subtask[r] = (float)xs;
+    if (a.r_trial) a.r_trial[r] = (float)xr;
+    if (a.eta) a.eta[r] = (float)e;
+}
+
+__device__ __forceinline__ void write_nan(const RewardArgs &a, int64_t r)
+{
+    const float nan = __int_as_float(0x7fc00000);
+    a.reward[r] = nan;
+    if (a.r_subtask) a.r_subtask[r] = nan;
+    if (a.r_trial) a.r_trial[r] = nan;
+    if (a.eta) a.eta[r] = nan;
+}
+
+/* One thread per group of G rows. */
 __global__ void __launch_bounds__(256) group_reward(RewardArgs a)
 {
     const int64_t grp = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -1039,13 +1079,7 @@ __global__ void __launch_bounds__(256) group_reward(RewardArgs a)
         lat_equal = lat_equal && a.latency[r0 + i] == a.latency[r0];
     }
     if (!evaluated) {
-        const float nan = __int_as_float(0x7fc00000);
-        for (int32_t i = 0; i < G; ++i) {
-            a.reward[r0 + i] = nan;
-            if (a.r_subtask) a.r_subtask[r0 + i] = nan;
-            if (a.r_trial) a.r_trial[r0 + i] = nan;
-            if (a.eta) a.eta[r0 + i] = nan;
-        }
+        for (int32_t i = 0; i < G; ++i) write_nan(a, r0 + i);
         return;
     }
     const bool sub_equal = same_ratio(a.n_subtask, a.total, r0, G);
@@ -1054,24 +1088,224 @@ __global__ void __launch_bounds__(256) group_reward(RewardArgs a)
     auto xs = [&](int32_t i) { return ratio(a.n_subtask[r0 + i], a.total[r0 + i]); };
     auto xr = [&](int32_t i) { return ratio(a.n_trial[r0 + i], a.total[r0 + i]); };
     const Moments mT = moments(xT, G), ms = moments(xs, G), mr = moments(xr, G);
+    for (int32_t i = 0; i < G; ++i)
+        write_reward(a, r0 + i, zscore(xT(i), mT, lat_equal), zscore(xs(i), ms, sub_equal),
+                     zscore(xr(i), mr, tri_equal), xs(i), xr(i));
+}
 
-    for (int32_t i = 0; i < G; ++i) {
-        const int64_t r = r0 + i;
-        const int32_t tot = a.total[r];
-        const double e = tot > 0 ? __dsub_rn(1.0, __ddiv_rn((double)a.latency[r], (double)tot)) : 0.0;
-        const bool valid = (a.flags[r] & PARASON_FLAG_VALID) != 0;
-        const bool c = a.correct[r] != 0 && (valid || (a.cfg_flags & PARASON_CFG_INVALID_KEEPS_CORRECTNESS));
-        const double accel = __dmul_rn(a.rho, e);
-        const double clipped = accel < a.rho_clip ? accel : a.rho_clip;
-        double inner = __dsub_rn(1.0, __dmul_rn(a.alpha, zscore(xT(i), mT, lat_equal)));
-        inner = __dadd_rn(inner, __dmul_rn(a.beta_s, zscore(xs(i), ms, sub_equal)));
-        inner = __dadd_rn(inner, __dmul_rn(a.beta_r, zscore(xr(i), mr, tri_equal)));
-        inner = __dadd_rn(inner, clipped);
-        const double R = __dadd_rn(-1.0, __dmul_rn(__dmul_rn(2.0, c ? 1.0 : 0.0), inner));
-        a.reward[r] = (float)R;
-        if (a.r_subtask) a.r_subtask[r] = (float)xs(i);
-        if (a.r_trial) a.r_trial[r] = (float)xr(i);
-        if (a.eta) a.eta[r] = (float)e;
+/* One thread per row; mu, sigma of the whole batch from batch_stats. */
+__global__ void __launch_bounds__(256) batch_reward(RewardArgs a)
+{
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= a.n) return;
+    const BatchStats &b = *a.batch;
+    if (b.not_evaluated) {
+        write_nan(a, r);
+        return;
+    }
+    const double xT = (double)a.latency[r], xs = ratio(a.n_subtask[r], a.total[r]), xr = ratio(a.n_trial[r], a.total[r]);
+    write_reward(a, r, zscore(xT, Moments{b.mu[0], b.sigma[0]}, b.all_equal[0] != 0),
+                 zscore(xs, Moments{b.mu[1], b.sigma[1]}, b.all_equal[1] != 0),
+                 zscore(xr, Moments{b.mu[2], b.sigma[2]}, b.all_equal[2] != 0), xs, xr);
+}
+
+/* ------------------------------------------------------------------ batch reductions */
+
+/* Deterministic sums: every thread adds its ROWS_PER_THREAD consecutive rows in
+ * index order, the block combines the threads in a fixed pairwise tree, and one
+ * block adds the block partials in block order. */
+constexpr int RED_THREADS = 256;
+constexpr int RED_TILE = RED_THREADS * ROWS_PER_THREAD;
+static_assert(RED_TILE == PLAN_TILE, "the reductions reuse the plan's tile count");
+
+template <class T, int K>
+__device__ __forceinline__ void block_tree_sum(T (&v)[K], T *lds /* [K][RED_THREADS] */)
+{
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int k = 0; k < K; ++k) lds[k * RED_THREADS + t] = v[k];
+    __syncthreads();
+    for (int stride = RED_THREADS / 2; stride > 0; stride >>= 1) {
+        if (t < stride) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) lds[k * RED_THREADS + t] += lds[k * RED_THREADS + t + stride];
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) v[k] = lds[k * RED_THREADS];
+    __syncthreads();
+}
+
+/* Sum of part[0 .. m) (each of K values) in index order by one block. */
+template <class T, int K>
+__device__ __forceinline__ void sum_partials(const T *part, int64_t m, T (&out)[K], T *lds)
+{
+    T v[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) v[k] = 0;
+    const int64_t per = (m + RED_THREADS - 1) / RED_THREADS;
+    const int64_t b0 = threadIdx.x * per, b1 = min(m, b0 + per);
+    for (int64_t b = b0; b < b1; ++b) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) v[k] += part[b * K + k];
+    }
+    block_tree_sum<T, K>(v, lds);
+#pragma unroll
+    for (int k = 0; k < K; ++k) out[k] = v[k];
+}
+
+struct StatsArgs {
+    const int32_t *total, *latency, *n_subtask, *n_trial;
+    const uint32_t *flags;
+    int64_t n;
+    double *dpart;    /* [tiles][3] */
+    int64_t *ipart;   /* [tiles][4]: not evaluated, latency differs, Subtask ratio differs, Trial ratio differs */
+    BatchStats *stats;
+};
+
+/* PASS 1: sums of the three statistics and the equality checks; PASS 2: sums
+ * of squared deviations from the batch means. */
+template <int PASS>
+__global__ void __launch_bounds__(RED_THREADS) batch_stats_tiles(StatsArgs a)
+{
+    __shared__ double dl[3 * RED_THREADS];
+    __shared__ int64_t il[4 * RED_THREADS];
+    const int64_t r0 = (int64_t)blockIdx.x * RED_TILE + (int64_t)threadIdx.x * ROWS_PER_THREAD;
+    double d[3] = {0.0, 0.0, 0.0};
+    int64_t c[4] = {0, 0, 0, 0};
+    const int64_t s0 = a.n_subtask[0], t0 = a.total[0] > 0 ? a.total[0] : 1, u0 = a.n_trial[0];
+    const int64_t n0s = a.total[0] > 0 ? s0 : 0, n0r = a.total[0] > 0 ? u0 : 0;
+    for (int j = 0; j < ROWS_PER_THREAD; ++j) {
+        const int64_t r = r0 + j;
+        if (r >= a.n) break;
+        const double x[3] = {(double)a.latency[r], ratio(a.n_subtask[r], a.total[r]), ratio(a.n_trial[r], a.total[r])};
+        if (PASS == 1) {
+#pragma unroll
+            for (int k = 0; k < 3; ++k) d[k] = __dadd_rn(d[k], x[k]);
+            const int64_t tr = a.total[r] > 0 ? a.total[r] : 1;
+            const int64_t ns = a.total[r] > 0 ? a.n_subtask[r] : 0, nr = a.total[r] > 0 ? a.n_trial[r] : 0;
+            c[0] += (a.flags[r] & NOT_EVALUATED) != 0;
+            c[1] += a.latency[r] != a.latency[0];
+            c[2] += ns * t0 != n0s * tr;
+            c[3] += nr * t0 != n0r * tr;
+        } else {
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                const double dv = __dsub_rn(x[k], a.stats->mu[k]);
+                d[k] = __dadd_rn(d[k], __dmul_rn(dv, dv));
+            }
+        }
+    }
+    block_tree_sum<double, 3>(d, dl);
+    if (PASS == 1) block_tree_sum<int64_t, 4>(c, il);
+    if (threadIdx.x == 0) {
+        for (int k = 0; k < 3; ++k) a.dpart[blockIdx.x * 3 + k] = d[k];
+        if (PASS == 1)
+            for (int k = 0; k < 4; ++k) a.ipart[blockIdx.x * 4 + k] = c[k];
+    }
+}
+
+template <int PASS>
+__global__ void __launch_bounds__(RED_THREADS) batch_stats_final(StatsArgs a, int64_t tiles)
+{
+    __shared__ double dl[3 * RED_THREADS];
+    __shared__ int64_t il[4 * RED_THREADS];
+    double d[3];
+    sum_partials<double, 3>(a.dpart, tiles, d, dl);
+    if (PASS == 1) {
+        int64_t c[4];
+        sum_partials<int64_t, 4>(a.ipart, tiles, c, il);
+        if (threadIdx.x == 0) {
+            for (int k = 0; k < 3; ++k) a.stats->mu[k] = __ddiv_rn(d[k], (double)a.n);
+            a.stats->not_evaluated = c[0] != 0;
+            for (int k = 0; k < 3; ++k) a.stats->all_equal[k] = c[k + 1] == 0;
+        }
+    } else if (threadIdx.x == 0) {
+        for (int k = 0; k < 3; ++k) a.stats->sigma[k] = __dsqrt_rn(__ddiv_rn(d[k], (double)a.n));
+    }
+}
+
+struct MetricsArgs {
+    const int32_t *total, *latency, *n_subtask, *n_trial;
+    const uint32_t *flags;
+    const uint8_t *correct;
+    const float *reward;
+    int64_t n;
+    int64_t *ipart; /* [tiles][9] */
+    double *dpart;  /* [tiles][1] */
+    double *metrics;
+};
+
+constexpr int NMI = 9; /* valid, triggered, correct, truncated, mismatch, sum total, latency, Subtask, Trial */
+
+__global__ void __launch_bounds__(RED_THREADS) metrics_tiles(MetricsArgs a)
+{
+    __shared__ int64_t il[NMI * RED_THREADS];
+    __shared__ double dl[RED_THREADS];
+    const int64_t r0 = (int64_t)blockIdx.x * RED_TILE + (int64_t)threadIdx.x * ROWS_PER_THREAD;
+    int64_t c[NMI];
+#pragma unroll
+    for (int k = 0; k < NMI; ++k) c[k] = 0;
+    double d[1] = {0.0};
+    for (int j = 0; j < ROWS_PER_THREAD; ++j) {
+        const int64_t r = r0 + j;
+        if (r >= a.n) break;
+        const uint32_t f = a.flags[r];
+        c[0] += (f & PARASON_FLAG_VALID) != 0;
+        c[1] += (f & PARASON_FLAG_TRIGGERED) != 0;
+        c[2] += a.correct[r] != 0;
+        c[3] += (f & PARASON_FLAG_TRUNCATED) != 0;
+        c[4] += (f & PARASON_FLAG_COUNT_MISMATCH) != 0;
+        c[5] += a.total[r];
+        c[6] += a.latency[r];
+        c[7] += a.n_subtask[r];
+        c[8] += a.n_trial[r];
+        d[0] = __dadd_rn(d[0], (double)a.reward[r]);
+    }
+    block_tree_sum<int64_t, NMI>(c, il);
+    block_tree_sum<double, 1>(d, dl);
+    if (threadIdx.x == 0) {
+        for (int k = 0; k < NMI; ++k) a.ipart[blockIdx.x * NMI + k] = c[k];
+        a.dpart[blockIdx.x] = d[0];
+    }
+}
+
+__global__ void __launch_bounds__(RED_THREADS) metrics_final(MetricsArgs a, int64_t tiles)
+{
+    __shared__ int64_t il[NMI * RED_THREADS];
+    __shared__ double dl[RED_THREADS];
+    int64_t c[NMI];
+    double d[1];
+    sum_partials<int64_t, NMI>(a.ipart, tiles, c, il);
+    sum_partials<double, 1>(a.dpart, tiles, d, dl);
+    if (threadIdx.x != 0) return;
+    double *m = a.metrics;
+    const double n = (double)a.n;
+    const int64_t st = c[5], sl = c[6];
+    for (int k = 0; k < PARASON_METRIC_COUNT; ++k) m[k] = 0.0;
+    m[PARASON_METRIC_ROWS] = n;
+    m[PARASON_METRIC_VALID] = (double)c[0];
+    m[PARASON_METRIC_TRIGGERED] = (double)c[1];
+    m[PARASON_METRIC_CORRECT] = (double)c[2];
+    m[PARASON_METRIC_TRUNCATED] = (double)c[3];
+    m[PARASON_METRIC_COUNT_MISMATCH] = (double)c[4];
+    m[PARASON_METRIC_SUM_TOTAL] = (double)st;
+    m[PARASON_METRIC_SUM_LATENCY] = (double)sl;
+    m[PARASON_METRIC_SUM_SUBTASK] = (double)c[7];
+    m[PARASON_METRIC_SUM_TRIAL] = (double)c[8];
+    if (a.n > 0) {
+        m[PARASON_METRIC_TRIGGER_RATIO] = __ddiv_rn((double)c[1], n);
+        m[PARASON_METRIC_MEAN_LATENCY] = __ddiv_rn((double)sl, n);
+        m[PARASON_METRIC_MEAN_TOTAL] = __ddiv_rn((double)st, n);
+        m[PARASON_METRIC_MEAN_SAVED] = __ddiv_rn((double)(st - sl), n);
+        m[PARASON_METRIC_ACCURACY] = __ddiv_rn((double)c[2], n);
+        m[PARASON_METRIC_MEAN_REWARD] = __ddiv_rn(d[0], n);
+    }
+    if (sl > 0) m[PARASON_METRIC_ACCELERATION] = __ddiv_rn((double)st, (double)sl);
+    if (st > 0) {
+        m[PARASON_METRIC_SUBTASK_SHARE] = __ddiv_rn((double)c[7], (double)st);
+        m[PARASON_METRIC_TRIAL_SHARE] = __ddiv_rn((double)c[8], (double)st);
     }
 }
 

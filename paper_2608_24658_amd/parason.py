@@ -25,6 +25,14 @@ FLAG_WS_OVERFLOW = 1 << 9
 FLAG_BAD_ROW = 1 << 10
 
 CFG_INVALID_KEEPS_CORRECTNESS = 1 << 0
+CFG_BATCH_STATS = 1 << 1
+
+METRICS = (
+    "rows", "valid", "triggered", "correct", "truncated", "count_mismatch",
+    "sum_total", "sum_latency", "sum_subtask", "sum_trial",
+    "trigger_ratio", "acceleration", "mean_latency", "mean_total", "mean_saved",
+    "subtask_share", "trial_share", "accuracy", "mean_reward",
+)
 
 MAX_DEPTH = 1 << 20
 MAX_OPEN_ENTRIES = 1 << 24
@@ -60,11 +68,13 @@ class Outputs(ctypes.Structure):
         ("r_subtask", ctypes.c_void_p),
         ("r_trial", ctypes.c_void_p),
         ("eta", ctypes.c_void_p),
+        ("metrics", ctypes.c_void_p),
     ]
 
 
 INT_FIELDS = ("total", "latency", "n_subtask", "n_trial", "n_blocks", "max_depth", "first_error_pos")
 FLOAT_FIELDS = ("reward", "r_subtask", "r_trial", "eta")
+OPTIONAL_FIELDS = ("r_subtask", "r_trial", "eta", "metrics")
 
 _lib = None
 
@@ -154,7 +164,7 @@ class Parason:
             raise ParasonError(rc, "parason_workspace_size")
         return b.value
 
-    def alloc_outputs(self, n_traj: int, device, derived: bool = True) -> dict:
+    def alloc_outputs(self, n_traj: int, device, derived: bool = True, metrics: bool = False) -> dict:
         import torch
 
         out = {k: torch.empty(n_traj, dtype=torch.int32, device=device) for k in INT_FIELDS}
@@ -163,6 +173,8 @@ class Parason:
         if derived:
             for k in ("r_subtask", "r_trial", "eta"):
                 out[k] = torch.empty(n_traj, dtype=torch.float32, device=device)
+        if metrics:
+            out["metrics"] = torch.empty(len(METRICS), dtype=torch.float64, device=device)
         return out
 
     def alloc_workspace(self, n_traj: int, total_tokens: int, device):
@@ -176,7 +188,7 @@ class Parason:
         o = Outputs()
         for k in INT_FIELDS + ("flags", "reward"):
             setattr(o, k, out[k].data_ptr())
-        for k in ("r_subtask", "r_trial", "eta"):
+        for k in OPTIONAL_FIELDS:
             setattr(o, k, out[k].data_ptr() if k in out and out[k] is not None else None)
         return lib().parason_run(self._h, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, int(n_traj),
                                  ctypes.byref(o), ws_ptr, int(ws_bytes), stream)
@@ -187,14 +199,14 @@ class Parason:
         o = Outputs()
         for k in INT_FIELDS + ("flags", "reward"):
             setattr(o, k, out[k].data_ptr())
-        for k in ("r_subtask", "r_trial", "eta"):
+        for k in OPTIONAL_FIELDS:
             setattr(o, k, out[k].data_ptr() if k in out and out[k] is not None else None)
         ev = ctypes.cast(scan_events, ctypes.c_void_p) if scan_events is not None else None
         return lib().parason_run_timed(self._h, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, int(n_traj),
                                        ctypes.byref(o), ws_ptr, int(ws_bytes), stream, ev)
 
     def run(self, tokens, starts, lengths, correct, out: dict | None = None, workspace=None, total_tokens=None,
-            derived: bool = True) -> dict:
+            derived: bool = True, metrics: bool = False) -> dict:
         """Evaluate a batch of rows held in device tensors (asynchronous on the
         current stream).  tokens int32, starts int64, lengths int32, correct uint8."""
         import torch
@@ -206,7 +218,7 @@ class Parason:
         if lengths.numel() != n or correct.numel() != n:
             raise ValueError("starts, lengths and correct must have the same length")
         if out is None:
-            out = self.alloc_outputs(n, tokens.device, derived)
+            out = self.alloc_outputs(n, tokens.device, derived, metrics)
         if workspace is None:
             if total_tokens is None:
                 total_tokens = int(lengths.to(torch.int64).clamp_min(0).sum().item()) if n else 0

@@ -1,0 +1,121 @@
+"""GPU parity of the batch metrics (Tables 2, 4 and 5 definitions) and of the
+batch-wide normalisation mode, against the CPU oracle.
+
+Tolerances: counts and token sums are exact; ratios and means of token counts
+are one double division of exact integers on both sides, so they must agree
+to 1e-15 relative.  The mean reward is taken over the stored float rewards on
+the GPU and over the oracle's double rewards, so it agrees to the float reward
+bound (2^-23 relative).  Batch-wide mu and sigma are summed in a different
+(fixed) order on the GPU than in the oracle's sequential loop; the resulting
+rewards are checked with the usual float bound."""
+import numpy as np
+import pytest
+
+from gpu_util import DEFAULT_COEF, compare, fetch, log, oracle_expect, run_gpu, to_dev
+from oracle import oracle as O
+from paper_2608_24658_amd import parason as PX
+from paper_2608_24658_amd.synth import synth as S
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+G = S.GROUP_SIZE
+TAGS = S.CONTIGUOUS_TAGS
+EXACT = ("rows", "valid", "triggered", "correct", "truncated", "count_mismatch", "sum_total", "sum_latency",
+         "sum_subtask", "sum_trial")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def check_metrics(got_m, rows, correct, R):
+    exp = O.batch_metrics(rows, correct, R)
+    for i, name in enumerate(PX.METRICS):
+        g, e = float(got_m[i]), exp[name]
+        if name in EXACT:
+            assert g == e, (name, g, e)
+        elif name == "mean_reward":
+            assert abs(g - e) <= 2.0 ** -23 * max(1.0, np.mean(np.maximum(1.0, np.abs(R)))), (name, g, e)
+        else:
+            assert abs(g - e) <= 1e-15 * max(1.0, abs(e)), (name, g, e)
+    return exp
+
+
+@pytest.mark.parametrize("workload", ["small", "ragged", "typical"])
+def test_metrics_parity(dev, workload):
+    log("case metrics %s" % workload)
+    P = S.make_params(workload)
+    n = S.n_rows_of(workload)
+    tok_h, st_h, ln_h, co_h = S.host_batch(P, n)
+    px = PX.Parason(TAGS, group_size=G, **DEFAULT_COEF)
+    out = px.run(to_dev(tok_h, torch.int32, dev), to_dev(st_h, torch.int64, dev), to_dev(ln_h, torch.int32, dev),
+                 to_dev(co_h, torch.uint8, dev), metrics=True)
+    torch.cuda.synchronize()
+    got = fetch(out)
+    rows, R, rs, rt, eta = oracle_expect(tok_h, st_h, ln_h, co_h, TAGS, G, DEFAULT_COEF)
+    compare(got, rows, R, rs, rt, eta, what=workload)
+    exp = check_metrics(got["metrics"], rows, co_h, R)
+    log("%s: trigger %.3f acceleration %.3f mean latency %.0f" % (
+        workload, exp["trigger_ratio"], exp["acceleration"], exp["mean_latency"]))
+
+
+@pytest.mark.parametrize("workload", ["tiny", "small", "ragged", "typical"])
+def test_batch_stats_parity(dev, workload):
+    log("case batch stats %s" % workload)
+    P = S.make_params(workload)
+    n = S.n_rows_of(workload)
+    tok_h, st_h, ln_h, co_h = S.host_batch(P, n)
+    coef = dict(alpha=0.1, beta_subtask=0.05, beta_trial=0.1, rho=0.5, rho_clip=0.25)
+    px = PX.Parason(TAGS, group_size=G, flags=PX.CFG_BATCH_STATS, **coef)
+    out = px.run(to_dev(tok_h, torch.int32, dev), to_dev(st_h, torch.int64, dev), to_dev(ln_h, torch.int32, dev),
+                 to_dev(co_h, torch.uint8, dev), metrics=True)
+    torch.cuda.synchronize()
+    got = fetch(out)
+    rows, R, rs, rt, eta = oracle_expect(tok_h, st_h, ln_h, co_h, TAGS, G, coef, O.CFG_BATCH_STATS)
+    compare(got, rows, R, rs, rt, eta, what="batch " + workload)
+    check_metrics(got["metrics"], rows, co_h, R)
+
+
+def test_batch_stats_constant_batch_and_not_evaluated(dev):
+    log("case batch stats edge")
+    # every row identical: sigma = 0 exactly, z = 0
+    one = np.array([TAGS[0]] + [5] * 40 + [TAGS[1]], np.int32)
+    n = 16
+    toks = np.tile(one, n)
+    lens = np.full(n, one.size, np.int32)
+    starts = (np.arange(n) * one.size).astype(np.int64)
+    co = np.ones(n, np.uint8)
+    px = PX.Parason(TAGS, group_size=G, flags=PX.CFG_BATCH_STATS, **DEFAULT_COEF)
+    got = run_gpu(px, to_dev(toks, torch.int32, dev), to_dev(starts, torch.int64, dev), to_dev(lens, torch.int32, dev),
+                  to_dev(co, torch.uint8, dev))
+    assert np.all(got["reward"] == 1.0)  # 1 + 2 min(rho * 0, clip)
+    # a row that is not evaluated makes the whole batch NaN
+    lens_bad = lens.copy()
+    lens_bad[3] = -1
+    got = run_gpu(px, to_dev(toks, torch.int32, dev), to_dev(starts, torch.int64, dev),
+                  to_dev(lens_bad, torch.int32, dev), to_dev(co, torch.uint8, dev))
+    assert got["flags"][3] == PX.FLAG_BAD_ROW and np.all(np.isnan(got["reward"]))
+
+
+def test_metrics_on_large_workload_properties(dev):
+    """Metrics of the 143 GB workload equal sums over the fetched per-row outputs."""
+    log("case metrics large")
+    P = S.make_params("large")
+    n = S.n_rows_of("large")
+    tok_d, st_d, ln_d, co_d = S.device_batch(P, n, device=dev)
+    px = PX.Parason(TAGS, group_size=G, **DEFAULT_COEF)
+    out = px.run(tok_d, st_d, ln_d, co_d, metrics=True, total_tokens=int(tok_d.numel()))
+    torch.cuda.synchronize()
+    got = fetch(out)
+    rows = np.zeros(n, dtype=O.ROW_DTYPE)
+    for k in PX.INT_FIELDS:
+        rows[k] = got[k]
+    rows["flags"] = got["flags"]
+    check_metrics(got["metrics"], rows, co_d.cpu().numpy(), got["reward"].astype(np.float64))
+    assert got["metrics"][PX.METRICS.index("sum_total")] == tok_d.numel()
+    del tok_d, out
+    torch.cuda.empty_cache()

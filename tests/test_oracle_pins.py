@@ -415,3 +415,58 @@ def test_group_size_must_divide():
     rows = _rows([1] * 6, [1] * 6, [0] * 6, [0] * 6)
     with pytest.raises(ValueError):
         O.group_reward(rows, np.ones(6), 4, 0, 0, 0, 0, 0)
+
+
+# --------------------------------------------------------------------------- batch metrics
+
+
+def test_batch_metrics_table5_and_table4_definitions():
+    """Batch metrics on rows that realise Table 5's averages: acceleration =
+    generated / latency tokens and saved = generated - latency as printed."""
+    g = json.load(open(os.path.join(GOLDEN, "table5_identities.json")))
+    for row in g["rows"]:
+        gen, lat_t = row["generated"], row["latency"]
+        saved = gen - lat_t
+        body = saved - 2
+        s = single_block(gen - (2 + 1 + (2 + 3 + 3) + 1 + 2 * saved), 0, [1, 1], [body, body])
+        one = np.array(G.to_tokens(s, TAGS), np.int32)
+        n = 6  # a few identical rows plus two sequential rows
+        seq = np.array(G.to_tokens([G.THINK] + [G.TEXT] * 98 + [G.END_THINK], TAGS), np.int32)
+        toks = np.concatenate([one] * n + [seq, seq])
+        lens = np.array([one.size] * n + [seq.size] * 2, np.int32)
+        starts = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+        rows = O.eval_rows(toks, starts, lens, TAGS)
+        correct = np.array([1, 0, 1, 1, 0, 1, 1, 0], np.uint8)
+        R, *_ = O.group_reward(rows, correct, 8, 0.1, 0.0, 0.1, 0.5, 0.25)
+        m = O.batch_metrics(rows, correct, R)
+        assert m["rows"] == 8 and m["valid"] == 8 and m["triggered"] == 6 and m["correct"] == 5
+        assert m["trigger_ratio"] == 6 / 8
+        assert m["sum_total"] == n * gen + 200 and m["sum_latency"] == n * lat_t + 200
+        assert m["acceleration"] == (n * gen + 200) / (n * lat_t + 200)
+        assert m["mean_saved"] == n * saved / 8
+        assert m["accuracy"] == 5 / 8
+        assert abs(m["mean_reward"] - R.mean()) < 1e-15
+        # the identical rows alone reproduce the printed ratio and saved tokens
+        m6 = O.batch_metrics(rows[:n], correct[:n], R[:n])
+        assert round(m6["acceleration"], 2) == row["acceleration"] and m6["mean_saved"] == row["saved"]
+        assert m6["trial_share"] == 2 * saved / gen and m6["subtask_share"] == 0
+
+
+def test_batch_stats_is_one_group_over_the_batch():
+    rng = np.random.default_rng(3)
+    n = 40
+    rows = np.zeros(n, dtype=O.ROW_DTYPE)
+    rows["total"] = rng.integers(10, 1000, n)
+    rows["latency"] = [rng.integers(1, t + 1) for t in rows["total"]]
+    rows["n_subtask"] = [rng.integers(0, t // 2) for t in rows["total"]]
+    rows["n_trial"] = [rng.integers(0, t // 2) for t in rows["total"]]
+    rows["flags"] = O.F_VALID
+    ones = np.ones(n)
+    a = O.group_reward(rows, ones, 8, 0.2, 0.1, 0.05, 0.5, 0.25, O.CFG_BATCH_STATS)
+    b = O.group_reward(rows, ones, n, 0.2, 0.1, 0.05, 0.5, 0.25)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+    # z over the batch: alpha = 1 isolates z_T; it matches numpy over all rows
+    R, *_ = O.group_reward(rows, ones, 8, 1.0, 0.0, 0.0, 0.0, 0.0, O.CFG_BATCH_STATS)
+    x = rows["latency"].astype(np.float64)
+    np.testing.assert_allclose((1 - R) / 2, (x - x.mean()) / x.std(), rtol=1e-12, atol=1e-12)
