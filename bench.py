@@ -111,6 +111,8 @@ def main():
     ap.add_argument("--workload", default="large", choices=["tiny", "small", "typical", "large", "ragged"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--step", default="accounting", choices=["accounting", "pg"],
+                    help="accounting: the hot path (default); pg: the policy-gradient step that consumes its rewards")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device-to-device copy of 4 GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -136,6 +138,9 @@ def main():
 
     from paper_2608_24658_amd import parason as PX
     from paper_2608_24658_amd.synth import synth as S
+
+    if args.step == "pg":
+        return bench_pg(args)
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
@@ -239,6 +244,72 @@ def main():
         log("timing the CPU oracle on a sample")
         res["cpu_baseline"] = cpu_baseline(tokens, starts.cpu().numpy(), lengths.cpu().numpy(),
                                            correct.cpu().numpy(), S.CONTIGUOUS_TAGS, coef, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+def bench_pg(args):
+    """The policy-gradient step (advantages + clipped surrogate + gradient) over
+    the first half of the large workload's rows: logp, logp_old and the
+    gradient for all of its 1.8e10 tokens take 215 GB."""
+    import numpy as np
+    import torch
+
+    from paper_2608_24658_amd import parason as PX
+    from paper_2608_24658_amd.synth import synth as S
+
+    dev = torch.device("cuda:0")
+    G = S.GROUP_SIZE
+    P = S.make_params(args.workload)
+    n_all = S.n_rows_of(args.workload)
+    n = n_all // 2 // G * G if args.workload == "large" else n_all
+    lengths_h, _ = S.host_rows(P, n)
+    starts_h = np.zeros(n, np.int64)
+    starts_h[1:] = np.cumsum(lengths_h[:-1].astype(np.int64))
+    N = int(lengths_h.astype(np.int64).sum())
+    log("pg: %d rows, %d tokens (%.1f GB of logp + logp_old + grad)" % (n, N, 12 * N / 1e9))
+    old, new = S.device_logp(P, N, device=dev)
+    rng = np.random.default_rng(0)
+    reward = torch.as_tensor(rng.choice([-1.0, 1.0, 1.25, 0.8], n).astype(np.float32)).to(dev)
+    starts = torch.as_tensor(starts_h).to(dev)
+    lengths = torch.as_tensor(lengths_h).to(dev)
+    grad = torch.empty_like(new)
+    ws = torch.empty(PX.pg_workspace_size(n), dtype=torch.uint8, device=dev)
+    for _ in range(args.warmup):
+        out = PX.pg_run(reward, new, old, starts, lengths, G, 0.2, 0.28, grad=grad, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        out = PX.pg_run(reward, new, old, starts, lengths, G, 0.2, 0.28, grad=grad, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ev_ms = e0.elapsed_time(e1) / args.steps
+    st = out["stats"].cpu().numpy()
+    alg = 12.0 * N + 20.0 * n
+    res = {
+        "metric": "policy-gradient step throughput (tokens/s) + achieved % of HBM roofline, 1×MI355X",
+        "value": N / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp32",
+        "data": "synthetic (seeded log-probabilities; no model)",
+        "config": {"workload": "%s, first %d rows: %d tokens" % (args.workload, n, N), "rows": n, "tokens": N,
+                   "group_size": G, "clip": [0.2, 0.28]},
+        "loss": float(st[0]),
+        "clipped": [int(st[2]), int(st[3])],
+        "roofline": {"kernel": "pg_run (all launches, HIP events)", "bound": "hbm",
+                     "achieved": alg / (ev_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": alg / (ev_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "traffic": None, "kernel_ms": ev_ms,
+                     "algorithmic_bytes": alg},
+    }
     print(json.dumps(res), flush=True)
 
 

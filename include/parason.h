@@ -187,6 +187,48 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
 
 void parason_destroy(parason_handle *h);
 
+/* ---- policy-gradient step ------------------------------------------------
+ * The update that consumes the rewards in PA-GRPO (Sec. 4 "Training
+ * Framework": GRPO with 8 rollouts per prompt, lower clip ratio 0.2, upper
+ * clip ratio 0.28).  The paper does not write the objective out; this is the
+ * standard one:
+ *   A_i   = (R_i - mean_g R) / std_g R over the G rollouts of a prompt
+ *           (population std; A_i = 0 when all G rewards are equal);
+ *   rho_t = exp(logp_t - logp_old_t);
+ *   J     = (1 / N) sum_t min(rho_t A, clip(rho_t, 1 - eps_low, 1 + eps_high) A)
+ *           over all N generated tokens of the batch (token-level mean);
+ *   loss  = -J, and grad_t = d loss / d logp_t.
+ * The clip decision compares the float log-ratio d = logp - logp_old with the
+ * float thresholds ln(1 - eps_low) and ln(1 + eps_high) (rho > 1 + eps_high
+ * exactly when d > ln(1 + eps_high)); values are float, the sum is double. */
+#define PARASON_PG_STAT_LOSS 0
+#define PARASON_PG_STAT_TOKENS 1
+#define PARASON_PG_STAT_CLIP_HIGH 2 /* tokens with A > 0 held at 1 + eps_high */
+#define PARASON_PG_STAT_CLIP_LOW 3  /* tokens with A < 0 held at 1 - eps_low */
+#define PARASON_PG_STAT_COUNT 4
+
+typedef struct parason_pg_config {
+    int32_t group_size;         /* G, as for parason_run */
+    double clip_low, clip_high; /* eps_low (0.2), eps_high (0.28); 0 <= eps_low < 1, eps_high >= 0 */
+} parason_pg_config;
+
+/* Bytes of device workspace parason_pg_run needs for n_traj rows. */
+int parason_pg_workspace_size(int64_t n_traj, size_t *bytes);
+
+/* One policy-gradient step, asynchronously on `stream`.  Device pointers:
+ *   reward     float[n_traj] (the rewards of parason_run)
+ *   logp, logp_old  float log-probabilities of the generated tokens; row i is
+ *              [starts[i], starts[i] + lengths[i]) as for parason_run; the
+ *              three float arrays must share their position modulo 16 bytes
+ *   advantage  float[n_traj] out: A_i
+ *   grad       float out, same layout as logp: d loss / d logp on every row
+ *              position (other positions are not written)
+ *   stats      double[PARASON_PG_STAT_COUNT] out
+ * Returns a negative status on host-side argument errors, before any launch. */
+int parason_pg_run(const parason_pg_config *cfg, const float *reward, const float *logp, const float *logp_old,
+                   const int64_t *starts, const int32_t *lengths, int64_t n_traj, float *advantage, float *grad,
+                   double *stats, void *workspace, size_t workspace_bytes, void *stream);
+
 /* Static description of a status code. */
 const char *parason_strerror(int status);
 

@@ -1,0 +1,98 @@
+"""CPU oracle of the GRPO advantage and token-level clipped surrogate.
+
+TEST INFRASTRUCTURE.  Only the tests and the smoke check may import this
+module; the product path never does.  Plain numpy in float64.
+
+The paper trains with GRPO in VeRL using "lower clip ratio 0.2, and upper clip
+ratio 0.28" and 8 rollouts per prompt (Sec. 4, "Training Framework"); it does
+not write the objective out.  This oracle therefore follows the textbook
+definitions, each a reading listed in the design notes:
+
+* advantage of rollout i (GRPO, Shao et al. 2024, outcome supervision): the
+  reward normalised within its group of G rollouts,
+  A_i = (R_i - mean_g R) / std_g R, population standard deviation, A_i = 0 when
+  every reward of the group is equal (no epsilon);
+* ratio rho_t = exp(logp_t - logp_old_t) per generated token;
+* clipped objective with separate lower and upper clip ratios (PPO clip with
+  DAPO's "clip-higher", Yu et al. 2025):
+  L_t = min(rho_t A, clip(rho_t, 1 - eps_low, 1 + eps_high) A);
+* token-level mean over every generated token of the batch:
+  J = sum_t L_t / N_tokens; the loss is -J; no KL or entropy term.
+
+The clip decision is taken on the float32 log-ratio d = logp - logp_old
+(computed in float32, as the kernel does) against the float32 thresholds
+ln(1 + eps_high) and ln(1 - eps_low): rho > 1 + eps_high exactly when
+d > ln(1 + eps_high).  Values (rho, L, gradient) are evaluated in float64.
+
+Gradient of the loss with respect to logp_t:
+  d(-J)/d logp_t = -A rho_t / N_tokens where the unclipped term is the minimum
+  (A > 0 and d <= thr_high, or A < 0 and d >= thr_low), else 0.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def thresholds(eps_low: float, eps_high: float):
+    """float32 ln(1 - eps_low), ln(1 + eps_high)."""
+    return np.float32(np.log1p(-np.float64(eps_low))), np.float32(np.log1p(np.float64(eps_high)))
+
+
+def advantages(reward, group_size: int) -> np.ndarray:
+    """Group-normalised advantages (float64) of float rewards."""
+    r = np.asarray(reward, dtype=np.float32).astype(np.float64)
+    n = r.size
+    assert n % group_size == 0
+    out = np.zeros(n, np.float64)
+    for g0 in range(0, n, group_size):
+        x = r[g0: g0 + group_size]
+        if np.all(x == x[0]):
+            continue  # sigma = 0: A = 0
+        mu = 0.0
+        for v in x:
+            mu = mu + v
+        mu = mu / group_size
+        ss = 0.0
+        for v in x:
+            ss = ss + (v - mu) * (v - mu)
+        sigma = np.sqrt(ss / group_size)
+        out[g0: g0 + group_size] = (x - mu) / sigma
+    return out
+
+
+def surrogate(logp, logp_old, starts, lengths, adv, eps_low: float, eps_high: float):
+    """Loss, gradient and clip counts.
+
+    logp, logp_old: float32 arrays; row i is [starts[i], starts[i] + lengths[i]).
+    adv: advantage per row (the kernel stores it as float32, so pass that).
+    Returns dict(loss, tokens, clip_high, clip_low, grad) where grad is float64
+    with NaN outside the rows."""
+    logp = np.asarray(logp, np.float32)
+    logp_old = np.asarray(logp_old, np.float32)
+    thr_low, thr_high = thresholds(eps_low, eps_high)
+    grad = np.full(logp.size, np.nan)
+    n_tok = int(np.sum(np.maximum(lengths, 0)))
+    total = 0.0
+    clip_hi = clip_lo = 0
+    for i in range(len(starts)):
+        a = float(np.float32(adv[i]))
+        s, n = int(starts[i]), int(lengths[i])
+        if n <= 0:
+            continue
+        d32 = (logp[s: s + n] - logp_old[s: s + n]).astype(np.float32)  # float32 subtraction
+        rho = np.exp(d32.astype(np.float64))
+        if a > 0:
+            unclipped = d32 <= thr_high
+            clip_hi += int(np.sum(~unclipped))
+        elif a < 0:
+            unclipped = d32 >= thr_low
+            clip_lo += int(np.sum(~unclipped))
+        else:
+            unclipped = np.ones(n, bool)
+        # min(rho A, clip(rho) A): the unclipped term where the decision says
+        # so, else the bound the clip holds rho at
+        L = np.where(unclipped, rho * a, np.where(a > 0, (1.0 + eps_high) * a, (1.0 - eps_low) * a))
+        total += float(np.sum(L))
+        grad[s: s + n] = np.where(unclipped, -a * rho / n_tok, 0.0) if n_tok else 0.0
+    loss = -total / n_tok if n_tok else 0.0
+    return dict(loss=loss, tokens=n_tok, clip_high=clip_hi, clip_low=clip_lo, grad=grad)

@@ -31,7 +31,8 @@ LIBS = {
     "parason": dict(
         out=os.path.join(PKG, "libparason.so"),
         srcs=[os.path.join(PKG, "csrc", "parason.hip")],
-        deps=[os.path.join(PKG, "csrc", "parason_kernels.h"), os.path.join(INCLUDE, "parason.h")],
+        deps=[os.path.join(PKG, "csrc", "parason_kernels.h"), os.path.join(PKG, "csrc", "pg_kernels.h"),
+              os.path.join(INCLUDE, "parason.h")],
         kind="hip",
     ),
     "synth": dict(

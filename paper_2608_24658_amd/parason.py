@@ -38,7 +38,9 @@ MAX_DEPTH = 1 << 20
 MAX_OPEN_ENTRIES = 1 << 24
 
 EXPORTED = ("parason_create", "parason_workspace_size", "parason_run", "parason_run_timed", "parason_destroy",
-            "parason_strerror")
+            "parason_strerror", "parason_pg_workspace_size", "parason_pg_run")
+
+PG_STATS = ("loss", "tokens", "clip_high", "clip_low")
 
 
 class Config(ctypes.Structure):
@@ -52,6 +54,10 @@ class Config(ctypes.Structure):
         ("rho_clip", ctypes.c_double),
         ("flags", ctypes.c_uint32),
     ]
+
+
+class PgConfig(ctypes.Structure):
+    _fields_ = [("group_size", ctypes.c_int32), ("clip_low", ctypes.c_double), ("clip_high", ctypes.c_double)]
 
 
 class Outputs(ctypes.Structure):
@@ -105,6 +111,14 @@ def lib():
         L.parason_run_timed.argtypes = L.parason_run.argtypes + [ctypes.c_void_p]
         L.parason_destroy.restype = None
         L.parason_destroy.argtypes = [ctypes.c_void_p]
+        L.parason_pg_workspace_size.restype = ctypes.c_int
+        L.parason_pg_workspace_size.argtypes = [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]
+        L.parason_pg_run.restype = ctypes.c_int
+        L.parason_pg_run.argtypes = [
+            ctypes.POINTER(PgConfig), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_size_t, ctypes.c_void_p,
+        ]
         L.parason_strerror.restype = ctypes.c_char_p
         L.parason_strerror.argtypes = [ctypes.c_int]
         _lib = L
@@ -230,3 +244,46 @@ class Parason:
         if rc != OK:
             raise ParasonError(rc, "parason_run")
         return out
+
+
+def pg_workspace_size(n_traj: int) -> int:
+    b = ctypes.c_size_t()
+    rc = lib().parason_pg_workspace_size(int(n_traj), ctypes.byref(b))
+    if rc != OK:
+        raise ParasonError(rc, "parason_pg_workspace_size")
+    return b.value
+
+
+def pg_run_raw(cfg: PgConfig, reward_ptr, logp_ptr, old_ptr, starts_ptr, lengths_ptr, n_traj, adv_ptr, grad_ptr,
+               stats_ptr, ws_ptr, ws_bytes, stream) -> int:
+    return lib().parason_pg_run(ctypes.byref(cfg), reward_ptr, logp_ptr, old_ptr, starts_ptr, lengths_ptr,
+                                int(n_traj), adv_ptr, grad_ptr, stats_ptr, ws_ptr, int(ws_bytes), stream)
+
+
+def pg_run(reward, logp, logp_old, starts, lengths, group_size=8, clip_low=0.2, clip_high=0.28, grad=None,
+           workspace=None) -> dict:
+    """Advantages, gradient d loss / d logp and the step statistics (device
+    tensors; asynchronous on the current stream).  reward float32[n], logp and
+    logp_old float32 in the row layout of starts/lengths."""
+    import torch
+
+    n = int(starts.numel())
+    for t, dt in ((reward, torch.float32), (logp, torch.float32), (logp_old, torch.float32),
+                  (starts, torch.int64), (lengths, torch.int32)):
+        if t.dtype != dt or not t.is_cuda or not t.is_contiguous():
+            raise TypeError("expected contiguous %s device tensors" % dt)
+    dev = logp.device
+    cfg = PgConfig(int(group_size), float(clip_low), float(clip_high))
+    adv = torch.empty(n, dtype=torch.float32, device=dev)
+    if grad is None:
+        grad = torch.empty_like(logp)
+    stats = torch.empty(len(PG_STATS), dtype=torch.float64, device=dev)
+    if workspace is None:
+        workspace = torch.empty(pg_workspace_size(n), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    rc = pg_run_raw(cfg, reward.data_ptr(), logp.data_ptr(), logp_old.data_ptr(), starts.data_ptr(),
+                    lengths.data_ptr(), n, adv.data_ptr(), grad.data_ptr(), stats.data_ptr(), workspace.data_ptr(),
+                    workspace.numel(), stream)
+    if rc != OK:
+        raise ParasonError(rc, "parason_pg_run")
+    return dict(advantage=adv, grad=grad, stats=stats)

@@ -142,6 +142,8 @@ def host_lib():
         L.synth_rows_host.argtypes = [ctypes.POINTER(SynthParams), ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
         L.synth_row_tokens_host.restype = ctypes.c_int64
         L.synth_row_tokens_host.argtypes = [ctypes.POINTER(SynthParams), ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int64]
+        L.synth_logp_host.restype = ctypes.c_int
+        L.synth_logp_host.argtypes = [ctypes.POINTER(SynthParams), ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
         _host = L
     return _host
 
@@ -152,11 +154,12 @@ def dev_lib():
         if not os.path.exists(DEV_LIB):
             raise RuntimeError("generator device library not built: run __graft_entry__.build()")
         L = ctypes.CDLL(DEV_LIB)
-        for f in ("synth_rows_device", "synth_text_device", "synth_tags_device"):
+        for f in ("synth_rows_device", "synth_text_device", "synth_tags_device", "synth_logp_device"):
             getattr(L, f).restype = ctypes.c_int
         L.synth_rows_device.argtypes = [ctypes.POINTER(SynthParams), ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         L.synth_text_device.argtypes = [ctypes.POINTER(SynthParams), ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
         L.synth_tags_device.argtypes = [ctypes.POINTER(SynthParams), ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        L.synth_logp_device.argtypes = [ctypes.POINTER(SynthParams), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
         _dev = L
     return _dev
 
@@ -218,3 +221,25 @@ def device_batch(P: SynthParams, n_rows: int, device="cuda", pad: int = 0):
         rc = L.synth_tags_device(ctypes.byref(P), 0, n_rows, starts.data_ptr(), tokens.data_ptr(), stream)
         assert rc == 0, rc
     return tokens, starts, lengths, correct
+
+
+def host_logp(P: SynthParams, p0: int, n: int):
+    """(logp_old, logp) float32 for flat positions [p0, p0 + n) (host mirror)."""
+    old = np.zeros(max(n, 1), np.float32)
+    new = np.zeros(max(n, 1), np.float32)
+    rc = host_lib().synth_logp_host(ctypes.byref(P), p0, n, old.ctypes.data, new.ctypes.data)
+    assert rc == 0
+    return old[:n], new[:n]
+
+
+def device_logp(P: SynthParams, n: int, device="cuda"):
+    """(logp_old, logp) float32 device tensors of n positions."""
+    import torch
+
+    old = torch.empty(n, dtype=torch.float32, device=device)
+    new = torch.empty(n, dtype=torch.float32, device=device)
+    if n:
+        rc = dev_lib().synth_logp_device(ctypes.byref(P), old.data_ptr(), new.data_ptr(), n,
+                                         torch.cuda.current_stream(device).cuda_stream)
+        assert rc == 0, rc
+    return old, new

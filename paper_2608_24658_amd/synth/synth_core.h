@@ -35,7 +35,7 @@ enum {
 /* Draw purposes (top byte of counter word 2). */
 enum {
     D_LEN = 1, D_LEN2, D_CORRECT, D_TRUNC, D_TRUNC_POS, D_TRIGGER, D_NBLOCKS,
-    D_KIND, D_K, D_NEST, D_NK, D_WEIGHT, D_OUTLIER, D_TEXT
+    D_KIND, D_K, D_NEST, D_NK, D_WEIGHT, D_OUTLIER, D_TEXT, D_LOGP
 };
 
 typedef struct synth_params {
@@ -318,4 +318,28 @@ __host__ __device__ static inline void sy_row_emit(const synth_params *P, uint64
     }
     sy_walk w = {P, row, 0, ri->len, out, write_text, flat0, ri->R, ri->W, 0, 0};
     sy_row(&w, &ri->shape);
+}
+
+/* Log-probabilities of the generated tokens at flat positions 4q .. 4q+3, for
+ * the policy-gradient step: logp_old uniform in (-8, 0], logp = logp_old +
+ * delta with delta triangular on (-0.25, 0.25).  Both come from integers by
+ * exact float operations (a conversion of an integer below 2^25 and power-of-
+ * two scalings) and one float addition, so host and device agree bit for bit. */
+__host__ __device__ static inline void sy_logp4(const synth_params *P, uint64_t q, float old4[4], float new4[4])
+{
+    uint32_t c[3][4];
+    for (int k = 0; k < 3; ++k) {
+        c[k][0] = (uint32_t)q;
+        c[k][1] = (uint32_t)(q >> 32);
+        c[k][2] = ((uint32_t)D_LOGP << 24) | (uint32_t)k;
+        c[k][3] = 0u;
+        sy_philox(c[k], P->seed_lo, P->seed_hi);
+    }
+    for (int j = 0; j < 4; ++j) {
+        float o = (float)(int32_t)(c[0][j] >> 8) * (-8.0f / 16777216.0f);
+        int32_t t = (int32_t)(c[1][j] >> 8) + (int32_t)(c[2][j] >> 8) - 16777216;
+        float delta = (float)t * (1.0f / 67108864.0f);
+        old4[j] = o;
+        new4[j] = o + delta;
+    }
 }

@@ -33,3 +33,16 @@ extern "C" int64_t synth_row_tokens_host(const synth_params *P, uint64_t row, ui
     sy_row_emit(P, row, &ri, out, flat0, 1);
     return ri.len;
 }
+
+/* logp_old and logp for flat positions [p0, p0 + n). */
+extern "C" int synth_logp_host(const synth_params *P, uint64_t p0, int64_t n, float *old_p, float *new_p)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        uint64_t pos = p0 + (uint64_t)i;
+        float o[4], w[4];
+        sy_logp4(P, pos >> 2, o, w);
+        old_p[i] = o[pos & 3];
+        new_p[i] = w[pos & 3];
+    }
+    return 0;
+}

@@ -1,0 +1,112 @@
+"""GPU parity of the policy-gradient step (advantages, clipped surrogate and
+its gradient) against the CPU oracle on the same seeded inputs.
+
+Tolerances: clip counts and the token count exact.  Advantages: the kernel
+evaluates the same double expression in the same order and stores float, so
+within 2^-23 * max(1, |A|).  Gradient: the kernel takes rho = expf(d) and
+-(A * rho) * (1/N) in float (a few float roundings) against the oracle's double
+values: 2^-20 relative, plus 1e-30 absolute.  Loss: float terms summed in
+double: 2^-20 relative."""
+import numpy as np
+import pytest
+
+from gpu_util import log, to_dev
+from oracle import oracle as O
+from oracle import pg_oracle as PG
+from paper_2608_24658_amd import parason as PX
+from paper_2608_24658_amd.synth import synth as S
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+G = S.GROUP_SIZE
+EPS_LO, EPS_HI = 0.2, 0.28
+TOL = 2.0 ** -20
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def rewards_for(P, n):
+    tok, st, ln, co = S.host_batch(P, n)
+    rows = O.eval_rows(tok, st, ln, S.CONTIGUOUS_TAGS)
+    R, *_ = O.group_reward(rows, co, G, 0.1, 0.0, 0.1, 0.5, 0.25)
+    return R.astype(np.float32), st, ln
+
+
+def check(got, exp, adv_exp, starts, lengths, what):
+    adv = got["advantage"].cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(adv - adv_exp) <= 2.0 ** -23 * np.maximum(1.0, np.abs(adv_exp))), what
+    st = got["stats"].cpu().numpy()
+    assert st[1] == exp["tokens"] and st[2] == exp["clip_high"] and st[3] == exp["clip_low"], (what, st, exp)
+    assert abs(st[0] - exp["loss"]) <= TOL * max(1e-6, abs(exp["loss"])), (what, st[0], exp["loss"])
+    g = got["grad"].cpu().numpy().astype(np.float64)
+    inside = ~np.isnan(exp["grad"])
+    err = np.abs(g[inside] - exp["grad"][inside])
+    lim = TOL * np.abs(exp["grad"][inside]) + 1e-30
+    assert np.all(err <= lim), (what, float(np.max(err / np.maximum(lim, 1e-300))))
+    return g, inside
+
+
+@pytest.mark.parametrize("workload", ["tiny", "small", "ragged", "typical"])
+def test_pg_parity(dev, workload):
+    log("case pg %s" % workload)
+    P = S.make_params(workload)
+    n = S.n_rows_of(workload)
+    reward, starts, lengths = rewards_for(P, n)
+    N = int(lengths.astype(np.int64).sum())
+    old_d, new_d = S.device_logp(P, N, device=dev)
+    old_h, new_h = S.host_logp(P, 0, N)
+    assert np.array_equal(old_d.cpu().numpy(), old_h) and np.array_equal(new_d.cpu().numpy(), new_h)
+    got = PX.pg_run(to_dev(reward, torch.float32, dev), new_d, old_d, to_dev(starts, torch.int64, dev),
+                    to_dev(lengths, torch.int32, dev), G, EPS_LO, EPS_HI)
+    torch.cuda.synchronize()
+    adv_exp = PG.advantages(reward, G)
+    exp = PG.surrogate(new_h, old_h, starts, lengths, adv_exp.astype(np.float32), EPS_LO, EPS_HI)
+    check(got, exp, adv_exp, starts, lengths, workload)
+    log("%s: %d tokens, loss %.6g, clipped %d/%d" % (workload, N, exp["loss"], exp["clip_high"], exp["clip_low"]))
+
+
+def test_pg_layout_gaps_and_misalignment(dev):
+    """Padded rows at every alignment: positions outside rows are not written."""
+    log("case pg layout")
+    rng = np.random.default_rng(5)
+    n = 24
+    lengths = rng.integers(0, 3000, n).astype(np.int32)
+    lengths[3] = 1
+    lmax = int(lengths.max()) + 5
+    starts = (np.arange(n) * lmax + 1).astype(np.int64)
+    total = n * lmax + 8
+    P = S.make_params("small")
+    old_h, new_h = S.host_logp(P, 0, total)
+    reward = rng.choice([-1.0, 0.5, 1.0, 1.7], n).astype(np.float32)
+    reward[16:24] = 1.0  # an all-equal group: A = 0
+    for shift in (0, 1, 3):
+        buf_o = to_dev(np.concatenate([np.zeros(shift, np.float32), old_h]), torch.float32, dev)[shift:]
+        buf_n = to_dev(np.concatenate([np.zeros(shift, np.float32), new_h]), torch.float32, dev)[shift:]
+        grad = to_dev(np.concatenate([np.zeros(shift, np.float32), np.full(total, 7.5, np.float32)]),
+                      torch.float32, dev)[shift:]
+        got = PX.pg_run(to_dev(reward, torch.float32, dev), buf_n, buf_o, to_dev(starts, torch.int64, dev),
+                        to_dev(lengths, torch.int32, dev), G, EPS_LO, EPS_HI, grad=grad)
+        torch.cuda.synchronize()
+        adv_exp = PG.advantages(reward, G)
+        exp = PG.surrogate(new_h, old_h, starts, lengths, adv_exp.astype(np.float32), EPS_LO, EPS_HI)
+        g, inside = check(got, exp, adv_exp, starts, lengths, "shift %d" % shift)
+        assert np.all(g[~inside] == 7.5)
+
+
+def test_pg_rejects_bad_arguments(dev):
+    log("case pg args")
+    t = torch.zeros(64, dtype=torch.float32, device=dev)
+    st = torch.zeros(8, dtype=torch.int64, device=dev)
+    ln = torch.zeros(8, dtype=torch.int32, device=dev)
+    with pytest.raises(PX.ParasonError):
+        PX.pg_run(t[:8], t, t, st, ln, group_size=3)  # 8 rows, G = 3
+    with pytest.raises(PX.ParasonError):
+        PX.pg_run(t[:8], t, t, st, ln, clip_low=1.0)
+    with pytest.raises(PX.ParasonError):
+        PX.pg_run(t[:8], t[1:33], t[:32], st, ln)  # different alignment modulo 16 bytes
