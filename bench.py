@@ -111,8 +111,10 @@ def main():
     ap.add_argument("--workload", default="large", choices=["tiny", "small", "typical", "large", "ragged"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
-    ap.add_argument("--step", default="accounting", choices=["accounting", "pg"],
-                    help="accounting: the hot path (default); pg: the policy-gradient step that consumes its rewards")
+    ap.add_argument("--step", default="accounting", choices=["accounting", "pg", "decode"],
+                    help="accounting: the hot path (default); pg: the policy-gradient step that consumes its "
+                         "rewards; decode: the grammar-constrained decode step of the rollouts")
+    ap.add_argument("--decode-batch", type=int, default=1024)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device-to-device copy of 4 GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -141,6 +143,8 @@ def main():
 
     if args.step == "pg":
         return bench_pg(args)
+    if args.step == "decode":
+        return bench_decode(args)
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
@@ -309,6 +313,89 @@ def bench_pg(args):
                      "achieved": alg / (ev_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": alg / (ev_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "traffic": None, "kernel_ms": ev_ms,
                      "algorithmic_bytes": alg},
+    }
+    print(json.dumps(res), flush=True)
+
+
+def bench_decode(args):
+    """The grammar-constrained decode step on a rollout batch of B sequences
+    over the Qwen-size vocabulary (151936 ids, bf16 logits).
+
+    Two regimes, each timed with HIP events over `steps` launches:
+      * rollout: the states follow B synthetic rollouts of the typical
+        workload token by token (mostly inside text, where only the tag and
+        end-of-sequence logits may change);
+      * structural: every sequence sits where no text may follow (the first
+        step of a rollout: only <think> is allowed), so every row is rewritten
+        with -inf: B * V * 2 bytes of HBM writes per launch.  This is the
+        kernel's roofline case."""
+    import numpy as np
+    import torch
+
+    from paper_2608_24658_amd import parason as PX
+    from paper_2608_24658_amd.synth import synth as S
+
+    dev = torch.device("cuda:0")
+    B, V = args.decode_batch, S.VOCAB
+    eos = 151643
+    px = PX.Parason(S.CONTIGUOUS_TAGS)
+    K = args.steps
+    P = S.make_params("typical")
+    tok_h, st_h, ln_h, _ = S.host_batch(P, B)
+    T = args.warmup + K + 1
+    assert int(ln_h.min()) >= T, "rollouts shorter than the timed steps"
+    idx = st_h[None, :] + np.arange(T, dtype=np.int64)[:, None]
+    step_tokens = torch.as_tensor(np.ascontiguousarray(tok_h[idx].astype(np.int32))).to(dev)  # [T, B]
+    logits = torch.randn(B, V, device=dev).to(torch.bfloat16)
+    states = PX.decode_init(B, dev)
+
+    def timed(fn, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for k in range(n):
+            fn(k)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    # rollout regime: the first step masks for <think>, then token k advances every sequence
+    px.decode_step(states, logits, None, eos)
+    for k in range(args.warmup):
+        px.decode_step(states, logits, step_tokens[k], eos)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    roll_ms = timed(lambda k: px.decode_step(states, logits, step_tokens[args.warmup + k], eos), K)
+    wall_ms = (time.perf_counter() - t0) * 1e3 / K
+    fl = PX.decode_fields(states)[:, 3].cpu().numpy()
+    assert not fl.any(), "synthetic rollouts must stay valid"
+
+    # structural regime: fresh states, no token yet: every row but one logit becomes -inf
+    fresh = PX.decode_init(B, dev)
+    for _ in range(args.warmup):
+        px.decode_step(fresh, logits, None, eos)
+    struct_ms = timed(lambda k: px.decode_step(fresh, logits, None, eos), K)
+    alg = B * (V * 2 + 16 + 16)  # logits written, state read + written
+    ach = alg / (struct_ms * 1e-3) / 1e9
+    res = {
+        "metric": "grammar-constrained decode step: sequences masked per second + % of HBM roofline, 1xMI355X",
+        "value": B / (roll_ms * 1e-3),
+        "unit": "sequence-steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": roll_ms,
+        "wall_ms_per_step": wall_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (rollout tokens of the typical workload; random logits)",
+        "config": {"workload": "decode batch %d, vocab %d, bf16 logits, contiguous tag ids" % (B, V),
+                   "batch": B, "vocab": V},
+        "structural_ms_per_step": struct_ms,
+        "roofline": {"kernel": "decode_step (structural regime)", "bound": "hbm", "achieved": ach,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": None,
+                     "kernel_ms": struct_ms, "algorithmic_bytes": alg},
     }
     print(json.dumps(res), flush=True)
 

@@ -229,6 +229,52 @@ int parason_pg_run(const parason_pg_config *cfg, const float *reward, const floa
                    const int64_t *starts, const int32_t *lengths, int64_t n_traj, float *advantage, float *grad,
                    double *stats, void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---- grammar-constrained decode step ------------------------------------
+ * During rollouts the tags are kept valid by grammar-constrained decoding
+ * (Sec. 3.4) over the grammar of Figure 4 (Sec. 3.2).  A token may follow a
+ * prefix when prefix + token is still a prefix of some valid stream; the
+ * end-of-sequence token may follow a prefix that is itself a complete stream
+ * (after </think>).  Text is every id that is neither a tag nor eos_id.
+ *
+ * Each sequence carries a 16-byte state in device memory.  One step
+ *   1. advances the state by the token sampled last (tokens[i]; NULL, or a
+ *      negative entry, advances nothing -- the first step of a rollout), then
+ *   2. writes -inf into every logit of row i that the new state forbids.
+ * Allowed logits are left untouched.  A sampled token that was not allowed
+ * sets PARASON_DECODE_ERROR; a sampled eos_id that was allowed sets
+ * PARASON_DECODE_DONE.  A state carrying either flag no longer changes and its
+ * rows are not masked.  Thread and outline-entry counts are not forced to
+ * match (as for parason_run, a mismatch is flagged, not invalid). */
+#define PARASON_DECODE_ERROR (1u << 0)
+#define PARASON_DECODE_DONE (1u << 1)
+
+#define PARASON_DTYPE_F32 0
+#define PARASON_DTYPE_BF16 1
+#define PARASON_DTYPE_F16 2
+
+typedef struct parason_decode_state {
+    int32_t state;  /* position in the grammar (opaque) */
+    int32_t depth;  /* open <Parallel> blocks */
+    int32_t entry;  /* open outline entry (opaque) */
+    uint32_t flags; /* PARASON_DECODE_* */
+} parason_decode_state;
+
+/* Set states[0 .. batch) to the start of a stream (device memory, 16-byte
+ * aligned), asynchronously on `stream`. */
+int parason_decode_init(parason_decode_state *states, int64_t batch, void *stream);
+
+/* One decode step for `batch` sequences, asynchronously on `stream`, with the
+ * tag ids of h.  Device pointers:
+ *   states   parason_decode_state[batch], updated in place
+ *   tokens   int32[batch] sampled last, or NULL
+ *   logits   row i at logits + i * row_stride elements, vocab elements each,
+ *            of type `dtype` (PARASON_DTYPE_*), aligned to the element size
+ * eos_id: the end-of-sequence id (< vocab, not a tag), or -1 for none.  Every
+ * tag id must be < vocab and row_stride >= vocab.  Host-side argument errors
+ * return a negative status before any launch. */
+int parason_decode_step(const parason_handle *h, parason_decode_state *states, const int32_t *tokens, int64_t batch,
+                        void *logits, int64_t vocab, int64_t row_stride, int32_t dtype, int32_t eos_id, void *stream);
+
 /* Static description of a status code. */
 const char *parason_strerror(int status);
 

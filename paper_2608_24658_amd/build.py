@@ -32,6 +32,7 @@ LIBS = {
         out=os.path.join(PKG, "libparason.so"),
         srcs=[os.path.join(PKG, "csrc", "parason.hip")],
         deps=[os.path.join(PKG, "csrc", "parason_kernels.h"), os.path.join(PKG, "csrc", "pg_kernels.h"),
+              os.path.join(PKG, "csrc", "decode_kernels.h"),
               os.path.join(INCLUDE, "parason.h")],
         kind="hip",
     ),

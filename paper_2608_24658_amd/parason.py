@@ -38,7 +38,13 @@ MAX_DEPTH = 1 << 20
 MAX_OPEN_ENTRIES = 1 << 24
 
 EXPORTED = ("parason_create", "parason_workspace_size", "parason_run", "parason_run_timed", "parason_destroy",
-            "parason_strerror", "parason_pg_workspace_size", "parason_pg_run")
+            "parason_strerror", "parason_pg_workspace_size", "parason_pg_run", "parason_decode_init",
+            "parason_decode_step")
+
+DECODE_ERROR = 1 << 0
+DECODE_DONE = 1 << 1
+DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
+DECODE_STATE_BYTES = 16
 
 PG_STATS = ("loss", "tokens", "clip_high", "clip_low")
 
@@ -118,6 +124,13 @@ def lib():
             ctypes.POINTER(PgConfig), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
             ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
             ctypes.c_size_t, ctypes.c_void_p,
+        ]
+        L.parason_decode_init.restype = ctypes.c_int
+        L.parason_decode_init.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+        L.parason_decode_step.restype = ctypes.c_int
+        L.parason_decode_step.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+            ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
         ]
         L.parason_strerror.restype = ctypes.c_char_p
         L.parason_strerror.argtypes = [ctypes.c_int]
@@ -219,6 +232,35 @@ class Parason:
         return lib().parason_run_timed(self._h, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, int(n_traj),
                                        ctypes.byref(o), ws_ptr, int(ws_bytes), stream, ev)
 
+    def decode_step_raw(self, states_ptr, tokens_ptr, batch, logits_ptr, vocab, row_stride, dtype, eos_id,
+                        stream) -> int:
+        """Direct parason_decode_step call with raw device pointers; returns the status."""
+        return lib().parason_decode_step(self._h, states_ptr, tokens_ptr, int(batch), logits_ptr, int(vocab),
+                                         int(row_stride), int(dtype), int(eos_id), stream)
+
+    def decode_step(self, states, logits, tokens=None, eos_id: int = -1):
+        """Advance the decode states by `tokens` (int32[batch] or None) and mask
+        `logits` ([batch, vocab] rows, float32/bfloat16/float16, unit stride
+        along the vocabulary) in place, on the current stream."""
+        import torch
+
+        dtypes = {torch.float32: DTYPE_F32, torch.bfloat16: DTYPE_BF16, torch.float16: DTYPE_F16}
+        if logits.dtype not in dtypes or logits.dim() != 2 or logits.stride(1) != 1 or not logits.is_cuda:
+            raise TypeError("logits must be a [batch, vocab] float32/bfloat16/float16 device tensor, unit stride")
+        batch, vocab = logits.shape
+        if states.dtype != torch.uint8 or states.numel() != batch * DECODE_STATE_BYTES or not states.is_contiguous():
+            raise TypeError("states must be a contiguous uint8 device tensor of batch * 16 bytes")
+        if tokens is not None and (tokens.dtype != torch.int32 or tokens.numel() != batch
+                                   or not tokens.is_contiguous()):
+            raise TypeError("tokens must be a contiguous int32 device tensor of batch entries")
+        stream = torch.cuda.current_stream(logits.device).cuda_stream
+        rc = self.decode_step_raw(states.data_ptr(), tokens.data_ptr() if tokens is not None else None, batch,
+                                  logits.data_ptr(), vocab, logits.stride(0) if batch > 1 else vocab,
+                                  dtypes[logits.dtype], eos_id, stream)
+        if rc != OK:
+            raise ParasonError(rc, "parason_decode_step")
+        return logits
+
     def run(self, tokens, starts, lengths, correct, out: dict | None = None, workspace=None, total_tokens=None,
             derived: bool = True, metrics: bool = False) -> dict:
         """Evaluate a batch of rows held in device tensors (asynchronous on the
@@ -244,6 +286,26 @@ class Parason:
         if rc != OK:
             raise ParasonError(rc, "parason_run")
         return out
+
+
+def decode_init(batch: int, device, states=None):
+    """Decode states (uint8[batch * 16] device tensor) set to the start of a stream."""
+    import torch
+
+    if states is None:
+        states = torch.empty(int(batch) * DECODE_STATE_BYTES, dtype=torch.uint8, device=device)
+    stream = torch.cuda.current_stream(states.device).cuda_stream
+    rc = lib().parason_decode_init(states.data_ptr(), int(batch), stream)
+    if rc != OK:
+        raise ParasonError(rc, "parason_decode_init")
+    return states
+
+
+def decode_fields(states):
+    """[batch, 4] int32 view of a states tensor: state, depth, entry, flags."""
+    import torch
+
+    return states.view(torch.int32).view(-1, 4)
 
 
 def pg_workspace_size(n_traj: int) -> int:

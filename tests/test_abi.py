@@ -108,3 +108,33 @@ def test_run_rejects_bad_arguments_before_launch():
     # workspace too small
     assert run(FAKE, FAKE, FAKE, FAKE, 16, out, FAKE, 1024, None) == P.ERR_WORKSPACE
     assert P.lib().parason_run(None, FAKE, FAKE, FAKE, FAKE, 16, None, FAKE, ws, None) == P.ERR_NULL
+
+
+def test_decode_rejects_bad_arguments_before_launch():
+    px = P.Parason(TAGS)
+    V = 151936
+    step = px.decode_step_raw
+    bf = P.DTYPE_BF16
+    assert P.lib().parason_decode_step(None, FAKE, FAKE, 4, FAKE, V, V, bf, 0, None) == P.ERR_NULL
+    assert step(FAKE, FAKE, -1, FAKE, V, V, bf, 0, None) == P.ERR_SIZE
+    assert step(FAKE, FAKE, 4, FAKE, 0, 0, bf, 0, None) == P.ERR_SIZE
+    assert step(FAKE, FAKE, 4, FAKE, V, V - 1, bf, 0, None) == P.ERR_SIZE
+    assert step(FAKE, FAKE, 4, FAKE, V, V, 7, 0, None) == P.ERR_PARAM
+    # every tag id and the eos id must be inside the vocabulary; eos is no tag
+    assert step(FAKE, FAKE, 4, FAKE, TAGS[-1], TAGS[-1], bf, 0, None) == P.ERR_TAGS
+    assert step(FAKE, FAKE, 4, FAKE, V, V, bf, TAGS[3], None) == P.ERR_TAGS
+    assert step(FAKE, FAKE, 4, FAKE, V, V, bf, V, None) == P.ERR_TAGS
+    assert step(FAKE, FAKE, 4, FAKE, V, V, bf, -2, None) == P.ERR_TAGS
+    # batch 0 is a no-op; NULL and misaligned pointers
+    assert step(0, 0, 0, 0, V, V, bf, 0, None) == P.OK
+    assert step(0, FAKE, 4, FAKE, V, V, bf, 0, None) == P.ERR_NULL
+    assert step(FAKE, FAKE, 4, 0, V, V, bf, 0, None) == P.ERR_NULL
+    assert step(FAKE + 4, FAKE, 4, FAKE, V, V, bf, 0, None) == P.ERR_ALIGN
+    assert step(FAKE, FAKE, 4, FAKE + 1, V, V, bf, 0, None) == P.ERR_ALIGN
+    assert step(FAKE, FAKE, 4, FAKE + 2, V, V, P.DTYPE_F32, 0, None) == P.ERR_ALIGN
+    assert step(FAKE, FAKE + 2, 4, FAKE, V, V, bf, 0, None) == P.ERR_ALIGN
+    init = P.lib().parason_decode_init
+    assert init(None, 4, None) == P.ERR_NULL
+    assert init(FAKE, -1, None) == P.ERR_SIZE
+    assert init(FAKE + 8, 4, None) == P.ERR_ALIGN
+    assert init(None, 0, None) == P.OK
