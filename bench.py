@@ -401,12 +401,15 @@ def bench_decode(args):
 
 
 def kernel_sha():
-    """Hash of the kernel sources with comments and whitespace removed."""
+    """Hash of the sources of the accounting path's kernels and launches, with
+    comments and whitespace removed (the other entry points of the library live
+    in files of their own and do not enter it)."""
     import hashlib
     import re
 
     h = hashlib.sha256()
-    for p in ("paper_2608_24658_amd/csrc/parason_kernels.h", "paper_2608_24658_amd/csrc/parason.hip"):
+    for p in ("paper_2608_24658_amd/csrc/device_common.h", "paper_2608_24658_amd/csrc/parason_kernels.h",
+              "paper_2608_24658_amd/csrc/abi_common.h", "paper_2608_24658_amd/csrc/parason.hip"):
         src = open(os.path.join(ROOT, p)).read()
         src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
         src = re.sub(r"//[^\n]*", "", src)

@@ -24,7 +24,7 @@
  * left unmasked.
  */
 #pragma once
-#include "parason_kernels.h"
+#include "device_common.h"
 
 namespace pk {
 

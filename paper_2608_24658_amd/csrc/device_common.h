@@ -1,0 +1,221 @@
+/*
+ * device_common.h -- constants and device helpers shared by the kernels of
+ * libparason.so: token classes and the tag test, the segment plan's geometry
+ * and cursor, wave helpers and the deterministic block reductions.  Only
+ * inline device code lives here; every kernel is defined in exactly one
+ * translation unit.
+ */
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "parason.h"
+
+namespace pk {
+
+constexpr int WAVE = 64;
+#ifndef PARASON_SEG_VEC
+#define PARASON_SEG_VEC 512
+#endif
+#ifndef PARASON_SCAN_WAVES_PER_SIMD
+#define PARASON_SCAN_WAVES_PER_SIMD 4
+#endif
+constexpr int SEG_VEC = PARASON_SEG_VEC; /* 16-byte vectors per segment (2048 tokens) */
+constexpr int SEG_TOK = 4 * SEG_VEC;     /* tokens per segment */
+constexpr int LOADS = SEG_VEC / WAVE;    /* vector loads per lane per segment */
+constexpr int EV_CAP = 128;              /* events stored per segment */
+constexpr int PLAN_TILE = 4096;          /* rows per plan tile */
+constexpr int PLAN_THREADS = 256;
+constexpr int ROWS_PER_THREAD = PLAN_TILE / PLAN_THREADS;
+#ifndef PARASON_FAST_DEPTH
+#define PARASON_FAST_DEPTH 8
+#endif
+constexpr int FAST_DEPTH = PARASON_FAST_DEPTH; /* LDS frames per row (depth <= FAST_DEPTH + 1) */
+constexpr int FAST_ENTRIES = 64;         /* entries per open block on the fast path */
+constexpr int FRAME_WORDS = 8;
+constexpr int64_t DEEP_FRAMES = PARASON_MAX_DEPTH;
+constexpr int64_t DEEP_ENTRY_BITS = PARASON_MAX_OPEN_ENTRIES;
+
+/* Token classes: 0 = Text, 1..12 = tags in tag_ids order. */
+enum : uint32_t {
+    C_TEXT = 0, C_THINK, C_END_THINK, C_PAR, C_END_PAR, C_OUT, C_END_OUT,
+    C_SUB, C_END_SUB, C_TRI, C_END_TRI, C_THR, C_END_THR
+};
+
+/* Branch type of the innermost enclosing thread. */
+enum : uint32_t { T_MAIN = 0, T_SUB = 1, T_TRI = 2 };
+
+struct TagMatch {
+    int32_t ids[12];
+    int32_t base;     /* contiguous case: smallest id */
+    uint32_t lut_lo;  /* contiguous case: class of id base+o in nibble o (o < 8) */
+    uint32_t lut_hi;  /* nibbles for o = 8..11 */
+    int32_t contiguous;
+};
+
+__device__ __forceinline__ uint32_t classify(const TagMatch &tm, int32_t t, bool contig)
+{
+    if (contig) {
+        uint32_t o = (uint32_t)t - (uint32_t)tm.base;
+        if (o >= 12u) return C_TEXT;
+        return o < 8u ? (tm.lut_lo >> (4u * o)) & 15u : (tm.lut_hi >> (4u * (o - 8u))) & 15u;
+    }
+    uint32_t c = C_TEXT;
+#pragma unroll
+    for (int k = 0; k < 12; ++k) c = (t == tm.ids[k]) ? (uint32_t)(k + 1) : c;
+    return c;
+}
+
+/* First 16-byte vector of a row's segments: the 128-byte line (8 vectors) that
+ * holds its first token, so every wave-wide load covers whole L2 lines. */
+__device__ __forceinline__ int64_t row_first_vec(int64_t g) { return (g >> 5) << 3; }
+
+/* One past the last vector holding a token of the row. */
+__device__ __forceinline__ int64_t row_end_vec(int64_t g, int32_t len) { return (g + (int64_t)len + 3) >> 2; }
+
+__device__ __forceinline__ int64_t row_segments(int64_t start, int32_t len, int64_t mis)
+{
+    if (start < 0 || len <= 0) return 0;
+    int64_t g = start + mis;
+    int64_t nvec = row_end_vec(g, len) - row_first_vec(g);
+    return (nvec + SEG_VEC - 1) / SEG_VEC;
+}
+
+__device__ __forceinline__ int64_t uniform64(int64_t x)
+{
+    uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+/* Inclusive prefix sum over the 64 lanes of a wave. */
+__device__ __forceinline__ int64_t wave_inclusive_scan(int64_t v)
+{
+    const int lane = threadIdx.x & (WAVE - 1);
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) {
+        int64_t o = __shfl_up(v, d, WAVE);
+        if (lane >= d) v += o;
+    }
+    return v;
+}
+
+/* A segment as the scan wave sees it (all fields wave-uniform). */
+struct SegView {
+    int64_t s;                  /* segment id */
+    int64_t row, first, last;   /* its row and the row's first and last segment */
+    int64_t v0, v1;             /* its vectors [v0, v1) */
+    int64_t g;                  /* row start on the element grid of tok_base */
+    int32_t len;
+    int32_t q_lo, q_hi;         /* segment positions that belong to the row */
+    bool edge;                  /* holds the first or the last vector of the row */
+    bool owned;                 /* every segment of the row is in this wave's range */
+};
+
+/* Walks a wave's contiguous range of segment ids, row by row. */
+struct SegCursor {
+    const int64_t *seg_off;
+    const int64_t *starts;
+    const int32_t *lengths;
+    int64_t mis, s_begin, s_end;
+    int64_t row, row_first, row_next;
+    int64_t g, vrow0, vend;
+    int32_t len;
+    bool loaded;
+
+    __device__ void seek(int64_t s, int64_t n)
+    {
+        /* the row holding s: seg_off[row] <= s < seg_off[row + 1] */
+        int64_t lo = 0, hi = n;
+        while (hi - lo > 1) {
+            int64_t mid = (lo + hi) >> 1;
+            if (seg_off[mid] <= s) lo = mid; else hi = mid;
+        }
+        row = uniform64(lo);
+        row_first = uniform64(seg_off[row]);
+        row_next = uniform64(seg_off[row + 1]);
+        loaded = false;
+    }
+
+    __device__ SegView view(int64_t s)
+    {
+        while (row_next <= s) {
+            ++row;
+            row_first = row_next;
+            row_next = uniform64(seg_off[row + 1]);
+            loaded = false;
+        }
+        if (!loaded) {
+            g = uniform64(starts[row] + mis);
+            len = __builtin_amdgcn_readfirstlane(lengths[row]);
+            vrow0 = row_first_vec(g);
+            vend = row_end_vec(g, len);
+            loaded = true;
+        }
+        SegView w;
+        w.s = s;
+        w.row = row;
+        w.first = row_first;
+        w.last = row_next - 1;
+        w.g = g;
+        w.len = len;
+        w.v0 = vrow0 + (s - row_first) * SEG_VEC;
+        w.v1 = min(w.v0 + (int64_t)SEG_VEC, vend);
+        w.edge = w.v0 == vrow0 || w.v1 == vend;
+        /* row positions g .. g+len-1 relative to the segment's first element */
+        const int64_t lo = g - 4 * w.v0, hi = g + (int64_t)len - 4 * w.v0;
+        w.q_lo = (int32_t)max((int64_t)0, lo);
+        w.q_hi = (int32_t)min((int64_t)4 * (w.v1 - w.v0), hi);
+        /* LDS events hold (position << 4 | class) in 32 bits */
+        w.owned = row_first >= s_begin && row_next <= s_end && len < (1 << 27);
+        return w;
+    }
+};
+
+/* ------------------------------------------------------------------ batch reductions */
+
+/* Deterministic sums: every thread adds its ROWS_PER_THREAD consecutive rows in
+ * index order, the block combines the threads in a fixed pairwise tree, and one
+ * block adds the block partials in block order. */
+constexpr int RED_THREADS = 256;
+constexpr int RED_TILE = RED_THREADS * ROWS_PER_THREAD;
+static_assert(RED_TILE == PLAN_TILE, "the reductions reuse the plan's tile count");
+
+template <class T, int K>
+__device__ __forceinline__ void block_tree_sum(T (&v)[K], T *lds /* [K][RED_THREADS] */)
+{
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int k = 0; k < K; ++k) lds[k * RED_THREADS + t] = v[k];
+    __syncthreads();
+    for (int stride = RED_THREADS / 2; stride > 0; stride >>= 1) {
+        if (t < stride) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) lds[k * RED_THREADS + t] += lds[k * RED_THREADS + t + stride];
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) v[k] = lds[k * RED_THREADS];
+    __syncthreads();
+}
+
+/* Sum of part[0 .. m) (each of K values) in index order by one block. */
+template <class T, int K>
+__device__ __forceinline__ void sum_partials(const T *part, int64_t m, T (&out)[K], T *lds)
+{
+    T v[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) v[k] = 0;
+    const int64_t per = (m + RED_THREADS - 1) / RED_THREADS;
+    const int64_t b0 = threadIdx.x * per, b1 = min(m, b0 + per);
+    for (int64_t b = b0; b < b1; ++b) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) v[k] += part[b * K + k];
+    }
+    block_tree_sum<T, K>(v, lds);
+#pragma unroll
+    for (int k = 0; k < K; ++k) out[k] = v[k];
+}
+
+} /* namespace pk */

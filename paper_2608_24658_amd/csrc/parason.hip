@@ -2,34 +2,27 @@
  * parason.hip -- C-ABI of the Parason accounting/reward path for gfx950.
  * The kernels are in parason_kernels.h; this file validates arguments, lays
  * out the caller's workspace and enqueues the launches on the caller's stream.
+ * The policy-gradient step (pg.hip) and the decode step (decode.hip) are
+ * further entry points of the same library.
  */
-#include <hip/hip_runtime.h>
-
-#include <atomic>
-#include <cmath>
 #include <cstring>
 #include <new>
 
-#include "parason.h"
+#include "abi_common.h"
 #include "parason_kernels.h"
-#include "pg_kernels.h"
-#include "decode_kernels.h"
 
-struct parason_handle {
-    parason_config cfg;
-    pk::TagMatch tm;
-};
+using abi::ALIGN;
+using abi::align_up;
+using abi::cu_count;
+using abi::is_finite;
 
 namespace {
 
-constexpr size_t ALIGN = 256;
 #ifndef PARASON_SCAN_BLOCKS_PER_CU
 #define PARASON_SCAN_BLOCKS_PER_CU 4
 #endif
 constexpr int SCAN_BLOCKS_PER_CU = PARASON_SCAN_BLOCKS_PER_CU; /* persistent grid of 4-wave blocks */
 constexpr int64_t MAX_SEGMENTS = (int64_t)1 << 40;
-
-size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 /* Byte offsets of the workspace sections for n rows. */
 struct Layout {
@@ -91,24 +84,19 @@ int64_t segment_bound(int64_t n, int64_t total)
     return (total + 7 * n) / (4 * pk::SEG_VEC) + 2 * n + 1;
 }
 
-int cu_count()
-{
-    static std::atomic<int> cached[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return -1;
-    if (dev >= 0 && dev < 64) {
-        int c = cached[dev].load(std::memory_order_relaxed);
-        if (c > 0) return c;
-    }
-    int cus = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return -1;
-    if (dev >= 0 && dev < 64) cached[dev].store(cus, std::memory_order_relaxed);
-    return cus;
-}
-
-bool is_finite(double x) { return std::isfinite(x); }
 
 }  // namespace
+
+void abi::launch_plan(const int64_t *starts, const int32_t *lengths, int64_t n, int64_t mis, int64_t n_tiles,
+                      int64_t *tile_sum, int64_t *tile_off, int64_t *seg_off, int32_t *counters, uint8_t *mode,
+                      hipStream_t stream)
+{
+    const unsigned tiles = (unsigned)n_tiles;
+    pk::plan_tiles<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n, mis, tile_sum);
+    pk::plan_top<<<dim3(1), dim3(1024), 0, stream>>>(tile_sum, n_tiles, tile_off, seg_off, n, counters);
+    pk::plan_rows<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n, mis, tile_off, seg_off,
+                                                                        mode);
+}
 
 extern "C" {
 
@@ -222,10 +210,7 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     uint32_t *events = (uint32_t *)(ws + align_up(L.seg_count + (size_t)cap * sizeof(int32_t)));
 
     const unsigned tiles = (unsigned)L.n_tiles;
-    pk::plan_tiles<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_sum);
-    pk::plan_top<<<dim3(1), dim3(1024), 0, stream>>>(tile_sum, L.n_tiles, tile_off, seg_off, n_traj, counters);
-    pk::plan_rows<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_off,
-                                                                        seg_off, mode);
+    abi::launch_plan(starts, lengths, n_traj, mis, L.n_tiles, tile_sum, tile_off, seg_off, counters, mode, stream);
 
     const pk::RowOut row_out{out->total,    out->latency,   out->n_subtask,       out->n_trial,
                              out->n_blocks, out->max_depth, out->first_error_pos, out->flags};
@@ -314,189 +299,6 @@ int parason_run(const parason_handle *h, const int32_t *tokens, const int64_t *s
 {
     return parason_run_timed(h, tokens, starts, lengths, correct, n_traj, out, workspace, workspace_bytes, stream,
                              nullptr);
-}
-
-/* ---- policy-gradient step ---------------------------------------------- */
-
-namespace {
-
-constexpr int PG_BLOCKS_PER_CU = 4;
-constexpr int64_t PG_MAX_WAVES = 1 << 16;
-
-struct PgLayout {
-    size_t seg_off, tile_sum, tile_off, counters, mode, len_part, n_tokens, wsum, wcnt, end;
-    int64_t n_tiles;
-};
-
-PgLayout pg_layout_for(int64_t n)
-{
-    PgLayout L;
-    L.n_tiles = n > 0 ? (n + pk::PLAN_TILE - 1) / pk::PLAN_TILE : 1;
-    size_t o = 0;
-    L.seg_off = o;
-    o = align_up(o + (size_t)(n + 1) * sizeof(int64_t));
-    L.tile_sum = o;
-    o = align_up(o + (size_t)L.n_tiles * sizeof(int64_t));
-    L.tile_off = o;
-    o = align_up(o + (size_t)L.n_tiles * sizeof(int64_t));
-    L.counters = o;
-    o = align_up(o + 4 * sizeof(int32_t));
-    L.mode = o;
-    o = align_up(o + (size_t)(n > 0 ? n : 1));
-    L.len_part = o;
-    o = align_up(o + (size_t)L.n_tiles * sizeof(int64_t));
-    L.n_tokens = o;
-    o = align_up(o + sizeof(int64_t));
-    L.wsum = o;
-    o = align_up(o + (size_t)PG_MAX_WAVES * sizeof(double));
-    L.wcnt = o;
-    o = align_up(o + (size_t)PG_MAX_WAVES * 2 * sizeof(int64_t));
-    L.end = o;
-    return L;
-}
-
-}  // namespace
-
-int parason_pg_workspace_size(int64_t n_traj, size_t *bytes)
-{
-    if (!bytes) return PARASON_ERR_NULL;
-    if (n_traj < 0 || n_traj > INT32_MAX) return PARASON_ERR_SIZE;
-    *bytes = pg_layout_for(n_traj).end;
-    return PARASON_OK;
-}
-
-int parason_pg_run(const parason_pg_config *cfg, const float *reward, const float *logp, const float *logp_old,
-                   const int64_t *starts, const int32_t *lengths, int64_t n_traj, float *advantage, float *grad,
-                   double *stats, void *workspace, size_t workspace_bytes, void *stream_ptr)
-{
-    if (!cfg) return PARASON_ERR_NULL;
-    if (n_traj < 0 || n_traj > INT32_MAX) return PARASON_ERR_SIZE;
-    if (cfg->group_size < 1 || n_traj % cfg->group_size != 0) return PARASON_ERR_GROUP;
-    if (!is_finite(cfg->clip_low) || !is_finite(cfg->clip_high) || cfg->clip_low < 0.0 || cfg->clip_low >= 1.0 ||
-        cfg->clip_high < 0.0)
-        return PARASON_ERR_PARAM;
-    if (n_traj == 0) return PARASON_OK;
-    if (!reward || !logp || !logp_old || !starts || !lengths || !advantage || !grad || !stats || !workspace)
-        return PARASON_ERR_NULL;
-    const uintptr_t a0 = (uintptr_t)logp, a1 = (uintptr_t)logp_old, a2 = (uintptr_t)grad;
-    if (((a0 | a1 | a2) & 3u) != 0 || (a0 & 15u) != (a1 & 15u) || (a0 & 15u) != (a2 & 15u) ||
-        ((uintptr_t)workspace & (ALIGN - 1)) != 0)
-        return PARASON_ERR_ALIGN;
-    const PgLayout L = pg_layout_for(n_traj);
-    if (workspace_bytes < L.end) return PARASON_ERR_WORKSPACE;
-    const int cus = cu_count();
-    if (cus <= 0) return PARASON_ERR_DEVICE;
-    const int64_t waves = (int64_t)cus * PG_BLOCKS_PER_CU * 4;
-    if (waves > PG_MAX_WAVES) return PARASON_ERR_DEVICE;
-    hipStream_t stream = (hipStream_t)stream_ptr;
-
-    const int64_t mis = (int64_t)((a0 & 15u) >> 2);
-    char *ws = (char *)workspace;
-    int64_t *seg_off = (int64_t *)(ws + L.seg_off);
-    int64_t *tile_sum = (int64_t *)(ws + L.tile_sum);
-    int64_t *tile_off = (int64_t *)(ws + L.tile_off);
-    int32_t *counters = (int32_t *)(ws + L.counters);
-    uint8_t *mode = (uint8_t *)(ws + L.mode);
-    int64_t *len_part = (int64_t *)(ws + L.len_part);
-    int64_t *n_tokens = (int64_t *)(ws + L.n_tokens);
-    double *wsum = (double *)(ws + L.wsum);
-    int64_t *wcnt = (int64_t *)(ws + L.wcnt);
-
-    const unsigned tiles = (unsigned)L.n_tiles;
-    pk::plan_tiles<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_sum);
-    pk::plan_top<<<dim3(1), dim3(1024), 0, stream>>>(tile_sum, L.n_tiles, tile_off, seg_off, n_traj, counters);
-    pk::plan_rows<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n_traj, mis, tile_off,
-                                                                        seg_off, mode);
-    pk::sum_lengths_tiles<<<dim3(tiles), dim3(pk::RED_THREADS), 0, stream>>>(lengths, n_traj, len_part);
-    pk::sum_lengths_final<<<dim3(1), dim3(pk::RED_THREADS), 0, stream>>>(len_part, L.n_tiles, n_tokens);
-    const int64_t n_groups = n_traj / cfg->group_size;
-    pk::pg_advantage<<<dim3((unsigned)((n_groups + 255) / 256)), dim3(256), 0, stream>>>(reward, n_groups,
-                                                                                          cfg->group_size, advantage);
-    pk::PgArgs pa;
-    pa.logp_base = logp - mis;
-    pa.old_base = logp_old - mis;
-    pa.grad_base = grad - mis;
-    pa.mis = mis;
-    pa.starts = starts;
-    pa.lengths = lengths;
-    pa.n = n_traj;
-    pa.seg_off = seg_off;
-    pa.adv = advantage;
-    pa.thr_low = (float)std::log1p(-cfg->clip_low);
-    pa.thr_high = (float)std::log1p(cfg->clip_high);
-    pa.lo_val = (float)(1.0 - cfg->clip_low);
-    pa.hi_val = (float)(1.0 + cfg->clip_high);
-    pa.n_tokens = n_tokens;
-    pa.wsum = wsum;
-    pa.wcnt = wcnt;
-    pk::pg_surrogate<<<dim3((unsigned)(cus * PG_BLOCKS_PER_CU)), dim3(256), 0, stream>>>(pa);
-    pk::pg_final<<<dim3(1), dim3(pk::RED_THREADS), 0, stream>>>(wsum, wcnt, waves, n_tokens, stats);
-    return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
-}
-
-/* ---- grammar-constrained decode step ----------------------------------- */
-
-static_assert(sizeof(parason_decode_state) == sizeof(pk::DecodeState), "decode state layout");
-static_assert(sizeof(parason_decode_state) == 16, "decode state is 16 bytes");
-
-namespace {
-constexpr int DECODE_BLOCKS_PER_CU = 8;
-}  // namespace
-
-int parason_decode_init(parason_decode_state *states, int64_t batch, void *stream_ptr)
-{
-    if (batch < 0 || batch > INT32_MAX) return PARASON_ERR_SIZE;
-    if (batch == 0) return PARASON_OK;
-    if (!states) return PARASON_ERR_NULL;
-    if (((uintptr_t)states & 15u) != 0) return PARASON_ERR_ALIGN;
-    hipStream_t stream = (hipStream_t)stream_ptr;
-    pk::decode_init<<<dim3((unsigned)((batch + 255) / 256)), dim3(256), 0, stream>>>(
-        reinterpret_cast<pk::DecodeState *>(states), batch);
-    return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
-}
-
-int parason_decode_step(const parason_handle *h, parason_decode_state *states, const int32_t *tokens, int64_t batch,
-                        void *logits, int64_t vocab, int64_t row_stride, int32_t dtype, int32_t eos_id,
-                        void *stream_ptr)
-{
-    if (!h) return PARASON_ERR_NULL;
-    if (batch < 0 || batch > INT32_MAX || vocab < 1 || vocab > INT32_MAX || row_stride < vocab) return PARASON_ERR_SIZE;
-    int32_t elem = 0;
-    uint32_t ninf = 0;
-    switch (dtype) {
-    case PARASON_DTYPE_F32: elem = 4, ninf = 0xFF800000u; break;
-    case PARASON_DTYPE_BF16: elem = 2, ninf = 0xFF80u; break;
-    case PARASON_DTYPE_F16: elem = 2, ninf = 0xFC00u; break;
-    default: return PARASON_ERR_PARAM;
-    }
-    for (int i = 0; i < 12; ++i)
-        if (h->tm.ids[i] >= vocab || h->tm.ids[i] == eos_id) return PARASON_ERR_TAGS;
-    if (eos_id < -1 || eos_id >= vocab) return PARASON_ERR_TAGS;
-    if (row_stride > INT64_MAX / 4 / (batch > 0 ? batch : 1)) return PARASON_ERR_SIZE;
-    if (batch == 0) return PARASON_OK;
-    if (!states || !logits) return PARASON_ERR_NULL;
-    if (((uintptr_t)states & 15u) != 0 || ((uintptr_t)logits & (uintptr_t)(elem - 1)) != 0 ||
-        (tokens && ((uintptr_t)tokens & 3u) != 0))
-        return PARASON_ERR_ALIGN;
-    const int cus = cu_count();
-    if (cus <= 0) return PARASON_ERR_DEVICE;
-    hipStream_t stream = (hipStream_t)stream_ptr;
-
-    pk::DecodeArgs da;
-    da.states = reinterpret_cast<pk::DecodeState *>(states);
-    da.tokens = tokens;
-    da.batch = batch;
-    da.logits = (char *)logits;
-    da.vocab = vocab;
-    da.row_bytes = row_stride * elem;
-    da.elem = elem;
-    da.ninf = ninf;
-    da.eos_id = eos_id;
-    da.tm = h->tm;
-    const int64_t max_blocks = (int64_t)cus * DECODE_BLOCKS_PER_CU;
-    const unsigned blocks = (unsigned)(batch < max_blocks ? batch : max_blocks);
-    pk::decode_step<<<dim3(blocks), dim3(256), 0, stream>>>(da);
-    return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
 }
 
 }  // extern "C"

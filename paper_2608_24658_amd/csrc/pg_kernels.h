@@ -20,7 +20,7 @@
  *   pg_final       loss, token count and clip counts in fixed order.
  */
 #pragma once
-#include "parason_kernels.h"
+#include "device_common.h"
 
 namespace pk {
 
