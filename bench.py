@@ -111,9 +111,10 @@ def main():
     ap.add_argument("--workload", default="large", choices=["tiny", "small", "typical", "large", "ragged"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
-    ap.add_argument("--step", default="accounting", choices=["accounting", "pg", "decode"],
+    ap.add_argument("--step", default="accounting", choices=["accounting", "pg", "decode", "fork"],
                     help="accounting: the hot path (default); pg: the policy-gradient step that consumes its "
-                         "rewards; decode: the grammar-constrained decode step of the rollouts")
+                         "rewards; decode: the grammar-constrained decode step of the rollouts; fork: fork/join "
+                         "packing of worker contexts for tool-call execution")
     ap.add_argument("--decode-batch", type=int, default=1024)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device-to-device copy of 4 GiB (HBM counter calibration)")
@@ -145,6 +146,8 @@ def main():
         return bench_pg(args)
     if args.step == "decode":
         return bench_decode(args)
+    if args.step == "fork":
+        return bench_fork(args)
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
@@ -292,6 +295,18 @@ def bench_pg(args):
     ev_ms = e0.elapsed_time(e1) / args.steps
     st = out["stats"].cpu().numpy()
     alg = 12.0 * N + 20.0 * n
+    # reference for the same traffic mix: torch's elementwise grad = logp - logp_old
+    # (two float streams read, one written; no plan, no reductions)
+    for _ in range(2):
+        torch.sub(new, old, out=grad)
+    torch.cuda.synchronize()
+    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    r0.record()
+    for _ in range(args.steps):
+        torch.sub(new, old, out=grad)
+    r1.record()
+    torch.cuda.synchronize()
+    ref_ms = r0.elapsed_time(r1) / args.steps
     res = {
         "metric": "policy-gradient step throughput (tokens/s) + achieved % of HBM roofline, 1×MI355X",
         "value": N / (ms * 1e-3),
@@ -313,6 +328,8 @@ def bench_pg(args):
                      "achieved": alg / (ev_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": alg / (ev_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "traffic": None, "kernel_ms": ev_ms,
                      "algorithmic_bytes": alg},
+        "reference": {"what": "torch.sub(logp, logp_old, out=grad): same 12 B per token", "ms": ref_ms,
+                      "GB/s": 12.0 * N / (ref_ms * 1e-3) / 1e9},
     }
     print(json.dumps(res), flush=True)
 
@@ -375,6 +392,10 @@ def bench_decode(args):
         px.decode_step(fresh, logits, None, eos)
     struct_ms = timed(lambda k: px.decode_step(fresh, logits, None, eos), K)
     alg = B * (V * 2 + 16 + 16)  # logits written, state read + written
+    # reference for a write-only stream of the same size: torch's fill
+    for _ in range(args.warmup):
+        logits.fill_(float("-inf"))
+    fill_ms = timed(lambda k: logits.fill_(float("-inf")), K)
     ach = alg / (struct_ms * 1e-3) / 1e9
     res = {
         "metric": "grammar-constrained decode step: sequences masked per second + % of HBM roofline, 1xMI355X",
@@ -396,6 +417,108 @@ def bench_decode(args):
         "roofline": {"kernel": "decode_step (structural regime)", "bound": "hbm", "achieved": ach,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": None,
                      "kernel_ms": struct_ms, "algorithmic_bytes": alg},
+        "reference": {"what": "torch fill_ of the same logits (write-only, B * V * 2 bytes)", "ms": fill_ms,
+                      "GB/s": B * V * 2 / (fill_ms * 1e-3) / 1e9},
+    }
+    print(json.dumps(res), flush=True)
+
+
+def bench_fork(args):
+    """Fork/join packing for tool-call execution on a batch of B = 1024
+    rollouts of the typical workload, each cut right after one of its
+    </Outlines> tags (13.4k-40.2k-token rows, 3-4 entries per outline).
+
+    fork: one context per outline entry (row + <Thread> + the entry's text);
+    join: each row followed by its workers' <Thread> ... </Thread> spans (64
+    generated tokens each) and </Parallel>.  Timed with HIP events over
+    `steps` calls each, outputs pre-sized (no synchronisation inside)."""
+    import numpy as np
+    import torch
+
+    from paper_2608_24658_amd import parason as PX
+    from paper_2608_24658_amd.synth import synth as S
+
+    dev = torch.device("cuda:0")
+    B = args.decode_batch
+    tags = [int(t) for t in S.CONTIGUOUS_TAGS]
+    P = S.make_params("typical")
+    tok_h, st_h, ln_h, _ = S.host_batch(P, B)
+    end_out = tags[5]
+    rng = np.random.default_rng(0)
+    cut = np.empty(B, np.int32)
+    for i in range(B):
+        ends = np.nonzero(tok_h[st_h[i]: st_h[i] + ln_h[i]] == end_out)[0]
+        cut[i] = int(rng.choice(ends)) + 1 if len(ends) else ln_h[i]
+    tokens = torch.as_tensor(tok_h).to(dev)
+    starts = torch.as_tensor(st_h).to(dev)
+    lengths = torch.as_tensor(cut).to(dev)
+    px = PX.Parason(tags)
+    first = px.fork(tokens, starts, lengths, seed=True)  # sizes the outputs
+    W, T, _ = (int(x) for x in first["totals"].cpu())
+    n_rows_forked = int((first["worker_off"][1:] > first["worker_off"][:-1]).sum().item())
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    fork_ms = timed(lambda: px.fork(tokens, starts, lengths, seed=True, max_workers=W, ctx_capacity=T))
+    # workers: their context + 64 generated tokens + </Thread>, packed
+    ctx_lens = first["ctx_lengths"].to(torch.int64)
+    wlen = ctx_lens + 65
+    wstarts = torch.zeros(W, dtype=torch.int64, device=dev)
+    wstarts[1:] = torch.cumsum(wlen, 0)[:-1]
+    wtokens = torch.full((int(wlen.sum().item()),), 11, dtype=torch.int32, device=dev)
+    # copy each context to the front of its worker sequence (setup, not timed)
+    idx = torch.repeat_interleave(torch.arange(W, device=dev), ctx_lens)
+    within = torch.arange(int(ctx_lens.sum().item()), device=dev) - torch.repeat_interleave(
+        first["ctx_starts"], ctx_lens)
+    wtokens[wstarts[idx] + within] = first["ctx_tokens"][first["ctx_starts"][idx] + within]
+    wtokens[wstarts + wlen - 1] = tags[11]
+    wl32 = wlen.to(torch.int32)
+    jfirst = px.join(tokens, starts, lengths, first["worker_off"], wtokens, wstarts, wl32)
+    JT = int(jfirst["totals"][0].item())
+    assert not jfirst["row_status"].any().item()
+    join_ms = timed(lambda: px.join(tokens, starts, lengths, first["worker_off"], wtokens, wstarts, wl32,
+                                    capacity=JT))
+    rows_read = int(cut.astype(np.int64).sum())
+    tail = JT - rows_read - B  # each worker's <Thread> ... </Thread> span
+    # fork: rows read once, contexts written, 24 B of record per worker, 28 B of offsets/status per row
+    fork_bytes = 4 * rows_read + 4 * T + 24 * W + 28 * B
+    # join: rows and worker spans read, joined rows written, 36 B per row and 20 B per worker of offsets/checks
+    join_bytes = 4 * rows_read + 4 * tail + 4 * JT + 36 * B + 20 * W
+    res = {
+        "metric": "fork/join packing for tool-call execution: context tokens written per second + % of HBM roofline, "
+                  "1xMI355X",
+        "value": T / (fork_ms * 1e-3),
+        "unit": "context tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": fork_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic (typical-workload rollouts cut after an outline; generated thread text is filler)",
+        "config": {"workload": "fork %d rows (%d tokens) into %d workers (%d context tokens); join back with 64 "
+                               "generated tokens per worker" % (B, rows_read, W, T),
+                   "rows": B, "rows_forked": n_rows_forked, "workers": W, "context_tokens": T, "joined_tokens": JT},
+        "join_ms": join_ms,
+        "join_tokens_per_s": JT / (join_ms * 1e-3),
+        "roofline": {"kernel": "parason_fork (all launches, HIP events)", "bound": "hbm",
+                     "achieved": fork_bytes / (fork_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": fork_bytes / (fork_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                     "kernel_ms": fork_ms, "algorithmic_bytes": fork_bytes},
+        "join_roofline": {"achieved": join_bytes / (join_ms * 1e-3) / 1e9, "unit": "GB/s",
+                          "frac": join_bytes / (join_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": join_bytes},
     }
     print(json.dumps(res), flush=True)
 

@@ -275,6 +275,87 @@ int parason_decode_init(parason_decode_state *states, int64_t batch, void *strea
 int parason_decode_step(const parason_handle *h, parason_decode_state *states, const int32_t *tokens, int64_t batch,
                         void *logits, int64_t vocab, int64_t row_stride, int32_t dtype, int32_t eos_id, void *stream);
 
+/* ---- fork/join packing for tool-call execution ---------------------------
+ * At inference the runtime decodes a trajectory until the outline of a
+ * <Parallel> region is complete, dispatches every <Subtask> / <Trial> entry as
+ * an independent worker and returns the workers' <Thread> outputs to the main
+ * trajectory (Sec. 3.4 "Inference"; format of Figure 4, Sec. 3.2).  These two
+ * calls are that data movement on token ids (KV-cache handling is the
+ * engine's).
+ *
+ * fork: row i must end with </Outlines>; its outline starts at the last
+ * <Outlines> before that, which must directly follow <Parallel>, and must hold
+ * one or more entries "<Subtask> text+ </Subtask>" or "<Trial> text+ </Trial>"
+ * back to back.  Worker k of row i gets the context
+ *     row i ++ <Thread> ++ (the text of entry k, with PARASON_FORK_SEED_ENTRY)
+ * Workers are numbered row by row, entry by entry.
+ *
+ * join: worker w of row i hands back its whole sequence (its context followed
+ * by what it generated, ending with its </Thread>).  Joined row i is
+ *     row i ++ seq_w[len(row i):] for the row's workers in order
+ *           ++ </Parallel> (with PARASON_JOIN_CLOSE_PARALLEL)
+ * i.e. each worker's <Thread> ... </Thread> span as the worker saw it; with
+ * PARASON_JOIN_APPEND_ONLY row i itself is left out of the output. */
+#define PARASON_FORK_SEED_ENTRY (1u << 0)
+#define PARASON_JOIN_CLOSE_PARALLEL (1u << 0)
+#define PARASON_JOIN_APPEND_ONLY (1u << 1)
+
+/* per-row status bits (row_status) */
+#define PARASON_PACK_NO_OUTLINE_END (1u << 0) /* fork: the row does not end with </Outlines> */
+#define PARASON_PACK_NO_OUTLINE (1u << 1)     /* fork: no <Outlines> before it, or not after <Parallel> */
+#define PARASON_PACK_BAD_ENTRY (1u << 2)      /* fork: the outline is not a run of well-formed entries */
+#define PARASON_PACK_BAD_THREAD (1u << 3)     /* join: a worker sequence is not <Thread> ... </Thread>
+                                                 after the row (copied as it is) */
+#define PARASON_PACK_TOO_LONG (1u << 4)       /* an output row would exceed INT32_MAX tokens (not written) */
+#define PARASON_PACK_BAD_ROW (1u << 5)        /* negative start or length, or (join) worker_off out of
+                                                 order or beyond n_workers (not written) */
+
+typedef struct parason_fork_outputs {
+    /* capacities: if the batch needs more, only worker_off, row_status and
+     * totals are written (totals[2] = 1); allocate totals[0] workers and
+     * totals[1] tokens and call again */
+    int64_t max_workers;
+    int64_t ctx_capacity;     /* int32 tokens */
+    int32_t *ctx_tokens;      /* [ctx_capacity] contexts, packed in worker order */
+    int64_t *ctx_starts;      /* [max_workers] */
+    int32_t *ctx_lengths;     /* [max_workers] */
+    int32_t *ctx_row;         /* [max_workers] the row a worker belongs to */
+    int32_t *ctx_entry;       /* [max_workers] its entry index in the outline */
+    int32_t *ctx_kind;        /* [max_workers] 1 = Subtask, 2 = Trial */
+    int64_t *worker_off;      /* [n_rows + 1] first worker of each row; [n_rows] = workers */
+    uint32_t *row_status;     /* [n_rows] PARASON_PACK_* (0: dispatched) */
+    int64_t *totals;          /* [3] workers, context tokens, over capacity (0/1) */
+} parason_fork_outputs;
+
+typedef struct parason_join_outputs {
+    int64_t capacity;         /* int32 tokens of out tokens; see parason_fork_outputs */
+    int32_t *tokens;          /* [capacity] joined rows, packed */
+    int64_t *starts;          /* [n_rows + 1]; [n_rows] = total tokens */
+    int32_t *lengths;         /* [n_rows] */
+    uint32_t *row_status;     /* [n_rows] PARASON_PACK_* */
+    int64_t *totals;          /* [2] tokens, over capacity (0/1) */
+} parason_join_outputs;
+
+/* Bytes of device workspace parason_fork / parason_join need for n_rows rows. */
+int parason_fork_workspace_size(int64_t n_rows, size_t *bytes);
+int parason_join_workspace_size(int64_t n_rows, size_t *bytes);
+
+/* Fork a batch of rows (device pointers as for parason_run; the output
+ * struct itself is host memory, its arrays device memory), asynchronously on
+ * `stream`.  The tag ids are those of h.  Host-side argument errors return a
+ * negative status before any launch; per-row problems go to row_status. */
+int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                 int64_t n_rows, uint32_t flags, const parason_fork_outputs *out, void *workspace,
+                 size_t workspace_bytes, void *stream);
+
+/* Join: rows as for parason_fork, worker_off[n_rows + 1] as parason_fork wrote
+ * it, and the n_workers worker sequences (wtokens, wstarts, wlengths), each
+ * beginning with its row (not checked) and continuing from its context. */
+int parason_join(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                 int64_t n_rows, const int64_t *worker_off, const int32_t *wtokens, const int64_t *wstarts,
+                 const int32_t *wlengths, int64_t n_workers, uint32_t flags, const parason_join_outputs *out,
+                 void *workspace, size_t workspace_bytes, void *stream);
+
 /* Static description of a status code. */
 const char *parason_strerror(int status);
 

@@ -1,7 +1,7 @@
 """Build steps for the native libraries (run on the CPU; hipcc cross-compiles gfx950).
 
 * ``libparason.so``      -- the hot path: HIP kernels + C-ABI (``csrc/parason.hip``,
-  ``csrc/pg.hip``, ``csrc/decode.hip``)
+  ``csrc/pg.hip``, ``csrc/decode.hip``, ``csrc/fork.hip``)
 * ``libparason_synth.so``-- device side of the synthetic generator (``synth/synth.hip``)
 * ``libparason_synth_host.so`` -- host mirror of the generator (g++)
 
@@ -31,9 +31,9 @@ HIP_FLAGS = [
 LIBS = {
     "parason": dict(
         out=os.path.join(PKG, "libparason.so"),
-        srcs=[os.path.join(PKG, "csrc", f) for f in ("parason.hip", "pg.hip", "decode.hip")],
+        srcs=[os.path.join(PKG, "csrc", f) for f in ("parason.hip", "pg.hip", "decode.hip", "fork.hip")],
         deps=[os.path.join(PKG, "csrc", f) for f in ("abi_common.h", "device_common.h", "parason_kernels.h",
-                                                       "pg_kernels.h", "decode_kernels.h")]
+                                                       "pg_kernels.h", "decode_kernels.h", "fork_kernels.h")]
         + [os.path.join(INCLUDE, "parason.h")],
         kind="hip",
     ),

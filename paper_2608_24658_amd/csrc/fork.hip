@@ -1,0 +1,202 @@
+/*
+ * fork.hip -- C-ABI of fork/join packing for tool-call execution (kernels in
+ * fork_kernels.h).
+ */
+#include <algorithm>
+
+#include "abi_common.h"
+#include "fork_kernels.h"
+
+using abi::align_up;
+using abi::cu_count;
+
+namespace {
+
+constexpr int COPY_BLOCKS_PER_CU = 8;
+
+/* Workspace of fork (K = 2 counts per row) or join (K = 1). */
+struct PackLayout {
+    size_t counts, outl, tile_sum, tile_off, tok_off, over, end;
+    int64_t tiles;
+};
+
+PackLayout pack_layout(int64_t n, int K)
+{
+    PackLayout L;
+    L.tiles = n > 0 ? (n + pk::PACK_TILE - 1) / pk::PACK_TILE : 1;
+    size_t o = 0;
+    L.counts = o;
+    o = align_up(o + (size_t)(n > 0 ? n : 1) * K * sizeof(int64_t));
+    L.outl = o;
+    o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    L.tile_sum = o;
+    o = align_up(o + (size_t)L.tiles * K * sizeof(int64_t));
+    L.tile_off = o;
+    o = align_up(o + (size_t)L.tiles * K * sizeof(int64_t));
+    L.tok_off = o;
+    o = align_up(o + (size_t)(n + 1) * sizeof(int64_t));
+    L.over = o;
+    o = align_up(o + sizeof(int32_t));
+    L.end = o;
+    return L;
+}
+
+bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int parason_fork_workspace_size(int64_t n_rows, size_t *bytes)
+{
+    if (!bytes) return PARASON_ERR_NULL;
+    if (n_rows < 0 || n_rows > INT32_MAX) return PARASON_ERR_SIZE;
+    *bytes = pack_layout(n_rows, 2).end;
+    return PARASON_OK;
+}
+
+int parason_join_workspace_size(int64_t n_rows, size_t *bytes)
+{
+    if (!bytes) return PARASON_ERR_NULL;
+    if (n_rows < 0 || n_rows > INT32_MAX) return PARASON_ERR_SIZE;
+    *bytes = pack_layout(n_rows, 1).end;
+    return PARASON_OK;
+}
+
+int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                 int64_t n_rows, uint32_t flags, const parason_fork_outputs *out, void *workspace,
+                 size_t workspace_bytes, void *stream_ptr)
+{
+    if (!h || !out) return PARASON_ERR_NULL;
+    if (n_rows < 0 || n_rows > INT32_MAX || out->max_workers < 0 || out->ctx_capacity < 0) return PARASON_ERR_SIZE;
+    if (flags & ~(uint32_t)PARASON_FORK_SEED_ENTRY) return PARASON_ERR_PARAM;
+    if (!out->worker_off || !out->totals || !workspace) return PARASON_ERR_NULL;
+    if (n_rows > 0 && (!tokens || !starts || !lengths || !out->row_status)) return PARASON_ERR_NULL;
+    if (out->max_workers > 0 &&
+        (!out->ctx_starts || !out->ctx_lengths || !out->ctx_row || !out->ctx_entry || !out->ctx_kind))
+        return PARASON_ERR_NULL;
+    if (out->ctx_capacity > 0 && !out->ctx_tokens) return PARASON_ERR_NULL;
+    if ((tokens && !aligned(tokens, 4)) || !aligned(workspace, abi::ALIGN)) return PARASON_ERR_ALIGN;
+    const PackLayout L = pack_layout(n_rows, 2);
+    if (workspace_bytes < L.end) return PARASON_ERR_WORKSPACE;
+    const int cus = cu_count();
+    if (cus <= 0) return PARASON_ERR_DEVICE;
+    hipStream_t stream = (hipStream_t)stream_ptr;
+    char *ws = (char *)workspace;
+
+    pk::ForkArgs fa;
+    fa.tokens = tokens;
+    fa.starts = starts;
+    fa.lengths = lengths;
+    fa.n = n_rows;
+    fa.tm = h->tm;
+    fa.seed = (flags & PARASON_FORK_SEED_ENTRY) != 0;
+    fa.thread_id = h->cfg.tag_ids[pk::C_THR - 1];
+    fa.status = out->row_status;
+    fa.counts = (int64_t *)(ws + L.counts);
+    fa.outl = (int32_t *)(ws + L.outl);
+    fa.worker_off = out->worker_off;
+    fa.tok_off = (const int64_t *)(ws + L.tok_off);
+    fa.over = (const int32_t *)(ws + L.over);
+    fa.ctx_starts = out->ctx_starts;
+    fa.ctx_lengths = out->ctx_lengths;
+    fa.ctx_row = out->ctx_row;
+    fa.ctx_entry = out->ctx_entry;
+    fa.ctx_kind = out->ctx_kind;
+    fa.ctx_tokens = out->ctx_tokens;
+
+    pk::PackScan<2> ps;
+    ps.vals = fa.counts;
+    ps.n = n_rows;
+    ps.tile_sum = (int64_t *)(ws + L.tile_sum);
+    ps.tile_off = (int64_t *)(ws + L.tile_off);
+    ps.out[0] = out->worker_off;
+    ps.out[1] = (int64_t *)(ws + L.tok_off);
+    ps.cap[0] = out->max_workers;
+    ps.cap[1] = out->ctx_capacity;
+    ps.totals = out->totals;
+    ps.over = (int32_t *)(ws + L.over);
+
+    const unsigned wave_blocks = (unsigned)std::min<int64_t>((n_rows + 3) / 4, (int64_t)cus * 8);
+    const unsigned tiles = (unsigned)L.tiles;
+    if (n_rows > 0) pk::fork_outline<false><<<dim3(wave_blocks), dim3(256), 0, stream>>>(fa);
+    if (n_rows > 0) pk::pack_tiles<2><<<dim3(tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
+    pk::pack_top<2><<<dim3(1), dim3(1024), 0, stream>>>(ps, n_rows > 0 ? L.tiles : 0);
+    if (n_rows > 0) {
+        pk::pack_rows<2><<<dim3(tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
+        pk::fork_outline<true><<<dim3(wave_blocks), dim3(256), 0, stream>>>(fa);
+        const unsigned copy_blocks = (unsigned)(cus * COPY_BLOCKS_PER_CU); /* persistent, tiled over the output */
+        pk::fork_copy<<<dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream>>>(fa);
+    }
+    return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
+}
+
+int parason_join(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                 int64_t n_rows, const int64_t *worker_off, const int32_t *wtokens, const int64_t *wstarts,
+                 const int32_t *wlengths, int64_t n_workers, uint32_t flags, const parason_join_outputs *out,
+                 void *workspace, size_t workspace_bytes, void *stream_ptr)
+{
+    if (!h || !out) return PARASON_ERR_NULL;
+    if (n_rows < 0 || n_rows > INT32_MAX || n_workers < 0 || out->capacity < 0) return PARASON_ERR_SIZE;
+    if (flags & ~(uint32_t)(PARASON_JOIN_CLOSE_PARALLEL | PARASON_JOIN_APPEND_ONLY)) return PARASON_ERR_PARAM;
+    if (!out->starts || !out->totals || !workspace) return PARASON_ERR_NULL;
+    if (n_rows > 0 && (!tokens || !starts || !lengths || !worker_off || !out->lengths || !out->row_status))
+        return PARASON_ERR_NULL;
+    if (n_workers > 0 && (!wtokens || !wstarts || !wlengths)) return PARASON_ERR_NULL;
+    if (out->capacity > 0 && !out->tokens) return PARASON_ERR_NULL;
+    if ((tokens && !aligned(tokens, 4)) || (wtokens && !aligned(wtokens, 4)) || !aligned(workspace, abi::ALIGN))
+        return PARASON_ERR_ALIGN;
+    const PackLayout L = pack_layout(n_rows, 1);
+    if (workspace_bytes < L.end) return PARASON_ERR_WORKSPACE;
+    const int cus = cu_count();
+    if (cus <= 0) return PARASON_ERR_DEVICE;
+    hipStream_t stream = (hipStream_t)stream_ptr;
+    char *ws = (char *)workspace;
+
+    pk::JoinArgs ja;
+    ja.tokens = tokens;
+    ja.starts = starts;
+    ja.lengths = lengths;
+    ja.n = n_rows;
+    ja.worker_off = worker_off;
+    ja.n_workers = n_workers;
+    ja.wtokens = wtokens;
+    ja.wstarts = wstarts;
+    ja.wlengths = wlengths;
+    ja.thread_id = h->cfg.tag_ids[pk::C_THR - 1];
+    ja.end_thread_id = h->cfg.tag_ids[pk::C_END_THR - 1];
+    ja.end_par_id = h->cfg.tag_ids[pk::C_END_PAR - 1];
+    ja.close = (flags & PARASON_JOIN_CLOSE_PARALLEL) != 0;
+    ja.append_only = (flags & PARASON_JOIN_APPEND_ONLY) != 0;
+    ja.status = out->row_status;
+    ja.out_len64 = (int64_t *)(ws + L.counts);
+    ja.out_lengths = out->lengths;
+    ja.out_starts = out->starts;
+    ja.over = (const int32_t *)(ws + L.over);
+    ja.out_tokens = out->tokens;
+
+    pk::PackScan<1> ps;
+    ps.vals = ja.out_len64;
+    ps.n = n_rows;
+    ps.tile_sum = (int64_t *)(ws + L.tile_sum);
+    ps.tile_off = (int64_t *)(ws + L.tile_off);
+    ps.out[0] = out->starts;
+    ps.cap[0] = out->capacity;
+    ps.totals = out->totals;
+    ps.over = (int32_t *)(ws + L.over);
+
+    const unsigned tiles = (unsigned)L.tiles;
+    if (n_rows > 0) {
+        pk::join_size<<<dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0, stream>>>(ja);
+        pk::pack_tiles<1><<<dim3(tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
+    }
+    pk::pack_top<1><<<dim3(1), dim3(1024), 0, stream>>>(ps, n_rows > 0 ? L.tiles : 0);
+    if (n_rows > 0) {
+        pk::pack_rows<1><<<dim3(tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
+        const unsigned copy_blocks = (unsigned)(cus * COPY_BLOCKS_PER_CU);
+        pk::join_copy<<<dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream>>>(ja);
+    }
+    return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,499 @@
+/*
+ * fork_kernels.h -- gfx950 kernels of fork/join packing for tool-call
+ * execution (Sec. 3.4 "Inference": the runtime decodes until an outline is
+ * complete, dispatches each <Subtask> / <Trial> entry as a worker and returns
+ * the workers' <Thread> outputs to the main trajectory; format of Figure 4).
+ *
+ * fork
+ *   fork_outline<false>  one wave per row: checks that the row ends with
+ *                        </Outlines>, searches backwards for the outline's
+ *                        <Outlines>, then walks the outline forwards in
+ *                        256-token chunks, compacting its tags in order with
+ *                        ballots and checking each against the one before it
+ *                        (entries open, hold text, close, back to back).
+ *                        Writes the row's worker and token counts.
+ *   pack_tiles/top/rows  exclusive scans of those counts (worker_off and the
+ *                        context token offsets), totals and the capacity check.
+ *   fork_outline<true>   the same walk again, now writing each worker's record
+ *                        (row, entry, kind, context start and length).
+ *   fork_copy            tiled over the context tokens: every block step
+ *                        fills 4096 consecutive tokens; a 64-way wave search
+ *                        over the context starts finds the first worker, each
+ *                        token is taken from the row, the <Thread> id or the
+ *                        entry's text.
+ * join
+ *   join_size            one thread per row: joined length and thread checks.
+ *   pack_*               exclusive scan of the joined lengths.
+ *   join_copy            tiled the same way over the joined tokens: the row,
+ *                        each worker's <Thread> ... </Thread> span, and
+ *                        </Parallel>.
+ *
+ * All copies are dword-granular and coalesced (rows and contexts start at any
+ * element offset); they are HBM-bound.  Tiling the output keeps every block's
+ * work the same size however long the rows are.
+ */
+#pragma once
+#include "device_common.h"
+
+namespace pk {
+
+constexpr int PACK_THREADS = 256;
+constexpr int PACK_ROWS_PER_THREAD = 16;
+constexpr int PACK_TILE = PACK_THREADS * PACK_ROWS_PER_THREAD;
+constexpr int CHUNK = 4 * WAVE; /* tokens per wave step of the outline walk */
+
+/* ---- exclusive scans of K int64 values per row -------------------------- */
+
+template <int K>
+struct PackScan {
+    const int64_t *vals;   /* [n][K] */
+    int64_t n;
+    int64_t *tile_sum;     /* [tiles][K] */
+    int64_t *tile_off;     /* [tiles][K] */
+    int64_t *out[K];       /* [n + 1] each: exclusive offsets, out[k][n] = total */
+    int64_t cap[K];        /* totals above these set *over */
+    int64_t *totals;       /* optional: [K + 1] totals and the over flag, for the caller */
+    int32_t *over;         /* workspace copy of the over flag */
+};
+
+template <int K>
+__global__ void __launch_bounds__(PACK_THREADS) pack_tiles(PackScan<K> a)
+{
+    __shared__ int64_t lds[K * PACK_THREADS];
+    const int64_t r0 = (int64_t)blockIdx.x * PACK_TILE + (int64_t)threadIdx.x * PACK_ROWS_PER_THREAD;
+    int64_t v[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) v[k] = 0;
+    for (int j = 0; j < PACK_ROWS_PER_THREAD; ++j) {
+        const int64_t r = r0 + j;
+        if (r < a.n) {
+#pragma unroll
+            for (int k = 0; k < K; ++k) v[k] += a.vals[r * K + k];
+        }
+    }
+    block_tree_sum<int64_t, K>(v, lds);
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) a.tile_sum[blockIdx.x * K + k] = v[k];
+    }
+}
+
+template <int K>
+__global__ void __launch_bounds__(1024) pack_top(PackScan<K> a, int64_t tiles)
+{
+    __shared__ int64_t part[K][1024 / WAVE];
+    __shared__ int64_t carry[K];
+    if (threadIdx.x < K) carry[threadIdx.x] = 0;
+    __syncthreads();
+    for (int64_t base = 0; base < tiles; base += 1024) {
+        const int64_t i = base + threadIdx.x;
+        int64_t v[K], inc[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            v[k] = i < tiles ? a.tile_sum[i * K + k] : 0;
+            inc[k] = wave_inclusive_scan(v[k]);
+            if ((threadIdx.x & (WAVE - 1)) == WAVE - 1) part[k][threadIdx.x / WAVE] = inc[k];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            int64_t before = carry[k];
+            for (int w = 0; w < (int)(threadIdx.x / WAVE); ++w) before += part[k][w];
+            if (i < tiles) a.tile_off[i * K + k] = before + inc[k] - v[k];
+        }
+        __syncthreads();
+        if (threadIdx.x < K) {
+            int64_t t = 0;
+            for (int w = 0; w < 1024 / WAVE; ++w) t += part[threadIdx.x][w];
+            carry[threadIdx.x] += t;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        int32_t over = 0;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            a.out[k][a.n] = carry[k];
+            over |= carry[k] > a.cap[k] ? 1 : 0;
+            if (a.totals) a.totals[k] = carry[k];
+        }
+        if (a.totals) a.totals[K] = over;
+        a.over[0] = over;
+    }
+}
+
+template <int K>
+__global__ void __launch_bounds__(PACK_THREADS) pack_rows(PackScan<K> a)
+{
+    __shared__ int64_t part[K][PACK_THREADS / WAVE];
+    const int64_t r0 = (int64_t)blockIdx.x * PACK_TILE + (int64_t)threadIdx.x * PACK_ROWS_PER_THREAD;
+    int64_t s[K], off[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        s[k] = 0;
+        for (int j = 0; j < PACK_ROWS_PER_THREAD; ++j) {
+            const int64_t r = r0 + j;
+            s[k] += r < a.n ? a.vals[r * K + k] : 0;
+        }
+        const int64_t inc = wave_inclusive_scan(s[k]);
+        if ((threadIdx.x & (WAVE - 1)) == WAVE - 1) part[k][threadIdx.x / WAVE] = inc;
+        off[k] = inc - s[k];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        off[k] += a.tile_off[blockIdx.x * K + k];
+        for (int w = 0; w < (int)(threadIdx.x / WAVE); ++w) off[k] += part[k][w];
+        for (int j = 0; j < PACK_ROWS_PER_THREAD; ++j) {
+            const int64_t r = r0 + j;
+            if (r < a.n) {
+                a.out[k][r] = off[k];
+                off[k] += a.vals[r * K + k];
+            }
+        }
+    }
+}
+
+/* ---- fork --------------------------------------------------------------- */
+
+struct ForkArgs {
+    const int32_t *tokens;
+    const int64_t *starts;
+    const int32_t *lengths;
+    int64_t n;
+    TagMatch tm;
+    bool seed;              /* contexts end with the entry's text */
+    int32_t thread_id;      /* token id of <Thread> */
+    uint32_t *status;       /* [n] PARASON_PACK_* */
+    int64_t *counts;        /* [n][2]: workers, context tokens */
+    int32_t *outl;          /* [n]: position of the outline's <Outlines> */
+    /* filled in by the scan, read by the write pass and the copy */
+    const int64_t *worker_off;
+    const int64_t *tok_off;
+    const int32_t *over;
+    int64_t *ctx_starts;
+    int32_t *ctx_lengths, *ctx_row, *ctx_entry, *ctx_kind;
+    int32_t *ctx_tokens;
+};
+
+__device__ __forceinline__ int64_t wave_max(int64_t v)
+{
+#pragma unroll
+    for (int d = WAVE / 2; d > 0; d >>= 1) {
+        const int64_t o = __shfl_xor(v, d, WAVE);
+        v = o > v ? o : v;
+    }
+    return v;
+}
+
+/* One wave per row (grid-stride).  WRITE = false: status and counts;
+ * WRITE = true: the worker records of rows whose outline is well formed. */
+template <bool WRITE>
+__global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
+{
+    __shared__ uint32_t ev_all[4][CHUNK]; /* per wave: (offset in chunk << 4) | class, in position order */
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int wv = threadIdx.x / WAVE;
+    uint32_t *ev = ev_all[wv];
+    const bool contig = a.tm.contiguous != 0;
+    if (WRITE && a.over[0]) return;
+    const int64_t n_waves = (int64_t)gridDim.x * 4;
+    for (int64_t i = uniform64((int64_t)blockIdx.x * 4 + wv); i < a.n; i += n_waves) {
+        const int64_t g = a.starts[i];
+        const int32_t L = a.lengths[i];
+        int64_t o;
+        if (WRITE) {
+            if (a.status[i] != 0 || a.counts[2 * i] == 0) continue;
+            o = a.outl[i];
+        } else {
+            uint32_t st = 0;
+            if (L < 0 || g < 0) st = PARASON_PACK_BAD_ROW;
+            else if (L == 0 || classify(a.tm, a.tokens[g + L - 1], contig) != C_END_OUT) st = PARASON_PACK_NO_OUTLINE_END;
+            o = -1;
+            if (st == 0) {
+                /* the last <Outlines> before the final </Outlines> */
+                for (int64_t e = (int64_t)L - 1; e > 0 && o < 0; e -= CHUNK) {
+                    const int64_t lo = e > CHUNK ? e - CHUNK : 0;
+                    int64_t best = -1;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int64_t p = lo + lane + WAVE * j;
+                        if (p < e && classify(a.tm, a.tokens[g + p], contig) == C_OUT) best = p > best ? p : best;
+                    }
+                    o = uniform64(wave_max(best));
+                }
+                if (o < 1 || classify(a.tm, a.tokens[g + o - 1], contig) != C_PAR) st = PARASON_PACK_NO_OUTLINE;
+            }
+            if (st != 0) {
+                if (lane == 0) {
+                    a.status[i] = st;
+                    a.counts[2 * i] = 0;
+                    a.counts[2 * i + 1] = 0;
+                    a.outl[i] = -1;
+                }
+                continue;
+            }
+        }
+        /* walk the outline [o + 1, L - 1) in chunks; events are its tags */
+        const int64_t end = (int64_t)L - 1;
+        int64_t m = 0;                       /* tags before this chunk */
+        int64_t prev_pos = o;                /* the tag before the current one */
+        uint32_t prev_cls = C_OUT;
+        bool ok = true;
+        const int64_t w0 = WRITE ? a.worker_off[i] : 0;
+        const int64_t t0 = WRITE ? a.tok_off[i] : 0;
+        for (int64_t lo = o + 1; lo < end; lo += CHUNK) {
+            uint64_t b[4];
+            uint32_t c[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t p = lo + lane + WAVE * j;
+                c[j] = p < end ? classify(a.tm, a.tokens[g + p], contig) : C_TEXT;
+                b[j] = __ballot(c[j] != C_TEXT);
+            }
+            uint32_t base = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (c[j] != C_TEXT) {
+                    const uint32_t idx = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(b[j] >> 32),
+                                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)b[j], 0u));
+                    ev[idx] = ((uint32_t)(lane + WAVE * j) << 4) | c[j];
+                }
+                base += (uint32_t)__popcll(b[j]);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            for (uint32_t e = lane; e < base; e += WAVE) {
+                const uint32_t x = ev[e];
+                const int64_t P = lo + (x >> 4);
+                const uint32_t cl = x & 15u;
+                int64_t pp = prev_pos;
+                uint32_t pc = prev_cls;
+                if (e > 0) {
+                    const uint32_t y = ev[e - 1];
+                    pp = lo + (y >> 4);
+                    pc = y & 15u;
+                }
+                const int64_t J = m + e;
+                if ((J & 1) == 0) {
+                    /* an entry opens right after <Outlines> or the previous entry */
+                    ok = ok && (cl == C_SUB || cl == C_TRI) && P == pp + 1;
+                } else {
+                    /* and closes with its own tag after at least one text token */
+                    ok = ok && (pc == C_SUB || pc == C_TRI) && cl == pc + 1 && P >= pp + 2;
+                    if (WRITE) {
+                        const int64_t k = J >> 1;
+                        const int64_t w = w0 + k;
+                        const int64_t len = P - pp - 1;
+                        /* the entry texts before entry k fill positions o+1 .. pp-1 but for 2k tags */
+                        const int64_t seed_before = pp - (o + 1) - 2 * k;
+                        a.ctx_starts[w] = t0 + k * ((int64_t)L + 1) + (a.seed ? seed_before : 0);
+                        a.ctx_lengths[w] = (int32_t)((int64_t)L + 1 + (a.seed ? len : 0));
+                        a.ctx_row[w] = (int32_t)i;
+                        a.ctx_entry[w] = (int32_t)k;
+                        a.ctx_kind[w] = pc == C_SUB ? (int32_t)T_SUB : (int32_t)T_TRI;
+                    }
+                }
+            }
+            if (base > 0) {
+                const uint32_t y = ev[base - 1];
+                prev_pos = lo + (y >> 4);
+                prev_cls = y & 15u;
+            }
+            m += base;
+            __builtin_amdgcn_wave_barrier(); /* ev is rewritten by the next chunk */
+        }
+        if (!WRITE) {
+            ok = __ballot(!ok) == 0;
+            /* an even, non-zero number of tags, the last one right before </Outlines> */
+            ok = ok && m >= 2 && (m & 1) == 0 && prev_pos == end - 1;
+            const int64_t n_e = ok ? m / 2 : 0;
+            const int64_t text = end - (o + 1) - m; /* entry text tokens of the whole outline */
+            int64_t toks = n_e * ((int64_t)L + 1) + (a.seed ? text : 0);
+            uint32_t st = ok ? 0u : (uint32_t)PARASON_PACK_BAD_ENTRY;
+            if (ok && (int64_t)L + 1 + (a.seed ? text : 0) > (int64_t)INT32_MAX) {
+                st = PARASON_PACK_TOO_LONG;
+                toks = 0;
+            }
+            if (lane == 0) {
+                a.status[i] = st;
+                a.counts[2 * i] = st == 0 ? n_e : 0;
+                a.counts[2 * i + 1] = st == 0 ? toks : 0;
+                a.outl[i] = (int32_t)o;
+            }
+        }
+    }
+}
+
+/* ---- tiled copies -------------------------------------------------------- */
+
+constexpr int64_t TILE = 16 * PACK_THREADS; /* output tokens per block step */
+
+/* Largest index s in [0, count) with offs[s] <= x (offs ascending, offs[0] <= x),
+ * by wave 0 in 64-way rounds; the result is returned to every thread. */
+__device__ __forceinline__ int64_t find_segment(const int64_t *offs, int64_t count, int64_t x, int64_t *lds)
+{
+    if (threadIdx.x < WAVE) {
+        const int lane = threadIdx.x;
+        int64_t lo = 0, hi = count;
+        while (hi - lo > 1) {
+            const int64_t step = (hi - lo + WAVE - 1) / WAVE;
+            const int64_t idx = lo + lane * step;
+            const uint64_t m = __ballot(idx < hi && offs[idx] <= x);
+            const int64_t last = 63 - __builtin_clzll(m | 1ull);
+            lo = lo + last * step;
+            hi = min(hi, lo + step);
+        }
+        if (lane == 0) lds[0] = lo;
+    }
+    __syncthreads();
+    const int64_t s = lds[0];
+    __syncthreads();
+    return s;
+}
+
+/* dst[d] = src(d) for d in [d0, d1) with the whole block, four loads in
+ * flight per thread; src(d) must be a pure function of d. */
+template <class Src>
+__device__ __forceinline__ void block_fill(int32_t *__restrict__ dst, int64_t d0, int64_t d1, const Src &src)
+{
+    for (int64_t base = d0; base < d1; base += 4 * PACK_THREADS) {
+        int32_t v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t d = base + j * PACK_THREADS + threadIdx.x;
+            if (d < d1) v[j] = src(d);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t d = base + j * PACK_THREADS + threadIdx.x;
+            if (d < d1) dst[d] = v[j];
+        }
+    }
+}
+
+/* Contexts, tiled over their tokens: each block step fills TILE consecutive
+ * context tokens, starting from the worker that holds the first of them. */
+__global__ void __launch_bounds__(PACK_THREADS) fork_copy(ForkArgs a)
+{
+    __shared__ int64_t found;
+    if (a.over[0]) return;
+    const int64_t W = a.worker_off[a.n];
+    const int64_t T = a.tok_off[a.n];
+    for (int64_t lo = (int64_t)blockIdx.x * TILE; lo < T; lo += (int64_t)gridDim.x * TILE) {
+        const int64_t hi = min(lo + TILE, T);
+        for (int64_t w = find_segment(a.ctx_starts, W, lo, &found); w < W; ++w) {
+            const int64_t cs = a.ctx_starts[w];
+            if (cs >= hi) break;
+            const int64_t r = a.ctx_row[w];
+            const int64_t L = a.lengths[r];
+            const int32_t *src = a.tokens + a.starts[r];
+            const int64_t k = a.ctx_entry[w];
+            /* first text token of entry k (see fork_outline): o + 2 + 2k + texts before it */
+            const int64_t first = a.outl[r] + 2 + 2 * k + (cs - a.tok_off[r] - k * (L + 1));
+            const int32_t thr = a.thread_id;
+            const int64_t end = min(hi, cs + (int64_t)a.ctx_lengths[w]);
+            block_fill(a.ctx_tokens, max(lo, cs), end, [=](int64_t d) {
+                const int64_t off = d - cs;
+                return off < L ? src[off] : (off == L ? thr : src[first + off - L - 1]);
+            });
+        }
+    }
+}
+
+/* ---- join --------------------------------------------------------------- */
+
+struct JoinArgs {
+    const int32_t *tokens;
+    const int64_t *starts;
+    const int32_t *lengths;
+    int64_t n;
+    const int64_t *worker_off;
+    int64_t n_workers;
+    const int32_t *wtokens;
+    const int64_t *wstarts;
+    const int32_t *wlengths;
+    int32_t thread_id, end_thread_id, end_par_id;
+    bool close, append_only;
+    uint32_t *status;
+    int64_t *out_len64;     /* [n] joined lengths for the scan (0 for rows not written) */
+    int32_t *out_lengths;
+    const int64_t *out_starts;
+    const int32_t *over;
+    int32_t *out_tokens;
+};
+
+__global__ void __launch_bounds__(256) join_size(JoinArgs a)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= a.n) return;
+    const int64_t L = a.lengths[i], g = a.starts[i];
+    const int64_t w0 = a.worker_off[i], w1 = a.worker_off[i + 1];
+    uint32_t st = 0;
+    int64_t tot = 0;
+    if (L < 0 || g < 0 || w0 < 0 || w1 < w0 || w1 > a.n_workers) {
+        st = PARASON_PACK_BAD_ROW;
+    } else {
+        tot = (a.append_only ? 0 : L) + (a.close ? 1 : 0);
+        for (int64_t w = w0; w < w1; ++w) {
+            const int64_t wl = a.wlengths[w], ws = a.wstarts[w];
+            if (wl < 0 || ws < 0) {
+                st |= PARASON_PACK_BAD_ROW;
+                continue;
+            }
+            const int64_t tail = wl > L ? wl - L : 0;
+            if (tail < 2 || a.wtokens[ws + L] != a.thread_id || a.wtokens[ws + wl - 1] != a.end_thread_id)
+                st |= PARASON_PACK_BAD_THREAD;
+            tot += tail;
+        }
+        if (st & PARASON_PACK_BAD_ROW) tot = 0;
+        else if (tot > (int64_t)INT32_MAX) {
+            st |= PARASON_PACK_TOO_LONG;
+            tot = 0;
+        }
+    }
+    a.status[i] = st;
+    a.out_len64[i] = tot;
+    a.out_lengths[i] = (int32_t)tot;
+}
+
+/* Joined rows, tiled over their tokens like fork_copy; inside a row the
+ * pieces (the row, each worker's span, </Parallel>) are walked in order. */
+__global__ void __launch_bounds__(PACK_THREADS) join_copy(JoinArgs a)
+{
+    __shared__ int64_t found;
+    if (a.over[0]) return;
+    const int64_t T = a.out_starts[a.n];
+    for (int64_t lo = (int64_t)blockIdx.x * TILE; lo < T; lo += (int64_t)gridDim.x * TILE) {
+        const int64_t hi = min(lo + TILE, T);
+        for (int64_t i = find_segment(a.out_starts, a.n, lo, &found); i < a.n; ++i) {
+            const int64_t os = a.out_starts[i];
+            if (os >= hi) break;
+            if (a.out_len64[i] == 0) continue;
+            const int64_t L = a.lengths[i];
+            int64_t pos = os;
+            if (!a.append_only) {
+                const int32_t *src = a.tokens + a.starts[i];
+                if (pos + L > lo) block_fill(a.out_tokens, max(lo, pos), min(hi, pos + L), [=](int64_t d) {
+                    return src[d - pos];
+                });
+                pos += L;
+            }
+            for (int64_t w = a.worker_off[i]; w < a.worker_off[i + 1] && pos < hi; ++w) {
+                const int64_t wl = a.wlengths[w];
+                const int64_t tail = wl > L ? wl - L : 0;
+                if (pos + tail > lo) {
+                    const int32_t *src = a.wtokens + a.wstarts[w] + L;
+                    block_fill(a.out_tokens, max(lo, pos), min(hi, pos + tail), [=](int64_t d) {
+                        return src[d - pos];
+                    });
+                }
+                pos += tail;
+            }
+            if (a.close && pos >= lo && pos < hi && threadIdx.x == 0) a.out_tokens[pos] = a.end_par_id;
+        }
+    }
+}
+
+} /* namespace pk */

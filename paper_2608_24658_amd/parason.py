@@ -39,7 +39,18 @@ MAX_OPEN_ENTRIES = 1 << 24
 
 EXPORTED = ("parason_create", "parason_workspace_size", "parason_run", "parason_run_timed", "parason_destroy",
             "parason_strerror", "parason_pg_workspace_size", "parason_pg_run", "parason_decode_init",
-            "parason_decode_step")
+            "parason_decode_step", "parason_fork_workspace_size", "parason_join_workspace_size", "parason_fork",
+            "parason_join")
+
+FORK_SEED_ENTRY = 1 << 0
+JOIN_CLOSE_PARALLEL = 1 << 0
+JOIN_APPEND_ONLY = 1 << 1
+PACK_NO_OUTLINE_END = 1 << 0
+PACK_NO_OUTLINE = 1 << 1
+PACK_BAD_ENTRY = 1 << 2
+PACK_BAD_THREAD = 1 << 3
+PACK_TOO_LONG = 1 << 4
+PACK_BAD_ROW = 1 << 5
 
 DECODE_ERROR = 1 << 0
 DECODE_DONE = 1 << 1
@@ -81,6 +92,33 @@ class Outputs(ctypes.Structure):
         ("r_trial", ctypes.c_void_p),
         ("eta", ctypes.c_void_p),
         ("metrics", ctypes.c_void_p),
+    ]
+
+
+class ForkOutputs(ctypes.Structure):
+    _fields_ = [
+        ("max_workers", ctypes.c_int64),
+        ("ctx_capacity", ctypes.c_int64),
+        ("ctx_tokens", ctypes.c_void_p),
+        ("ctx_starts", ctypes.c_void_p),
+        ("ctx_lengths", ctypes.c_void_p),
+        ("ctx_row", ctypes.c_void_p),
+        ("ctx_entry", ctypes.c_void_p),
+        ("ctx_kind", ctypes.c_void_p),
+        ("worker_off", ctypes.c_void_p),
+        ("row_status", ctypes.c_void_p),
+        ("totals", ctypes.c_void_p),
+    ]
+
+
+class JoinOutputs(ctypes.Structure):
+    _fields_ = [
+        ("capacity", ctypes.c_int64),
+        ("tokens", ctypes.c_void_p),
+        ("starts", ctypes.c_void_p),
+        ("lengths", ctypes.c_void_p),
+        ("row_status", ctypes.c_void_p),
+        ("totals", ctypes.c_void_p),
     ]
 
 
@@ -131,6 +169,20 @@ def lib():
         L.parason_decode_step.argtypes = [
             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
             ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+        ]
+        for name in ("parason_fork_workspace_size", "parason_join_workspace_size"):
+            getattr(L, name).restype = ctypes.c_int
+            getattr(L, name).argtypes = [ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]
+        L.parason_fork.restype = ctypes.c_int
+        L.parason_fork.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32,
+            ctypes.POINTER(ForkOutputs), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+        ]
+        L.parason_join.restype = ctypes.c_int
+        L.parason_join.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32,
+            ctypes.POINTER(JoinOutputs), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
         ]
         L.parason_strerror.restype = ctypes.c_char_p
         L.parason_strerror.argtypes = [ctypes.c_int]
@@ -261,6 +313,84 @@ class Parason:
             raise ParasonError(rc, "parason_decode_step")
         return logits
 
+    def fork_raw(self, tokens_ptr, starts_ptr, lengths_ptr, n_rows, flags, out: ForkOutputs, ws_ptr, ws_bytes,
+                 stream) -> int:
+        return lib().parason_fork(self._h, tokens_ptr, starts_ptr, lengths_ptr, int(n_rows), int(flags),
+                                  ctypes.byref(out), ws_ptr, int(ws_bytes), stream)
+
+    def join_raw(self, tokens_ptr, starts_ptr, lengths_ptr, n_rows, worker_off_ptr, wtokens_ptr, wstarts_ptr,
+                 wlengths_ptr, n_workers, flags, out: JoinOutputs, ws_ptr, ws_bytes, stream) -> int:
+        return lib().parason_join(self._h, tokens_ptr, starts_ptr, lengths_ptr, int(n_rows), worker_off_ptr,
+                                  wtokens_ptr, wstarts_ptr, wlengths_ptr, int(n_workers), int(flags),
+                                  ctypes.byref(out), ws_ptr, int(ws_bytes), stream)
+
+    def fork(self, tokens, starts, lengths, seed: bool = True, max_workers=None, ctx_capacity=None) -> dict:
+        """Worker contexts of a batch of rows (device tensors).  Without
+        capacities, a first call sizes the outputs (one synchronisation)."""
+        import torch
+
+        _check_rows(tokens, starts, lengths)
+        dev, n = starts.device, int(starts.numel())
+        flags = FORK_SEED_ENTRY if seed else 0
+        ws = torch.empty(_ws_size("parason_fork_workspace_size", n), dtype=torch.uint8, device=dev)
+        stream = torch.cuda.current_stream(dev).cuda_stream
+        i64 = dict(dtype=torch.int64, device=dev)
+        i32 = dict(dtype=torch.int32, device=dev)
+        res = dict(worker_off=torch.empty(n + 1, **i64), row_status=torch.empty(max(n, 1), **i32)[:n],
+                   totals=torch.empty(3, **i64))
+
+        def call(W, T):
+            res.update(ctx_tokens=torch.empty(max(T, 1), **i32)[:T], ctx_starts=torch.empty(max(W, 1), **i64)[:W],
+                       ctx_lengths=torch.empty(max(W, 1), **i32)[:W], ctx_row=torch.empty(max(W, 1), **i32)[:W],
+                       ctx_entry=torch.empty(max(W, 1), **i32)[:W], ctx_kind=torch.empty(max(W, 1), **i32)[:W])
+            o = ForkOutputs(int(W), int(T), *[res[k].data_ptr() for k in (
+                "ctx_tokens", "ctx_starts", "ctx_lengths", "ctx_row", "ctx_entry", "ctx_kind", "worker_off",
+                "row_status", "totals")])
+            rc = self.fork_raw(_ptr(tokens, starts), starts.data_ptr(), lengths.data_ptr(), n, flags, o,
+                               ws.data_ptr(), ws.numel(), stream)
+            if rc != OK:
+                raise ParasonError(rc, "parason_fork")
+
+        if max_workers is None or ctx_capacity is None:
+            call(0, 0)
+            W, T, _ = (int(x) for x in res["totals"].cpu())
+            max_workers = W if max_workers is None else max_workers
+            ctx_capacity = T if ctx_capacity is None else ctx_capacity
+        call(max_workers, ctx_capacity)
+        return res
+
+    def join(self, tokens, starts, lengths, worker_off, wtokens, wstarts, wlengths, close: bool = True,
+             append_only: bool = False, capacity=None) -> dict:
+        """Joined rows (device tensors); sizing as for fork."""
+        import torch
+
+        _check_rows(tokens, starts, lengths)
+        _check_rows(wtokens, wstarts, wlengths)
+        dev, n, nw = starts.device, int(starts.numel()), int(wstarts.numel())
+        flags = (JOIN_CLOSE_PARALLEL if close else 0) | (JOIN_APPEND_ONLY if append_only else 0)
+        ws = torch.empty(_ws_size("parason_join_workspace_size", n), dtype=torch.uint8, device=dev)
+        stream = torch.cuda.current_stream(dev).cuda_stream
+        res = dict(starts=torch.empty(n + 1, dtype=torch.int64, device=dev),
+                   lengths=torch.empty(max(n, 1), dtype=torch.int32, device=dev)[:n],
+                   row_status=torch.empty(max(n, 1), dtype=torch.int32, device=dev)[:n],
+                   totals=torch.empty(2, dtype=torch.int64, device=dev))
+
+        def call(T):
+            res["tokens"] = torch.empty(max(T, 1), dtype=torch.int32, device=dev)[:T]
+            o = JoinOutputs(int(T), *[res[k].data_ptr() for k in ("tokens", "starts", "lengths", "row_status",
+                                                                   "totals")])
+            rc = self.join_raw(_ptr(tokens, starts), starts.data_ptr(), lengths.data_ptr(), n,
+                               worker_off.data_ptr(), _ptr(wtokens, wstarts), wstarts.data_ptr(),
+                               wlengths.data_ptr(), nw, flags, o, ws.data_ptr(), ws.numel(), stream)
+            if rc != OK:
+                raise ParasonError(rc, "parason_join")
+
+        if capacity is None:
+            call(0)
+            capacity = int(res["totals"][0].item())
+        call(capacity)
+        return res
+
     def run(self, tokens, starts, lengths, correct, out: dict | None = None, workspace=None, total_tokens=None,
             derived: bool = True, metrics: bool = False) -> dict:
         """Evaluate a batch of rows held in device tensors (asynchronous on the
@@ -286,6 +416,28 @@ class Parason:
         if rc != OK:
             raise ParasonError(rc, "parason_run")
         return out
+
+
+def _check_rows(tokens, starts, lengths):
+    import torch
+
+    for t, dt in ((tokens, torch.int32), (starts, torch.int64), (lengths, torch.int32)):
+        if t.dtype != dt or not t.is_cuda or not t.is_contiguous():
+            raise TypeError("expected contiguous %s device tensors" % dt)
+    if starts.numel() != lengths.numel():
+        raise ValueError("starts and lengths must have the same length")
+
+
+def _ptr(tokens, fallback):
+    return tokens.data_ptr() if tokens.numel() else fallback.data_ptr()
+
+
+def _ws_size(name: str, n: int) -> int:
+    b = ctypes.c_size_t()
+    rc = getattr(lib(), name)(int(n), ctypes.byref(b))
+    if rc != OK:
+        raise ParasonError(rc, name)
+    return b.value
 
 
 def decode_init(batch: int, device, states=None):

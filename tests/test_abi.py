@@ -138,3 +138,41 @@ def test_decode_rejects_bad_arguments_before_launch():
     assert init(FAKE, -1, None) == P.ERR_SIZE
     assert init(FAKE + 8, 4, None) == P.ERR_ALIGN
     assert init(None, 0, None) == P.OK
+
+
+def test_fork_join_reject_bad_arguments_before_launch():
+    px = P.Parason(TAGS)
+    ws = ctypes.c_size_t()
+    assert P.lib().parason_fork_workspace_size(16, ctypes.byref(ws)) == P.OK and ws.value > 0
+    assert P.lib().parason_fork_workspace_size(-1, ctypes.byref(ws)) == P.ERR_SIZE
+    assert P.lib().parason_join_workspace_size(16, None) == P.ERR_NULL
+    P.lib().parason_fork_workspace_size(16, ctypes.byref(ws))
+    W = ws.value
+    fo = P.ForkOutputs(4, 100, *([FAKE] * 9))
+    fork = px.fork_raw
+    assert P.lib().parason_fork(None, FAKE, FAKE, FAKE, 16, 0, ctypes.byref(fo), FAKE, W, None) == P.ERR_NULL
+    assert fork(FAKE, FAKE, FAKE, -1, 0, fo, FAKE, W, None) == P.ERR_SIZE
+    assert fork(FAKE, FAKE, FAKE, 16, 4, fo, FAKE, W, None) == P.ERR_PARAM
+    assert fork(0, FAKE, FAKE, 16, 0, fo, FAKE, W, None) == P.ERR_NULL
+    assert fork(FAKE, FAKE, FAKE, 16, 0, fo, 0, W, None) == P.ERR_NULL
+    assert fork(FAKE + 2, FAKE, FAKE, 16, 0, fo, FAKE, W, None) == P.ERR_ALIGN
+    assert fork(FAKE, FAKE, FAKE, 16, 0, fo, FAKE + 8, W, None) == P.ERR_ALIGN
+    assert fork(FAKE, FAKE, FAKE, 16, 0, fo, FAKE, W - 1, None) == P.ERR_WORKSPACE
+    for k in ("ctx_tokens", "ctx_starts", "ctx_kind", "worker_off", "row_status", "totals"):
+        bad = P.ForkOutputs(4, 100, *([FAKE] * 9))
+        setattr(bad, k, None)
+        assert fork(FAKE, FAKE, FAKE, 16, 0, bad, FAKE, W, None) == P.ERR_NULL, k
+    neg = P.ForkOutputs(-1, 100, *([FAKE] * 9))
+    assert fork(FAKE, FAKE, FAKE, 16, 0, neg, FAKE, W, None) == P.ERR_SIZE
+    P.lib().parason_join_workspace_size(16, ctypes.byref(ws))
+    W = ws.value
+    jo = P.JoinOutputs(100, *([FAKE] * 5))
+    join = px.join_raw
+    assert join(FAKE, FAKE, FAKE, 16, FAKE, FAKE, FAKE, FAKE, 32, 4, jo, FAKE, W, None) == P.ERR_PARAM
+    assert join(FAKE, FAKE, FAKE, 16, FAKE, FAKE, FAKE, FAKE, -1, 0, jo, FAKE, W, None) == P.ERR_SIZE
+    assert join(FAKE, FAKE, FAKE, 16, 0, FAKE, FAKE, FAKE, 32, 0, jo, FAKE, W, None) == P.ERR_NULL
+    assert join(FAKE, FAKE, FAKE, 16, FAKE, 0, FAKE, FAKE, 32, 0, jo, FAKE, W, None) == P.ERR_NULL
+    assert join(FAKE, FAKE, FAKE, 16, FAKE, FAKE + 1, FAKE, FAKE, 32, 0, jo, FAKE, W, None) == P.ERR_ALIGN
+    assert join(FAKE, FAKE, FAKE, 16, FAKE, FAKE, FAKE, FAKE, 32, 0, jo, FAKE, 64, None) == P.ERR_WORKSPACE
+    bad = P.JoinOutputs(100, None, FAKE, FAKE, FAKE, FAKE)
+    assert join(FAKE, FAKE, FAKE, 16, FAKE, FAKE, FAKE, FAKE, 32, 0, bad, FAKE, W, None) == P.ERR_NULL

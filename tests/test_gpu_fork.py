@@ -1,0 +1,286 @@
+"""GPU parity of fork/join packing against the CPU oracle.
+
+Main rows are synthetic rollouts cut right after one of their </Outlines>
+tags (so the outlines sit at every depth of nesting and after long text),
+plus hand-made rows that the fork must reject, long outlines that span many
+256-token chunks, and rows of length 0 and 1.  Every fork output (row status,
+worker offsets, each worker's row, entry, kind, context start, length and
+tokens) must equal the oracle's exactly; joins of worker sequences laid out
+out of order with gaps (some of them malformed on purpose) must equal the
+oracle's joined rows exactly, with and without </Parallel> and append-only."""
+import numpy as np
+import pytest
+
+from gpu_util import log, to_dev
+from oracle import fork_oracle as F
+from paper_2608_24658_amd import parason as PX
+from paper_2608_24658_amd.synth import synth as S
+from tests import grammar_pins as GP
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+CONTIG = [int(t) for t in S.CONTIGUOUS_TAGS]
+SCATTERED = [91, 5, 40000, 17, 151000, 12, 333, 77777, 2, 64, 99999, 150001]
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def synthetic_main_rows(workload, n, tags, seed, p_raw=0.05):
+    """Rows of a synthetic workload cut right after a random </Outlines>."""
+    P = S.make_params(workload, tag_ids=tags)
+    tok, st, ln, _ = S.host_batch(P, n)
+    end_out = tags[GP.END_OUT - 1]
+    rng = np.random.default_rng(seed)
+    rows = []
+    for i in range(n):
+        row = tok[st[i]: st[i] + ln[i]]
+        ends = np.nonzero(row == end_out)[0]
+        if len(ends) == 0 or rng.random() < p_raw:
+            rows.append(row[: rng.integers(0, len(row) + 1)].tolist())
+        else:
+            rows.append(row[: int(rng.choice(ends)) + 1].tolist())
+    return rows
+
+
+def hand_rows(tags, text_ids):
+    def t(names):
+        out = []
+        for k, c in enumerate(GP.parse_names(names)):
+            out.append(tags[c - 1] if c else text_ids[k % len(text_ids)])
+        return out
+
+    rows = [t(x) for x in (
+        "think t5 Par Out Sub t3 /Sub Sub t2 /Sub Sub t4 /Sub /Out",
+        "think Par Out Sub t /Sub",
+        "think t /Out",
+        "think Out Sub t /Sub /Out",
+        "think Par t Out Sub t /Sub /Out",
+        "think Par Out /Out",
+        "think Par Out Sub /Sub /Out",
+        "think Par Out Sub t /Tri /Out",
+        "think Par Out Sub t /Sub t Tri t /Tri /Out",
+        "think Par Out t Sub t /Sub /Out",
+        "think Par Out Sub t Thr /Sub /Out",
+        "/Out",
+        "Out /Out",
+        "Par Out Tri t /Tri /Out",
+        "think Par Out Sub t /Sub /Out Thr t /Thr /Par Par Out Tri t2 /Tri Tri t /Tri /Out",
+    )]
+    rows += [[], [tags[GP.END_OUT - 1]]]
+    # outlines spanning many 256-token chunks: long entry texts, many short entries
+    rows.append(t("think t300 Par Out Sub t700 /Sub Tri t1 /Tri Sub t257 /Sub /Out"))
+    rows.append(t("think t3 Par Out " + "Sub t /Sub Tri t /Tri " * 300 + "/Out"))
+    rows.append(t("think t3 Par Out " + "Sub t /Sub Tri t /Tri " * 300 + "Sub /Sub /Out"))  # last entry empty
+    rows.append(t("think t900 Par t2 Out " + "Tri t40 /Tri " * 30 + "/Out"))  # <Parallel> text <Outlines>
+    # the <Outlines> sits exactly on chunk edges
+    for pad in (250, 251, 252, 253, 254, 255, 256, 257):
+        rows.append(t("think t%d Par Out Sub t2 /Sub /Out" % pad))
+    return rows
+
+
+def oracle_fork(rows, tags, seed):
+    res = F.fork(rows, tags, flags=F.FORK_SEED_ENTRY if seed else 0)
+    lens = np.array([len(c) for c in res["ctx"]], dtype=np.int64)
+    starts = np.zeros(len(lens), dtype=np.int64)
+    if len(lens):
+        starts[1:] = np.cumsum(lens[:-1])
+    flat = np.array([x for c in res["ctx"] for x in c], dtype=np.int32)
+    return res, starts, lens, flat
+
+
+def layout(rows, rng, gaps=True, shuffle=True):
+    """Rows placed in one buffer in a random order with random gaps."""
+    order = rng.permutation(len(rows)) if shuffle else np.arange(len(rows))
+    starts = np.zeros(len(rows), dtype=np.int64)
+    pieces = []
+    pos = 0
+    for i in order:
+        g = int(rng.integers(0, 5)) if gaps else 0
+        pieces.append(np.zeros(g, np.int32))
+        pos += g
+        starts[i] = pos
+        pieces.append(np.asarray(rows[i], dtype=np.int32))
+        pos += len(rows[i])
+    buf = np.concatenate(pieces) if pieces else np.zeros(0, np.int32)
+    return (buf if buf.size else np.zeros(1, np.int32)), starts, np.array([len(r) for r in rows], dtype=np.int32)
+
+
+def check_fork(dev, px, rows, tags, seed, rng, what):
+    tok, st, ln = layout(rows, rng)
+    res, exp_starts, exp_lens, exp_flat = oracle_fork(rows, tags, seed)
+    got = px.fork(to_dev(tok, torch.int32, dev), to_dev(st, torch.int64, dev), to_dev(ln, torch.int32, dev), seed=seed)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in got.items()}
+    assert np.array_equal(g["row_status"].view(np.uint32), np.array(res["status"], np.uint32)), what
+    assert np.array_equal(g["worker_off"], np.array(res["worker_off"], np.int64)), what
+    W = res["worker_off"][-1]
+    assert list(g["totals"]) == [W, int(exp_lens.sum()), 0], what
+    assert np.array_equal(g["ctx_row"], np.array(res["row"], np.int32)), what
+    assert np.array_equal(g["ctx_entry"], np.array(res["entry"], np.int32)), what
+    assert np.array_equal(g["ctx_kind"], np.array([1 if k == F.SUB else 2 for k in res["kind"]], np.int32)), what
+    assert np.array_equal(g["ctx_starts"], exp_starts), what
+    assert np.array_equal(g["ctx_lengths"], exp_lens.astype(np.int32)), what
+    if not np.array_equal(g["ctx_tokens"], exp_flat):
+        bad = np.nonzero(g["ctx_tokens"] != exp_flat)[0]
+        w = int(np.searchsorted(exp_starts, bad[0], side="right") - 1)
+        raise AssertionError("%s: %d context tokens differ, first at %d (worker %d, row %d)" % (
+            what, bad.size, bad[0], w, res["row"][w]))
+    return res, got
+
+
+def worker_sequences(res, tags, rng, p_bad=0.0):
+    thr_end = tags[GP.END_THR - 1]
+    seqs = []
+    for c in res["ctx"]:
+        gen = [int(x) for x in rng.integers(0, 1000, size=int(rng.integers(0, 60)))]
+        s = list(c) + gen + [thr_end]
+        if rng.random() < p_bad:
+            s = s[: int(rng.integers(0, len(s)))]  # cut anywhere, even inside the row
+        seqs.append(s)
+    return seqs
+
+
+def check_join(dev, px, rows, res, seqs, tags, rng, flags, what):
+    tok, st, ln = layout(rows, rng)
+    wtok, wst, wln = layout(seqs, rng)
+    exp, exp_st = F.join(rows, res["worker_off"], seqs, tags, flags=flags)
+    got = px.join(to_dev(tok, torch.int32, dev), to_dev(st, torch.int64, dev), to_dev(ln, torch.int32, dev),
+                  to_dev(np.array(res["worker_off"], np.int64), torch.int64, dev), to_dev(wtok, torch.int32, dev),
+                  to_dev(wst, torch.int64, dev), to_dev(wln, torch.int32, dev),
+                  close=bool(flags & F.JOIN_CLOSE_PARALLEL), append_only=bool(flags & F.JOIN_APPEND_ONLY))
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in got.items()}
+    assert np.array_equal(g["row_status"].view(np.uint32), np.array(exp_st, np.uint32)), what
+    lens = np.array([len(r) for r in exp], np.int64)
+    assert np.array_equal(g["lengths"], lens.astype(np.int32)), what
+    assert g["starts"][0] == 0 and np.array_equal(np.diff(g["starts"]), lens), what
+    flat = np.array([x for r in exp for x in r], np.int32)
+    assert np.array_equal(g["tokens"], flat), what
+    assert list(g["totals"]) == [int(lens.sum()), 0], what
+
+
+@pytest.mark.parametrize("tags", [CONTIG, SCATTERED], ids=["contiguous", "scattered"])
+@pytest.mark.parametrize("seed", [True, False], ids=["seed", "noseed"])
+def test_fork_join_hand_rows(dev, tags, seed):
+    log("case fork hand rows tags=%s seed=%s" % (tags[0], seed))
+    rng = np.random.default_rng(1)
+    px = PX.Parason(tags)
+    rows = hand_rows(tags, [7, 8, 9, 1000, 150000])
+    res, _ = check_fork(dev, px, rows, tags, seed, rng, "hand")
+    assert sum(s == 0 for s in res["status"]) >= 12
+    seqs = worker_sequences(res, tags, rng, p_bad=0.2)
+    for flags in (F.JOIN_CLOSE_PARALLEL, 0, F.JOIN_APPEND_ONLY, F.JOIN_CLOSE_PARALLEL | F.JOIN_APPEND_ONLY):
+        check_join(dev, px, rows, res, seqs, tags, rng, flags, "hand join %d" % flags)
+
+
+@pytest.mark.parametrize("workload,n", [("small", 256), ("ragged", 512)])
+def test_fork_join_synthetic(dev, workload, n):
+    log("case fork synthetic %s n=%d" % (workload, n))
+    rng = np.random.default_rng(2)
+    px = PX.Parason(CONTIG)
+    rows = synthetic_main_rows(workload, n, CONTIG, seed=3)
+    res, _ = check_fork(dev, px, rows, CONTIG, True, rng, workload)
+    assert res["worker_off"][-1] > n // 2
+    seqs = worker_sequences(res, CONTIG, rng, p_bad=0.05)
+    check_join(dev, px, rows, res, seqs, CONTIG, rng, F.JOIN_CLOSE_PARALLEL, workload + " join")
+
+
+def test_fork_join_scattered_synthetic(dev):
+    log("case fork synthetic scattered")
+    rng = np.random.default_rng(4)
+    px = PX.Parason(SCATTERED)
+    rows = synthetic_main_rows("small", 128, SCATTERED, seed=5)
+    res, _ = check_fork(dev, px, rows, SCATTERED, False, rng, "scattered")
+    seqs = worker_sequences(res, SCATTERED, rng)
+    check_join(dev, px, rows, res, seqs, SCATTERED, rng, F.JOIN_CLOSE_PARALLEL | F.JOIN_APPEND_ONLY, "sc join")
+
+
+def test_fork_capacity_and_bad_rows(dev):
+    log("case fork capacity / bad rows")
+    px = PX.Parason(CONTIG)
+    rows = hand_rows(CONTIG, [7, 8])
+    rng = np.random.default_rng(6)
+    tok, st, ln = layout(rows, rng)
+    res, _, exp_lens, _ = oracle_fork(rows, CONTIG, True)
+    W, T = res["worker_off"][-1], int(exp_lens.sum())
+    args = (to_dev(tok, torch.int32, dev), to_dev(st, torch.int64, dev), to_dev(ln, torch.int32, dev))
+    for mw, cap in ((W - 1, T), (W, T - 1), (0, 0)):
+        got = px.fork(*args, seed=True, max_workers=mw, ctx_capacity=cap)
+        torch.cuda.synchronize()
+        assert list(got["totals"].cpu().numpy()) == [W, T, 1]
+        assert np.array_equal(got["worker_off"].cpu().numpy(), np.array(res["worker_off"]))
+        assert np.array_equal(got["row_status"].cpu().numpy().view(np.uint32), np.array(res["status"], np.uint32))
+    # negative lengths and starts are flagged, never read
+    ln2, st2 = ln.copy(), st.copy()
+    ln2[0], st2[1] = -5, -1
+    got = px.fork(args[0], to_dev(st2, torch.int64, dev), to_dev(ln2, torch.int32, dev), seed=True)
+    torch.cuda.synchronize()
+    stat = got["row_status"].cpu().numpy().view(np.uint32)
+    assert stat[0] == PX.PACK_BAD_ROW and stat[1] == PX.PACK_BAD_ROW
+    assert np.array_equal(stat[2:], np.array(res["status"][2:], np.uint32))
+    # join: worker offsets out of order or beyond the worker count
+    seqs = worker_sequences(res, CONTIG, rng)
+    wtok, wst, wln = layout(seqs, rng)
+    off = np.array(res["worker_off"], np.int64)
+    off_bad = off.copy()
+    off_bad[1] = off_bad[2] + 1  # row 0 ends after row 1 begins: row 1 has w1 < w0
+    got = px.join(*args, to_dev(off_bad, torch.int64, dev), to_dev(wtok, torch.int32, dev),
+                  to_dev(wst, torch.int64, dev), to_dev(wln, torch.int32, dev), capacity=None)
+    torch.cuda.synchronize()
+    stat = got["row_status"].cpu().numpy().view(np.uint32)
+    assert stat[1] & PX.PACK_BAD_ROW and got["lengths"].cpu().numpy()[1] == 0
+
+
+def test_fork_join_typical_batch(dev):
+    """The bench's batch: 1024 rollouts of the typical workload cut at an
+    outline; 64 sampled rows (their status, workers, contexts and joined
+    rows) compared with the oracle, the totals checked for all."""
+    log("case fork typical 1024")
+    rng = np.random.default_rng(7)
+    px = PX.Parason(CONTIG)
+    rows = [np.asarray(r, np.int32) for r in synthetic_main_rows("typical", 1024, CONTIG, seed=8, p_raw=0.0)]
+    tok, st, ln = layout(rows, rng)
+    got = px.fork(to_dev(tok, torch.int32, dev), to_dev(st, torch.int64, dev), to_dev(ln, torch.int32, dev),
+                  seed=True)
+    torch.cuda.synchronize()
+    g = {k: v.cpu().numpy() for k, v in got.items()}
+    off = g["worker_off"]
+    W = int(off[-1])
+    assert W > 1024 and g["totals"][0] == W and g["totals"][2] == 0
+    assert g["totals"][1] == int(g["ctx_lengths"].astype(np.int64).sum())
+    sample = sorted(rng.choice(1024, size=64, replace=False).tolist())
+    for i in sample:
+        res = F.fork([rows[i].tolist()], CONTIG)
+        assert g["row_status"][i] == res["status"][0], i
+        assert off[i + 1] - off[i] == len(res["ctx"]), i
+        for k, c in enumerate(res["ctx"]):
+            w = off[i] + k
+            assert g["ctx_row"][w] == i and g["ctx_entry"][w] == k
+            assert g["ctx_kind"][w] == (1 if res["kind"][k] == F.SUB else 2)
+            s0, n0 = int(g["ctx_starts"][w]), int(g["ctx_lengths"][w])
+            assert np.array_equal(g["ctx_tokens"][s0: s0 + n0], np.asarray(c, np.int32)), (i, k)
+    # workers: context + generated text + </Thread>, laid out out of order
+    end_thr = CONTIG[GP.END_THR - 1]
+    seqs = []
+    for w in range(W):
+        s0, n0 = int(g["ctx_starts"][w]), int(g["ctx_lengths"][w])
+        gen = rng.integers(0, 1000, size=int(rng.integers(0, 60))).astype(np.int32)
+        seqs.append(np.concatenate([g["ctx_tokens"][s0: s0 + n0], gen, np.array([end_thr], np.int32)]))
+    wtok, wst, wln = layout(seqs, rng)
+    j = px.join(to_dev(tok, torch.int32, dev), to_dev(st, torch.int64, dev), to_dev(ln, torch.int32, dev),
+                got["worker_off"], to_dev(wtok, torch.int32, dev), to_dev(wst, torch.int64, dev),
+                to_dev(wln, torch.int32, dev))
+    torch.cuda.synchronize()
+    jg = {k: v.cpu().numpy() for k, v in j.items()}
+    assert not jg["row_status"].any() and jg["totals"][1] == 0
+    for i in sample:
+        ws = [seqs[w].tolist() for w in range(off[i], off[i + 1])]
+        exp, est = F.join([rows[i].tolist()], [0, len(ws)], ws, CONTIG)
+        s0, n0 = int(jg["starts"][i]), int(jg["lengths"][i])
+        assert est == [0] and np.array_equal(jg["tokens"][s0: s0 + n0], np.asarray(exp[0], np.int32)), i
