@@ -353,20 +353,24 @@ __device__ __forceinline__ int64_t find_segment(const int64_t *offs, int64_t cou
     return s;
 }
 
-/* dst[d] = src(d) for d in [d0, d1) with the whole block, four loads in
- * flight per thread; src(d) must be a pure function of d. */
+/* dst[d] = src(d) for d in [d0, d1) with the whole block, U loads in flight
+ * per thread; src(d) must be a pure function of d. */
+#ifndef PARASON_FILL_UNROLL
+#define PARASON_FILL_UNROLL 4
+#endif
 template <class Src>
 __device__ __forceinline__ void block_fill(int32_t *__restrict__ dst, int64_t d0, int64_t d1, const Src &src)
 {
-    for (int64_t base = d0; base < d1; base += 4 * PACK_THREADS) {
-        int32_t v[4];
+    constexpr int U = PARASON_FILL_UNROLL;
+    for (int64_t base = d0; base < d1; base += U * PACK_THREADS) {
+        int32_t v[U];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < U; ++j) {
             const int64_t d = base + j * PACK_THREADS + threadIdx.x;
             if (d < d1) v[j] = src(d);
         }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < U; ++j) {
             const int64_t d = base + j * PACK_THREADS + threadIdx.x;
             if (d < d1) dst[d] = v[j];
         }
