@@ -11,7 +11,10 @@ static_assert(sizeof(parason_decode_state) == sizeof(pk::DecodeState), "decode s
 static_assert(sizeof(parason_decode_state) == 16, "decode state is 16 bytes");
 
 namespace {
-constexpr int DECODE_BLOCKS_PER_CU = 8;
+#ifndef PARASON_DECODE_BLOCKS_PER_CU
+#define PARASON_DECODE_BLOCKS_PER_CU 8
+#endif
+constexpr int DECODE_BLOCKS_PER_CU = PARASON_DECODE_BLOCKS_PER_CU;
 }  // namespace
 
 extern "C" {
@@ -68,7 +71,7 @@ int parason_decode_step(const parason_handle *h, parason_decode_state *states, c
     da.tm = h->tm;
     const int64_t max_blocks = (int64_t)cus * DECODE_BLOCKS_PER_CU;
     const unsigned blocks = (unsigned)(batch < max_blocks ? batch : max_blocks);
-    pk::decode_step<<<dim3(blocks), dim3(256), 0, stream>>>(da);
+    pk::decode_step<<<dim3(blocks), dim3(pk::DECODE_THREADS), 0, stream>>>(da);
     return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
 }
 

@@ -130,8 +130,13 @@ __device__ __forceinline__ void store_ninf(char *row, int64_t i, const DecodeArg
     else reinterpret_cast<uint32_t *>(row)[i] = a.ninf;
 }
 
+#ifndef PARASON_DECODE_THREADS
+#define PARASON_DECODE_THREADS 256
+#endif
+constexpr int DECODE_THREADS = PARASON_DECODE_THREADS;
+
 /* One block per row, grid-stride over the rows. */
-__global__ void __launch_bounds__(256) decode_step(DecodeArgs a)
+__global__ void __launch_bounds__(DECODE_THREADS) decode_step(DecodeArgs a)
 {
     __shared__ uint32_t allow_s;
     for (int64_t r = blockIdx.x; r < a.batch; r += gridDim.x) {
@@ -175,7 +180,11 @@ __global__ void __launch_bounds__(256) decode_step(DecodeArgs a)
         const uint32_t w = a.elem == 2 ? (a.ninf | (a.ninf << 16)) : a.ninf;
         const uint4 ninf4 = make_uint4(w, w, w, w);
         uint4 *vrow = reinterpret_cast<uint4 *>(row + head * a.elem);
-        for (int64_t v = threadIdx.x; v < n_vec; v += blockDim.x) {
+#ifndef PARASON_DECODE_UNROLL
+#define PARASON_DECODE_UNROLL 1
+#endif
+#pragma unroll PARASON_DECODE_UNROLL
+        for (int64_t v = threadIdx.x; v < n_vec; v += DECODE_THREADS) {
             const int64_t e0 = head + v * per;
             const bool clean = (uint64_t)(keep0 - e0) >= (uint64_t)per && (uint64_t)(keep1 - e0) >= (uint64_t)per &&
                                (uint64_t)(keep2 - e0) >= (uint64_t)per;
@@ -186,9 +195,9 @@ __global__ void __launch_bounds__(256) decode_step(DecodeArgs a)
                     if (e != keep0 && e != keep1 && e != keep2) store_ninf(row, e, a);
             }
         }
-        for (int64_t e = threadIdx.x; e < head; e += blockDim.x)
+        for (int64_t e = threadIdx.x; e < head; e += DECODE_THREADS)
             if (e != keep0 && e != keep1 && e != keep2) store_ninf(row, e, a);
-        for (int64_t e = tail0 + threadIdx.x; e < a.vocab; e += blockDim.x)
+        for (int64_t e = tail0 + threadIdx.x; e < a.vocab; e += DECODE_THREADS)
             if (e != keep0 && e != keep1 && e != keep2) store_ninf(row, e, a);
     }
 }

@@ -15,15 +15,15 @@ namespace pk {
 
 constexpr int WAVE = 64;
 #ifndef PARASON_SEG_VEC
-#define PARASON_SEG_VEC 512
+#define PARASON_SEG_VEC 256
 #endif
 #ifndef PARASON_SCAN_WAVES_PER_SIMD
 #define PARASON_SCAN_WAVES_PER_SIMD 4
 #endif
-constexpr int SEG_VEC = PARASON_SEG_VEC; /* 16-byte vectors per segment (2048 tokens) */
+constexpr int SEG_VEC = PARASON_SEG_VEC; /* 16-byte vectors per segment (1024 tokens) */
 constexpr int SEG_TOK = 4 * SEG_VEC;     /* tokens per segment */
 constexpr int LOADS = SEG_VEC / WAVE;    /* vector loads per lane per segment */
-constexpr int EV_CAP = 128;              /* events stored per segment */
+constexpr int EV_CAP = 64;               /* events stored per segment */
 constexpr int PLAN_TILE = 4096;          /* rows per plan tile */
 constexpr int PLAN_THREADS = 256;
 constexpr int ROWS_PER_THREAD = PLAN_TILE / PLAN_THREADS;

@@ -764,9 +764,10 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
     return w.s == w.last && !rc.global;
 }
 
-/* One wave per segment; waves take contiguous ranges of segment ids.  A wave
- * issues the loads of its next segment as soon as the current one is
- * compacted, before it flushes a finished row's events. */
+/* One wave per segment; waves take contiguous ranges of segment ids.  Two
+ * register buffers alternate: the loads of segment s + 1 are issued before
+ * segment s is compacted (and a finished row's events flushed), so a wave
+ * always has a segment in flight. */
 template <bool CONTIG>
 __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD) scan_rows(ScanArgs a)
 {
@@ -797,17 +798,30 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
     rc.lcnt = 0;
     rc.global = true; /* a row already begun in the previous wave's range */
     SegView w = cur.view(s_begin);
-    int4 x[LOADS];
-    issue_loads(x, src, w, lane);
-    for (int64_t s = s_begin; s < s_end; ++s) {
-        const bool row_in_lds = collect_segment<CONTIG>(a, x, w, rc, lev, lane);
-        const int64_t row = w.row, first = w.first, last = w.last;
-        /* the next segment's loads fly while a finished row's automaton runs */
-        if (s + 1 < s_end) {
-            w = cur.view(s + 1);
-            issue_loads(x, src, w, lane);
+    /* two register buffers: segment s + 1 is in flight while s is compacted */
+    int4 xa[LOADS], xb[LOADS];
+    issue_loads(xa, src, w, lane);
+    int64_t s = s_begin;
+    while (true) {
+        SegView wn;
+        bool more = s + 1 < s_end;
+        if (more) {
+            wn = cur.view(s + 1);
+            issue_loads(xb, src, wn, lane);
         }
-        if (row_in_lds) flush_row(a, row, first, last, rc.lcnt, lev, lane);
+        if (collect_segment<CONTIG>(a, xa, w, rc, lev, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, lane);
+        if (!more) break;
+        ++s;
+        w = wn;
+        more = s + 1 < s_end;
+        if (more) {
+            wn = cur.view(s + 1);
+            issue_loads(xa, src, wn, lane);
+        }
+        if (collect_segment<CONTIG>(a, xb, w, rc, lev, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, lane);
+        if (!more) break;
+        ++s;
+        w = wn;
     }
 }
 

@@ -12,7 +12,8 @@
  *                  order; A = 0 when all rewards of the group are equal).
  *   sum_lengths_*  exact token count N (deterministic block sums).
  *   pg_surrogate   HBM-bound, one wave per segment of a row (the segment plan
- *                  of the accounting path): d = logp - logp_old in float,
+ *                  of the accounting path, two segments in flight per wave):
+ *                  d = logp - logp_old in float,
  *                  rho = exp(d), the clip decision on d against float
  *                  thresholds ln(1 - eps_low), ln(1 + eps_high), the objective
  *                  term summed in double, the gradient of the loss -J with
@@ -119,7 +120,69 @@ __device__ __forceinline__ int64_t wave_sum(int64_t v)
     return v;
 }
 
-/* One wave per segment of the plan; the wave's segments are contiguous. */
+/* Loads of one segment: logp and logp_old vectors v0 + i*WAVE + lane. */
+__device__ __forceinline__ void pg_loads(const PgArgs &a, const SegView &w, int lane, float4 (&xn)[LOADS],
+                                         float4 (&xo)[LOADS])
+{
+    const float4 *pn = reinterpret_cast<const float4 *>(a.logp_base);
+    const float4 *po = reinterpret_cast<const float4 *>(a.old_base);
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+        const int64_t v = w.v0 + i * WAVE + lane;
+        if (!w.edge || v < w.v1) {
+            xn[i] = load_f4(pn + v);
+            xo[i] = load_f4(po + v);
+        } else {
+            xn[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            xo[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    }
+}
+
+/* Objective terms, clip counts and gradient stores of one loaded segment. */
+__device__ __forceinline__ void pg_segment(const PgArgs &a, const SegView &w, int lane, const float4 (&xn)[LOADS],
+                                           const float4 (&xo)[LOADS], float inv_n, double &acc, int64_t &clip_hi,
+                                           int64_t &clip_lo)
+{
+    const float A = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(a.adv[w.row])));
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+        const int64_t v = w.v0 + i * WAVE + lane;
+        const int32_t q0 = 4 * (i * WAVE + lane);
+        const float nn[4] = {xn[i].x, xn[i].y, xn[i].z, xn[i].w};
+        const float oo[4] = {xo[i].x, xo[i].y, xo[i].z, xo[i].w};
+        float g[4];
+        bool in[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            in[j] = !w.edge || (q0 + j >= w.q_lo && q0 + j < w.q_hi);
+            const float d = __fsub_rn(nn[j], oo[j]);
+            const float rho = expf(d);
+            bool unclipped = true;
+            if (A > 0.0f) unclipped = d <= a.thr_high;
+            else if (A < 0.0f) unclipped = d >= a.thr_low;
+            const float L = unclipped ? rho * A : (A > 0.0f ? a.hi_val : a.lo_val) * A;
+            g[j] = unclipped ? -(A * rho) * inv_n : 0.0f;
+            if (in[j]) {
+                acc += (double)L;
+                clip_hi += (!unclipped && A > 0.0f) ? 1 : 0;
+                clip_lo += (!unclipped && A < 0.0f) ? 1 : 0;
+            }
+        }
+        float *dst = a.grad_base + 4 * v;
+        if (!w.edge) {
+            store_f4(reinterpret_cast<float4 *>(dst), g[0], g[1], g[2], g[3]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (in[j]) dst[j] = g[j];
+        }
+    }
+}
+
+/* One wave per segment of the plan; the wave's segments are contiguous.  Two
+ * register buffers alternate so that the next segment's loads are in flight
+ * while the current one is evaluated. */
 __global__ void __launch_bounds__(256, 4) pg_surrogate(PgArgs a)
 {
     const int lane = threadIdx.x & (WAVE - 1);
@@ -140,56 +203,30 @@ __global__ void __launch_bounds__(256, 4) pg_surrogate(PgArgs a)
         cur.s_begin = s_begin;
         cur.s_end = s_end;
         cur.seek(s_begin, a.n);
-        const float4 *pn = reinterpret_cast<const float4 *>(a.logp_base);
-        const float4 *po = reinterpret_cast<const float4 *>(a.old_base);
-        for (int64_t s = s_begin; s < s_end; ++s) {
-            const SegView w = cur.view(s);
-            const float A = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(a.adv[w.row])));
-            float4 xn[LOADS], xo[LOADS];
-#pragma unroll
-            for (int i = 0; i < LOADS; ++i) {
-                const int64_t v = w.v0 + i * WAVE + lane;
-                if (!w.edge || v < w.v1) {
-                    xn[i] = load_f4(pn + v);
-                    xo[i] = load_f4(po + v);
-                } else {
-                    xn[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-                    xo[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-                }
+        float4 na[LOADS], oa[LOADS], nb[LOADS], ob[LOADS];
+        SegView w = cur.view(s_begin);
+        pg_loads(a, w, lane, na, oa);
+        int64_t s = s_begin;
+        while (true) {
+            SegView wn;
+            bool more = s + 1 < s_end;
+            if (more) {
+                wn = cur.view(s + 1);
+                pg_loads(a, wn, lane, nb, ob);
             }
-#pragma unroll
-            for (int i = 0; i < LOADS; ++i) {
-                const int64_t v = w.v0 + i * WAVE + lane;
-                const int32_t q0 = 4 * (i * WAVE + lane);
-                const float nn[4] = {xn[i].x, xn[i].y, xn[i].z, xn[i].w};
-                const float oo[4] = {xo[i].x, xo[i].y, xo[i].z, xo[i].w};
-                float g[4];
-                bool in[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    in[j] = !w.edge || (q0 + j >= w.q_lo && q0 + j < w.q_hi);
-                    const float d = __fsub_rn(nn[j], oo[j]);
-                    const float rho = expf(d);
-                    bool unclipped = true;
-                    if (A > 0.0f) unclipped = d <= a.thr_high;
-                    else if (A < 0.0f) unclipped = d >= a.thr_low;
-                    const float L = unclipped ? rho * A : (A > 0.0f ? a.hi_val : a.lo_val) * A;
-                    g[j] = unclipped ? -(A * rho) * inv_n : 0.0f;
-                    if (in[j]) {
-                        acc += (double)L;
-                        clip_hi += (!unclipped && A > 0.0f) ? 1 : 0;
-                        clip_lo += (!unclipped && A < 0.0f) ? 1 : 0;
-                    }
-                }
-                float *dst = a.grad_base + 4 * v;
-                if (!w.edge) {
-                    store_f4(reinterpret_cast<float4 *>(dst), g[0], g[1], g[2], g[3]);
-                } else {
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        if (in[j]) dst[j] = g[j];
-                }
+            pg_segment(a, w, lane, na, oa, inv_n, acc, clip_hi, clip_lo);
+            if (!more) break;
+            ++s;
+            w = wn;
+            more = s + 1 < s_end;
+            if (more) {
+                wn = cur.view(s + 1);
+                pg_loads(a, wn, lane, na, oa);
             }
+            pg_segment(a, w, lane, nb, ob, inv_n, acc, clip_hi, clip_lo);
+            if (!more) break;
+            ++s;
+            w = wn;
         }
     }
     acc = wave_sum(acc);

@@ -209,7 +209,7 @@ def test_bad_rows_and_workspace_overflow(dev):
     keep = np.r_[0:8, 16:32]
     compare({k: v[keep] for k, v in got.items()},
             *oracle_expect(tok_h, st_h[keep], ln_h[keep], co_h[keep], TAGS, G, coef), what="bad-row rest")
-    # a workspace sized for no tokens at all, for rows of 4-10 segments each
+    # a workspace sized for no tokens at all, for rows of many segments each
     Pt = S.make_params("typical")
     tok_t, st_t, ln_t, co_t = S.host_batch(Pt, 32)
     got = run_gpu(px, to_dev(tok_t, torch.int32, dev), to_dev(st_t, torch.int64, dev),
