@@ -60,18 +60,21 @@ def advantages(reward, group_size: int) -> np.ndarray:
     return out
 
 
-def surrogate(logp, logp_old, starts, lengths, adv, eps_low: float, eps_high: float):
+def surrogate(logp, logp_old, starts, lengths, adv, eps_low: float, eps_high: float, n_tokens=None):
     """Loss, gradient and clip counts.
 
     logp, logp_old: float32 arrays; row i is [starts[i], starts[i] + lengths[i]).
     adv: advantage per row (the kernel stores it as float32, so pass that).
+    n_tokens: N of the token-level mean, the generated tokens of the whole
+    batch; by default the tokens of the rows given (pass the batch's N when
+    the rows are a sample of a larger batch).
     Returns dict(loss, tokens, clip_high, clip_low, grad) where grad is float64
     with NaN outside the rows."""
     logp = np.asarray(logp, np.float32)
     logp_old = np.asarray(logp_old, np.float32)
     thr_low, thr_high = thresholds(eps_low, eps_high)
     grad = np.full(logp.size, np.nan)
-    n_tok = int(np.sum(np.maximum(lengths, 0)))
+    n_tok = int(np.sum(np.maximum(lengths, 0))) if n_tokens is None else int(n_tokens)
     total = 0.0
     clip_hi = clip_lo = 0
     for i in range(len(starts)):

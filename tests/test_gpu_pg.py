@@ -110,3 +110,40 @@ def test_pg_rejects_bad_arguments(dev):
         PX.pg_run(t[:8], t, t, st, ln, clip_low=1.0)
     with pytest.raises(PX.ParasonError):
         PX.pg_run(t[:8], t[1:33], t[:32], st, ln)  # different alignment modulo 16 bytes
+
+
+def test_pg_large_half_sampled(dev):
+    """The configuration bench.py --step pg times: the first 356,000 rows of the
+    large workload (1.79e10 tokens, logp + logp_old + grad = 215 GB).  The
+    gradient of 48 sampled rows (every position, so every clip decision) and
+    the advantages of all groups are compared with the oracle; the token count
+    is exact."""
+    log("case pg large half (215 GB)")
+    P = S.make_params("large")
+    n = S.n_rows_of("large") // 2 // G * G
+    lengths, _ = S.host_rows(P, n)
+    starts = np.zeros(n, np.int64)
+    starts[1:] = np.cumsum(lengths[:-1].astype(np.int64))
+    N = int(lengths.astype(np.int64).sum())
+    rng = np.random.default_rng(5)
+    reward = rng.choice([-1.0, 1.0, 1.25, 0.8, 1.5], n).astype(np.float32)
+    old_d, new_d = S.device_logp(P, N, device=dev)
+    grad = torch.empty_like(new_d)
+    got = PX.pg_run(to_dev(reward, torch.float32, dev), new_d, old_d, to_dev(starts, torch.int64, dev),
+                    to_dev(lengths, torch.int32, dev), G, EPS_LO, EPS_HI, grad=grad)
+    torch.cuda.synchronize()
+    adv_exp = PG.advantages(reward, G)
+    adv = got["advantage"].cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(adv - adv_exp) <= 2.0 ** -23 * np.maximum(1.0, np.abs(adv_exp)))
+    st = got["stats"].cpu().numpy()
+    assert st[1] == N and 0 <= st[2] + st[3] <= N and np.isfinite(st[0])
+    for i in sorted(rng.choice(n, size=48, replace=False).tolist()):
+        s0, ln = int(starts[i]), int(lengths[i])
+        old_h, new_h = S.host_logp(P, s0, ln)
+        exp = PG.surrogate(new_h, old_h, np.array([0]), np.array([ln]), adv_exp[i: i + 1].astype(np.float32),
+                           EPS_LO, EPS_HI, n_tokens=N)
+        g = grad[s0: s0 + ln].cpu().numpy().astype(np.float64)
+        err = np.abs(g - exp["grad"])
+        assert np.all(err <= TOL * np.abs(exp["grad"]) + 1e-30), (i, float(np.max(err)))
+    del old_d, new_d, grad
+    torch.cuda.empty_cache()
