@@ -497,7 +497,7 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
         uint32_t c = 0;
         for (;;) {
             if (!dense && e < cnt) {
-                /* stored lists start 512-byte aligned and their slots are
+                /* stored lists start 256-byte aligned and their slots are
                  * multiples of 4 events: read them 16 bytes at a time */
                 if ((e & 3) == 0) quad = *reinterpret_cast<const uint4 *>(ev + e);
                 const uint32_t k = (uint32_t)e & 3u;
