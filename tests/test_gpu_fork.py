@@ -239,48 +239,57 @@ def test_fork_capacity_and_bad_rows(dev):
 
 def test_fork_join_typical_batch(dev):
     """The bench's batch: 1024 rollouts of the typical workload cut at an
-    outline; 64 sampled rows (their status, workers, contexts and joined
-    rows) compared with the oracle, the totals checked for all."""
+    outline.  Every row's outline is parsed by the oracle; every context, worker
+    record and joined row is compared.  The worker sequences handed to the join
+    are built on the host from the oracle's contexts."""
     log("case fork typical 1024")
     rng = np.random.default_rng(7)
     px = PX.Parason(CONTIG)
     rows = [np.asarray(r, np.int32) for r in synthetic_main_rows("typical", 1024, CONTIG, seed=8, p_raw=0.0)]
+    thr, end_thr, end_par = CONTIG[GP.THR - 1], CONTIG[GP.END_THR - 1], CONTIG[GP.END_PAR - 1]
+    # oracle: the outline of every row, its contexts (row + <Thread> + entry text)
+    status, off, ctx, kinds, w_row, w_entry = [], [0], [], [], [], []
+    for i, r in enumerate(rows):
+        st, entries = F.parse_outline(r.tolist(), CONTIG)
+        status.append(st)
+        for k, (kind, a, b) in enumerate(entries):
+            ctx.append(np.concatenate([r, np.array([thr], np.int32), r[a:b]]))
+            kinds.append(1 if kind == F.SUB else 2)
+            w_row.append(i)
+            w_entry.append(k)
+        off.append(off[-1] + len(entries))
+    W = off[-1]
     tok, st, ln = layout(rows, rng)
     got = px.fork(to_dev(tok, torch.int32, dev), to_dev(st, torch.int64, dev), to_dev(ln, torch.int32, dev),
                   seed=True)
     torch.cuda.synchronize()
     g = {k: v.cpu().numpy() for k, v in got.items()}
-    off = g["worker_off"]
-    W = int(off[-1])
-    assert W > 1024 and g["totals"][0] == W and g["totals"][2] == 0
-    assert g["totals"][1] == int(g["ctx_lengths"].astype(np.int64).sum())
-    sample = sorted(rng.choice(1024, size=64, replace=False).tolist())
-    for i in sample:
-        res = F.fork([rows[i].tolist()], CONTIG)
-        assert g["row_status"][i] == res["status"][0], i
-        assert off[i + 1] - off[i] == len(res["ctx"]), i
-        for k, c in enumerate(res["ctx"]):
-            w = off[i] + k
-            assert g["ctx_row"][w] == i and g["ctx_entry"][w] == k
-            assert g["ctx_kind"][w] == (1 if res["kind"][k] == F.SUB else 2)
-            s0, n0 = int(g["ctx_starts"][w]), int(g["ctx_lengths"][w])
-            assert np.array_equal(g["ctx_tokens"][s0: s0 + n0], np.asarray(c, np.int32)), (i, k)
-    # workers: context + generated text + </Thread>, laid out out of order
-    end_thr = CONTIG[GP.END_THR - 1]
-    seqs = []
-    for w in range(W):
-        s0, n0 = int(g["ctx_starts"][w]), int(g["ctx_lengths"][w])
-        gen = rng.integers(0, 1000, size=int(rng.integers(0, 60))).astype(np.int32)
-        seqs.append(np.concatenate([g["ctx_tokens"][s0: s0 + n0], gen, np.array([end_thr], np.int32)]))
+    assert np.array_equal(g["row_status"].view(np.uint32), np.array(status, np.uint32))
+    assert np.array_equal(g["worker_off"], np.array(off, np.int64)) and W > 1024
+    assert np.array_equal(g["ctx_row"], np.array(w_row, np.int32))
+    assert np.array_equal(g["ctx_entry"], np.array(w_entry, np.int32))
+    assert np.array_equal(g["ctx_kind"], np.array(kinds, np.int32))
+    lens = np.array([c.size for c in ctx], np.int64)
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+    assert np.array_equal(g["ctx_lengths"], lens.astype(np.int32)) and np.array_equal(g["ctx_starts"], starts)
+    assert list(g["totals"]) == [W, int(lens.sum()), 0]
+    assert np.array_equal(g["ctx_tokens"], np.concatenate(ctx))
+    # workers: the oracle's context + generated text + </Thread>, laid out out of order
+    seqs = [np.concatenate([c, rng.integers(0, 1000, size=int(rng.integers(0, 60))).astype(np.int32),
+                            np.array([end_thr], np.int32)]) for c in ctx]
     wtok, wst, wln = layout(seqs, rng)
     j = px.join(to_dev(tok, torch.int32, dev), to_dev(st, torch.int64, dev), to_dev(ln, torch.int32, dev),
-                got["worker_off"], to_dev(wtok, torch.int32, dev), to_dev(wst, torch.int64, dev),
-                to_dev(wln, torch.int32, dev))
+                to_dev(np.array(off, np.int64), torch.int64, dev), to_dev(wtok, torch.int32, dev),
+                to_dev(wst, torch.int64, dev), to_dev(wln, torch.int32, dev))
     torch.cuda.synchronize()
     jg = {k: v.cpu().numpy() for k, v in j.items()}
     assert not jg["row_status"].any() and jg["totals"][1] == 0
-    for i in sample:
+    exp = [np.concatenate([r] + [seqs[w][r.size:] for w in range(off[i], off[i + 1])] +
+                          [np.array([end_par], np.int32)]) for i, r in enumerate(rows)]
+    assert np.array_equal(jg["lengths"], np.array([e.size for e in exp], np.int32))
+    assert np.array_equal(jg["tokens"], np.concatenate(exp))
+    # and the oracle's join itself on a sample of rows
+    for i in sorted(rng.choice(1024, size=16, replace=False).tolist()):
         ws = [seqs[w].tolist() for w in range(off[i], off[i + 1])]
-        exp, est = F.join([rows[i].tolist()], [0, len(ws)], ws, CONTIG)
-        s0, n0 = int(jg["starts"][i]), int(jg["lengths"][i])
-        assert est == [0] and np.array_equal(jg["tokens"][s0: s0 + n0], np.asarray(exp[0], np.int32)), i
+        e, est = F.join([rows[i].tolist()], [0, len(ws)], ws, CONTIG)
+        assert est == [0] and np.array_equal(np.asarray(e[0], np.int32), exp[i]), i
