@@ -80,6 +80,11 @@ extern "C" {
  * alternative reading of the normalisation population).  A batch holding any
  * row that was not evaluated gets NaN rewards throughout. */
 #define PARASON_CFG_BATCH_STATS (1u << 1)
+/* The token scan tests each token against the twelve tag ids one by one even
+ * when a hash separates them (tag ids that are not twelve consecutive values
+ * are otherwise looked up in a 64-slot table).  Same results, slower; there
+ * for tag sets no hash of the scan separates, and for testing that path. */
+#define PARASON_CFG_TAG_COMPARE (1u << 2)
 
 /* ---- batch metrics (parason_outputs.metrics, doubles) ------------------- */
 /* As the paper reports them: trigger ratio = share of rows with >= 1

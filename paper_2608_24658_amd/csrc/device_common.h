@@ -24,6 +24,8 @@ constexpr int SEG_VEC = PARASON_SEG_VEC; /* 16-byte vectors per segment (1024 to
 constexpr int SEG_TOK = 4 * SEG_VEC;     /* tokens per segment */
 constexpr int LOADS = SEG_VEC / WAVE;    /* vector loads per lane per segment */
 constexpr int EV_CAP = 64;               /* events stored per segment */
+static_assert(SEG_VEC % WAVE == 0, "a segment is a whole number of wave-wide loads");
+static_assert(EV_CAP % 4 == 0, "stored events are read 16 bytes at a time");
 constexpr int PLAN_TILE = 4096;          /* rows per plan tile */
 constexpr int PLAN_THREADS = 256;
 constexpr int ROWS_PER_THREAD = PLAN_TILE / PLAN_THREADS;
@@ -45,13 +47,28 @@ enum : uint32_t {
 /* Branch type of the innermost enclosing thread. */
 enum : uint32_t { T_MAIN = 0, T_SUB = 1, T_TRI = 2 };
 
+constexpr int TAG_SLOTS = 64; /* slots of the tag hash: one per lane */
+
 struct TagMatch {
     int32_t ids[12];
     int32_t base;     /* contiguous case: smallest id */
     uint32_t lut_lo;  /* contiguous case: class of id base+o in nibble o (o < 8) */
     uint32_t lut_hi;  /* nibbles for o = 8..11 */
     int32_t contiguous;
+    /* other tag sets, when a pair of shifts separates them: slot(t) =
+     * ((t >> hash_a) ^ (t >> hash_b)) mod 64 is distinct for the twelve ids,
+     * slot_id[s] is the id in slot s (or an id of another slot, which no token
+     * hashing to s can equal) */
+    int32_t hashed;
+    int32_t hash_a, hash_b;
+    int32_t slot_id[TAG_SLOTS];
 };
+
+__device__ __forceinline__ uint32_t tag_slot(const TagMatch &tm, int32_t t)
+{
+    const uint32_t u = (uint32_t)t;
+    return ((u >> tm.hash_a) ^ (u >> tm.hash_b)) & (uint32_t)(TAG_SLOTS - 1);
+}
 
 __device__ __forceinline__ uint32_t classify(const TagMatch &tm, int32_t t, bool contig)
 {

@@ -85,6 +85,33 @@ int64_t segment_bound(int64_t n, int64_t total)
 }
 
 
+/* The first shift pair (a < b) whose slot function separates the twelve ids;
+ * tm.hashed stays 0 when none does (the scan then compares with all twelve). */
+void find_tag_hash(pk::TagMatch &tm)
+{
+    for (int a = 0; a < 32; ++a) {
+        for (int b = a + 1; b < 32; ++b) {
+            uint64_t used = 0;
+            int32_t slot[12];
+            bool ok = true;
+            for (int i = 0; i < 12 && ok; ++i) {
+                const uint32_t u = (uint32_t)tm.ids[i];
+                slot[i] = (int32_t)(((u >> a) ^ (u >> b)) & (uint32_t)(pk::TAG_SLOTS - 1));
+                ok = !((used >> slot[i]) & 1u);
+                used |= (uint64_t)1 << slot[i];
+            }
+            if (!ok) continue;
+            tm.hashed = 1;
+            tm.hash_a = a;
+            tm.hash_b = b;
+            /* an empty slot holds an id of another slot: no token of this slot equals it */
+            for (int s = 0; s < pk::TAG_SLOTS; ++s) tm.slot_id[s] = s == slot[0] ? tm.ids[1] : tm.ids[0];
+            for (int i = 0; i < 12; ++i) tm.slot_id[slot[i]] = tm.ids[i];
+            return;
+        }
+    }
+}
+
 }  // namespace
 
 void abi::launch_plan(const int64_t *starts, const int32_t *lengths, int64_t n, int64_t mis, int64_t n_tiles,
@@ -150,6 +177,8 @@ int parason_create(const parason_config *cfg, parason_handle **out)
             if (o < 8) h->tm.lut_lo |= c << (4 * o);
             else h->tm.lut_hi |= c << (4 * (o - 8));
         }
+    } else if (!(cfg->flags & PARASON_CFG_TAG_COMPARE)) {
+        find_tag_hash(h->tm);
     }
     *out = h;
     return PARASON_OK;
@@ -229,9 +258,11 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     const unsigned scan_blocks = (unsigned)(cus * SCAN_BLOCKS_PER_CU);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[0], stream) != hipSuccess) return PARASON_ERR_HIP;
     if (h->tm.contiguous)
-        pk::scan_rows<true><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
+        pk::scan_rows<pk::TM_CONTIG><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
+    else if (h->tm.hashed)
+        pk::scan_rows<pk::TM_HASH><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
     else
-        pk::scan_rows<false><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
+        pk::scan_rows<pk::TM_LINEAR><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[1], stream) != hipSuccess) return PARASON_ERR_HIP;
 
     pk::RowArgs ra;

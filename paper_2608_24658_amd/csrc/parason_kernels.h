@@ -613,9 +613,16 @@ __device__ __forceinline__ int4 load_vec(const int4 *p)
     return make_int4(v.x, v.y, v.z, v.w);
 }
 
-__device__ __forceinline__ bool is_tag(const TagMatch &tm, int32_t t, bool contig)
+/* Tag tests of the token scan: contiguous ids (a range check), hashed ids (one
+ * lookup in the slot table held across the wave's lanes, tab = slot_id[lane])
+ * or, for tag sets no shift pair separates, twelve compares. */
+enum : int { TM_CONTIG = 0, TM_HASH = 1, TM_LINEAR = 2 };
+
+template <int MODE>
+__device__ __forceinline__ bool is_tag(const TagMatch &tm, int32_t t, int32_t tab)
 {
-    if (contig) return (uint32_t)t - (uint32_t)tm.base < 12u;
+    if (MODE == TM_CONTIG) return (uint32_t)t - (uint32_t)tm.base < 12u;
+    if (MODE == TM_HASH) return __builtin_amdgcn_ds_bpermute((int)(tag_slot(tm, t) << 2), tab) == t;
     bool h = false;
 #pragma unroll
     for (int k = 0; k < 12; ++k) h = h || (t == tm.ids[k]);
@@ -629,10 +636,10 @@ __device__ __forceinline__ uint32_t lane_bit(uint64_t mask, int lane) { return (
  * q = 4*(i*WAVE + lane) + j is the position in the segment; cnt counts all of
  * them, stored or not.  EDGE: the segment holds the first or last vector of its
  * row, so only positions q_lo <= q < q_hi belong to the row. */
-template <bool CONTIG, bool EDGE>
+template <int MODE, bool EDGE>
 __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_lo, int32_t q_hi,
                                              uint32_t *__restrict__ dst, uint32_t cap, int32_t bias, uint32_t &cnt,
-                                             const TagMatch &tm, int lane)
+                                             const TagMatch &tm, int32_t tab, int lane)
 {
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
@@ -641,7 +648,7 @@ __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_l
         uint64_t b[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            bool hit = is_tag(tm, t[j], CONTIG);
+            bool hit = is_tag<MODE>(tm, t[j], tab);
             if (EDGE) hit = hit && q0 + j >= q_lo && q0 + j < q_hi;
             b[j] = __ballot(hit);
         }
@@ -657,7 +664,7 @@ __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_l
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 if (mine & (1u << j)) {
-                    if (idx < cap) dst[idx] = ((uint32_t)(q0 + j + bias) << 4) | classify(tm, t[j], CONTIG);
+                    if (idx < cap) dst[idx] = ((uint32_t)(q0 + j + bias) << 4) | classify(tm, t[j], MODE == TM_CONTIG);
                     ++idx;
                 }
             }
@@ -734,9 +741,9 @@ __device__ __forceinline__ void flush_row(const ScanArgs &a, int64_t row, int64_
  * its events in the wave's LDS buffer; any other row leaves its events in the
  * global per-segment slots for rows_fast.  Returns true when this segment
  * completes a row whose events are all in the LDS buffer (rc.lcnt of them). */
-template <bool CONTIG>
+template <int MODE>
 __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&x)[LOADS], const SegView &w,
-                                                RowCollect &rc, uint32_t *lev, int lane)
+                                                RowCollect &rc, uint32_t *lev, int32_t tab, int lane)
 {
     if (w.s == w.first) {
         rc.lcnt = 0;
@@ -746,8 +753,8 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
     if (!rc.global) {
         const int32_t bias = (int32_t)(4 * w.v0 - w.g); /* row position of segment position 0 */
         const uint32_t cap = (uint32_t)EVL - rc.lcnt;
-        if (!w.edge) scan_vectors<CONTIG, false>(x, 0, SEG_TOK, lev + rc.lcnt, cap, bias, cnt, a.tm, lane);
-        else scan_vectors<CONTIG, true>(x, w.q_lo, w.q_hi, lev + rc.lcnt, cap, bias, cnt, a.tm, lane);
+        if (!w.edge) scan_vectors<MODE, false>(x, 0, SEG_TOK, lev + rc.lcnt, cap, bias, cnt, a.tm, tab, lane);
+        else scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, lev + rc.lcnt, cap, bias, cnt, a.tm, tab, lane);
         if (cnt > cap) {
             /* the row's events overflow the LDS buffer: its segments so far are
              * classified again by the row kernel, the rest use global slots */
@@ -757,8 +764,10 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
             rc.lcnt += cnt;
         }
     } else {
-        if (!w.edge) scan_vectors<CONTIG, false>(x, 0, SEG_TOK, a.events + w.s * EV_CAP, EV_CAP, 0, cnt, a.tm, lane);
-        else scan_vectors<CONTIG, true>(x, w.q_lo, w.q_hi, a.events + w.s * EV_CAP, EV_CAP, 0, cnt, a.tm, lane);
+        if (!w.edge)
+            scan_vectors<MODE, false>(x, 0, SEG_TOK, a.events + w.s * EV_CAP, EV_CAP, 0, cnt, a.tm, tab, lane);
+        else
+            scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, a.events + w.s * EV_CAP, EV_CAP, 0, cnt, a.tm, tab, lane);
         if (lane == 0) a.seg_count[w.s] = (int32_t)cnt;
     }
     return w.s == w.last && !rc.global;
@@ -768,7 +777,7 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
  * register buffers alternate: the loads of segment s + 1 are issued before
  * segment s is compacted (and a finished row's events flushed), so a wave
  * always has a segment in flight. */
-template <bool CONTIG>
+template <int MODE>
 __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD) scan_rows(ScanArgs a)
 {
     __shared__ uint32_t lds_ev[SCAN_WAVES][EVL];
@@ -793,6 +802,7 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
     cur.s_end = s_end;
     cur.seek(s_begin, a.n);
     uint32_t *lev = lds_ev[wib];
+    const int32_t tab = MODE == TM_HASH ? a.tm.slot_id[lane] : 0;
 
     RowCollect rc;
     rc.lcnt = 0;
@@ -809,7 +819,7 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
             wn = cur.view(s + 1);
             issue_loads(xb, src, wn, lane);
         }
-        if (collect_segment<CONTIG>(a, xa, w, rc, lev, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, lane);
+        if (collect_segment<MODE>(a, xa, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, lane);
         if (!more) break;
         ++s;
         w = wn;
@@ -818,7 +828,7 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
             wn = cur.view(s + 1);
             issue_loads(xa, src, wn, lane);
         }
-        if (collect_segment<CONTIG>(a, xb, w, rc, lev, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, lane);
+        if (collect_segment<MODE>(a, xb, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, lane);
         if (!more) break;
         ++s;
         w = wn;

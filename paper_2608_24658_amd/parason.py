@@ -26,6 +26,7 @@ FLAG_BAD_ROW = 1 << 10
 
 CFG_INVALID_KEEPS_CORRECTNESS = 1 << 0
 CFG_BATCH_STATS = 1 << 1
+CFG_TAG_COMPARE = 1 << 2
 
 METRICS = (
     "rows", "valid", "triggered", "correct", "truncated", "count_mismatch",

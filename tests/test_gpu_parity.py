@@ -28,10 +28,15 @@ def dev():
     return torch.device("cuda:0")
 
 
-def px_for(tags=TAGS, **kw):
+# twelve of the ids 0..15, not consecutive: the scan's hash separates them while
+# the text ids next to them (5, 7, 12, 14) land in slots of their own
+LOW_IDS = np.array([3, 9, 4, 11, 0, 13, 1, 6, 15, 2, 10, 8], dtype=np.int32)
+
+
+def px_for(tags=TAGS, flags=0, **kw):
     coef = dict(DEFAULT_COEF)
     coef.update(kw)
-    return PX.Parason(tags, group_size=G, **coef), coef
+    return PX.Parason(tags, group_size=G, flags=flags, **coef), coef
 
 
 @pytest.mark.parametrize("workload", ["tiny", "small", "ragged", "typical"])
@@ -51,14 +56,18 @@ def test_workload_parity(dev, workload):
     log("%s: %d rows, %d tokens, %d/%d rewards bit-exact" % (workload, n, tok_h.size, n_exact, n))
 
 
-def test_scattered_tag_ids(dev):
-    log("case scattered tags")
+@pytest.mark.parametrize("tag_test", ["hash", "compare"])
+def test_scattered_tag_ids(dev, tag_test):
+    """Tag ids that are not twelve consecutive values: the scan's hashed lookup
+    and, with PARASON_CFG_TAG_COMPARE, its twelve-compare test."""
+    log("case scattered tags %s" % tag_test)
     P = S.make_params("small", tag_ids=S.SCATTERED_TAGS)
     n = S.n_rows_of("small")
     tok_d, st_d, ln_d, co_d = S.device_batch(P, n, device=dev)
     tok_h, st_h, ln_h, co_h = S.host_batch(P, n)
     assert np.array_equal(tok_d.cpu().numpy(), tok_h)
-    px, coef = px_for(S.SCATTERED_TAGS, alpha=0.0, beta_subtask=0.05, beta_trial=0.0)
+    flags = PX.CFG_TAG_COMPARE if tag_test == "compare" else 0
+    px, coef = px_for(S.SCATTERED_TAGS, flags=flags, alpha=0.0, beta_subtask=0.05, beta_trial=0.0)
     got = run_gpu(px, tok_d, st_d, ln_d, co_d)
     compare(got, *oracle_expect(tok_h, st_h, ln_h, co_h, S.SCATTERED_TAGS, G, coef), what="scattered")
 
@@ -144,14 +153,14 @@ def adversarial_streams():
     return streams
 
 
-@pytest.mark.parametrize("tags", ["contiguous", "scattered"])
+@pytest.mark.parametrize("tags", ["contiguous", "scattered", "scattered-compare", "low-ids"])
 def test_adversarial_streams(dev, tags):
     log("case adversarial tags=%s" % tags)
-    tag_ids = TAGS if tags == "contiguous" else S.SCATTERED_TAGS
+    tag_ids = {"contiguous": TAGS, "low-ids": LOW_IDS}.get(tags, S.SCATTERED_TAGS)
     tokens, starts, lengths = pack(adversarial_streams(), tag_ids)
     n = lengths.size
     correct = (np.arange(n) % 3 != 0).astype(np.uint8)
-    px, coef = px_for(tag_ids)
+    px, coef = px_for(tag_ids, flags=PX.CFG_TAG_COMPARE if tags == "scattered-compare" else 0)
     got = run_gpu(px, to_dev(tokens, torch.int32, dev), to_dev(starts, torch.int64, dev),
                   to_dev(lengths, torch.int32, dev), to_dev(correct, torch.uint8, dev))
     compare(got, *oracle_expect(tokens, starts, lengths, correct, tag_ids, G, coef), what="adversarial")
