@@ -359,7 +359,8 @@ def bench_decode(args):
     K = args.steps
     P = S.make_params("typical")
     tok_h, st_h, ln_h, _ = S.host_batch(P, B)
-    T = args.warmup + K + 1
+    GRAPH_STEPS = 64
+    T = max(args.warmup + K + 1, GRAPH_STEPS)
     assert int(ln_h.min()) >= T, "rollouts shorter than the timed steps"
     idx = st_h[None, :] + np.arange(T, dtype=np.int64)[:, None]
     step_tokens = torch.as_tensor(np.ascontiguousarray(tok_h[idx].astype(np.int32))).to(dev)  # [T, B]
@@ -391,6 +392,25 @@ def bench_decode(args):
     for _ in range(args.warmup):
         px.decode_step(fresh, logits, None, eos)
     struct_ms = timed(lambda k: px.decode_step(fresh, logits, None, eos), K)
+    # the first 64 steps of the rollouts as one call sequence (initialisation,
+    # the step without a token, 63 steps), eagerly and as a replayed HIP graph
+    gstates = torch.empty(B * PX.DECODE_STATE_BYTES, dtype=torch.uint8, device=dev)
+
+    def sequence():
+        PX.decode_init(B, dev, states=gstates)
+        px.decode_step(gstates, logits, None, eos)
+        for k in range(GRAPH_STEPS - 1):
+            px.decode_step(gstates, logits, step_tokens[k], eos)
+
+    eager_seq_ms = timed(lambda k: sequence(), 10)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        sequence()
+    graph.replay()
+    torch.cuda.synchronize()
+    graph_seq_ms = timed(lambda k: graph.replay(), 10)
+    assert not PX.decode_fields(gstates)[:, 3].any().item(), "synthetic rollouts must stay valid"
+
     alg = B * (V * 2 + 16 + 16)  # logits written, state read + written
     # reference for a write-only stream of the same size: torch's fill
     for _ in range(args.warmup):
@@ -414,6 +434,8 @@ def bench_decode(args):
         "config": {"workload": "decode batch %d, vocab %d, bf16 logits, contiguous tag ids" % (B, V),
                    "batch": B, "vocab": V},
         "structural_ms_per_step": struct_ms,
+        "first_64_steps": {"eager_ms_per_step": eager_seq_ms / GRAPH_STEPS,
+                           "hip_graph_ms_per_step": graph_seq_ms / GRAPH_STEPS},
         "roofline": {"kernel": "decode_step (structural regime)", "bound": "hbm", "achieved": ach,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS, "traffic": None,
                      "kernel_ms": struct_ms, "algorithmic_bytes": alg},
