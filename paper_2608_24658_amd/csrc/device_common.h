@@ -30,9 +30,10 @@ constexpr int PLAN_TILE = 4096;          /* rows per plan tile */
 constexpr int PLAN_THREADS = 256;
 constexpr int ROWS_PER_THREAD = PLAN_TILE / PLAN_THREADS;
 #ifndef PARASON_FAST_DEPTH
-#define PARASON_FAST_DEPTH 8
+#define PARASON_FAST_DEPTH 4
 #endif
 constexpr int FAST_DEPTH = PARASON_FAST_DEPTH; /* LDS frames per row (depth <= FAST_DEPTH + 1) */
+constexpr int MID_DEPTH = 32;            /* LDS frames per row handed to the second tier */
 constexpr int FAST_ENTRIES = 64;         /* entries per open block on the fast path */
 constexpr int FRAME_WORDS = 8;
 constexpr int64_t DEEP_FRAMES = PARASON_MAX_DEPTH;

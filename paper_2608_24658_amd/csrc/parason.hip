@@ -23,10 +23,11 @@ namespace {
 #endif
 constexpr int SCAN_BLOCKS_PER_CU = PARASON_SCAN_BLOCKS_PER_CU; /* persistent grid of 4-wave blocks */
 constexpr int64_t MAX_SEGMENTS = (int64_t)1 << 40;
+constexpr int MID_BLOCKS_PER_CU = 2; /* rows_mid blocks hold 64 KB of LDS frames each */
 
 /* Byte offsets of the workspace sections for n rows. */
 struct Layout {
-    size_t seg_off, tile_sum, tile_off, counters, mode, deep_rows, deep_frames, deep_bits, seg_count, events;
+    size_t seg_off, tile_sum, tile_off, counters, mode, mid_rows, deep_rows, deep_frames, deep_bits, seg_count, events;
     size_t red_d, red_i, stats;
     size_t fixed;  /* bytes before the per-segment sections */
     int64_t n_tiles;
@@ -47,6 +48,8 @@ Layout layout_for(int64_t n)
     o = align_up(o + 4 * sizeof(int32_t));
     L.mode = o;
     o = align_up(o + (size_t)(n > 0 ? n : 1));
+    L.mid_rows = o;
+    o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
     L.deep_rows = o;
     o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
     L.deep_frames = o;
@@ -229,6 +232,7 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     int64_t *tile_off = (int64_t *)(ws + L.tile_off);
     int32_t *counters = (int32_t *)(ws + L.counters);
     uint8_t *mode = (uint8_t *)(ws + L.mode);
+    int32_t *mid_rows = (int32_t *)(ws + L.mid_rows);
     int32_t *deep_rows = (int32_t *)(ws + L.deep_rows);
     int32_t *deep_frames = (int32_t *)(ws + L.deep_frames);
     uint32_t *deep_bits = (uint32_t *)(ws + L.deep_bits);
@@ -278,7 +282,9 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.tm = h->tm;
     ra.out = row_out;
     const unsigned row_blocks = (unsigned)((n_traj + 63) / 64);
-    pk::rows_fast<<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows);
+    pk::rows_fast<<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows);
+    pk::rows_mid<<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows,
+                                                                                     deep_rows);
     pk::rows_deep<<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);
 
     pk::RewardArgs rw;

@@ -20,8 +20,11 @@
  *        the gaps between event positions.  A segment holding more than EV_CAP
  *        tags, or marked DENSE by the scan, is classified again token by token.
  *        Frames of open blocks in LDS (FAST_DEPTH per row, 64 outline entries
- *        per block); a row that needs more is handed to rows_deep.
- *   rows_deep  (one thread, only rows handed over)
+ *        per block); a row that needs more is handed to rows_mid.
+ *   rows_mid  (one thread per handed-over row, MID_DEPTH frames in LDS)
+ *        The same automaton for deeper rows; a row that needs more still is
+ *        handed to rows_deep.
+ *   rows_deep  (one thread, only rows rows_mid handed over)
  *        The same automaton with frames and entry types in global workspace.
  *   group_reward  (one thread per group of G rows)
  *        Statistics and Definition 3.1 in IEEE double, fixed order.
@@ -138,14 +141,15 @@ struct Top {
     uint64_t ent;       /* fast store: entry-type bits; deep store: first bit index */
 };
 
-/* Fast store: FAST_DEPTH frames per thread in LDS, entry types as a 64-bit mask. */
+/* LDS store: DEPTH frames per thread in LDS, entry types as a 64-bit mask. */
+template <int DEPTH>
 struct LdsStore {
-    int32_t *lds; /* [FAST_DEPTH][FRAME_WORDS][blockDim] */
+    int32_t *lds; /* [DEPTH][FRAME_WORDS][blockDim] */
     int tid, nt;
     __device__ int32_t &at(int d, int f) { return lds[(d * FRAME_WORDS + f) * nt + tid]; }
     __device__ bool push(const Top &t, int d)
     {
-        if (d > FAST_DEPTH) return false;
+        if (d > DEPTH) return false;
         at(d - 1, 0) = t.saved_acc;
         at(d - 1, 1) = t.block_main;
         at(d - 1, 2) = t.max_w;
@@ -546,9 +550,12 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
 }
 
 /* One thread per row.  mode[r] == 1: the scan left the row's events as one
- * compact list; 0: per-segment slots. */
+ * compact list; 0: per-segment slots.  A row that needs more than FAST_DEPTH
+ * frames (or more than 64 entries in an open block) is listed for rows_mid.
+ * Few frames keep the LDS per block small, so that many waves hide the
+ * latency of the branchy automaton. */
 __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__restrict__ mode,
-                                                int32_t *__restrict__ counters, int32_t *__restrict__ deep_rows)
+                                                int32_t *__restrict__ counters, int32_t *__restrict__ mid_rows)
 {
     __shared__ int32_t lds[FAST_DEPTH * FRAME_WORDS * 64];
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -563,7 +570,7 @@ __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__rest
         write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
         return;
     }
-    Automaton<LdsStore> A;
+    Automaton<LdsStore<FAST_DEPTH>> A;
     A.st.lds = lds;
     A.st.tid = threadIdx.x;
     A.st.nt = blockDim.x;
@@ -571,13 +578,41 @@ __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__rest
     if (drive_row(a, r, start + a.mis, len, mode[r] == 1, A)) A.finish(len);
     if (A.overflow) {
         int32_t slot = atomicAdd(&counters[0], 1);
-        deep_rows[slot] = (int32_t)r;
-        return; /* rows_deep writes this row */
+        mid_rows[slot] = (int32_t)r;
+        return; /* rows_mid writes this row */
     }
     write_result(a.out, r, len, A);
 }
 
-/* Rows whose nesting or entry count exceeded the fast store, one after the
+/* The rows rows_fast listed, one thread each (grid-stride over the list), with
+ * MID_DEPTH frames per row in LDS; rows that need still more are listed for
+ * rows_deep. */
+__global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restrict__ mode,
+                                               int32_t *__restrict__ counters, const int32_t *__restrict__ mid_rows,
+                                               int32_t *__restrict__ deep_rows)
+{
+    __shared__ int32_t lds[MID_DEPTH * FRAME_WORDS * 64];
+    const int32_t n_mid = counters[0];
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_mid;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = mid_rows[i];
+        const int32_t len = a.lengths[r];
+        Automaton<LdsStore<MID_DEPTH>> A;
+        A.st.lds = lds;
+        A.st.tid = threadIdx.x;
+        A.st.nt = blockDim.x;
+        A.init();
+        if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
+        if (A.overflow) {
+            int32_t slot = atomicAdd(&counters[1], 1);
+            deep_rows[slot] = (int32_t)r;
+        } else {
+            write_result(a.out, r, len, A);
+        }
+    }
+}
+
+/* Rows whose nesting or entry count exceeded the LDS stores, one after the
  * other, on a single thread with frames in global workspace. */
 __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__restrict__ mode,
                                                 const int32_t *__restrict__ counters,
@@ -585,7 +620,7 @@ __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__rest
                                                 uint32_t *__restrict__ bits)
 {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    const int32_t n_deep = counters[0];
+    const int32_t n_deep = counters[1];
     for (int32_t i = 0; i < n_deep; ++i) {
         const int64_t r = deep_rows[i];
         const int32_t len = a.lengths[r];

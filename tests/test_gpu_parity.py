@@ -126,8 +126,9 @@ def adversarial_streams():
         streams.append(s[: int(rng.integers(0, len(s) + 1))])
     # empty rows, single tokens
     streams += [[], [GP.THINK], [GP.TEXT], [GP.END_THINK]]
-    # nesting: fast-path limit is 9 levels, then the deep path
-    streams += [deep_stream(d) for d in (1, 2, 8, 9, 10, 40, 1000)]
+    # nesting across the three tiers: LDS frames for 5 levels (rows_fast), for
+    # 33 (rows_mid), then global frames (rows_deep)
+    streams += [deep_stream(d) for d in (1, 2, 4, 5, 6, 9, 10, 32, 33, 34, 40, 1000)]
     streams.append(deep_stream(300, GP.TRI)[:-5])  # truncated deep
     # fan-out beyond the 64 entries of the fast path, with a thread-count mismatch
     streams += [fanout_stream(64), fanout_stream(65), fanout_stream(200, 150), fanout_stream(70, 90)]
@@ -166,6 +167,26 @@ def test_adversarial_streams(dev, tags):
     compare(got, *oracle_expect(tokens, starts, lengths, correct, tag_ids, G, coef), what="adversarial")
     assert int(np.sum(got["max_depth"] == 1000)) == 1
     log("adversarial: %d rows ok" % n)
+
+
+def test_many_rows_beyond_the_first_tier(dev):
+    """40,000 rows nested 6-33 deep (more than the second tier has threads, so
+    its threads stride over the handed-over list) and 48 rows nested 34-60
+    deep (the single-thread tier), mixed with shallow rows."""
+    log("case tiers")
+    rng = np.random.default_rng(12)
+    depths = np.concatenate([rng.integers(6, 34, size=40000), rng.integers(34, 61, size=48),
+                             rng.integers(1, 6, size=8000)])
+    rng.shuffle(depths)
+    streams = [deep_stream(int(d), GP.TRI if d % 2 else GP.SUB) for d in depths]
+    tokens, starts, lengths = pack(streams, TAGS)
+    n = lengths.size
+    correct = (np.arange(n) % 5 != 0).astype(np.uint8)
+    px, coef = px_for()
+    got = run_gpu(px, to_dev(tokens, torch.int32, dev), to_dev(starts, torch.int64, dev),
+                  to_dev(lengths, torch.int32, dev), to_dev(correct, torch.uint8, dev))
+    compare(got, *oracle_expect(tokens, starts, lengths, correct, TAGS, G, coef), what="tiers")
+    assert np.array_equal(got["max_depth"][: depths.size], depths.astype(np.int32))
 
 
 def test_layouts_misaligned_padded_overlapping_reversed(dev):
