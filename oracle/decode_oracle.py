@@ -11,7 +11,9 @@ exactly that with the parser of ``parason_oracle.c``: class c is allowed after
 `prefix` iff the parser reports prefix + [c] as valid or as truncated (it never
 fails inside it); the end-of-sequence token is allowed iff the prefix itself is
 a complete valid stream.  Text stands for every id that is not a tag and not
-the end-of-sequence id.
+the end-of-sequence id.  ``cfg_flags`` selects the language as for the
+accounting (CFG_LENIENT_GAPS: Text runs between the structural tags of a
+parallel region).
 """
 from __future__ import annotations
 
@@ -22,20 +24,20 @@ from oracle import oracle as O
 TEXT = 0
 
 
-def allowed_classes(prefix_tokens, tag_ids, text_id: int):
+def allowed_classes(prefix_tokens, tag_ids, text_id: int, cfg_flags: int = 0):
     """(set of allowed classes 0..12, eos_allowed) after the token prefix."""
     prefix = list(int(t) for t in prefix_tokens)
     allowed = set()
     for c in range(13):
         tok = text_id if c == TEXT else int(tag_ids[c - 1])
-        r = O.eval_stream(prefix + [tok], tag_ids)
+        r = O.eval_stream(prefix + [tok], tag_ids, cfg_flags)
         if r["flags"] & (O.F_VALID | O.F_TRUNCATED):
             allowed.add(c)
-    r = O.eval_stream(prefix, tag_ids)
+    r = O.eval_stream(prefix, tag_ids, cfg_flags)
     return allowed, bool(r["flags"] & O.F_VALID)
 
 
-def allowed_batch(prefixes, tag_ids, text_id: int):
+def allowed_batch(prefixes, tag_ids, text_id: int, cfg_flags: int = 0):
     """allowed_classes for many prefixes with one call of the parser: for each
     prefix p the rows p, p + [Text], p + [tag 1], ..., p + [tag 12]."""
     cands = [int(text_id)] + [int(t) for t in tag_ids]
@@ -50,7 +52,8 @@ def allowed_batch(prefixes, tag_ids, text_id: int):
             lengths.append(len(row))
             pos += len(row)
     tokens = np.array([t for c in chunks for t in c] or [0], dtype=np.int32)
-    res = O.eval_rows(tokens, np.array(starts, dtype=np.int64), np.array(lengths, dtype=np.int32), tag_ids)
+    res = O.eval_rows(tokens, np.array(starts, dtype=np.int64), np.array(lengths, dtype=np.int32), tag_ids,
+                      cfg_flags)
     out = []
     for i in range(len(prefixes)):
         r = res[14 * i: 14 * (i + 1)]
@@ -59,6 +62,6 @@ def allowed_batch(prefixes, tag_ids, text_id: int):
     return out
 
 
-def prefix_is_viable(prefix_tokens, tag_ids) -> bool:
-    r = O.eval_stream(list(int(t) for t in prefix_tokens), tag_ids)
+def prefix_is_viable(prefix_tokens, tag_ids, cfg_flags: int = 0) -> bool:
+    r = O.eval_stream(list(int(t) for t in prefix_tokens), tag_ids, cfg_flags)
     return bool(r["flags"] & (O.F_VALID | O.F_TRUNCATED)) or len(prefix_tokens) == 0

@@ -42,6 +42,7 @@ F_TRIGGERED = 1 << 3
 
 CFG_INVALID_KEEPS_CORRECTNESS = 1 << 0
 CFG_BATCH_STATS = 1 << 1
+CFG_LENIENT_GAPS = 1 << 3  # Text runs allowed between the structural tags of a parallel region
 
 METRICS = (
     "rows", "valid", "triggered", "correct", "truncated", "count_mismatch",
@@ -80,7 +81,7 @@ def lib():
         L.oracle_eval_rows.restype = ctypes.c_int
         L.oracle_eval_rows.argtypes = [
             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
-            ctypes.c_void_p, ctypes.c_void_p,
+            ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p,
         ]
         L.oracle_group_reward.restype = ctypes.c_int
         L.oracle_group_reward.argtypes = [
@@ -99,8 +100,9 @@ def _ptr(a: np.ndarray) -> int:
     return a.ctypes.data
 
 
-def eval_rows(tokens, starts, lengths, tag_ids) -> np.ndarray:
-    """Per-row accounting.  Row i is tokens[starts[i] : starts[i] + lengths[i]]."""
+def eval_rows(tokens, starts, lengths, tag_ids, cfg_flags: int = 0) -> np.ndarray:
+    """Per-row accounting.  Row i is tokens[starts[i] : starts[i] + lengths[i]].
+    cfg_flags: CFG_LENIENT_GAPS or 0."""
     tokens = np.ascontiguousarray(tokens, dtype=np.int32)
     starts = np.ascontiguousarray(starts, dtype=np.int64)
     lengths = np.ascontiguousarray(lengths, dtype=np.int32)
@@ -115,16 +117,17 @@ def eval_rows(tokens, starts, lengths, tag_ids) -> np.ndarray:
         return out
     if tokens.size == 0:
         tokens = np.zeros(1, dtype=np.int32)
-    rc = lib().oracle_eval_rows(_ptr(tokens), _ptr(starts), _ptr(lengths), n, _ptr(tag_ids), _ptr(out))
+    rc = lib().oracle_eval_rows(_ptr(tokens), _ptr(starts), _ptr(lengths), n, _ptr(tag_ids),
+                                cfg_flags & CFG_LENIENT_GAPS, _ptr(out))
     if rc != 0:
         raise RuntimeError("oracle_eval_rows failed: %d" % rc)
     return out
 
 
-def eval_stream(stream, tag_ids) -> np.void:
+def eval_stream(stream, tag_ids, cfg_flags: int = 0) -> np.void:
     """Accounting of a single token stream."""
     s = np.asarray(stream, dtype=np.int32)
-    return eval_rows(s, np.array([0]), np.array([s.size]), tag_ids)[0]
+    return eval_rows(s, np.array([0]), np.array([s.size]), tag_ids, cfg_flags)[0]
 
 
 def group_reward(rows: np.ndarray, correct, group_size: int, alpha: float, beta_subtask: float,

@@ -40,6 +40,13 @@
  *   - mean and standard deviation are taken over the G rollouts of one prompt
  *     (population form); z = 0 when every member of the group has the same
  *     value (sigma = 0 in exact arithmetic) or the computed sigma is 0.
+ *   - strict by default: no Text between the structural tags of a parallel
+ *     region, as the grammar is printed.  With CFG_LENIENT_GAPS (the layout of
+ *     Figure 3, which puts line breaks there) a run of Text may follow
+ *     <Parallel>, <Outlines>, each outline entry, </Outlines> and each
+ *     </Thread> of a region; those tokens are decoded by the enclosing path,
+ *     like the outline, so they add to lat(P) and take the enclosing branch
+ *     type.
  *
  * Deep nesting recurses; the batch entry point runs the parser on a worker
  * thread with a large stack so adversarial depth cannot overflow the C stack.
@@ -71,6 +78,7 @@ enum { CTX_MAIN = 0, CTX_SUBTASK = 1, CTX_TRIAL = 2 };
 
 /* Configuration flag bits (interface contract). */
 #define CFG_INVALID_KEEPS_CORRECTNESS (1u << 0)
+#define CFG_LENIENT_GAPS (1u << 3)
 
 typedef struct {
     int32_t total;
@@ -94,6 +102,7 @@ typedef struct {
     int64_t n_blocks;
     int64_t depth, max_depth;
     int mismatch;
+    int lenient; /* CFG_LENIENT_GAPS */
 } parser_t;
 
 static int class_at(const parser_t *p, int64_t i)
@@ -150,6 +159,19 @@ static int64_t parse_T(parser_t *p, int ctx)
     return n;
 }
 
+/* A gap between structural tags of a parallel region: with CFG_LENIENT_GAPS
+ * any run of Text (possibly empty), otherwise nothing.  Returns its length. */
+static int64_t parse_gap(parser_t *p, int ctx)
+{
+    int64_t n = 0;
+    if (!p->lenient || p->failed) return 0;
+    while (peek(p) == K_TEXT) {
+        take(p, ctx);
+        ++n;
+    }
+    return n;
+}
+
 /* B -> T B | P B | epsilon.  Returns lat(B): text counts once per token, a
  * parallel region contributes lat(P). */
 static int64_t parse_B(parser_t *p, int ctx)
@@ -202,20 +224,23 @@ static void entries_push(entries_t *e, int t)
     e->type[e->n++] = t;
 }
 
-/* G -> E G | E */
+/* G -> E G | E  (each E followed by a gap when lenient) */
 static void parse_G(parser_t *p, int ctx, entries_t *entries)
 {
     do {
         int t = parse_E(p, ctx);
         if (p->failed) return;
         entries_push(entries, t);
+        parse_gap(p, ctx);
     } while (peek(p) == K_SUB || peek(p) == K_TRI);
 }
 
-/* O -> <Outlines> G </Outlines>.  Entry types are returned in order. */
+/* O -> <Outlines> G </Outlines>  (a gap after <Outlines> when lenient).
+ * Entry types are returned in order. */
 static void parse_O(parser_t *p, int ctx, entries_t *entries)
 {
     if (!expect(p, K_OUT, ctx)) return;
+    parse_gap(p, ctx);
     parse_G(p, ctx, entries);
     expect(p, K_END_OUT, ctx);
 }
@@ -230,8 +255,10 @@ static int64_t parse_W(parser_t *p, int type)
     return 2 + body;
 }
 
-/* H -> W H | W.  Thread k is paired with entry k.  Returns max_k lat(W_k). */
-static int64_t parse_H(parser_t *p, const entries_t *entries)
+/* H -> W H | W  (each W followed by a gap when lenient; the gap tokens are the
+ * enclosing path's, added to *gaps).  Thread k is paired with entry k.
+ * Returns max_k lat(W_k). */
+static int64_t parse_H(parser_t *p, const entries_t *entries, int ctx, int64_t *gaps)
 {
     int64_t k = 0, longest = 0;
     do {
@@ -239,6 +266,7 @@ static int64_t parse_H(parser_t *p, const entries_t *entries)
         int64_t lat = parse_W(p, type);
         if (p->failed) return 0;
         if (lat > longest) longest = lat;
+        *gaps += parse_gap(p, ctx);
         ++k;
     } while (peek(p) == K_THR);
     if (k != entries->n) p->mismatch = 1;
@@ -248,7 +276,9 @@ static int64_t parse_H(parser_t *p, const entries_t *entries)
 /* P -> <Parallel> O H </Parallel>.  <Parallel> and the outline are decoded on
  * the enclosing path before dispatch, the block then waits for its longest
  * thread, then </Parallel> follows:
- *   lat(P) = 1 + |O| + max_k lat(W_k) + 1. */
+ *   lat(P) = 1 + |O| + max_k lat(W_k) + 1
+ * and, when lenient, + the gap tokens after <Parallel>, </Outlines> and each
+ * thread (the gaps inside O are part of |O|). */
 static int64_t parse_P(parser_t *p, int ctx)
 {
     p->n_blocks += 1;
@@ -256,17 +286,19 @@ static int64_t parse_P(parser_t *p, int ctx)
     if (p->depth > p->max_depth) p->max_depth = p->depth;
 
     if (!expect(p, K_PAR, ctx)) return 0;
+    int64_t gaps = parse_gap(p, ctx);
     int64_t o_start = p->pos;
     entries_t entries = {0, 0, 0};
     parse_O(p, ctx, &entries);
     int64_t o_len = p->pos - o_start;
+    gaps += parse_gap(p, ctx);
     int64_t longest = 0;
-    if (!p->failed) longest = parse_H(p, &entries);
+    if (!p->failed) longest = parse_H(p, &entries, ctx, &gaps);
     free(entries.type);
     if (!expect(p, K_END_PAR, ctx)) return 0;
 
     p->depth -= 1;
-    return 1 + o_len + longest + 1;
+    return 1 + gaps + o_len + longest + 1;
 }
 
 /* S -> <think> B </think>, followed by free text (the answer). */
@@ -310,13 +342,14 @@ static void parse_row(parser_t *p, oracle_row_t *out)
 }
 
 void oracle_eval_row(const int32_t *tok, int32_t len, const int32_t tag_ids[12],
-                     oracle_row_t *out)
+                     uint32_t cfg_flags, oracle_row_t *out)
 {
     parser_t p;
     memset(&p, 0, sizeof(p));
     p.tok = tok;
     p.len = len < 0 ? 0 : len;
     p.tag_ids = tag_ids;
+    p.lenient = (cfg_flags & CFG_LENIENT_GAPS) != 0;
     parse_row(&p, out);
 }
 
@@ -326,6 +359,7 @@ typedef struct {
     const int32_t *lengths;
     int64_t n_rows;
     const int32_t *tag_ids;
+    uint32_t cfg_flags;
     oracle_row_t *out;
 } batch_t;
 
@@ -333,17 +367,18 @@ static void *batch_main(void *arg)
 {
     batch_t *b = (batch_t *)arg;
     for (int64_t i = 0; i < b->n_rows; ++i)
-        oracle_eval_row(b->tokens + b->starts[i], b->lengths[i], b->tag_ids, &b->out[i]);
+        oracle_eval_row(b->tokens + b->starts[i], b->lengths[i], b->tag_ids, b->cfg_flags, &b->out[i]);
     return NULL;
 }
 
 /* Evaluate rows [0, n_rows); row i is tokens[starts[i] .. starts[i]+lengths[i]).
+ * cfg_flags: CFG_LENIENT_GAPS or 0 (other bits are ignored here).
  * Runs single-threaded on one worker thread whose stack is large enough for
  * any nesting a row of up to 2^31 tokens can hold.  Returns 0 on success. */
 int oracle_eval_rows(const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
-                     int64_t n_rows, const int32_t tag_ids[12], oracle_row_t *out)
+                     int64_t n_rows, const int32_t tag_ids[12], uint32_t cfg_flags, oracle_row_t *out)
 {
-    batch_t b = {tokens, starts, lengths, n_rows, tag_ids, out};
+    batch_t b = {tokens, starts, lengths, n_rows, tag_ids, cfg_flags, out};
     int32_t max_len = 0;
     for (int64_t i = 0; i < n_rows; ++i)
         if (lengths[i] > max_len) max_len = lengths[i];

@@ -7,11 +7,15 @@ a textbook algorithm applied directly to the paper's definitions:
   "Context-Free Grammar for Parason" (Sec. 3.2), extended by the reading that
   free text may follow </think>.  A prefix is viable exactly when its Earley set
   is non-empty (every non-terminal of the grammar is productive), which gives an
-  independent first-error position.
+  independent first-error position.  ``grammar="lenient"`` adds a nullable
+  ``Gap -> Text Gap | epsilon`` after <Parallel>, <Outlines>, every outline
+  entry, </Outlines> and every thread (the line breaks of Figure 3).
 * ``dag_latency`` -- builds the fork/join dependency DAG of a valid stream (each
-  token waits for the previous token on its own path; the threads of a block
-  fork after </Outlines> and </Parallel> joins all of them) and takes the longest
-  path, which is the "longest generation path" of Sec. 4 ("Evaluation").
+  token waits for the previous token on its own path; the tokens of a block
+  outside its threads form the block's own sequential chain, its threads fork
+  after the last of them, and </Parallel> joins all threads) and takes the
+  longest path, which is the "longest generation path" of Sec. 4
+  ("Evaluation").
 * ``enumerate_valid`` -- grammar-directed enumeration of every valid class
   string up to a length bound.
 
@@ -41,15 +45,26 @@ GRAMMAR = {
     "W": [[THR, "B", END_THR]],
     "T": [[TEXT, "T"], [TEXT]],
 }
+# The same grammar with optional Text runs between the structural tags of a
+# parallel region.
+LENIENT_GRAMMAR = dict(
+    GRAMMAR,
+    P=[[PAR, "Gap", "O", "Gap", "H", END_PAR]],
+    O=[[OUT, "Gap", "G", END_OUT]],
+    G=[["E", "Gap", "G"], ["E", "Gap"]],
+    H=[["W", "Gap", "H"], ["W", "Gap"]],
+    Gap=[[TEXT, "Gap"], []],
+)
+GRAMMARS = {"strict": GRAMMAR, "lenient": LENIENT_GRAMMAR}
 START = "S0"
 
 
-def _nullable():
+def _nullable(grammar):
     null = set()
     changed = True
     while changed:
         changed = False
-        for a, alts in GRAMMAR.items():
+        for a, alts in grammar.items():
             if a in null:
                 continue
             for rhs in alts:
@@ -60,16 +75,18 @@ def _nullable():
     return null
 
 
-NULLABLE = _nullable()
+NULLABLE = {name: _nullable(g) for name, g in GRAMMARS.items()}
 
 
-def earley(classes):
+def earley(classes, grammar="strict"):
     """Return (accepted, first_error_pos).
 
     first_error_pos is the length of the longest viable prefix when that prefix
     is shorter than the input; len(classes) when the whole input is viable but
     not a sentence (truncated); -1 when accepted.
     """
+    GR = GRAMMARS[grammar]
+    nullable = NULLABLE[grammar]
     n = len(classes)
     sets = [set() for _ in range(n + 1)]
     # item = (lhs, alt_index, dot, origin)
@@ -80,36 +97,36 @@ def earley(classes):
             work.append(item)
 
     work = []
-    for ai in range(len(GRAMMAR[START])):
+    for ai in range(len(GR[START])):
         add(0, (START, ai, 0, 0), work)
     for k in range(n + 1):
         work = list(sets[k])
         while work:
             lhs, ai, dot, org = work.pop()
-            rhs = GRAMMAR[lhs][ai]
+            rhs = GR[lhs][ai]
             if dot < len(rhs):
                 sym = rhs[dot]
                 if isinstance(sym, str):  # predict
-                    for bi in range(len(GRAMMAR[sym])):
+                    for bi in range(len(GR[sym])):
                         add(k, (sym, bi, 0, k), work)
-                    if sym in NULLABLE:
+                    if sym in nullable:
                         add(k, (lhs, ai, dot + 1, org), work)
             else:  # complete
                 for (l2, a2, d2, o2) in list(sets[org]):
-                    r2 = GRAMMAR[l2][a2]
+                    r2 = GR[l2][a2]
                     if d2 < len(r2) and r2[d2] == lhs:
                         add(k, (l2, a2, d2 + 1, o2), work)
         if k == n:
             break
         tok = classes[k]
         for (lhs, ai, dot, org) in sets[k]:
-            rhs = GRAMMAR[lhs][ai]
+            rhs = GR[lhs][ai]
             if dot < len(rhs) and rhs[dot] == tok:
                 sets[k + 1].add((lhs, ai, dot + 1, org))
         if not sets[k + 1]:
             return False, k
     accepted = any(
-        lhs == START and dot == len(GRAMMAR[lhs][ai]) and org == 0
+        lhs == START and dot == len(GR[lhs][ai]) and org == 0
         for (lhs, ai, dot, org) in sets[n]
     )
     return (True, -1) if accepted else (False, n)
@@ -118,37 +135,85 @@ def earley(classes):
 def dag_latency(classes):
     """Longest path (in tokens) through the fork/join DAG of a *valid* stream.
 
+    Nodes are tokens, each costing 1.  Edges:
+      * a token on a path (the root, a thread, or a block's own chain) waits
+        for the previous token on that path;
+      * a block's own chain is <Parallel> and every token of the block outside
+        its threads except </Parallel> (the outline, and gap Text where the
+        lenient grammar allows it); <Parallel> waits for the enclosing path;
+      * every <Thread> of the block waits for the last token of that chain
+        (the threads are dispatched once the main trajectory has decoded it);
+      * </Parallel> waits for every </Thread> of the block, and the enclosing
+        path continues from </Parallel>.
     Returns (latency, thread_latencies) where thread_latencies is a list with
     one list per block, in order of the block's </Parallel>, holding each
     thread's own longest path (from its <Thread> to its </Thread>).
     """
-    dist = [0] * len(classes)
-    blocks = []  # stack of dicts: fork node, thread end nodes, thread start nodes
+    n = len(classes)
+    deps = [[] for _ in range(n)]
+    fork_of = {}  # <Thread> index -> block id (resolved after the block closes)
+    blocks = []  # open blocks: {"id", "chain_last", "ends", "starts"}
+    paths = [None]  # per open path, the previous token on it; root first
+    kinds = ["root"]  # "root", "block" or "thread" for each open path
+    closed = {}
     finished = []
-    pred = None
+    bid = 0
     for i, c in enumerate(classes):
         if c == PAR:
-            deps = [pred]
-            blocks.append({"fork": None, "ends": [], "starts": []})
-        elif c == END_OUT:
-            deps = [pred]
-            blocks[-1]["fork"] = i
+            deps[i] = [paths[-1]]
+            blocks.append({"id": bid, "chain_last": i, "ends": [], "starts": []})
+            bid += 1
+            paths.append(i)
+            kinds.append("block")
         elif c == THR:
-            deps = [blocks[-1]["fork"]]
-            blocks[-1]["starts"].append(i)
+            b = blocks[-1]
+            fork_of[i] = b["id"]
+            b["starts"].append(i)
+            paths.append(i)
+            kinds.append("thread")
         elif c == END_THR:
-            deps = [pred]
+            deps[i] = [paths[-1]]
+            paths.pop()
+            kinds.pop()
             blocks[-1]["ends"].append(i)
         elif c == END_PAR:
-            deps = blocks[-1]["ends"]
             b = blocks.pop()
-            finished.append([dist[e] - dist[s] + 1 for s, e in zip(b["starts"], b["ends"])])
+            deps[i] = list(b["ends"])
+            closed[b["id"]] = b["chain_last"]
+            finished.append(b)
+            paths.pop()
+            kinds.pop()
+            paths[-1] = i
+            continue
         else:
-            deps = [pred]
-        base = max((dist[d] for d in deps if d is not None), default=0)
-        dist[i] = base + 1
-        pred = i if c != END_THR else None
-    return (dist[-1] if classes else 0), finished
+            deps[i] = [paths[-1]]
+            if kinds[-1] == "block":
+                blocks[-1]["chain_last"] = i
+        if c != END_THR:
+            paths[-1] = i
+    for t, b in fork_of.items():
+        deps[t] = [closed[b]]
+    dist = [None] * n
+
+    def longest(i):
+        stack = [i]
+        while stack:
+            j = stack[-1]
+            if dist[j] is not None:
+                stack.pop()
+                continue
+            todo = [d for d in deps[j] if d is not None and dist[d] is None]
+            if todo:
+                stack.extend(todo)
+                continue
+            dist[j] = 1 + max((dist[d] for d in deps[j] if d is not None), default=0)
+            stack.pop()
+        return dist[i]
+
+    for i in range(n):
+        longest(i)
+    per_block = [[dist[e] - dist[s] + 1 for s, e in zip(b["starts"], b["ends"])] for b in finished]
+    return (dist[-1] if classes else 0), per_block
 
 
 def thread_types(classes):
@@ -182,47 +247,47 @@ def thread_types(classes):
 
 
 @functools.lru_cache(maxsize=None)
-def _gen(sym, maxlen):
+def _gen(sym, maxlen, grammar):
     """All terminal strings (tuples) of length <= maxlen derivable from sym."""
     if maxlen < 0:
         return frozenset()
     if isinstance(sym, int):
         return frozenset([(sym,)]) if maxlen >= 1 else frozenset()
     res = set()
-    for rhs in GRAMMAR[sym]:
-        res |= _seq(tuple(rhs), maxlen)
+    for rhs in GRAMMARS[grammar][sym]:
+        res |= _seq(tuple(rhs), maxlen, grammar)
     return frozenset(res)
 
 
 @functools.lru_cache(maxsize=None)
-def _seq(rhs, maxlen):
+def _seq(rhs, maxlen, grammar):
     if not rhs:
         return frozenset([()])
     head, rest = rhs[0], rhs[1:]
     # every symbol derives at least its minimal length; bound the head accordingly
     res = set()
-    min_rest = sum(_minlen(s) for s in rest)
-    for h in _gen(head, maxlen - min_rest):
-        for r in _seq(rest, maxlen - len(h)):
+    min_rest = sum(_minlen(s, grammar) for s in rest)
+    for h in _gen(head, maxlen - min_rest, grammar):
+        for r in _seq(rest, maxlen - len(h), grammar):
             res.add(h + r)
     return frozenset(res)
 
 
 @functools.lru_cache(maxsize=None)
-def _minlen(sym):
+def _minlen(sym, grammar):
     if isinstance(sym, int):
         return 1
     best = None
-    for rhs in GRAMMAR[sym]:
+    for rhs in GRAMMARS[grammar][sym]:
         if sym in rhs:  # skip directly recursive alternatives
             continue
-        v = sum(_minlen(s) for s in rhs)
+        v = sum(_minlen(s, grammar) for s in rhs)
         best = v if best is None else min(best, v)
     return best
 
 
-def enumerate_valid(maxlen):
-    return sorted(_gen(START, maxlen), key=lambda s: (len(s), s))
+def enumerate_valid(maxlen, grammar="strict"):
+    return sorted(_gen(START, maxlen, grammar), key=lambda s: (len(s), s))
 
 
 def parse_names(text):
