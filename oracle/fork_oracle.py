@@ -14,7 +14,10 @@ fork
     A main row must end with </Outlines>.  Its outline is the region from the
     last <Outlines> before that end, which must directly follow a <Parallel>,
     and must hold one or more entries <Subtask> text+ </Subtask> or
-    <Trial> text+ </Trial> back to back.  Worker k of the row gets the context
+    <Trial> text+ </Trial> back to back.  With ``lenient`` (the lenient-gaps
+    reading of the grammar) Text may stand between <Parallel> and <Outlines>,
+    after <Outlines>, between entries and before </Outlines>; the seed is still
+    the entry's own text.  Worker k of the row gets the context
         row ++ [<Thread>] ++ (text of entry k, if seeding)
     Workers are numbered row by row, entry by entry; worker_off[i] is the
     first worker of row i.  A row whose outline breaks these rules gets no
@@ -52,7 +55,7 @@ def _classes(row, tag_ids):
     return [cls.get(int(t), 0) for t in row]
 
 
-def parse_outline(row, tag_ids):
+def parse_outline(row, tag_ids, lenient=False):
     """(status, entries) of a main row; entries = [(kind, text_start, text_end)]
     with kind SUB or TRI and the entry's text at row[text_start:text_end]."""
     c = _classes(row, tag_ids)
@@ -62,11 +65,18 @@ def parse_outline(row, tag_ids):
     o = L - 2
     while o >= 0 and c[o] != OUT:
         o -= 1
-    if o < 1 or c[o - 1] != PAR:
+    q = o - 1  # the token that must be <Parallel>
+    while lenient and q >= 0 and c[q] == 0:
+        q -= 1
+    if o < 0 or q < 0 or c[q] != PAR:
         return ST_NO_OUTLINE, []
     entries = []
     p = o + 1
     while p < L - 1:
+        while lenient and p < L - 1 and c[p] == 0:  # a gap
+            p += 1
+        if p == L - 1:
+            break
         if c[p] not in (SUB, TRI):
             return ST_BAD_ENTRY, []
         q = p + 1
@@ -81,7 +91,7 @@ def parse_outline(row, tag_ids):
     return 0, entries
 
 
-def fork(rows, tag_ids, flags=FORK_SEED_ENTRY):
+def fork(rows, tag_ids, flags=FORK_SEED_ENTRY, lenient=False):
     """rows: list of int sequences.  Returns dict with per-row status and
     worker_off (n + 1), and per-worker context (list of lists), row, entry index,
     kind."""
@@ -90,7 +100,7 @@ def fork(rows, tag_ids, flags=FORK_SEED_ENTRY):
     ctx, w_row, w_entry, w_kind = [], [], [], []
     for i, row in enumerate(rows):
         row = [int(t) for t in row]
-        st, entries = parse_outline(row, tag_ids)
+        st, entries = parse_outline(row, tag_ids, lenient)
         status.append(st)
         for k, (kind, a, b) in enumerate(entries):
             seed = row[a:b] if flags & FORK_SEED_ENTRY else []

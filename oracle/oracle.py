@@ -160,6 +160,20 @@ def group_reward(rows: np.ndarray, correct, group_size: int, alpha: float, beta_
     return reward, r_sub, r_tri, eta
 
 
+def row_acceleration(rows: np.ndarray):
+    """Per-row acceleration ratio and saved tokens (float64, int64).
+
+    Acceleration = total tokens / longest-path tokens (Table 4 caption;
+    Table 5 divides generated by latency tokens), 1 for an empty row; saved
+    tokens = generated - latency (Table 5)."""
+    total = rows["total"].astype(np.int64)
+    lat = rows["latency"].astype(np.int64)
+    accel = np.ones(len(rows), np.float64)
+    nz = total > 0
+    accel[nz] = total[nz].astype(np.float64) / lat[nz].astype(np.float64)
+    return accel, total - lat
+
+
 def batch_metrics(rows: np.ndarray, correct, reward) -> dict:
     """Batch metrics of Tables 2, 4 and 5 (see oracle_batch_metrics)."""
     rows = np.ascontiguousarray(rows, dtype=ROW_DTYPE)

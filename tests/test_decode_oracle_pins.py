@@ -11,6 +11,7 @@ import random
 import pytest
 
 from oracle import decode_oracle as D
+from oracle import oracle as O
 from tests import grammar_pins as GP
 
 TAGS = list(range(100, 112))
@@ -109,3 +110,67 @@ def test_matches_brute_force_over_short_streams():
 def test_eos_never_before_end_think():
     assert D.allowed_classes([], TAGS, TEXT_ID)[1] is False
     assert D.allowed_classes(_toks(GP.parse_names("think t")), TAGS, TEXT_ID)[1] is False
+
+
+# --------------------------------------------------------------------------- lenient gaps
+
+LENIENT = O.CFG_LENIENT_GAPS
+
+# with the lenient-gaps reading Text joins the allowed set between a region's
+# structural tags, and leaves every other state as it was
+WORKED_LENIENT = [
+    ("", {GP.THINK}, False),
+    ("think", {GP.TEXT, GP.PAR, GP.END_THINK}, False),
+    ("think Par", {GP.TEXT, GP.OUT}, False),
+    ("think Par t2", {GP.TEXT, GP.OUT}, False),
+    ("think Par t Out", {GP.TEXT, GP.SUB, GP.TRI}, False),
+    ("think Par Out Sub", {GP.TEXT}, False),
+    ("think Par Out Tri t", {GP.TEXT, GP.END_TRI}, False),
+    ("think Par Out Tri t /Tri", {GP.TEXT, GP.SUB, GP.TRI, GP.END_OUT}, False),
+    ("think Par Out Tri t /Tri t", {GP.TEXT, GP.SUB, GP.TRI, GP.END_OUT}, False),
+    ("think Par Out Sub t /Sub /Out", {GP.TEXT, GP.THR}, False),
+    ("think Par Out Sub t /Sub /Out t", {GP.TEXT, GP.THR}, False),
+    ("think Par Out Sub t /Sub /Out Thr", {GP.TEXT, GP.PAR, GP.END_THR}, False),
+    ("think Par Out Sub t /Sub /Out Thr /Thr", {GP.TEXT, GP.THR, GP.END_PAR}, False),
+    ("think Par Out Sub t /Sub /Out Thr /Thr t3", {GP.TEXT, GP.THR, GP.END_PAR}, False),
+    ("think Par Out Sub t /Sub /Out Thr /Thr /Par", {GP.TEXT, GP.PAR, GP.END_THINK}, False),
+    ("think /think", {GP.TEXT}, True),
+    ("t", set(), False),
+    ("think Par Out t /Out", set(), False),
+]
+
+
+@pytest.mark.parametrize("prefix,allowed,eos", WORKED_LENIENT)
+def test_worked_states_lenient(prefix, allowed, eos):
+    got, got_eos = D.allowed_classes(_toks(GP.parse_names(prefix)), TAGS, TEXT_ID, LENIENT)
+    assert got == allowed
+    assert got_eos == eos
+
+
+def _earley_allowed_lenient(classes):
+    allowed = set()
+    for c in range(13):
+        ok, pos = GP.earley(classes + [c], "lenient")
+        if ok or pos == len(classes) + 1:
+            allowed.add(c)
+    return allowed, GP.earley(classes, "lenient")[0]
+
+
+def test_lenient_matches_earley_on_random_walks():
+    rng = random.Random(12)
+    prefixes = []
+    for _ in range(60):
+        cls = []
+        for _ in range(rng.randrange(0, 40)):
+            allowed, _ = _earley_allowed_lenient(cls)
+            if not allowed:
+                break
+            tags = sorted(allowed - {GP.TEXT})
+            cls.append(rng.choice(tags) if tags and rng.random() < 0.6 else rng.choice(sorted(allowed)))
+        prefixes.append(cls)
+        bad = sorted(set(range(13)) - _earley_allowed_lenient(cls)[0])
+        if bad:
+            prefixes.append(cls + [rng.choice(bad)])
+    got = D.allowed_batch([_toks(p) for p in prefixes], TAGS, TEXT_ID, LENIENT)
+    for p, g in zip(prefixes, got):
+        assert g == _earley_allowed_lenient(p), [GP.NAMES[c] for c in p]

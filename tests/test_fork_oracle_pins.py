@@ -216,3 +216,95 @@ def test_join_flags_bad_threads():
         assert out[0] == main + good[len(main):] + bad[len(main):] + [TAGS[GP.END_PAR - 1]]
     out, st = F.join([main], [0, 2], [good, good], TAGS, flags=0)
     assert st == [0] and out[0] == main + [thr, 7, ethr] * 2
+
+
+# --------------------------------------------------------------------------- lenient gaps
+# With the lenient-gaps reading, Text may stand between <Parallel> and
+# <Outlines>, after <Outlines>, between entries and before </Outlines> (and
+# after </Outlines> and every thread, which the fork never sees).
+
+
+def test_outline_check_matches_earley_lenient():
+    rng = random.Random(11)
+    n_ok = n_gap = 0
+    for region in _regions():
+        pre = [GP.TEXT] * rng.choice([0, 0, 1, 2])
+        row = [GP.THINK, GP.PAR] + pre + [GP.OUT] + region + [GP.END_OUT]
+        st, entries = F.parse_outline(toks(row), TAGS, lenient=True)
+        o = max(p for p, c in enumerate(row[:-1]) if c == GP.OUT)
+        q = o - 1
+        while q >= 0 and row[q] == GP.TEXT:
+            q -= 1
+        local = [GP.THINK] + row[q:]
+        ok, pos = GP.earley(local, "lenient")
+        viable = ok or pos == len(local)
+        assert (st == 0) == (viable and row[q] == GP.PAR), [GP.NAMES[c] for c in row]
+        if st == 0:
+            assert len(entries) == sum(1 for c in row[o:] if c in (GP.SUB, GP.TRI))
+            for kind, a, b in entries:  # the seed is exactly the entry's text
+                assert row[a - 1] == kind and row[b] == kind + 1 and set(row[a:b]) == {GP.TEXT}
+            n_ok += 1
+            n_gap += not GP.earley(local)[0] and GP.earley(local)[1] != len(local)
+    assert n_ok > 10 and n_gap > 10
+
+
+def _round_trip_lenient(classes, text_ids):
+    tok = [TAGS[c - 1] if c else text_ids[p] for p, c in enumerate(classes)]
+    n_checked = 0
+    for outl, threads, endp, n_entries in blocks_of(classes):
+        if len(threads) != n_entries:
+            continue
+        main = tok[:outl + 1]
+        res = F.fork([main], TAGS, flags=F.FORK_SEED_ENTRY, lenient=True)
+        assert res["status"] == [0] and res["worker_off"] == [0, n_entries]
+        # seeds: the text between each entry's own tags, found by scanning the outline
+        o = max(p for p in range(outl) if classes[p] == GP.OUT)
+        seeds, p = [], o + 1
+        while p < outl:
+            if classes[p] in (GP.SUB, GP.TRI):
+                q = p + 1
+                while classes[q] == GP.TEXT:
+                    q += 1
+                seeds.append(tok[p + 1:q])
+                p = q
+            p += 1
+        thr = TAGS[GP.THR - 1]
+        assert res["ctx"] == [main + [thr] + sd for sd in seeds]
+        seqs = [main + tok[a:b + 1] for a, b in threads]
+        joined, st = F.join([main], res["worker_off"], seqs, TAGS)
+        assert st == [0]
+        # the join rebuilds the block without its gaps after </Outlines> and after threads
+        inside = set()
+        for a, b in threads:
+            inside.update(range(a, b + 1))
+        expect = main + [tok[x] for x in range(outl + 1, endp) if x in inside] + [tok[endp]]
+        assert joined[0] == expect
+        n_checked += 1
+    return n_checked
+
+
+def test_round_trip_lenient_streams():
+    rng = random.Random(21)
+    strings = [list(s) for s in GP.enumerate_valid(16, "lenient")]
+    n = 0
+    for s in rng.sample(strings, 3000):
+        n += _round_trip_lenient(s, [rng.randrange(0, 99) for _ in s])
+    assert n > 500
+
+
+@pytest.mark.parametrize("names,strict,lenient", [
+    ("think Par t Out Sub t /Sub /Out", F.ST_NO_OUTLINE, 0),
+    ("think Par Out t Sub t /Sub /Out", F.ST_BAD_ENTRY, 0),
+    ("think Par Out Sub t /Sub t t Tri t /Tri t /Out", F.ST_BAD_ENTRY, 0),
+    ("think Par t t Out t Sub t t /Sub t /Out", F.ST_NO_OUTLINE, 0),
+    ("think Par Out t /Out", F.ST_BAD_ENTRY, F.ST_BAD_ENTRY),
+    ("think t Out Sub t /Sub /Out", F.ST_NO_OUTLINE, F.ST_NO_OUTLINE),
+    ("think Thr t Out Sub t /Sub /Out", F.ST_NO_OUTLINE, F.ST_NO_OUTLINE),
+    ("t t Out Sub t /Sub /Out", F.ST_NO_OUTLINE, F.ST_NO_OUTLINE),
+    ("think Par Out Sub /Sub t /Out", F.ST_BAD_ENTRY, F.ST_BAD_ENTRY),
+    ("think Par Out Sub t /Sub t Thr /Out", F.ST_BAD_ENTRY, F.ST_BAD_ENTRY),
+])
+def test_rows_strict_and_lenient(names, strict, lenient):
+    row = toks(GP.parse_names(names))
+    assert F.fork([row], TAGS)["status"] == [strict]
+    assert F.fork([row], TAGS, lenient=True)["status"] == [lenient]

@@ -239,6 +239,23 @@ def test_table5_identities():
         assert r["total"] - r["latency"] == row["saved"]
         _, _, _, eta = O.group_reward(rows, [1], 1, 0, 0, 0, 1.0, 1.0)
         assert abs(1.0 / (1.0 - eta[0]) - row["acceleration"]) < 0.005
+        accel, saved_o = O.row_acceleration(rows)
+        assert round(accel[0], 2) == row["acceleration"] and saved_o[0] == row["saved"]
+
+
+def test_row_acceleration_definitions():
+    rng = np.random.default_rng(3)
+    rows = np.zeros(200, dtype=O.ROW_DTYPE)
+    rows["total"] = rng.integers(0, 60000, 200)
+    rows["latency"] = np.minimum(rows["total"], rng.integers(1, 60000, 200))
+    rows["total"][:3] = 0
+    rows["latency"][:3] = 0
+    accel, saved = O.row_acceleration(rows)
+    assert np.all(accel[:3] == 1.0) and np.all(saved[:3] == 0)
+    _, _, _, eta = O.group_reward(rows, np.ones(200, np.uint8), 1, 0, 0, 0, 1.0, 1.0)
+    # acceleration = 1 / (1 - eta) and saved = eta * total (eta of Sec. 3.3)
+    assert np.allclose(accel, 1.0 / (1.0 - eta), rtol=1e-12)
+    assert np.allclose(saved, eta * rows["total"], rtol=0, atol=1e-6)
 
 
 # --------------------------------------------------------------------------- invariants on random trees
