@@ -27,6 +27,8 @@
  *     threads are untyped and the row gets PARASON_FLAG_COUNT_MISMATCH;
  *   - free Text may follow </think> and counts sequentially; nothing may
  *     precede <think>;
+ *   - strict by default: no Text between the structural tags of a parallel
+ *     region, as the grammar is printed (PARASON_CFG_LENIENT_GAPS relaxes it);
  *   - an invalid or truncated stream is sequential (latency = total, no branch
  *     tokens, no blocks, depth 0); first_error_pos is the length of its longest
  *     prefix that is a prefix of some valid stream;
@@ -66,8 +68,9 @@ extern "C" {
 #define PARASON_FLAG_TRUNCATED (1u << 1)      /* invalid only because it ends early */
 #define PARASON_FLAG_COUNT_MISMATCH (1u << 2) /* valid; some block has #threads != #entries */
 #define PARASON_FLAG_TRIGGERED (1u << 3)      /* valid and holds >= 1 <Parallel> block (Table 4) */
-/* The row was not evaluated; its integer outputs are 0, its reward (and the
- * rewards of its whole group) are NaN: */
+/* The row was not evaluated; its counts are 0 (total is its length, 0 for a
+ * bad row, and saved is 0), its float outputs (and those of its whole group)
+ * are NaN: */
 #define PARASON_FLAG_DEPTH_LIMIT (1u << 8)    /* nesting or entry count beyond the slow path's store */
 #define PARASON_FLAG_WS_OVERFLOW (1u << 9)    /* the rows need more workspace than was passed */
 #define PARASON_FLAG_BAD_ROW (1u << 10)       /* negative start or length */
@@ -85,6 +88,15 @@ extern "C" {
  * are otherwise looked up in a 64-slot table).  Same results, slower; there
  * for tag sets no hash of the scan separates, and for testing that path. */
 #define PARASON_CFG_TAG_COMPARE (1u << 2)
+/* Runs of Text may stand between the structural tags of a parallel region:
+ * after <Parallel>, <Outlines>, each outline entry, </Outlines> and each
+ * </Thread> of the region (the line breaks of Figure 3, which the grammar of
+ * Figure 4 as printed does not allow).  Their tokens are decoded by the
+ * enclosing path, like the outline: they add to the region's latency and count
+ * toward the enclosing branch type.  Without the flag such Text is an error at
+ * its first token.  Honoured by parason_run, parason_decode_step (Text becomes
+ * allowed in those positions) and parason_fork (the outline check). */
+#define PARASON_CFG_LENIENT_GAPS (1u << 3)
 
 /* ---- batch metrics (parason_outputs.metrics, doubles) ------------------- */
 /* As the paper reports them: trigger ratio = share of rows with >= 1
@@ -135,7 +147,7 @@ typedef struct parason_config {
 } parason_config;
 
 /* Caller-owned device arrays of n_traj elements each.  All are required except
- * r_subtask, r_trial, eta and metrics, which may be NULL. */
+ * r_subtask, r_trial, eta, metrics, accel and saved, which may be NULL. */
 typedef struct parason_outputs {
     int32_t *total;           /* L_total = length of the row */
     int32_t *latency;         /* T_i = L_latency (longest generation path) */
@@ -151,6 +163,9 @@ typedef struct parason_outputs {
     float *eta;               /* optional: eta(s) = 1 - latency / total */
     double *metrics;          /* optional: PARASON_METRIC_COUNT batch metrics (mean reward
                                  over the stored float rewards) */
+    float *accel;             /* optional: total / latency, the acceleration ratio of
+                                 Tables 4 and 5 (1 if total == 0) */
+    int32_t *saved;           /* optional: total - latency, the saved tokens of Table 5 */
 } parason_outputs;
 
 typedef struct parason_handle parason_handle;

@@ -69,6 +69,7 @@ int parason_decode_step(const parason_handle *h, parason_decode_state *states, c
     da.ninf = ninf;
     da.eos_id = eos_id;
     da.tm = h->tm;
+    da.lenient = (h->cfg.flags & PARASON_CFG_LENIENT_GAPS) != 0;
     const int64_t max_blocks = (int64_t)cus * DECODE_BLOCKS_PER_CU;
     const unsigned blocks = (unsigned)(batch < max_blocks ? batch : max_blocks);
     pk::decode_step<<<dim3(blocks), dim3(pk::DECODE_THREADS), 0, stream>>>(da);

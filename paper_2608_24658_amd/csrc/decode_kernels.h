@@ -17,6 +17,10 @@
  *   W_DONE   <Thread>, </Parallel>
  *   TRAIL    Text, end of sequence
  *
+ * With PARASON_CFG_LENIENT_GAPS Text is also allowed in P_OPEN, O_OPEN,
+ * E_DONE, O_DONE and W_DONE (a gap between the structural tags of a region)
+ * and leaves the state unchanged.
+ *
  * When Text is allowed only the (at most 13) tag and end-of-sequence logits
  * can change: a handful of scattered stores.  Otherwise the whole row becomes
  * -inf except the allowed tags: a full-row HBM write, 16 bytes per store.
@@ -42,27 +46,28 @@ constexpr uint32_t A_ALL = 0xFFFFFFFFu;
 
 __device__ __forceinline__ uint32_t bit(uint32_t c) { return 1u << c; }
 
-__device__ __forceinline__ uint32_t allowed_set(const DecodeState &s)
+__device__ __forceinline__ uint32_t allowed_set(const DecodeState &s, bool lenient)
 {
     if (s.flags & (PARASON_DECODE_ERROR | PARASON_DECODE_DONE)) return A_ALL;
+    const uint32_t gap = lenient ? bit(C_TEXT) : 0u;
     switch (s.state) {
     case D_START: return bit(C_THINK);
     case D_BODY: return bit(C_TEXT) | bit(C_PAR) | (s.depth == 0 ? bit(C_END_THINK) : bit(C_END_THR));
-    case D_P_OPEN: return bit(C_OUT);
-    case D_O_OPEN: return bit(C_SUB) | bit(C_TRI);
+    case D_P_OPEN: return gap | bit(C_OUT);
+    case D_O_OPEN: return gap | bit(C_SUB) | bit(C_TRI);
     case D_ENTRY: return bit(C_TEXT) | ((s.entry & 0x100) ? bit((uint32_t)(s.entry & 0xFF) + 1u) : 0u);
-    case D_E_DONE: return bit(C_SUB) | bit(C_TRI) | bit(C_END_OUT);
-    case D_O_DONE: return bit(C_THR);
-    case D_W_DONE: return bit(C_THR) | bit(C_END_PAR);
+    case D_E_DONE: return gap | bit(C_SUB) | bit(C_TRI) | bit(C_END_OUT);
+    case D_O_DONE: return gap | bit(C_THR);
+    case D_W_DONE: return gap | bit(C_THR) | bit(C_END_PAR);
     default: return bit(C_TEXT) | A_EOS; /* D_TRAIL */
     }
 }
 
 /* Advance by one sampled token of class c (eos: it is the end-of-sequence id). */
-__device__ __forceinline__ void advance(DecodeState &s, uint32_t c, bool eos)
+__device__ __forceinline__ void advance(DecodeState &s, uint32_t c, bool eos, bool lenient)
 {
     if (s.flags & (PARASON_DECODE_ERROR | PARASON_DECODE_DONE)) return;
-    const uint32_t allow = allowed_set(s);
+    const uint32_t allow = allowed_set(s, lenient);
     const uint32_t want = eos ? A_EOS : bit(c);
     if (!(allow & want)) {
         s.flags |= PARASON_DECODE_ERROR;
@@ -70,6 +75,10 @@ __device__ __forceinline__ void advance(DecodeState &s, uint32_t c, bool eos)
     }
     if (eos) {
         s.flags |= PARASON_DECODE_DONE;
+        return;
+    }
+    if (c == C_TEXT) { /* allowed Text changes nothing but an entry's has-text bit */
+        if (s.state == D_ENTRY) s.entry |= 0x100;
         return;
     }
     switch (s.state) {
@@ -94,10 +103,7 @@ __device__ __forceinline__ void advance(DecodeState &s, uint32_t c, bool eos)
             s.entry = (int32_t)c;
         }
         break;
-    case D_ENTRY:
-        if (c == C_TEXT) s.entry |= 0x100;
-        else s.state = D_E_DONE;
-        break;
+    case D_ENTRY: s.state = D_E_DONE; break;
     case D_O_DONE: s.state = D_BODY; break;
     case D_W_DONE:
         if (c == C_THR) {
@@ -121,6 +127,7 @@ struct DecodeArgs {
     int32_t elem;          /* bytes per logit: 2 or 4 */
     uint32_t ninf;         /* bit pattern of -inf in the logit type (low elem bytes) */
     int32_t eos_id;        /* < 0: none */
+    bool lenient;          /* PARASON_CFG_LENIENT_GAPS */
     TagMatch tm;
 };
 
@@ -143,9 +150,9 @@ __global__ void __launch_bounds__(DECODE_THREADS) decode_step(DecodeArgs a)
         if (threadIdx.x == 0) {
             DecodeState s = a.states[r];
             const int32_t t = a.tokens ? a.tokens[r] : -1;
-            if (t >= 0) advance(s, classify(a.tm, t, a.tm.contiguous != 0), t == a.eos_id);
+            if (t >= 0) advance(s, classify(a.tm, t, a.tm.contiguous != 0), t == a.eos_id, a.lenient);
             a.states[r] = s;
-            allow_s = allowed_set(s);
+            allow_s = allowed_set(s, a.lenient);
         }
         __syncthreads();
         const uint32_t allow = allow_s;

@@ -91,6 +91,7 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
     fa.n = n_rows;
     fa.tm = h->tm;
     fa.seed = (flags & PARASON_FORK_SEED_ENTRY) != 0;
+    fa.lenient = (h->cfg.flags & PARASON_CFG_LENIENT_GAPS) != 0;
     fa.thread_id = h->cfg.tag_ids[pk::C_THR - 1];
     fa.status = out->row_status;
     fa.counts = (int64_t *)(ws + L.counts);

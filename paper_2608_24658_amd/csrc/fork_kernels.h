@@ -28,6 +28,13 @@
  *                        each worker's <Thread> ... </Thread> span, and
  *                        </Parallel>.
  *
+ * With PARASON_CFG_LENIENT_GAPS Text may stand between <Parallel> and
+ * <Outlines>, after <Outlines>, between entries and before </Outlines>: the
+ * walk then checks only the order of the tags, takes the entry text lengths
+ * from the tag positions (a wave prefix scan gives each worker's seed offset,
+ * in both modes), and fork_copy finds entry k's text by a ballot search of the
+ * outline.
+ *
  * All copies are dword-granular and coalesced (rows and contexts start at any
  * element offset); they are HBM-bound.  Tiling the output keeps every block's
  * work the same size however long the rows are.
@@ -163,6 +170,7 @@ struct ForkArgs {
     int64_t n;
     TagMatch tm;
     bool seed;              /* contexts end with the entry's text */
+    bool lenient;           /* PARASON_CFG_LENIENT_GAPS */
     int32_t thread_id;      /* token id of <Thread> */
     uint32_t *status;       /* [n] PARASON_PACK_* */
     int64_t *counts;        /* [n][2]: workers, context tokens */
@@ -184,6 +192,35 @@ __device__ __forceinline__ int64_t wave_max(int64_t v)
         v = o > v ? o : v;
     }
     return v;
+}
+
+/* Inclusive prefix sum over the wave's lanes (every lane must call it). */
+__device__ __forceinline__ int64_t wave_incl_scan(int64_t v, int lane)
+{
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) {
+        const int64_t o = __shfl_up(v, (unsigned)d, WAVE);
+        v += lane >= d ? o : 0;
+    }
+    return v;
+}
+
+/* Position of the last tag before position o of the row at g (-1 if none);
+ * called by a whole wave. */
+__device__ __forceinline__ int64_t last_tag_before(const ForkArgs &a, int64_t g, int64_t o, int lane, bool contig)
+{
+    for (int64_t e = o; e > 0; e -= CHUNK) {
+        const int64_t lo = e > CHUNK ? e - CHUNK : 0;
+        int64_t best = -1;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t p = lo + lane + WAVE * j;
+            if (p < e && classify(a.tm, a.tokens[g + p], contig) != C_TEXT) best = p > best ? p : best;
+        }
+        best = uniform64(wave_max(best));
+        if (best >= 0) return best;
+    }
+    return -1;
 }
 
 /* One wave per row (grid-stride).  WRITE = false: status and counts;
@@ -222,7 +259,10 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
                     }
                     o = uniform64(wave_max(best));
                 }
-                if (o < 1 || classify(a.tm, a.tokens[g + o - 1], contig) != C_PAR) st = PARASON_PACK_NO_OUTLINE;
+                /* the tag before <Outlines> must be <Parallel>: right before it,
+                 * or with only Text between when lenient */
+                const int64_t q = (a.lenient && o >= 1) ? last_tag_before(a, g, o, lane, contig) : o - 1;
+                if (o < 0 || q < 0 || classify(a.tm, a.tokens[g + q], contig) != C_PAR) st = PARASON_PACK_NO_OUTLINE;
             }
             if (st != 0) {
                 if (lane == 0) {
@@ -239,6 +279,7 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
         int64_t m = 0;                       /* tags before this chunk */
         int64_t prev_pos = o;                /* the tag before the current one */
         uint32_t prev_cls = C_OUT;
+        int64_t text = 0;                    /* entry text tokens so far (the same in every lane) */
         bool ok = true;
         const int64_t w0 = WRITE ? a.worker_off[i] : 0;
         const int64_t t0 = WRITE ? a.tok_off[i] : 0;
@@ -264,37 +305,46 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            for (uint32_t e = lane; e < base; e += WAVE) {
-                const uint32_t x = ev[e];
-                const int64_t P = lo + (x >> 4);
-                const uint32_t cl = x & 15u;
-                int64_t pp = prev_pos;
-                uint32_t pc = prev_cls;
-                if (e > 0) {
-                    const uint32_t y = ev[e - 1];
-                    pp = lo + (y >> 4);
-                    pc = y & 15u;
-                }
-                const int64_t J = m + e;
-                if ((J & 1) == 0) {
-                    /* an entry opens right after <Outlines> or the previous entry */
-                    ok = ok && (cl == C_SUB || cl == C_TRI) && P == pp + 1;
-                } else {
-                    /* and closes with its own tag after at least one text token */
-                    ok = ok && (pc == C_SUB || pc == C_TRI) && cl == pc + 1 && P >= pp + 2;
-                    if (WRITE) {
-                        const int64_t k = J >> 1;
-                        const int64_t w = w0 + k;
-                        const int64_t len = P - pp - 1;
-                        /* the entry texts before entry k fill positions o+1 .. pp-1 but for 2k tags */
-                        const int64_t seed_before = pp - (o + 1) - 2 * k;
-                        a.ctx_starts[w] = t0 + k * ((int64_t)L + 1) + (a.seed ? seed_before : 0);
-                        a.ctx_lengths[w] = (int32_t)((int64_t)L + 1 + (a.seed ? len : 0));
-                        a.ctx_row[w] = (int32_t)i;
-                        a.ctx_entry[w] = (int32_t)k;
-                        a.ctx_kind[w] = pc == C_SUB ? (int32_t)T_SUB : (int32_t)T_TRI;
+            for (uint32_t e0 = 0; e0 < base; e0 += WAVE) { /* the same trip count in every lane */
+                const uint32_t e = e0 + (uint32_t)lane;
+                const bool act = e < base;
+                int64_t len = 0; /* text tokens of the entry this lane closes */
+                int64_t J = 0;
+                uint32_t pc = 0;
+                if (act) {
+                    const uint32_t x = ev[e];
+                    const int64_t P = lo + (x >> 4);
+                    const uint32_t cl = x & 15u;
+                    int64_t pp = prev_pos;
+                    pc = prev_cls;
+                    if (e > 0) {
+                        const uint32_t y = ev[e - 1];
+                        pp = lo + (y >> 4);
+                        pc = y & 15u;
+                    }
+                    J = m + e;
+                    if ((J & 1) == 0) {
+                        /* an entry opens after <Outlines> or the previous entry:
+                         * right after it, or after a gap when lenient */
+                        ok = ok && (cl == C_SUB || cl == C_TRI) && (a.lenient || P == pp + 1);
+                    } else {
+                        /* and closes with its own tag after at least one text token */
+                        ok = ok && (pc == C_SUB || pc == C_TRI) && cl == pc + 1 && P >= pp + 2;
+                        len = P - pp - 1;
                     }
                 }
+                const int64_t incl = wave_incl_scan(len, lane);
+                if (WRITE && act && (J & 1)) {
+                    const int64_t k = J >> 1;
+                    const int64_t w = w0 + k;
+                    const int64_t seed_before = text + incl - len; /* texts of entries 0 .. k-1 */
+                    a.ctx_starts[w] = t0 + k * ((int64_t)L + 1) + (a.seed ? seed_before : 0);
+                    a.ctx_lengths[w] = (int32_t)((int64_t)L + 1 + (a.seed ? len : 0));
+                    a.ctx_row[w] = (int32_t)i;
+                    a.ctx_entry[w] = (int32_t)k;
+                    a.ctx_kind[w] = pc == C_SUB ? (int32_t)T_SUB : (int32_t)T_TRI;
+                }
+                text += __shfl(incl, WAVE - 1, WAVE);
             }
             if (base > 0) {
                 const uint32_t y = ev[base - 1];
@@ -306,10 +356,10 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
         }
         if (!WRITE) {
             ok = __ballot(!ok) == 0;
-            /* an even, non-zero number of tags, the last one right before </Outlines> */
-            ok = ok && m >= 2 && (m & 1) == 0 && prev_pos == end - 1;
+            /* an even, non-zero number of tags, the last one right before
+             * </Outlines> (or followed by a gap when lenient) */
+            ok = ok && m >= 2 && (m & 1) == 0 && (a.lenient || prev_pos == end - 1);
             const int64_t n_e = ok ? m / 2 : 0;
-            const int64_t text = end - (o + 1) - m; /* entry text tokens of the whole outline */
             int64_t toks = n_e * ((int64_t)L + 1) + (a.seed ? text : 0);
             uint32_t st = ok ? 0u : (uint32_t)PARASON_PACK_BAD_ENTRY;
             if (ok && (int64_t)L + 1 + (a.seed ? text : 0) > (int64_t)INT32_MAX) {
@@ -377,6 +427,39 @@ __device__ __forceinline__ void block_fill(int32_t *__restrict__ dst, int64_t d0
     }
 }
 
+/* Position of the first text token of entry k of the outline that starts at
+ * o in the row src of length L (its k-th <Subtask>/<Trial> tag, plus one), by
+ * wave 0 in 64-token ballot rounds; returned to every thread.  The row's
+ * outline passed the walk, so entry k exists. */
+__device__ __forceinline__ int64_t entry_text_pos(const ForkArgs &a, const int32_t *src, int64_t o, int64_t k,
+                                                  int64_t L, int64_t *lds)
+{
+    if (threadIdx.x < WAVE) {
+        const int lane = threadIdx.x;
+        const bool contig = a.tm.contiguous != 0;
+        int64_t seen = 0, pos = -1;
+        for (int64_t lo = o + 1; lo < L - 1 && pos < 0; lo += WAVE) {
+            const int64_t p = lo + lane;
+            const uint32_t c = p < L - 1 ? classify(a.tm, src[p], contig) : C_TEXT;
+            const bool open = c == C_SUB || c == C_TRI;
+            const uint64_t b = __ballot(open);
+            const int64_t cnt = __popcll(b);
+            if (seen + cnt > k) {
+                const uint32_t rank =
+                    __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+                const uint64_t hit = __ballot(open && (int64_t)rank == k - seen);
+                pos = lo + __builtin_ctzll(hit) + 1;
+            }
+            seen += cnt;
+        }
+        if (lane == 0) lds[0] = pos < 0 ? 0 : pos;
+    }
+    __syncthreads();
+    const int64_t f = lds[0];
+    __syncthreads();
+    return f;
+}
+
 /* Contexts, tiled over their tokens: each block step fills TILE consecutive
  * context tokens, starting from the worker that holds the first of them. */
 __global__ void __launch_bounds__(PACK_THREADS) fork_copy(ForkArgs a)
@@ -394,8 +477,11 @@ __global__ void __launch_bounds__(PACK_THREADS) fork_copy(ForkArgs a)
             const int64_t L = a.lengths[r];
             const int32_t *src = a.tokens + a.starts[r];
             const int64_t k = a.ctx_entry[w];
-            /* first text token of entry k (see fork_outline): o + 2 + 2k + texts before it */
-            const int64_t first = a.outl[r] + 2 + 2 * k + (cs - a.tok_off[r] - k * (L + 1));
+            /* first text token of entry k: without gaps, o + 2 + 2k + the texts
+             * before it (see fork_outline); with gaps, searched */
+            const int64_t first = (a.lenient && a.seed)
+                                      ? entry_text_pos(a, src, a.outl[r], k, L, &found)
+                                      : a.outl[r] + 2 + 2 * k + (cs - a.tok_off[r] - k * (L + 1));
             const int32_t thr = a.thread_id;
             const int64_t end = min(hi, cs + (int64_t)a.ctx_lengths[w]);
             block_fill(a.ctx_tokens, max(lo, cs), end, [=](int64_t d) {

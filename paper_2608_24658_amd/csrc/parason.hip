@@ -281,6 +281,7 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.events = events;
     ra.tm = h->tm;
     ra.out = row_out;
+    ra.lenient = (h->cfg.flags & PARASON_CFG_LENIENT_GAPS) != 0;
     const unsigned row_blocks = (unsigned)((n_traj + 63) / 64);
     pk::rows_fast<<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows);
     pk::rows_mid<<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows,
@@ -306,6 +307,8 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     rw.r_subtask = out->r_subtask;
     rw.r_trial = out->r_trial;
     rw.eta = out->eta;
+    rw.accel = out->accel;
+    rw.saved = out->saved;
     rw.batch = nullptr;
     rw.n = n_traj;
     if (h->cfg.flags & PARASON_CFG_BATCH_STATS) {

@@ -247,10 +247,12 @@ struct Automaton {
     int32_t err;       /* first error position, -1 while none */
     bool mismatch;
     bool overflow;     /* the store ran out: hand the row to the slow path */
+    bool lenient;      /* PARASON_CFG_LENIENT_GAPS: Text between a region's structural tags */
     Top top;
 
-    __device__ void init()
+    __device__ void init(bool lenient_gaps)
     {
+        lenient = lenient_gaps;
         prev = -1;
         state = S_START;
         acc = 0;
@@ -286,9 +288,20 @@ struct Automaton {
         case S_TRAIL:
             acc += n;
             break;
-        default:
+        case S_START:
             err = prev + 1;
             return false;
+        default:
+            /* between structural tags of an open region (after <Parallel>,
+             * <Outlines>, an entry, </Outlines> or a thread): a gap, decoded
+             * by the enclosing path like the outline */
+            if (!lenient) {
+                err = prev + 1;
+                return false;
+            }
+            top.block_main += n;
+            attribute(n);
+            break;
         }
         prev += n;
         return true;
@@ -467,6 +480,7 @@ struct RowArgs {
     const uint32_t *events;
     TagMatch tm;
     RowOut out;
+    bool lenient; /* PARASON_CFG_LENIENT_GAPS */
 };
 
 /* Feed row r's events to A.  Returns false when A stopped early.
@@ -574,7 +588,7 @@ __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__rest
     A.st.lds = lds;
     A.st.tid = threadIdx.x;
     A.st.nt = blockDim.x;
-    A.init();
+    A.init(a.lenient);
     if (drive_row(a, r, start + a.mis, len, mode[r] == 1, A)) A.finish(len);
     if (A.overflow) {
         int32_t slot = atomicAdd(&counters[0], 1);
@@ -601,7 +615,7 @@ __global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restr
         A.st.lds = lds;
         A.st.tid = threadIdx.x;
         A.st.nt = blockDim.x;
-        A.init();
+        A.init(a.lenient);
         if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
         if (A.overflow) {
             int32_t slot = atomicAdd(&counters[1], 1);
@@ -628,7 +642,7 @@ __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__rest
         A.st.frames = frames;
         A.st.bits = bits;
         A.st.esp = 0;
-        A.init();
+        A.init(a.lenient);
         if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
         if (A.overflow)
             write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_DEPTH_LIMIT);
@@ -891,6 +905,8 @@ struct RewardArgs {
     double alpha, beta_s, beta_r, rho, rho_clip;
     uint32_t cfg_flags;
     float *reward, *r_subtask, *r_trial, *eta;
+    float *accel;   /* optional: total / latency */
+    int32_t *saved; /* optional: total - latency */
 };
 
 constexpr uint32_t NOT_EVALUATED = PARASON_FLAG_DEPTH_LIMIT | PARASON_FLAG_WS_OVERFLOW | PARASON_FLAG_BAD_ROW;
@@ -953,6 +969,9 @@ __device__ __forceinline__ void write_reward(const RewardArgs &a, int64_t r, dou
     if (a.r_subtask) a.r_subtask[r] = (float)xs;
     if (a.r_trial) a.r_trial[r] = (float)xr;
     if (a.eta) a.eta[r] = (float)e;
+    /* a row with tokens has latency >= 1 (an invalid row's latency is its length) */
+    if (a.accel) a.accel[r] = tot > 0 ? (float)__ddiv_rn((double)tot, (double)a.latency[r]) : 1.0f;
+    if (a.saved) a.saved[r] = tot - a.latency[r];
 }
 
 __device__ __forceinline__ void write_nan(const RewardArgs &a, int64_t r)
@@ -962,6 +981,8 @@ __device__ __forceinline__ void write_nan(const RewardArgs &a, int64_t r)
     if (a.r_subtask) a.r_subtask[r] = nan;
     if (a.r_trial) a.r_trial[r] = nan;
     if (a.eta) a.eta[r] = nan;
+    if (a.accel) a.accel[r] = nan;
+    if (a.saved) a.saved[r] = (a.flags[r] & NOT_EVALUATED) ? 0 : a.total[r] - a.latency[r];
 }
 
 /* One thread per group of G rows. */

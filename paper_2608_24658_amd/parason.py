@@ -27,6 +27,7 @@ FLAG_BAD_ROW = 1 << 10
 CFG_INVALID_KEEPS_CORRECTNESS = 1 << 0
 CFG_BATCH_STATS = 1 << 1
 CFG_TAG_COMPARE = 1 << 2
+CFG_LENIENT_GAPS = 1 << 3
 
 METRICS = (
     "rows", "valid", "triggered", "correct", "truncated", "count_mismatch",
@@ -93,6 +94,8 @@ class Outputs(ctypes.Structure):
         ("r_trial", ctypes.c_void_p),
         ("eta", ctypes.c_void_p),
         ("metrics", ctypes.c_void_p),
+        ("accel", ctypes.c_void_p),
+        ("saved", ctypes.c_void_p),
     ]
 
 
@@ -124,8 +127,8 @@ class JoinOutputs(ctypes.Structure):
 
 
 INT_FIELDS = ("total", "latency", "n_subtask", "n_trial", "n_blocks", "max_depth", "first_error_pos")
-FLOAT_FIELDS = ("reward", "r_subtask", "r_trial", "eta")
-OPTIONAL_FIELDS = ("r_subtask", "r_trial", "eta", "metrics")
+FLOAT_FIELDS = ("reward", "r_subtask", "r_trial", "eta", "accel")
+OPTIONAL_FIELDS = ("r_subtask", "r_trial", "eta", "metrics", "accel", "saved")
 
 _lib = None
 
@@ -251,8 +254,9 @@ class Parason:
         out["flags"] = torch.empty(n_traj, dtype=torch.int32, device=device)  # uint32 bits
         out["reward"] = torch.empty(n_traj, dtype=torch.float32, device=device)
         if derived:
-            for k in ("r_subtask", "r_trial", "eta"):
+            for k in ("r_subtask", "r_trial", "eta", "accel"):
                 out[k] = torch.empty(n_traj, dtype=torch.float32, device=device)
+            out["saved"] = torch.empty(n_traj, dtype=torch.int32, device=device)
         if metrics:
             out["metrics"] = torch.empty(len(METRICS), dtype=torch.float64, device=device)
         return out

@@ -6,7 +6,9 @@ first error position, flags) must be bit-exact.  Both sides evaluate the reward
 in IEEE double in the same order; the GPU rounds it once to float, so
 |R_gpu - R_oracle| <= 2^-24 |R| for correctly rounded double arithmetic.  The
 test bound is 2^-23 * max(1, |R|) (one float ulp at |R| = 1); the same bound
-holds for R_subtask, R_trial and eta.
+holds for R_subtask, R_trial and eta, and 2^-23 |a| for the acceleration ratio
+(a correctly rounded double quotient rounded once to float); saved tokens are
+exact.
 """
 import sys
 
@@ -32,7 +34,7 @@ def to_dev(a, dtype, device):
 
 
 def oracle_expect(tokens, starts, lengths, correct, tag_ids, G=8, coef=DEFAULT_COEF, cfg_flags=0):
-    rows = O.eval_rows(tokens, starts, lengths, tag_ids)
+    rows = O.eval_rows(tokens, starts, lengths, tag_ids, cfg_flags)
     R, rs, rt, eta = O.group_reward(rows, correct, G, coef["alpha"], coef["beta_subtask"], coef["beta_trial"],
                                     coef["rho"], coef["rho_clip"], cfg_flags)
     return rows, R, rs, rt, eta
@@ -68,6 +70,15 @@ def compare(got, rows, R, rs, rt, eta, idx=None, what=""):
         if not np.all(err <= lim):
             i = int(np.argmax(err - lim))
             raise AssertionError("%s %s row %d: gpu %.9g oracle %.17g" % (what, name, i, v[i], ref[i]))
+    accel, saved = O.row_acceleration(rows)
+    if "saved" in got and not np.array_equal(sel(got["saved"]), saved):
+        bad = np.nonzero(sel(got["saved"]) != saved)[0]
+        raise AssertionError("%s saved differs at %d rows, first %d" % (what, bad.size, bad[0]))
+    if "accel" in got:
+        v = sel(got["accel"]).astype(np.float64)
+        if not np.all(np.abs(v - accel) <= TOL * accel):
+            i = int(np.argmax(np.abs(v - accel) - TOL * accel))
+            raise AssertionError("%s accel row %d: gpu %.9g oracle %.17g" % (what, i, v[i], accel[i]))
     n_exact = int(np.sum(sel(got["reward"]) == R.astype(np.float32)))
     return n_exact
 
@@ -78,3 +89,29 @@ def run_gpu(px, tokens_d, starts_d, lengths_d, correct_d, ws_total=None):
     out = px.run(tokens_d, starts_d, lengths_d, correct_d, total_tokens=ws_total)
     torch.cuda.synchronize()
     return fetch(out)
+
+
+# Tags after which the lenient-gaps reading allows a run of Text: <Parallel>,
+# <Outlines>, </Subtask>, </Trial>, </Outlines>, </Thread> (class order of the
+# tag_ids argument: 1-based index into it).
+GAP_OPENERS = (3, 5, 8, 10, 6, 12)
+
+
+def insert_gaps(row, tag_ids, rng, p=0.5, max_len=3, keep_last=False):
+    """Copy of a token row with a Text run of 1..max_len random non-tag ids
+    inserted after each gap-opening tag with probability p (never after the
+    last token when keep_last).  A valid strict stream becomes a valid lenient
+    stream with the same structure."""
+    row = np.asarray(row, dtype=np.int32)
+    openers = np.array([tag_ids[c - 1] for c in GAP_OPENERS], dtype=np.int32)
+    pos = np.nonzero(np.isin(row, openers))[0]
+    if keep_last:
+        pos = pos[pos != row.size - 1]
+    pos = pos[rng.random(pos.size) < p]
+    if pos.size == 0:
+        return row
+    lens = rng.integers(1, max_len + 1, size=pos.size)
+    where = np.repeat(pos + 1, lens)
+    vals = rng.integers(0, 150000, size=where.size).astype(np.int32)
+    vals = np.where(np.isin(vals, np.asarray(tag_ids, dtype=np.int32)), 7, vals)
+    return np.insert(row, where, vals)

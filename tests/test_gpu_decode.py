@@ -60,11 +60,13 @@ def expected_mask(allowed, eos_ok, tags, eos, V):
 
 
 def simulate(dev, *, B, steps, V, tags, eos, dtype, seed, pad=0, p_bad=0.0, p_skip=0.0, p_deep=0.0,
-             p_end=0.03, max_depth=1 << 30):
-    """Run `steps` decode steps on B sequences; returns counters for coverage checks."""
+             p_end=0.03, max_depth=1 << 30, cfg_flags=0):
+    """Run `steps` decode steps on B sequences; returns counters for coverage checks.
+    cfg_flags: the handle's configuration flags (PX.CFG_LENIENT_GAPS selects the
+    lenient language on both sides)."""
     rng = random.Random(seed)
     gen = torch.Generator().manual_seed(seed)
-    px = PX.Parason(tags)
+    px = PX.Parason(tags, flags=cfg_flags)
     tag_set = set(tags)
     text_pool = [t for t in range(min(V, 4096)) if t not in tag_set and t != eos]
     states = PX.decode_init(B, dev)
@@ -81,7 +83,7 @@ def simulate(dev, *, B, steps, V, tags, eos, dtype, seed, pad=0, p_bad=0.0, p_sk
         got = logits.cpu()
         st = PX.decode_fields(states).cpu().numpy()
         live = [i for i in range(B) if flags[i] == 0]
-        allowed = dict(zip(live, D.allowed_batch([prefixes[i] for i in live], tags, text_pool[0])))
+        allowed = dict(zip(live, D.allowed_batch([prefixes[i] for i in live], tags, text_pool[0], cfg_flags)))
         exp = full.clone()
         for i in range(B):
             if flags[i]:
@@ -90,6 +92,8 @@ def simulate(dev, *, B, steps, V, tags, eos, dtype, seed, pad=0, p_bad=0.0, p_sk
             m = torch.from_numpy(expected_mask(a, eos_ok, tags, eos, V))
             exp[i, :V][m] = float("-inf")
             seen["full_rows" if 0 not in a else "text_rows"] += 1
+            # Text allowed between a region's structural tags (lenient gaps)
+            seen["gap_rows"] = seen.get("gap_rows", 0) + (0 in a and 3 not in a and bool(a & {5, 7, 9, 11}))
         iv = INT_VIEW[dtype]
         if not torch.equal(got.view(iv), exp.view(iv)):
             bad = (got.view(iv) != exp.view(iv)).nonzero()
@@ -210,3 +214,22 @@ def test_decode_state_fields(dev):
     assert int(PX.decode_fields(st)[0, 3].item()) == 0
     px.decode_step(st, logits, torch.tensor([tags[1]], dtype=torch.int32, device=dev), -1)  # </think> after <Outlines>
     assert int(PX.decode_fields(st)[0, 3].item()) == PX.DECODE_ERROR
+
+
+def test_decode_lenient_gaps(dev):
+    """Text allowed between the structural tags of a region: the masks follow
+    the lenient language, the rows that used to be rewritten whole now keep
+    their Text logits."""
+    log("case decode lenient V=2048 bf16 B=64")
+    seen = simulate(dev, B=64, steps=200, V=2048, tags=scattered_tags(2048, 13), eos=9, dtype="bf16", seed=8,
+                    p_bad=0.01, p_deep=0.3, max_depth=8, cfg_flags=PX.CFG_LENIENT_GAPS)
+    assert seen["text_rows"] > 5000 and seen["errors"] > 0 and seen["gap_rows"] > 500
+    # only the start of a stream forbids Text in the lenient language
+    assert seen["full_rows"] == 64
+
+
+def test_decode_lenient_full_vocabulary(dev):
+    log("case decode lenient V=151936 f32 B=8 contiguous tags")
+    seen = simulate(dev, B=8, steps=60, V=S.VOCAB, tags=CONTIG, eos=151643, dtype="f32", seed=9, p_bad=0.02,
+                    cfg_flags=PX.CFG_LENIENT_GAPS)
+    assert seen["text_rows"] > 200

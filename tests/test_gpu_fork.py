@@ -11,7 +11,7 @@ oracle's joined rows exactly, with and without </Parallel> and append-only."""
 import numpy as np
 import pytest
 
-from gpu_util import log, to_dev
+from gpu_util import insert_gaps, log, to_dev
 from oracle import fork_oracle as F
 from paper_2608_24658_amd import parason as PX
 from paper_2608_24658_amd.synth import synth as S
@@ -84,8 +84,8 @@ def hand_rows(tags, text_ids):
     return rows
 
 
-def oracle_fork(rows, tags, seed):
-    res = F.fork(rows, tags, flags=F.FORK_SEED_ENTRY if seed else 0)
+def oracle_fork(rows, tags, seed, lenient=False):
+    res = F.fork(rows, tags, flags=F.FORK_SEED_ENTRY if seed else 0, lenient=lenient)
     lens = np.array([len(c) for c in res["ctx"]], dtype=np.int64)
     starts = np.zeros(len(lens), dtype=np.int64)
     if len(lens):
@@ -111,9 +111,9 @@ def layout(rows, rng, gaps=True, shuffle=True):
     return (buf if buf.size else np.zeros(1, np.int32)), starts, np.array([len(r) for r in rows], dtype=np.int32)
 
 
-def check_fork(dev, px, rows, tags, seed, rng, what):
+def check_fork(dev, px, rows, tags, seed, rng, what, lenient=False):
     tok, st, ln = layout(rows, rng)
-    res, exp_starts, exp_lens, exp_flat = oracle_fork(rows, tags, seed)
+    res, exp_starts, exp_lens, exp_flat = oracle_fork(rows, tags, seed, lenient)
     got = px.fork(to_dev(tok, torch.int32, dev), to_dev(st, torch.int64, dev), to_dev(ln, torch.int32, dev), seed=seed)
     torch.cuda.synchronize()
     g = {k: v.cpu().numpy() for k, v in got.items()}
@@ -293,3 +293,58 @@ def test_fork_join_typical_batch(dev):
         ws = [seqs[w].tolist() for w in range(off[i], off[i + 1])]
         e, est = F.join([rows[i].tolist()], [0, len(ws)], ws, CONTIG)
         assert est == [0] and np.array_equal(np.asarray(e[0], np.int32), exp[i]), i
+
+
+# --------------------------------------------------------------------------- lenient gaps
+
+
+def lenient_hand_rows(tags, text_ids):
+    def t(names):
+        out = []
+        for k, c in enumerate(GP.parse_names(names)):
+            out.append(tags[c - 1] if c else text_ids[k % len(text_ids)])
+        return out
+
+    rows = [t(x) for x in (
+        "think Par t Out t Sub t3 /Sub t2 Tri t /Tri t /Out",
+        "think Par t2 Out Sub t /Sub /Out",
+        "think Par Out t Sub t /Sub t Tri t2 /Tri /Out",
+        "think Par Out t /Out",
+        "think Par t t Out",
+        "think Thr t Out Sub t /Sub /Out",
+        "think Par Out Sub t /Sub t /Out Thr t /Thr t /Par Par t Out t Tri t2 /Tri t Tri t /Tri t3 /Out",
+        "think Par Out Sub /Sub t /Out",
+    )]
+    # a gap before <Outlines> that spans chunks, and gaps between many entries
+    rows.append(t("think t5 Par t600 Out Sub t2 /Sub /Out"))
+    rows.append(t("think Par t300 Out t300 " + "Sub t /Sub t3 Tri t2 /Tri " * 200 + "t500 /Out"))
+    for pad in (250, 253, 254, 255, 256):  # <Outlines> and the first entry near chunk edges
+        rows.append(t("think Par t%d Out t%d Sub t2 /Sub t /Out" % (pad, 256 - pad % 7)))
+    return rows
+
+
+@pytest.mark.parametrize("tags", [CONTIG, SCATTERED], ids=["contiguous", "scattered"])
+@pytest.mark.parametrize("seed", [True, False], ids=["seed", "noseed"])
+def test_fork_join_lenient_hand_rows(dev, tags, seed):
+    log("case fork lenient hand rows tags=%s seed=%s" % (tags[0], seed))
+    rng = np.random.default_rng(11)
+    px = PX.Parason(tags, flags=PX.CFG_LENIENT_GAPS)
+    rows = hand_rows(tags, [7, 8, 9, 1000, 150000]) + lenient_hand_rows(tags, [7, 8, 1001, 149999])
+    res, _ = check_fork(dev, px, rows, tags, seed, rng, "lenient hand", lenient=True)
+    strict = F.fork(rows, tags, flags=F.FORK_SEED_ENTRY if seed else 0)
+    assert sum(s == 0 for s in res["status"]) > sum(s == 0 for s in strict["status"]) + 8
+    seqs = worker_sequences(res, tags, rng, p_bad=0.1)
+    check_join(dev, px, rows, res, seqs, tags, rng, F.JOIN_CLOSE_PARALLEL, "lenient hand join")
+
+
+@pytest.mark.parametrize("workload,n", [("small", 256), ("ragged", 512)])
+def test_fork_join_lenient_synthetic(dev, workload, n):
+    log("case fork lenient synthetic %s n=%d" % (workload, n))
+    rng = np.random.default_rng(12)
+    px = PX.Parason(SCATTERED, flags=PX.CFG_LENIENT_GAPS)
+    rows = [insert_gaps(r, SCATTERED, rng, p=0.6, max_len=4, keep_last=True).tolist()
+            for r in synthetic_main_rows(workload, n, SCATTERED, seed=13)]
+    res, _ = check_fork(dev, px, rows, SCATTERED, True, rng, "lenient " + workload, lenient=True)
+    assert res["worker_off"][-1] > n // 2
+    seqs = worker_sequences(res, SCATTERED, rng, p_bad=0.05)
+    check_join(dev, px, rows, res, seqs, SCATTERED, rng, F.JOIN_CLOSE_PARALLEL, "lenient " + workload + " join")
