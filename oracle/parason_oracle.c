@@ -374,18 +374,23 @@ static void *batch_main(void *arg)
 /* Evaluate rows [0, n_rows); row i is tokens[starts[i] .. starts[i]+lengths[i]).
  * cfg_flags: CFG_LENIENT_GAPS or 0 (other bits are ignored here).
  * Runs single-threaded on one worker thread whose stack is large enough for
- * any nesting a row of up to 2^31 tokens can hold.  Returns 0 on success. */
+ * the deepest nesting any of the rows can reach.  Returns 0 on success. */
 int oracle_eval_rows(const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
                      int64_t n_rows, const int32_t tag_ids[12], uint32_t cfg_flags, oracle_row_t *out)
 {
     batch_t b = {tokens, starts, lengths, n_rows, tag_ids, cfg_flags, out};
-    int32_t max_len = 0;
-    for (int64_t i = 0; i < n_rows; ++i)
-        if (lengths[i] > max_len) max_len = lengths[i];
-    /* Each nesting level needs at least 6 tokens and at most a few hundred
-     * bytes of C stack across parse_B/parse_P/parse_H/parse_W. */
+    /* The parser recurses once per <Parallel> it has consumed and not yet
+     * closed, so a row's <Parallel> count bounds its depth; each level takes
+     * at most a few hundred bytes of C stack across parse_B/parse_P/parse_H/
+     * parse_W. */
+    int64_t max_par = 0;
+    for (int64_t i = 0; i < n_rows; ++i) {
+        int64_t np = 0;
+        for (int64_t j = 0; j < (int64_t)lengths[i]; ++j) np += tokens[starts[i] + j] == tag_ids[K_PAR - 1];
+        if (np > max_par) max_par = np;
+    }
     size_t stack = (size_t)64 << 20;
-    size_t need = ((size_t)max_len / 6 + 64) * 640;
+    size_t need = ((size_t)max_par + 64) * 640;
     if (need > stack) stack = need;
     pthread_attr_t attr;
     pthread_t th;
