@@ -72,3 +72,78 @@ def test_large_workload_sampled(request):
         n, total, rows_idx.size, n_exact))
     del tok_d, out
     torch.cuda.empty_cache()
+
+
+def max_row(tags, rng, extra=0):
+    """A row of INT32_MAX tokens: <think>, a block straddling position 2^30,
+    a block just before </think>, then 100 answer tokens; and its accounting
+    in closed form.  The buffer has `extra` more tokens after the row."""
+    L = 2**31 - 1
+    tok = np.full(L + extra, 7, np.int32)  # one text id; random text ids around the blocks and the ends
+    for lo in (0, 2**30 - 70000, L - 70000):
+        w = rng.integers(0, 150000, size=65536).astype(np.int32)
+        tok[lo: lo + w.size] = np.where(np.isin(w, tags), 7, w)
+
+    def place(off, names):
+        import grammar_pins as GP
+
+        for i, c in enumerate(GP.parse_names(names)):
+            if c:
+                tok[off + i] = tags[c - 1]
+        return len(GP.parse_names(names))
+
+    place(0, "think")
+    n_a = place(2**30 - 7, "Par Out Sub t3 /Sub Tri t1 /Tri /Out Thr t5000 /Thr Thr t10 /Thr /Par")
+    n_b = place(L - 141, "Par Out Tri t2 /Tri Tri t2 /Tri /Out Thr t7 /Thr Thr t9 /Thr /Par")
+    place(L - 101, "/think")
+    assert (n_a, n_b) == (5026, 32)
+    # block A: lat = 1 + 10 + max(5002, 12) + 1 = 5014 of 5026 tokens (saves 12);
+    # thread 0 pairs with the Subtask entry (5002 tokens), thread 1 with the Trial (12);
+    # block B: lat = 1 + 10 + max(9, 11) + 1 = 23 of 32 tokens (saves 9), 20 Trial tokens
+    expect = dict(total=L, latency=L - 21, n_subtask=5002, n_trial=32, n_blocks=2, max_depth=1,
+                  first_error_pos=-1, flags=PX.FLAG_VALID | PX.FLAG_TRIGGERED)
+    return tok, expect
+
+
+def test_rows_of_int32_max_tokens():
+    """Rows at the largest length the interface takes (INT32_MAX tokens):
+    one complete, overlapping prefixes of it (valid after </think>, truncated
+    before it), a copy that starts one token late (misaligned, invalid at 0),
+    and four small rows; closed forms and the oracle."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(17)
+    tags = S.CONTIGUOUS_TAGS
+    log("case int32-max rows: host row")
+    P = S.make_params("tiny")
+    tok_s, st_s, ln_s, co_s = S.host_batch(P, 4)
+    tokens, expect = max_row(tags, rng, extra=tok_s.size)
+    L = expect["total"]
+    tokens[L:] = tok_s
+    starts = np.array([0, 0, 1, 0] + list(st_s + L), np.int64)
+    lengths = np.array([L, L - 200, L - 1, L - 50] + list(ln_s), np.int32)
+    correct = np.array([1, 1, 1, 0] + list(co_s), np.uint8)
+    px = PX.Parason(tags, group_size=G, **DEFAULT_COEF)
+    log("case int32-max rows: run (%d tokens in the buffer)" % tokens.size)
+    tok_d = torch.from_numpy(tokens).to(dev)
+    out = px.run(tok_d, torch.from_numpy(starts).to(dev), torch.from_numpy(lengths).to(dev),
+                 torch.from_numpy(correct).to(dev))
+    torch.cuda.synchronize()
+    got = fetch(out)
+    del tok_d, out
+    torch.cuda.empty_cache()
+    for k, v in expect.items():
+        assert int(got[k][0]) == v, (k, int(got[k][0]), v)
+    assert int(got["first_error_pos"][1]) == L - 200 and got["flags"][1] == PX.FLAG_TRUNCATED
+    assert int(got["latency"][1]) == L - 200
+    assert int(got["first_error_pos"][2]) == 0 and got["flags"][2] == 0
+    assert int(got["latency"][3]) == L - 50 - 21 and got["flags"][3] == expect["flags"]
+    assert int(got["saved"][0]) == 21
+    log("case int32-max rows: oracle")
+    rows = O.eval_rows(tokens, starts, lengths, tags)
+    c = DEFAULT_COEF
+    R, rs, rt, eta = O.group_reward(rows, correct, G, c["alpha"], c["beta_subtask"], c["beta_trial"], c["rho"],
+                                    c["rho_clip"])
+    compare(got, rows, R, rs, rt, eta, what="int32-max rows")
+    log("int32-max rows match")
