@@ -115,6 +115,18 @@ void find_tag_hash(pk::TagMatch &tm)
     }
 }
 
+/* The three tiers of the row automaton, in the grammar's strict or lenient
+ * form. */
+template <bool LENIENT>
+void launch_rows(const pk::RowArgs &ra, unsigned row_blocks, int cus, const uint8_t *mode, int32_t *counters,
+                 int32_t *mid_rows, int32_t *deep_rows, int32_t *deep_frames, uint32_t *deep_bits, hipStream_t stream)
+{
+    pk::rows_fast<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows);
+    pk::rows_mid<LENIENT><<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(ra, mode, counters,
+                                                                                              mid_rows, deep_rows);
+    pk::rows_deep<LENIENT><<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);
+}
+
 }  // namespace
 
 void abi::launch_plan(const int64_t *starts, const int32_t *lengths, int64_t n, int64_t mis, int64_t n_tiles,
@@ -281,12 +293,11 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.events = events;
     ra.tm = h->tm;
     ra.out = row_out;
-    ra.lenient = (h->cfg.flags & PARASON_CFG_LENIENT_GAPS) != 0;
     const unsigned row_blocks = (unsigned)((n_traj + 63) / 64);
-    pk::rows_fast<<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows);
-    pk::rows_mid<<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows,
-                                                                                     deep_rows);
-    pk::rows_deep<<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);
+    if (h->cfg.flags & PARASON_CFG_LENIENT_GAPS)
+        launch_rows<true>(ra, row_blocks, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
+    else
+        launch_rows<false>(ra, row_blocks, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
 
     pk::RewardArgs rw;
     rw.total = out->total;

@@ -232,8 +232,10 @@ struct GlobalStore {
 enum : uint32_t { S_START, S_BODY, S_P_OPEN, S_O_OPEN, S_ENTRY, S_E_DONE, S_O_DONE, S_W_DONE, S_TRAIL };
 
 /* Pushdown automaton of the grammar, fed with tag events in position order.
- * Text runs are the gaps between consecutive event positions. */
-template <class Store>
+ * Text runs are the gaps between consecutive event positions.  LENIENT:
+ * PARASON_CFG_LENIENT_GAPS (a compile-time choice, so that the strict
+ * automaton carries no code for it). */
+template <class Store, bool LENIENT>
 struct Automaton {
     Store st;
     int32_t prev;      /* position of the last token consumed */
@@ -247,12 +249,10 @@ struct Automaton {
     int32_t err;       /* first error position, -1 while none */
     bool mismatch;
     bool overflow;     /* the store ran out: hand the row to the slow path */
-    bool lenient;      /* PARASON_CFG_LENIENT_GAPS: Text between a region's structural tags */
     Top top;
 
-    __device__ void init(bool lenient_gaps)
+    __device__ void init()
     {
-        lenient = lenient_gaps;
         prev = -1;
         state = S_START;
         acc = 0;
@@ -288,14 +288,11 @@ struct Automaton {
         case S_TRAIL:
             acc += n;
             break;
-        case S_START:
-            err = prev + 1;
-            return false;
         default:
             /* between structural tags of an open region (after <Parallel>,
-             * <Outlines>, an entry, </Outlines> or a thread): a gap, decoded
-             * by the enclosing path like the outline */
-            if (!lenient) {
+             * <Outlines>, an entry, </Outlines> or a thread): when lenient a
+             * gap, decoded by the enclosing path like the outline */
+            if (!LENIENT || state == S_START) {
                 err = prev + 1;
                 return false;
             }
@@ -455,8 +452,8 @@ __device__ __forceinline__ void write_row(const RowOut &o, int64_t r, int32_t to
     o.flags[r] = fl;
 }
 
-template <class Store>
-__device__ __forceinline__ void write_result(const RowOut &o, int64_t r, int32_t len, const Automaton<Store> &A)
+template <class Store, bool LENIENT>
+__device__ __forceinline__ void write_result(const RowOut &o, int64_t r, int32_t len, const Automaton<Store, LENIENT> &A)
 {
     if (A.err < 0) {
         uint32_t fl = PARASON_FLAG_VALID;
@@ -480,7 +477,6 @@ struct RowArgs {
     const uint32_t *events;
     TagMatch tm;
     RowOut out;
-    bool lenient; /* PARASON_CFG_LENIENT_GAPS */
 };
 
 /* Feed row r's events to A.  Returns false when A stopped early.
@@ -493,8 +489,9 @@ struct RowArgs {
  * automaton (one per source) the gfx950 build returned wrong results for dense
  * segments although the same source is correct when compiled for the CPU, so
  * the sources are merged into one fetch loop. */
-template <class Store>
-__device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, bool compact, Automaton<Store> &A)
+template <class Store, bool LENIENT>
+__device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, bool compact,
+                          Automaton<Store, LENIENT> &A)
 {
     const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
     const int64_t vrow0 = row_first_vec(g), vend = row_end_vec(g, len);
@@ -568,6 +565,7 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
  * frames (or more than 64 entries in an open block) is listed for rows_mid.
  * Few frames keep the LDS per block small, so that many waves hide the
  * latency of the branchy automaton. */
+template <bool LENIENT>
 __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__restrict__ mode,
                                                 int32_t *__restrict__ counters, int32_t *__restrict__ mid_rows)
 {
@@ -584,11 +582,11 @@ __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__rest
         write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
         return;
     }
-    Automaton<LdsStore<FAST_DEPTH>> A;
+    Automaton<LdsStore<FAST_DEPTH>, LENIENT> A;
     A.st.lds = lds;
     A.st.tid = threadIdx.x;
     A.st.nt = blockDim.x;
-    A.init(a.lenient);
+    A.init();
     if (drive_row(a, r, start + a.mis, len, mode[r] == 1, A)) A.finish(len);
     if (A.overflow) {
         int32_t slot = atomicAdd(&counters[0], 1);
@@ -601,6 +599,7 @@ __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__rest
 /* The rows rows_fast listed, one thread each (grid-stride over the list), with
  * MID_DEPTH frames per row in LDS; rows that need still more are listed for
  * rows_deep. */
+template <bool LENIENT>
 __global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restrict__ mode,
                                                int32_t *__restrict__ counters, const int32_t *__restrict__ mid_rows,
                                                int32_t *__restrict__ deep_rows)
@@ -611,11 +610,11 @@ __global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restr
          i += (int64_t)gridDim.x * blockDim.x) {
         const int64_t r = mid_rows[i];
         const int32_t len = a.lengths[r];
-        Automaton<LdsStore<MID_DEPTH>> A;
+        Automaton<LdsStore<MID_DEPTH>, LENIENT> A;
         A.st.lds = lds;
         A.st.tid = threadIdx.x;
         A.st.nt = blockDim.x;
-        A.init(a.lenient);
+        A.init();
         if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
         if (A.overflow) {
             int32_t slot = atomicAdd(&counters[1], 1);
@@ -628,6 +627,7 @@ __global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restr
 
 /* Rows whose nesting or entry count exceeded the LDS stores, one after the
  * other, on a single thread with frames in global workspace. */
+template <bool LENIENT>
 __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__restrict__ mode,
                                                 const int32_t *__restrict__ counters,
                                                 const int32_t *__restrict__ deep_rows, int32_t *__restrict__ frames,
@@ -638,11 +638,11 @@ __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__rest
     for (int32_t i = 0; i < n_deep; ++i) {
         const int64_t r = deep_rows[i];
         const int32_t len = a.lengths[r];
-        Automaton<GlobalStore> A;
+        Automaton<GlobalStore, LENIENT> A;
         A.st.frames = frames;
         A.st.bits = bits;
         A.st.esp = 0;
-        A.init(a.lenient);
+        A.init();
         if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
         if (A.overflow)
             write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_DEPTH_LIMIT);
