@@ -24,10 +24,13 @@ namespace {
 constexpr int SCAN_BLOCKS_PER_CU = PARASON_SCAN_BLOCKS_PER_CU; /* persistent grid of 4-wave blocks */
 constexpr int64_t MAX_SEGMENTS = (int64_t)1 << 40;
 constexpr int MID_BLOCKS_PER_CU = 2; /* rows_mid blocks hold 64 KB of LDS frames each */
+constexpr int GATHER_BLOCKS_PER_CU = 8; /* 4-wave blocks of gather_rows */
+constexpr int ROWS_WAVES_PER_CU = 20;   /* rows_fast waves a CU holds (8 KB of LDS frames each) */
 
 /* Byte offsets of the workspace sections for n rows. */
 struct Layout {
-    size_t seg_off, tile_sum, tile_off, counters, mode, mid_rows, deep_rows, deep_frames, deep_bits, seg_count, events;
+    size_t seg_off, tile_sum, tile_off, counters, mode, mid_rows, deep_rows, split_rows, deep_frames, deep_bits,
+        seg_count, events;
     size_t red_d, red_i, stats;
     size_t fixed;  /* bytes before the per-segment sections */
     int64_t n_tiles;
@@ -51,6 +54,8 @@ Layout layout_for(int64_t n)
     L.mid_rows = o;
     o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
     L.deep_rows = o;
+    o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    L.split_rows = o;
     o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
     L.deep_frames = o;
     o = align_up(o + (size_t)pk::DEEP_FRAMES * pk::FRAME_WORDS * sizeof(int32_t));
@@ -118,10 +123,16 @@ void find_tag_hash(pk::TagMatch &tm)
 /* The three tiers of the row automaton, in the grammar's strict or lenient
  * form. */
 template <bool LENIENT>
-void launch_rows(const pk::RowArgs &ra, unsigned row_blocks, int cus, const uint8_t *mode, int32_t *counters,
-                 int32_t *mid_rows, int32_t *deep_rows, int32_t *deep_frames, uint32_t *deep_bits, hipStream_t stream)
+void launch_rows(const pk::RowArgs &ra, int cus, const uint8_t *mode, int32_t *counters, int32_t *mid_rows,
+                 int32_t *deep_rows, int32_t *deep_frames, uint32_t *deep_bits, hipStream_t stream)
 {
-    pk::rows_fast<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows);
+    /* rows per wave of rows_fast: enough waves to fill ROWS_WAVES_PER_CU on
+     * every CU, 64 (one per lane) once the batch is large enough */
+    int64_t per_wave = 1;
+    while (per_wave < 64 && ra.n / (per_wave * 2) >= (int64_t)cus * ROWS_WAVES_PER_CU) per_wave *= 2;
+    const unsigned row_blocks = (unsigned)((ra.n + per_wave - 1) / per_wave);
+    pk::rows_fast<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows,
+                                                                      (int32_t)(64 / per_wave));
     pk::rows_mid<LENIENT><<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(ra, mode, counters,
                                                                                               mid_rows, deep_rows);
     pk::rows_deep<LENIENT><<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);
@@ -246,6 +257,7 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     uint8_t *mode = (uint8_t *)(ws + L.mode);
     int32_t *mid_rows = (int32_t *)(ws + L.mid_rows);
     int32_t *deep_rows = (int32_t *)(ws + L.deep_rows);
+    int32_t *split_rows = (int32_t *)(ws + L.split_rows);
     int32_t *deep_frames = (int32_t *)(ws + L.deep_frames);
     uint32_t *deep_bits = (uint32_t *)(ws + L.deep_bits);
     int32_t *seg_count = (int32_t *)(ws + L.seg_count);
@@ -271,6 +283,8 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     sa.events = events;
     sa.mode = mode;
     sa.tm = h->tm;
+    sa.split_count = counters + 2;
+    sa.split_rows = split_rows;
     const unsigned scan_blocks = (unsigned)(cus * SCAN_BLOCKS_PER_CU);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[0], stream) != hipSuccess) return PARASON_ERR_HIP;
     if (h->tm.contiguous)
@@ -280,6 +294,9 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     else
         pk::scan_rows<pk::TM_LINEAR><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[1], stream) != hipSuccess) return PARASON_ERR_HIP;
+
+    pk::GatherArgs ga{starts, n_traj, mis, seg_off, cap, seg_count, events, mode, counters + 2, split_rows};
+    pk::gather_rows<<<dim3((unsigned)(cus * GATHER_BLOCKS_PER_CU)), dim3(256), 0, stream>>>(ga);
 
     pk::RowArgs ra;
     ra.tok_base = tok_base;
@@ -293,11 +310,10 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.events = events;
     ra.tm = h->tm;
     ra.out = row_out;
-    const unsigned row_blocks = (unsigned)((n_traj + 63) / 64);
     if (h->cfg.flags & PARASON_CFG_LENIENT_GAPS)
-        launch_rows<true>(ra, row_blocks, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
+        launch_rows<true>(ra, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
     else
-        launch_rows<false>(ra, row_blocks, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
+        launch_rows<false>(ra, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
 
     pk::RewardArgs rw;
     rw.total = out->total;
@@ -331,8 +347,7 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
         rw.batch = stats;
         pk::batch_reward<<<dim3((unsigned)((n_traj + 255) / 256)), dim3(256), 0, stream>>>(rw);
     } else {
-        const unsigned reward_blocks = (unsigned)((rw.n_groups + 255) / 256);
-        pk::group_reward<<<dim3(reward_blocks), dim3(256), 0, stream>>>(rw);
+        pk::group_reward<<<dim3((unsigned)((n_traj + 255) / 256)), dim3(256), 0, stream>>>(rw);
     }
     if (out->metrics) {
         pk::MetricsArgs ma{out->total, out->latency, out->n_subtask, out->n_trial, out->flags, correct,

@@ -567,10 +567,16 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
  * latency of the branchy automaton. */
 template <bool LENIENT>
 __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__restrict__ mode,
-                                                int32_t *__restrict__ counters, int32_t *__restrict__ mid_rows)
+                                                int32_t *__restrict__ counters, int32_t *__restrict__ mid_rows,
+                                                int32_t lane_stride)
 {
     __shared__ int32_t lds[FAST_DEPTH * FRAME_WORDS * 64];
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    /* every lane_stride-th lane takes a row (64 / lane_stride rows per wave):
+     * few rows per wave when the batch is small, so that the waves spread
+     * over the GPU and a wave follows only its rows' paths through the
+     * automaton */
+    if (threadIdx.x % lane_stride != 0) return;
+    const int64_t r = (int64_t)blockIdx.x * (blockDim.x / lane_stride) + threadIdx.x / lane_stride;
     if (r >= a.n) return;
     const int64_t start = a.starts[r];
     const int32_t len = a.lengths[r];
@@ -756,6 +762,8 @@ struct ScanArgs {
     uint32_t *events;
     uint8_t *mode;
     TagMatch tm;
+    int32_t *split_count; /* rows of more than one segment that no scan wave owns ... */
+    int32_t *split_rows;  /* ... listed here for gather_rows */
 };
 
 /* Row being collected by a scan wave, in processing order. */
@@ -797,6 +805,10 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
     if (w.s == w.first) {
         rc.lcnt = 0;
         rc.global = !w.owned;
+        /* the wave holding the first segment of a split row lists it for
+         * gather_rows (rows of 2^27 tokens or more stay per segment) */
+        if (!w.owned && w.last > w.first && w.len < (1 << 27) && lane == 0)
+            a.split_rows[atomicAdd(a.split_count, 1)] = (int32_t)w.row;
     }
     uint32_t cnt = 0; /* wave-uniform */
     if (!rc.global) {
@@ -882,6 +894,105 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
         ++s;
         w = wn;
     }
+}
+
+/* ------------------------------------------------------------------ gather */
+
+struct GatherArgs {
+    const int64_t *starts;
+    int64_t n, mis;
+    const int64_t *seg_off;
+    int64_t seg_cap;
+    int32_t *seg_count;
+    uint32_t *events;
+    uint8_t *mode;
+    const int32_t *split_count;
+    const int32_t *split_rows;
+};
+
+/* Inclusive prefix sum over the wave's lanes (every lane must call it). */
+__device__ __forceinline__ int32_t wave_incl_scan32(int32_t v, int lane)
+{
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) {
+        const int32_t o = __shfl_up(v, (unsigned)d, WAVE);
+        v += lane >= d ? o : 0;
+    }
+    return v;
+}
+
+/* The largest lane j with x (held by lane j) <= f, for x non-decreasing over
+ * the lanes and x of lane 0 <= f (every lane must call it). */
+__device__ __forceinline__ int32_t last_lane_at_most(int32_t x, int32_t f)
+{
+    int32_t lo = 0;
+#pragma unroll
+    for (int step = WAVE / 2; step > 0; step >>= 1) {
+        const int32_t cand = lo + step;
+        lo = __shfl(x, cand, WAVE) <= f ? cand : lo;
+    }
+    return lo;
+}
+
+/* Move the events of row `row` (split between scan waves: one list per
+ * segment, segment positions) into one list at the start of its slot range,
+ * in position order, with row positions (the compact form, mode 1).  The move
+ * is in place: the k-th event of the row goes to slot k, which is never later
+ * than the slot it comes from (a segment holds at most EV_CAP events), and
+ * each wave-wide round loads all of its events before it stores any.  Rows
+ * with a segment of more than EV_CAP events (or marked DENSE) are left as
+ * they are; the whole wave calls this. */
+__device__ __forceinline__ void gather_row(const GatherArgs &a, int64_t row, int lane)
+{
+    const int64_t s0 = uniform64(a.seg_off[row]), s1 = uniform64(a.seg_off[row + 1]);
+    const int64_t g = uniform64(a.starts[row] + a.mis);
+    const int64_t vrow0 = row_first_vec(g);
+    bool dense = false;
+    for (int64_t c0 = s0; c0 < s1; c0 += WAVE) {
+        const int64_t s = c0 + lane;
+        dense = dense || (s < s1 && a.seg_count[s] > EV_CAP);
+    }
+    if (__ballot(dense) != 0) return;
+    uint32_t *list = a.events + s0 * EV_CAP;
+    int64_t carry = 0; /* events of the segments before this chunk */
+    for (int64_t c0 = s0; c0 < s1; c0 += WAVE) {
+        const int64_t s = c0 + lane;
+        const int32_t cnt = s < s1 ? a.seg_count[s] : 0;
+        const int32_t incl = wave_incl_scan32(cnt, lane);
+        const int32_t excl = incl - cnt;
+        const int32_t total = __shfl(incl, WAVE - 1, WAVE);
+        for (int32_t f0 = 0; f0 < total; f0 += WAVE) {
+            const int32_t f = f0 + lane; /* the chunk's f-th event, of segment c0 + j */
+            const int32_t j = last_lane_at_most(excl, f);
+            const int32_t first = __shfl(excl, j, WAVE);
+            if (f < total) {
+                const int64_t seg = c0 + j;
+                const uint32_t w = a.events[seg * EV_CAP + (f - first)];
+                /* row position of segment position 0 */
+                const int64_t base = 4 * (vrow0 + (seg - s0) * SEG_VEC) - g;
+                const uint32_t pos = (uint32_t)(base + (int64_t)(w >> 4));
+                list[carry + f] = (pos << 4) | (w & 15u);
+            }
+        }
+        carry += total;
+    }
+    if (lane == 0) {
+        a.seg_count[s0] = (int32_t)carry;
+        a.mode[row] = 1;
+    }
+}
+
+/* The rows the scan listed as split between its waves: when a batch holds
+ * few rows, as an RL step does, that is nearly every row.  One wave per
+ * listed row (grid-stride over the list). */
+__global__ void __launch_bounds__(256) gather_rows(GatherArgs a)
+{
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int64_t wave = uniform64(((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / WAVE);
+    const int64_t n_waves = (int64_t)gridDim.x * (blockDim.x / WAVE);
+    if (a.seg_off[a.n] > a.seg_cap) return; /* the scan wrote nothing: the row kernel reports it */
+    const int32_t n_split = __builtin_amdgcn_readfirstlane(*a.split_count);
+    for (int64_t i = wave; i < n_split; i += n_waves) gather_row(a, uniform64(a.split_rows[i]), lane);
 }
 
 /* ------------------------------------------------------------------ reward */
@@ -985,13 +1096,16 @@ __device__ __forceinline__ void write_nan(const RewardArgs &a, int64_t r)
     if (a.saved) a.saved[r] = (a.flags[r] & NOT_EVALUATED) ? 0 : a.total[r] - a.latency[r];
 }
 
-/* One thread per group of G rows. */
+/* One thread per row.  Every thread of a group computes the group's moments
+ * itself, in the same fixed order, so they all hold the same values; a group
+ * thus takes G threads instead of one, which keeps the GPU busy when a batch
+ * has few groups (an RL step has 128). */
 __global__ void __launch_bounds__(256) group_reward(RewardArgs a)
 {
-    const int64_t grp = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (grp >= a.n_groups) return;
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= a.n) return;
     const int32_t G = a.G;
-    const int64_t r0 = grp * G;
+    const int64_t r0 = r - r % G;
 
     bool evaluated = true;
     bool lat_equal = true;
@@ -1000,7 +1114,7 @@ __global__ void __launch_bounds__(256) group_reward(RewardArgs a)
         lat_equal = lat_equal && a.latency[r0 + i] == a.latency[r0];
     }
     if (!evaluated) {
-        for (int32_t i = 0; i < G; ++i) write_nan(a, r0 + i);
+        write_nan(a, r);
         return;
     }
     const bool sub_equal = same_ratio(a.n_subtask, a.total, r0, G);
@@ -1009,9 +1123,9 @@ __global__ void __launch_bounds__(256) group_reward(RewardArgs a)
     auto xs = [&](int32_t i) { return ratio(a.n_subtask[r0 + i], a.total[r0 + i]); };
     auto xr = [&](int32_t i) { return ratio(a.n_trial[r0 + i], a.total[r0 + i]); };
     const Moments mT = moments(xT, G), ms = moments(xs, G), mr = moments(xr, G);
-    for (int32_t i = 0; i < G; ++i)
-        write_reward(a, r0 + i, zscore(xT(i), mT, lat_equal), zscore(xs(i), ms, sub_equal),
-                     zscore(xr(i), mr, tri_equal), xs(i), xr(i));
+    const int32_t i = (int32_t)(r - r0);
+    write_reward(a, r, zscore(xT(i), mT, lat_equal), zscore(xs(i), ms, sub_equal), zscore(xr(i), mr, tri_equal),
+                 xs(i), xr(i));
 }
 
 /* One thread per row; mu, sigma of the whole batch from batch_stats. */
