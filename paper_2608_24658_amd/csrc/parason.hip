@@ -131,8 +131,11 @@ void launch_rows(const pk::RowArgs &ra, int cus, const uint8_t *mode, int32_t *c
     int64_t per_wave = 1;
     while (per_wave < 64 && ra.n / (per_wave * 2) >= (int64_t)cus * ROWS_WAVES_PER_CU) per_wave *= 2;
     const unsigned row_blocks = (unsigned)((ra.n + per_wave - 1) / per_wave);
-    pk::rows_fast<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows,
-                                                                      (int32_t)(64 / per_wave));
+    if (per_wave == 1)
+        pk::rows_fast<LENIENT, true><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows, 64);
+    else
+        pk::rows_fast<LENIENT, false><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows,
+                                                                                 (int32_t)(64 / per_wave));
     pk::rows_mid<LENIENT><<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(ra, mode, counters,
                                                                                               mid_rows, deep_rows);
     pk::rows_deep<LENIENT><<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);

@@ -489,10 +489,14 @@ struct RowArgs {
  * automaton (one per source) the gfx950 build returned wrong results for dense
  * segments although the same source is correct when compiled for the CPU, so
  * the sources are merged into one fetch loop. */
-template <class Store, bool LENIENT>
+template <bool WIDE, class Store, bool LENIENT>
 __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, bool compact,
                           Automaton<Store, LENIENT> &A)
 {
+    /* WIDE: the whole wave follows this one row in uniform control flow, so
+     * stored events are read 64 at a time (one per lane) and taken lane by
+     * lane with readlane; otherwise each lane reads its row 16 bytes at a
+     * time */
     const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
     const int64_t vrow0 = row_first_vec(g), vend = row_end_vec(g, len);
     int64_t s = s0;              /* next segment to open */
@@ -502,6 +506,7 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
     bool dense = false;
     int64_t q = 0, q_end = 0;    /* dense cursor (element index on the token grid) */
     uint4 quad = make_uint4(0u, 0u, 0u, 0u);
+    uint32_t win = 0;            /* WIDE: this lane's event of the current 64 */
     if (compact) {
         ev = a.events + s0 * EV_CAP;
         cnt = a.seg_count[s0];
@@ -512,11 +517,19 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
         uint32_t c = 0;
         for (;;) {
             if (!dense && e < cnt) {
-                /* stored lists start 256-byte aligned and their slots are
-                 * multiples of 4 events: read them 16 bytes at a time */
-                if ((e & 3) == 0) quad = *reinterpret_cast<const uint4 *>(ev + e);
-                const uint32_t k = (uint32_t)e & 3u;
-                const uint32_t w = k == 0 ? quad.x : k == 1 ? quad.y : k == 2 ? quad.z : quad.w;
+                uint32_t w;
+                if (WIDE) {
+                    /* a list's slots are a multiple of 64 events, so the 64
+                     * events from a multiple of 64 below cnt are in them */
+                    if ((e & (WAVE - 1)) == 0) win = ev[e + (int32_t)(threadIdx.x & (WAVE - 1))];
+                    w = (uint32_t)__builtin_amdgcn_readlane((int)win, e & (WAVE - 1));
+                } else {
+                    /* stored lists start 256-byte aligned and their slots are
+                     * multiples of 4 events: read them 16 bytes at a time */
+                    if ((e & 3) == 0) quad = *reinterpret_cast<const uint4 *>(ev + e);
+                    const uint32_t k = (uint32_t)e & 3u;
+                    w = k == 0 ? quad.x : k == 1 ? quad.y : k == 2 ? quad.z : quad.w;
+                }
                 ++e;
                 p = (int32_t)(base + (w >> 4));
                 c = w & 15u;
@@ -565,41 +578,46 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
  * frames (or more than 64 entries in an open block) is listed for rows_mid.
  * Few frames keep the LDS per block small, so that many waves hide the
  * latency of the branchy automaton. */
-template <bool LENIENT>
+template <bool LENIENT, bool ONE_ROW>
 __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__restrict__ mode,
                                                 int32_t *__restrict__ counters, int32_t *__restrict__ mid_rows,
                                                 int32_t lane_stride)
 {
     __shared__ int32_t lds[FAST_DEPTH * FRAME_WORDS * 64];
-    /* every lane_stride-th lane takes a row (64 / lane_stride rows per wave):
-     * few rows per wave when the batch is small, so that the waves spread
-     * over the GPU and a wave follows only its rows' paths through the
-     * automaton */
-    if (threadIdx.x % lane_stride != 0) return;
-    const int64_t r = (int64_t)blockIdx.x * (blockDim.x / lane_stride) + threadIdx.x / lane_stride;
+    /* ONE_ROW: the wave takes row blockIdx.x with all its lanes, in uniform
+     * control flow, so that the automaton runs on the scalar unit (a small
+     * batch: one wave per row spreads the rows over the GPU).  Otherwise every
+     * lane_stride-th lane takes a row (64 / lane_stride rows per wave). */
+    int64_t r;
+    if (ONE_ROW) {
+        r = blockIdx.x;
+    } else {
+        if (threadIdx.x % lane_stride != 0) return;
+        r = (int64_t)blockIdx.x * (blockDim.x / lane_stride) + threadIdx.x / lane_stride;
+    }
     if (r >= a.n) return;
+    const bool writer = !ONE_ROW || threadIdx.x == 0; /* one lane stores a uniform row's results */
     const int64_t start = a.starts[r];
     const int32_t len = a.lengths[r];
     if (start < 0 || len < 0) {
-        write_row(a.out, r, 0, 0, 0, 0, 0, 0, 0, PARASON_FLAG_BAD_ROW);
+        if (writer) write_row(a.out, r, 0, 0, 0, 0, 0, 0, 0, PARASON_FLAG_BAD_ROW);
         return;
     }
     if (a.seg_off[a.n] > a.seg_cap) {
-        write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
+        if (writer) write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
         return;
     }
     Automaton<LdsStore<FAST_DEPTH>, LENIENT> A;
     A.st.lds = lds;
-    A.st.tid = threadIdx.x;
-    A.st.nt = blockDim.x;
+    A.st.tid = ONE_ROW ? 0 : threadIdx.x;
+    A.st.nt = ONE_ROW ? 1 : blockDim.x;
     A.init();
-    if (drive_row(a, r, start + a.mis, len, mode[r] == 1, A)) A.finish(len);
+    if (drive_row<ONE_ROW>(a, r, start + a.mis, len, mode[r] == 1, A)) A.finish(len);
     if (A.overflow) {
-        int32_t slot = atomicAdd(&counters[0], 1);
-        mid_rows[slot] = (int32_t)r;
+        if (writer) mid_rows[atomicAdd(&counters[0], 1)] = (int32_t)r;
         return; /* rows_mid writes this row */
     }
-    write_result(a.out, r, len, A);
+    if (writer) write_result(a.out, r, len, A);
 }
 
 /* The rows rows_fast listed, one thread each (grid-stride over the list), with
@@ -621,7 +639,7 @@ __global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restr
         A.st.tid = threadIdx.x;
         A.st.nt = blockDim.x;
         A.init();
-        if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
+        if (drive_row<false>(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
         if (A.overflow) {
             int32_t slot = atomicAdd(&counters[1], 1);
             deep_rows[slot] = (int32_t)r;
@@ -649,7 +667,7 @@ __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__rest
         A.st.bits = bits;
         A.st.esp = 0;
         A.init();
-        if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
+        if (drive_row<false>(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
         if (A.overflow)
             write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_DEPTH_LIMIT);
         else
