@@ -26,7 +26,6 @@ constexpr int LOADS = SEG_VEC / WAVE;    /* vector loads per lane per segment */
 constexpr int EV_CAP = 128;              /* events stored per segment (12.5 % of its tokens) */
 static_assert(SEG_VEC % WAVE == 0, "a segment is a whole number of wave-wide loads");
 static_assert(EV_CAP % 4 == 0, "stored events are read 16 bytes at a time");
-static_assert(EV_CAP % WAVE == 0, "a one-row wave reads stored events 64 at a time");
 constexpr int PLAN_TILE = 4096;          /* rows per plan tile */
 constexpr int PLAN_THREADS = 256;
 constexpr int ROWS_PER_THREAD = PLAN_TILE / PLAN_THREADS;

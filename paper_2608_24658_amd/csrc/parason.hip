@@ -126,16 +126,21 @@ template <bool LENIENT>
 void launch_rows(const pk::RowArgs &ra, int cus, const uint8_t *mode, int32_t *counters, int32_t *mid_rows,
                  int32_t *deep_rows, int32_t *deep_frames, uint32_t *deep_bits, hipStream_t stream)
 {
-    /* rows per wave of rows_fast: enough waves to fill ROWS_WAVES_PER_CU on
-     * every CU, 64 (one per lane) once the batch is large enough */
+    /* A small batch (fewer rows than ROWS_WAVES_PER_CU waves on every CU):
+     * rows_par, one wave per row, its lanes over the row's events.  A larger
+     * one: rows_fast, one row per lane, with as many rows per wave as keep
+     * ROWS_WAVES_PER_CU waves on every CU (64 once the batch is large). */
     int64_t per_wave = 1;
-    while (per_wave < 64 && ra.n / (per_wave * 2) >= (int64_t)cus * ROWS_WAVES_PER_CU) per_wave *= 2;
+    int32_t lane_shift = 6; /* log2(64 / per_wave) */
+    while (per_wave < 64 && ra.n / (per_wave * 2) >= (int64_t)cus * ROWS_WAVES_PER_CU) {
+        per_wave *= 2;
+        --lane_shift;
+    }
     const unsigned row_blocks = (unsigned)((ra.n + per_wave - 1) / per_wave);
     if (per_wave == 1)
-        pk::rows_fast<LENIENT, true><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows, 64);
+        pk::rows_par<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows);
     else
-        pk::rows_fast<LENIENT, false><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows,
-                                                                                 (int32_t)(64 / per_wave));
+        pk::rows_fast<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows, lane_shift);
     pk::rows_mid<LENIENT><<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(ra, mode, counters,
                                                                                               mid_rows, deep_rows);
     pk::rows_deep<LENIENT><<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);
@@ -148,10 +153,15 @@ void abi::launch_plan(const int64_t *starts, const int32_t *lengths, int64_t n, 
                       hipStream_t stream)
 {
     const unsigned tiles = (unsigned)n_tiles;
+    if (n_tiles == 1) {
+        pk::plan_rows<true><<<dim3(1), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n, mis, nullptr, seg_off,
+                                                                          mode, counters);
+        return;
+    }
     pk::plan_tiles<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n, mis, tile_sum);
     pk::plan_top<<<dim3(1), dim3(1024), 0, stream>>>(tile_sum, n_tiles, tile_off, seg_off, n, counters);
-    pk::plan_rows<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n, mis, tile_off, seg_off,
-                                                                        mode);
+    pk::plan_rows<false><<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n, mis, tile_off,
+                                                                           seg_off, mode, counters);
 }
 
 extern "C" {

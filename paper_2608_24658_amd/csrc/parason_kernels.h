@@ -96,11 +96,17 @@ __global__ void __launch_bounds__(1024) plan_top(const int64_t *__restrict__ til
 }
 
 /* seg_off[i] = first segment of row i; mode[i] = 0 (events in per-segment slots). */
+/* SINGLE: the batch is one tile, and this one block also does plan_top's
+ * work (seg_off[n], clearing the counters), so a small batch is planned with
+ * one launch instead of three. */
+template <bool SINGLE>
 __global__ void __launch_bounds__(PLAN_THREADS) plan_rows(const int64_t *__restrict__ starts,
                                                           const int32_t *__restrict__ lengths, int64_t n,
                                                           int64_t mis, const int64_t *__restrict__ tile_off,
-                                                          int64_t *__restrict__ seg_off, uint8_t *__restrict__ mode)
+                                                          int64_t *__restrict__ seg_off, uint8_t *__restrict__ mode,
+                                                          int32_t *__restrict__ counters)
 {
+    if (SINGLE && threadIdx.x < 4) counters[threadIdx.x] = 0;
     __shared__ int64_t part[PLAN_THREADS / WAVE];
     /* thread t owns the ROWS_PER_THREAD consecutive rows starting at r0 + t*ROWS_PER_THREAD */
     int64_t r0 = (int64_t)blockIdx.x * PLAN_TILE + (int64_t)threadIdx.x * ROWS_PER_THREAD;
@@ -115,7 +121,7 @@ __global__ void __launch_bounds__(PLAN_THREADS) plan_rows(const int64_t *__restr
     int64_t inc = wave_inclusive_scan(s);
     if ((threadIdx.x & (WAVE - 1)) == WAVE - 1) part[threadIdx.x / WAVE] = inc;
     __syncthreads();
-    int64_t off = tile_off[blockIdx.x] + inc - s;
+    int64_t off = (SINGLE ? 0 : tile_off[blockIdx.x]) + inc - s;
     for (int w = 0; w < (int)(threadIdx.x / WAVE); ++w) off += part[w];
 #pragma unroll
     for (int j = 0; j < ROWS_PER_THREAD; ++j) {
@@ -126,6 +132,7 @@ __global__ void __launch_bounds__(PLAN_THREADS) plan_rows(const int64_t *__restr
         }
         off += cnt[j];
     }
+    if (SINGLE && threadIdx.x == PLAN_THREADS - 1) seg_off[n] = off; /* the last thread ends at the total */
 }
 
 /* ------------------------------------------------------------------ automaton */
@@ -489,14 +496,10 @@ struct RowArgs {
  * automaton (one per source) the gfx950 build returned wrong results for dense
  * segments although the same source is correct when compiled for the CPU, so
  * the sources are merged into one fetch loop. */
-template <bool WIDE, class Store, bool LENIENT>
+template <class Store, bool LENIENT>
 __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, bool compact,
                           Automaton<Store, LENIENT> &A)
 {
-    /* WIDE: the whole wave follows this one row in uniform control flow, so
-     * stored events are read 64 at a time (one per lane) and taken lane by
-     * lane with readlane; otherwise each lane reads its row 16 bytes at a
-     * time */
     const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
     const int64_t vrow0 = row_first_vec(g), vend = row_end_vec(g, len);
     int64_t s = s0;              /* next segment to open */
@@ -506,7 +509,6 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
     bool dense = false;
     int64_t q = 0, q_end = 0;    /* dense cursor (element index on the token grid) */
     uint4 quad = make_uint4(0u, 0u, 0u, 0u);
-    uint32_t win = 0;            /* WIDE: this lane's event of the current 64 */
     if (compact) {
         ev = a.events + s0 * EV_CAP;
         cnt = a.seg_count[s0];
@@ -517,19 +519,11 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
         uint32_t c = 0;
         for (;;) {
             if (!dense && e < cnt) {
-                uint32_t w;
-                if (WIDE) {
-                    /* a list's slots are a multiple of 64 events, so the 64
-                     * events from a multiple of 64 below cnt are in them */
-                    if ((e & (WAVE - 1)) == 0) win = ev[e + (int32_t)(threadIdx.x & (WAVE - 1))];
-                    w = (uint32_t)__builtin_amdgcn_readlane((int)win, e & (WAVE - 1));
-                } else {
-                    /* stored lists start 256-byte aligned and their slots are
-                     * multiples of 4 events: read them 16 bytes at a time */
-                    if ((e & 3) == 0) quad = *reinterpret_cast<const uint4 *>(ev + e);
-                    const uint32_t k = (uint32_t)e & 3u;
-                    w = k == 0 ? quad.x : k == 1 ? quad.y : k == 2 ? quad.z : quad.w;
-                }
+                /* stored lists start 256-byte aligned and their slots are
+                 * multiples of 4 events: read them 16 bytes at a time */
+                if ((e & 3) == 0) quad = *reinterpret_cast<const uint4 *>(ev + e);
+                const uint32_t k = (uint32_t)e & 3u;
+                const uint32_t w = k == 0 ? quad.x : k == 1 ? quad.y : k == 2 ? quad.z : quad.w;
                 ++e;
                 p = (int32_t)(base + (w >> 4));
                 c = w & 15u;
@@ -578,46 +572,37 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
  * frames (or more than 64 entries in an open block) is listed for rows_mid.
  * Few frames keep the LDS per block small, so that many waves hide the
  * latency of the branchy automaton. */
-template <bool LENIENT, bool ONE_ROW>
+template <bool LENIENT>
 __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__restrict__ mode,
                                                 int32_t *__restrict__ counters, int32_t *__restrict__ mid_rows,
-                                                int32_t lane_stride)
+                                                int32_t lane_shift)
 {
     __shared__ int32_t lds[FAST_DEPTH * FRAME_WORDS * 64];
-    /* ONE_ROW: the wave takes row blockIdx.x with all its lanes, in uniform
-     * control flow, so that the automaton runs on the scalar unit (a small
-     * batch: one wave per row spreads the rows over the GPU).  Otherwise every
-     * lane_stride-th lane takes a row (64 / lane_stride rows per wave). */
-    int64_t r;
-    if (ONE_ROW) {
-        r = blockIdx.x;
-    } else {
-        if (threadIdx.x % lane_stride != 0) return;
-        r = (int64_t)blockIdx.x * (blockDim.x / lane_stride) + threadIdx.x / lane_stride;
-    }
+    /* every (1 << lane_shift)-th lane takes a row (64 >> lane_shift rows per wave) */
+    if ((threadIdx.x & ((1u << lane_shift) - 1u)) != 0) return;
+    const int64_t r = (int64_t)blockIdx.x * (blockDim.x >> lane_shift) + (threadIdx.x >> lane_shift);
     if (r >= a.n) return;
-    const bool writer = !ONE_ROW || threadIdx.x == 0; /* one lane stores a uniform row's results */
     const int64_t start = a.starts[r];
     const int32_t len = a.lengths[r];
     if (start < 0 || len < 0) {
-        if (writer) write_row(a.out, r, 0, 0, 0, 0, 0, 0, 0, PARASON_FLAG_BAD_ROW);
+        write_row(a.out, r, 0, 0, 0, 0, 0, 0, 0, PARASON_FLAG_BAD_ROW);
         return;
     }
     if (a.seg_off[a.n] > a.seg_cap) {
-        if (writer) write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
+        write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
         return;
     }
     Automaton<LdsStore<FAST_DEPTH>, LENIENT> A;
     A.st.lds = lds;
-    A.st.tid = ONE_ROW ? 0 : threadIdx.x;
-    A.st.nt = ONE_ROW ? 1 : blockDim.x;
+    A.st.tid = threadIdx.x;
+    A.st.nt = blockDim.x;
     A.init();
-    if (drive_row<ONE_ROW>(a, r, start + a.mis, len, mode[r] == 1, A)) A.finish(len);
+    if (drive_row(a, r, start + a.mis, len, mode[r] == 1, A)) A.finish(len);
     if (A.overflow) {
-        if (writer) mid_rows[atomicAdd(&counters[0], 1)] = (int32_t)r;
+        mid_rows[atomicAdd(&counters[0], 1)] = (int32_t)r;
         return; /* rows_mid writes this row */
     }
-    if (writer) write_result(a.out, r, len, A);
+    write_result(a.out, r, len, A);
 }
 
 /* The rows rows_fast listed, one thread each (grid-stride over the list), with
@@ -639,7 +624,7 @@ __global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restr
         A.st.tid = threadIdx.x;
         A.st.nt = blockDim.x;
         A.init();
-        if (drive_row<false>(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
+        if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
         if (A.overflow) {
             int32_t slot = atomicAdd(&counters[1], 1);
             deep_rows[slot] = (int32_t)r;
@@ -667,11 +652,310 @@ __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__rest
         A.st.bits = bits;
         A.st.esp = 0;
         A.init();
-        if (drive_row<false>(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
+        if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
         if (A.overflow)
             write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_DEPTH_LIMIT);
         else
             write_result(a.out, r, len, A);
+    }
+}
+
+/* ------------------------------------------------------------------ rows_par */
+
+constexpr int PAR_EVENTS = 512; /* events of a row rows_par holds in LDS */
+constexpr int PAR_LEVELS = 16;  /* nesting rows_par evaluates */
+
+/* The classes that may follow state st (one bit per class). */
+__device__ __forceinline__ uint32_t allowed_classes(uint32_t st)
+{
+    switch (st) {
+    case S_START: return 1u << C_THINK;
+    case S_BODY: return (1u << C_PAR) | (1u << C_END_THINK) | (1u << C_END_THR);
+    case S_P_OPEN: return 1u << C_OUT;
+    case S_O_OPEN: return (1u << C_SUB) | (1u << C_TRI);
+    case S_ENTRY: return (1u << C_END_SUB) | (1u << C_END_TRI);
+    case S_E_DONE: return (1u << C_SUB) | (1u << C_TRI) | (1u << C_END_OUT);
+    case S_O_DONE: return 1u << C_THR;
+    case S_W_DONE: return (1u << C_THR) | (1u << C_END_PAR);
+    default: return 0u; /* S_TRAIL */
+    }
+}
+
+/* The state after a tag of class c: the class alone decides it. */
+__device__ __forceinline__ uint32_t state_after(int32_t c)
+{
+    switch (c) {
+    case C_THINK: return S_BODY;
+    case C_END_THINK: return S_TRAIL;
+    case C_PAR: return S_P_OPEN;
+    case C_END_PAR: return S_BODY;
+    case C_OUT: return S_O_OPEN;
+    case C_END_OUT: return S_O_DONE;
+    case C_SUB:
+    case C_TRI: return S_ENTRY;
+    case C_END_SUB:
+    case C_END_TRI: return S_E_DONE;
+    case C_THR: return S_BODY;
+    default: return S_W_DONE; /* C_END_THR */
+    }
+}
+
+/* Inclusive prefix sum over the wave's lanes (every lane must call it). */
+__device__ __forceinline__ int32_t wave_incl_scan32(int32_t v, int lane)
+{
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) {
+        const int32_t o = __shfl_up(v, (unsigned)d, WAVE);
+        v += lane >= d ? o : 0;
+    }
+    return v;
+}
+
+/* Inclusive scans over the wave's lanes, every lane calling.  The segmented
+ * forms restart at lanes with head set; lanes before the chunk's first head
+ * continue from carry (the previous chunk's last value). */
+__device__ __forceinline__ int32_t wave_incl_max32(int32_t v, int lane)
+{
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) {
+        const int32_t o = __shfl_up(v, (unsigned)d, WAVE);
+        v = (lane >= d && o > v) ? o : v;
+    }
+    return v;
+}
+
+template <bool MAX>
+__device__ __forceinline__ int32_t wave_seg_scan(int32_t v, bool head, int32_t carry, int lane)
+{
+    int32_t f = head ? 1 : 0;
+#pragma unroll
+    for (int d = 1; d < WAVE; d <<= 1) {
+        const int32_t vo = __shfl_up(v, (unsigned)d, WAVE);
+        const int32_t fo = __shfl_up(f, (unsigned)d, WAVE);
+        if (lane >= d && !f) {
+            v = MAX ? (vo > v ? vo : v) : v + vo;
+            f = fo;
+        }
+    }
+    return f ? v : (MAX ? (carry > v ? carry : v) : v + carry);
+}
+
+__device__ __forceinline__ int32_t wave_sum32(int32_t v)
+{
+#pragma unroll
+    for (int d = WAVE / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, WAVE);
+    return v;
+}
+
+__device__ __forceinline__ int32_t wave_min32(int32_t v)
+{
+#pragma unroll
+    for (int d = WAVE / 2; d > 0; d >>= 1) {
+        const int32_t o = __shfl_xor(v, d, WAVE);
+        v = o < v ? o : v;
+    }
+    return v;
+}
+
+__device__ __forceinline__ int32_t wave_max32(int32_t v)
+{
+#pragma unroll
+    for (int d = WAVE / 2; d > 0; d >>= 1) {
+        const int32_t o = __shfl_xor(v, d, WAVE);
+        v = o > v ? o : v;
+    }
+    return v;
+}
+
+/* One wave per row, its lanes over the row's events (a small batch).  The
+ * same results as the automaton, from the structure of the grammar:
+ *   - the state before a tag is fixed by the class of the tag before it, and
+ *     the nesting depth before it is a prefix sum, so every check of the
+ *     automaton is local to an event and its predecessor; the row's first
+ *     error is the smallest error position over the events (phase A);
+ *   - for a valid row, with saved(P) = sum_k tokens(W_k) - max_k lat(W_k)
+ *     over the threads W_k of block P, and lat(W) = tokens(W) - the saved
+ *     tokens of the blocks directly inside W, the latency is the row's
+ *     length less the saved tokens of its top-level blocks; a thread's own
+ *     tokens (its tokens less those of the threads nested in it) take the
+ *     type of the outline entry it pairs with.  Evaluated level by level,
+ *     deepest first, with segmented scans (phase B).
+ * Rows holding more than PAR_EVENTS events, nested deeper than PAR_LEVELS,
+ * or with a dense segment, go to rows_mid. */
+template <bool LENIENT>
+__global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restrict__ mode,
+                                               int32_t *__restrict__ counters, int32_t *__restrict__ mid_rows)
+{
+    __shared__ int32_t sP[PAR_EVENTS], sC[PAR_EVENTS], sD[PAR_EVENTS], sT[PAR_EVENTS];
+    __shared__ int32_t sTOK[PAR_EVENTS], sLAT[PAR_EVENTS], sOWN[PAR_EVENTS], sSAV[PAR_EVENTS];
+    const int lane = threadIdx.x;
+    const int64_t r = blockIdx.x;
+    if (r >= a.n) return;
+    const int64_t start = a.starts[r];
+    const int32_t len = a.lengths[r];
+    if (start < 0 || len < 0) {
+        if (lane == 0) write_row(a.out, r, 0, 0, 0, 0, 0, 0, 0, PARASON_FLAG_BAD_ROW);
+        return;
+    }
+    if (a.seg_off[a.n] > a.seg_cap) {
+        if (lane == 0) write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
+        return;
+    }
+    /* the row's events: one compact list (row positions), or the one list of
+     * a row of a single segment (segment positions) */
+    const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
+    const int64_t g = start + a.mis;
+    int32_t m = 0;
+    int64_t base = 0;
+    bool listed = s1 == s0; /* no segment: an empty row, no events */
+    if (mode[r] == 1) {
+        m = a.seg_count[s0];
+        listed = true;
+    } else if (s1 - s0 == 1 && a.seg_count[s0] <= EV_CAP) {
+        m = a.seg_count[s0];
+        base = 4 * row_first_vec(g) - g;
+        listed = true;
+    }
+    if (!listed || m > PAR_EVENTS) {
+        if (lane == 0) mid_rows[atomicAdd(&counters[0], 1)] = (int32_t)r;
+        return;
+    }
+    const uint32_t *list = a.events + s0 * EV_CAP;
+    for (int32_t i = lane; i < m; i += WAVE) {
+        const uint32_t w = list[i];
+        sP[i] = (int32_t)(base + (int64_t)(w >> 4));
+        sC[i] = (int32_t)(w & 15u);
+    }
+    __syncthreads();
+
+    /* phase A: validity, first error, depth and open threads before each event */
+    int32_t prev_c = -1, prev_p = -1, depth = 0, threads = 0, err = INT32_MAX, max_depth = 0, n_blocks = 0;
+    for (int32_t i0 = 0; i0 < m && err == INT32_MAX; i0 += WAVE) {
+        const int32_t i = i0 + lane;
+        const bool act = i < m;
+        const int32_t c = act ? sC[i] : 0, p = act ? sP[i] : 0;
+        int32_t pc = __shfl_up(c, 1u, WAVE), pp = __shfl_up(p, 1u, WAVE);
+        if (lane == 0) {
+            pc = prev_c;
+            pp = prev_p;
+        }
+        const int32_t dd = act ? (c == C_PAR) - (c == C_END_PAR) : 0;
+        const int32_t dt = act ? (c == C_THR) - (c == C_END_THR) : 0;
+        const int32_t d_in = wave_incl_scan32(dd, lane), t_in = wave_incl_scan32(dt, lane);
+        const int32_t db = depth + d_in - dd, tb = threads + t_in - dt;
+        int32_t e = INT32_MAX, open_depth = 0;
+        if (act) {
+            const uint32_t st = pc < 0 ? (uint32_t)S_START : state_after(pc);
+            const int32_t gap = p - pp - 1;
+            const bool text_ok = gap == 0 || st == S_BODY || st == S_TRAIL || st == S_ENTRY || (LENIENT && st != S_START);
+            const bool tag_ok = ((allowed_classes(st) >> c) & 1u) && !(c == C_END_THINK && db != 0) &&
+                                !(c == C_END_THR && db == 0) &&
+                                !((c == C_END_SUB || c == C_END_TRI) && (c != pc + 1 || gap == 0));
+            e = !text_ok ? pp + 1 : (!tag_ok ? p : INT32_MAX);
+            sD[i] = db;
+            sT[i] = tb;
+            open_depth = c == C_PAR ? db + 1 : 0;
+        }
+        err = wave_min32(e);
+        max_depth = max(max_depth, wave_max32(open_depth));
+        n_blocks += wave_sum32(act && c == C_PAR ? 1 : 0);
+        const int last = min(WAVE - 1, m - 1 - i0);
+        prev_c = __shfl(c, last, WAVE);
+        prev_p = __shfl(p, last, WAVE);
+        depth += __shfl(d_in, WAVE - 1, WAVE);
+        threads += __shfl(t_in, WAVE - 1, WAVE);
+    }
+    if (err == INT32_MAX) {
+        /* the end of the row: the text after the last tag, then </think> must have come */
+        const uint32_t st = prev_c < 0 ? (uint32_t)S_START : state_after(prev_c);
+        const int32_t gap = len - prev_p - 1;
+        const bool text_ok = gap == 0 || st == S_BODY || st == S_TRAIL || st == S_ENTRY || (LENIENT && st != S_START);
+        if (!text_ok) err = prev_p + 1;
+        else if (st != S_TRAIL) err = len;
+    }
+    if (err != INT32_MAX) {
+        if (lane == 0) write_row(a.out, r, len, len, 0, 0, 0, 0, err, err == len ? PARASON_FLAG_TRUNCATED : 0u);
+        return;
+    }
+    if (max_depth > PAR_LEVELS) {
+        if (lane == 0) mid_rows[atomicAdd(&counters[0], 1)] = (int32_t)r;
+        return;
+    }
+    __syncthreads();
+
+    /* phase B: level by level, deepest first */
+    int32_t my_sub = 0, my_tri = 0, my_saved = 0;
+    bool my_mismatch = false;
+    for (int32_t lev = max_depth; lev >= 1; --lev) {
+        /* threads of level lev: tokens, latency, own tokens */
+        int32_t c_thr = -1, c_S = 0, c_CH = 0;
+        for (int32_t i0 = 0; i0 < m; i0 += WAVE) {
+            const int32_t i = i0 + lane;
+            const bool act = i < m;
+            const int32_t c = act ? sC[i] : 0, db = act ? sD[i] : -1, tb = act ? sT[i] : -1;
+            const bool thr = act && c == C_THR && tb == lev - 1;
+            const bool ethr = act && c == C_END_THR && tb == lev;
+            const bool epar_in = act && c == C_END_PAR && db == lev + 1;
+            const bool ethr_in = act && c == C_END_THR && tb == lev + 1;
+            const int32_t thr_idx = max(c_thr, wave_incl_max32(thr ? i : -1, lane));
+            const int32_t S = wave_seg_scan<false>(epar_in ? sSAV[i] : 0, thr, c_S, lane);
+            const int32_t CH = wave_seg_scan<false>(ethr_in ? sTOK[i] : 0, thr, c_CH, lane);
+            if (ethr) {
+                const int32_t tok = sP[i] - sP[thr_idx] + 1;
+                sTOK[i] = tok;
+                sLAT[i] = tok - S;
+                sOWN[i] = tok - CH;
+            }
+            c_thr = __shfl(thr_idx, WAVE - 1, WAVE);
+            c_S = __shfl(S, WAVE - 1, WAVE);
+            c_CH = __shfl(CH, WAVE - 1, WAVE);
+        }
+        __syncthreads();
+        /* blocks of level lev: saved tokens, thread types, count mismatch */
+        int32_t c_sum = 0, c_max = 0, c_n = 0, c_par = -1, c_eout = -1;
+        for (int32_t i0 = 0; i0 < m; i0 += WAVE) {
+            const int32_t i = i0 + lane;
+            const bool act = i < m;
+            const int32_t c = act ? sC[i] : 0, db = act ? sD[i] : -1, tb = act ? sT[i] : -1;
+            const bool par = act && c == C_PAR && db == lev - 1;
+            const bool epar = act && c == C_END_PAR && db == lev;
+            const bool eout = act && c == C_END_OUT && db == lev && tb == lev - 1;
+            const bool ethr = act && c == C_END_THR && tb == lev;
+            const int32_t sum = wave_seg_scan<false>(ethr ? sTOK[i] : 0, par, c_sum, lane);
+            const int32_t mx = wave_seg_scan<true>(ethr ? sLAT[i] : 0, par, c_max, lane);
+            const int32_t nt = wave_seg_scan<false>(ethr ? 1 : 0, par, c_n, lane);
+            const int32_t par_idx = max(c_par, wave_incl_max32(par ? i : -1, lane));
+            const int32_t eout_idx = max(c_eout, wave_incl_max32(eout ? i : -1, lane));
+            const int32_t n_e = (eout_idx - par_idx - 2) / 2;
+            if (ethr) {
+                const int32_t k = nt - 1; /* thread k pairs with entry k */
+                if (k < n_e) {
+                    const int32_t t = sC[par_idx + 2 + 2 * k];
+                    my_sub += t == C_SUB ? sOWN[i] : 0;
+                    my_tri += t == C_TRI ? sOWN[i] : 0;
+                }
+            }
+            if (epar) {
+                const int32_t saved = sum - mx;
+                sSAV[i] = saved;
+                my_mismatch = my_mismatch || nt != n_e;
+                my_saved += lev == 1 ? saved : 0;
+            }
+            c_sum = __shfl(sum, WAVE - 1, WAVE);
+            c_max = __shfl(mx, WAVE - 1, WAVE);
+            c_n = __shfl(nt, WAVE - 1, WAVE);
+            c_par = __shfl(par_idx, WAVE - 1, WAVE);
+            c_eout = __shfl(eout_idx, WAVE - 1, WAVE);
+        }
+        __syncthreads();
+    }
+    const int32_t n_sub = wave_sum32(my_sub), n_tri = wave_sum32(my_tri), saved = wave_sum32(my_saved);
+    const bool mismatch = __ballot(my_mismatch) != 0;
+    if (lane == 0) {
+        uint32_t fl = PARASON_FLAG_VALID;
+        if (mismatch) fl |= PARASON_FLAG_COUNT_MISMATCH;
+        if (n_blocks > 0) fl |= PARASON_FLAG_TRIGGERED;
+        write_row(a.out, r, len, len - saved, n_sub, n_tri, n_blocks, max_depth, -1, fl);
     }
 }
 
@@ -928,17 +1212,6 @@ struct GatherArgs {
     const int32_t *split_rows;
 };
 
-/* Inclusive prefix sum over the wave's lanes (every lane must call it). */
-__device__ __forceinline__ int32_t wave_incl_scan32(int32_t v, int lane)
-{
-#pragma unroll
-    for (int d = 1; d < WAVE; d <<= 1) {
-        const int32_t o = __shfl_up(v, (unsigned)d, WAVE);
-        v += lane >= d ? o : 0;
-    }
-    return v;
-}
-
 /* The largest lane j with x (held by lane j) <= f, for x non-decreasing over
  * the lanes and x of lane 0 <= f (every lane must call it). */
 __device__ __forceinline__ int32_t last_lane_at_most(int32_t x, int32_t f)
@@ -1114,15 +1387,49 @@ __device__ __forceinline__ void write_nan(const RewardArgs &a, int64_t r)
     if (a.saved) a.saved[r] = (a.flags[r] & NOT_EVALUATED) ? 0 : a.total[r] - a.latency[r];
 }
 
-/* One thread per row.  Every thread of a group computes the group's moments
- * itself, in the same fixed order, so they all hold the same values; a group
- * thus takes G threads instead of one, which keeps the GPU busy when a batch
- * has few groups (an RL step has 128). */
+/* A group of G rows (G a power of two up to 64) in G consecutive lanes of one
+ * wave: each lane loads its own row once and reads the others' values with
+ * shuffles, in the group's order. */
+__device__ __forceinline__ void group_reward_lanes(const RewardArgs &a, int64_t r, int32_t G)
+{
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int gl = lane & ~(G - 1); /* the group's first lane */
+    const uint64_t gmask = (G == WAVE ? ~0ull : ((1ull << G) - 1ull)) << gl;
+    const uint32_t fl = a.flags[r];
+    const int32_t lat = a.latency[r], tot = a.total[r], ns = a.n_subtask[r], nt = a.n_trial[r];
+    if ((__ballot(!(fl & NOT_EVALUATED)) & gmask) != gmask) {
+        write_nan(a, r);
+        return; /* the whole group returns here */
+    }
+    const bool lat_equal = (__ballot(lat == __shfl(lat, gl, WAVE)) & gmask) == gmask;
+    /* exact equality of the ratios, cross-multiplied against the group's first row */
+    const int64_t d = tot > 0 ? tot : 1;
+    const int64_t d0 = __shfl(d, gl, WAVE);
+    const int64_t s_n = tot > 0 ? ns : 0, t_n = tot > 0 ? nt : 0;
+    const bool sub_equal = (__ballot(s_n * d0 == __shfl(s_n, gl, WAVE) * d) & gmask) == gmask;
+    const bool tri_equal = (__ballot(t_n * d0 == __shfl(t_n, gl, WAVE) * d) & gmask) == gmask;
+    const double xT = (double)lat, xs = ratio(ns, tot), xr = ratio(nt, tot);
+    const Moments mT = moments([&](int32_t j) { return __shfl(xT, gl + j, WAVE); }, G);
+    const Moments ms = moments([&](int32_t j) { return __shfl(xs, gl + j, WAVE); }, G);
+    const Moments mr = moments([&](int32_t j) { return __shfl(xr, gl + j, WAVE); }, G);
+    write_reward(a, r, zscore(xT, mT, lat_equal), zscore(xs, ms, sub_equal), zscore(xr, mr, tri_equal), xs, xr);
+}
+
+/* One thread per row.  A group within one wave shares its values by shuffles
+ * (group_reward_lanes); otherwise every thread of a group computes the group's
+ * moments itself from memory.  Either way the sums run in the group's row
+ * order, so every thread of a group holds the same values; a group takes G
+ * threads instead of one, which keeps the GPU busy when a batch has few
+ * groups (an RL step has 128). */
 __global__ void __launch_bounds__(256) group_reward(RewardArgs a)
 {
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= a.n) return;
+    if (r >= a.n) return; /* n is a multiple of G: whole groups only */
     const int32_t G = a.G;
+    if (G <= WAVE && (G & (G - 1)) == 0) {
+        group_reward_lanes(a, r, G);
+        return;
+    }
     const int64_t r0 = r - r % G;
 
     bool evaluated = true;
