@@ -251,7 +251,49 @@ def main():
         log("timing the CPU oracle on a sample")
         res["cpu_baseline"] = cpu_baseline(tokens, starts.cpu().numpy(), lengths.cpu().numpy(),
                                            correct.cpu().numpy(), S.CONTIGUOUS_TAGS, coef, args.cpu_budget)
+    if args.workload == "large":
+        # the same step on a batch of the size of one training step (latency-bound, not HBM-bound)
+        del tokens, starts, lengths, correct, out, ws
+        torch.cuda.empty_cache()
+        res["typical_batch"] = time_small_batch("typical", coef, args.steps * 5, args.warmup)
     print(json.dumps(res), flush=True)
+
+
+def time_small_batch(workload, coef, steps, warmup):
+    """Whole-step time of the accounting path on a small batch (wall clock
+    around `steps` calls, inputs resident)."""
+    import torch
+
+    from paper_2608_24658_amd import parason as PX
+    from paper_2608_24658_amd.synth import synth as S
+
+    dev = torch.device("cuda:0")
+    G = S.GROUP_SIZE
+    P = S.make_params(workload)
+    n = S.n_rows_of(workload)
+    tokens, starts, lengths, correct = S.device_batch(P, n, device=dev)
+    n_tok = int(tokens.numel())
+    px = PX.Parason(S.CONTIGUOUS_TAGS, group_size=G, **coef)
+    out = px.alloc_outputs(n, dev)
+    ws = px.alloc_workspace(n, n_tok, dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def step():
+        rc = px.run_raw(tokens.data_ptr(), starts.data_ptr(), lengths.data_ptr(), correct.data_ptr(), n, out,
+                        ws.data_ptr(), ws.numel(), stream)
+        if rc != PX.OK:
+            raise PX.ParasonError(rc, "parason_run")
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    return {"workload": "%s: %d groups x %d rollouts, %d rows, %d tokens" % (workload, n // G, G, n, n_tok),
+            "ms_per_step": ms, "tokens_per_s": n_tok / (ms * 1e-3), "rows_per_s": n / (ms * 1e-3)}
 
 
 def bench_pg(args):
