@@ -110,6 +110,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="large", choices=["tiny", "small", "typical", "large", "ragged"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-typical-batch", action="store_true",
+                    help="skip the typical-workload step timed after the large one (for profiler runs, so that "
+                         "per-kernel averages cover one workload)")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--step", default="accounting", choices=["accounting", "pg", "decode", "fork"],
                     help="accounting: the hot path (default); pg: the policy-gradient step that consumes its "
@@ -251,7 +254,7 @@ def main():
         log("timing the CPU oracle on a sample")
         res["cpu_baseline"] = cpu_baseline(tokens, starts.cpu().numpy(), lengths.cpu().numpy(),
                                            correct.cpu().numpy(), S.CONTIGUOUS_TAGS, coef, args.cpu_budget)
-    if args.workload == "large":
+    if args.workload == "large" and not args.no_typical_batch:
         # the same step on a batch of the size of one training step (latency-bound, not HBM-bound)
         del tokens, starts, lengths, correct, out, ws
         torch.cuda.empty_cache()
