@@ -3,7 +3,7 @@
  *
  * Data flow of one parason_run (all on the caller's stream):
  *
- *   plan_tiles / plan_top / plan_rows
+ *   plan_tiles / plan_top / plan_rows  (one plan_rows block for one tile)
  *        Each row is cut into segments of SEG_VEC 16-byte vectors, starting at
  *        the 128-byte line that holds its first token.  A three-pass exclusive
  *        scan gives seg_off[i] (first segment of row i) and the segment count
@@ -14,8 +14,16 @@
  *        0.1-1% of tokens) in position order.  A row whose segments all fall in
  *        one wave's range collects its events in that wave's LDS buffer and is
  *        written out, coalesced, as one compact list (mode[i] = 1).  Other rows
- *        leave their events in per-segment global slots (mode[i] = 0).
- *   rows_fast  (one thread per row)
+ *        leave their events in per-segment global slots (mode[i] = 0) and are
+ *        listed as split.
+ *   gather_rows  (one wave per split row)
+ *        Moves a split row's per-segment events, in place and in order, into
+ *        one compact list with row positions (mode[i] = 1).
+ *   rows_par  (small batches: one wave per row, lanes over its events)
+ *        Validity from local checks and a depth prefix sum; latency and branch
+ *        tokens level by level with segmented scans.  Rows it cannot hold go
+ *        to rows_mid.
+ *   rows_fast  (larger batches: one thread per row)
  *        The grammar's pushdown automaton over the row's events; Text runs are
  *        the gaps between event positions.  A segment holding more than EV_CAP
  *        tags, or marked DENSE by the scan, is classified again token by token.
@@ -26,7 +34,7 @@
  *        handed to rows_deep.
  *   rows_deep  (one thread, only rows rows_mid handed over)
  *        The same automaton with frames and entry types in global workspace.
- *   group_reward  (one thread per group of G rows)
+ *   group_reward  (one thread per row)
  *        Statistics and Definition 3.1 in IEEE double, fixed order.
  *
  * Paper references: grammar -- figure "Context-Free Grammar for Parason"
