@@ -145,3 +145,22 @@ def test_hand_streams_with_gaps(dev, tags):
     for k, v in golden["expected"].items():
         assert int(got[k][i]) == v, k
     assert int(np.max(got["max_depth"])) == 60
+
+
+def test_many_rows_with_gaps(dev):
+    """24,576 rows (more than the one-wave-per-row kernel takes): the lenient
+    form of the per-lane automaton, several rows per wave."""
+    log("case lenient many rows")
+    tag_ids = S.CONTIGUOUS_TAGS
+    P = S.make_params("small", tag_ids=tag_ids)
+    n0 = S.n_rows_of("small")
+    tok, st, ln, co = S.host_batch(P, n0)
+    rng = np.random.default_rng(31)
+    rows = []
+    for rep in range(96):
+        for i in range(n0):
+            rows.append(insert_gaps(tok[st[i]: st[i] + ln[i]], tag_ids, rng, p=0.3, max_len=2))
+    tokens, starts, lengths = packed(rows)
+    correct = np.tile(co, 96)
+    got, _ = run_both(dev, tokens, starts, lengths, correct, tag_ids, "many rows")
+    assert len(rows) == 24576 and int(np.sum(got["flags"] & PX.FLAG_VALID)) > 20000
