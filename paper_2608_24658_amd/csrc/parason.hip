@@ -123,8 +123,9 @@ void find_tag_hash(pk::TagMatch &tm)
 /* The three tiers of the row automaton, in the grammar's strict or lenient
  * form. */
 template <bool LENIENT>
-void launch_rows(const pk::RowArgs &ra, int cus, const uint8_t *mode, int32_t *counters, int32_t *mid_rows,
-                 int32_t *deep_rows, int32_t *deep_frames, uint32_t *deep_bits, hipStream_t stream)
+void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, const uint8_t *mode, int32_t *counters,
+                 int32_t *mid_rows, int32_t *deep_rows, int32_t *deep_frames, uint32_t *deep_bits,
+                 hipStream_t stream)
 {
     /* A small batch (fewer rows than ROWS_WAVES_PER_CU waves on every CU):
      * rows_par, one wave per row, its lanes over the row's events.  A larger
@@ -137,10 +138,13 @@ void launch_rows(const pk::RowArgs &ra, int cus, const uint8_t *mode, int32_t *c
         --lane_shift;
     }
     const unsigned row_blocks = (unsigned)((ra.n + per_wave - 1) / per_wave);
-    if (per_wave == 1)
+    if (per_wave == 1) {
         pk::rows_par<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows);
-    else
+    } else {
+        /* the per-lane automaton reads split rows best as compact lists */
+        pk::gather_rows<<<dim3((unsigned)(cus * GATHER_BLOCKS_PER_CU)), dim3(256), 0, stream>>>(ga);
         pk::rows_fast<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows, lane_shift);
+    }
     pk::rows_mid<LENIENT><<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(ra, mode, counters,
                                                                                               mid_rows, deep_rows);
     pk::rows_deep<LENIENT><<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);
@@ -308,9 +312,6 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
         pk::scan_rows<pk::TM_LINEAR><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[1], stream) != hipSuccess) return PARASON_ERR_HIP;
 
-    pk::GatherArgs ga{starts, n_traj, mis, seg_off, cap, seg_count, events, mode, counters + 2, split_rows};
-    pk::gather_rows<<<dim3((unsigned)(cus * GATHER_BLOCKS_PER_CU)), dim3(256), 0, stream>>>(ga);
-
     pk::RowArgs ra;
     ra.tok_base = tok_base;
     ra.mis = mis;
@@ -323,10 +324,11 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.events = events;
     ra.tm = h->tm;
     ra.out = row_out;
+    const pk::GatherArgs ga{starts, n_traj, mis, seg_off, cap, seg_count, events, mode, counters + 2, split_rows};
     if (h->cfg.flags & PARASON_CFG_LENIENT_GAPS)
-        launch_rows<true>(ra, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
+        launch_rows<true>(ra, ga, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
     else
-        launch_rows<false>(ra, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
+        launch_rows<false>(ra, ga, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
 
     pk::RewardArgs rw;
     rw.total = out->total;

@@ -719,6 +719,19 @@ __device__ __forceinline__ int32_t wave_incl_scan32(int32_t v, int lane)
     return v;
 }
 
+/* The largest lane j with x (held by lane j) <= f, for x non-decreasing over
+ * the lanes and x of lane 0 <= f (every lane must call it). */
+__device__ __forceinline__ int32_t last_lane_at_most(int32_t x, int32_t f)
+{
+    int32_t lo = 0;
+#pragma unroll
+    for (int step = WAVE / 2; step > 0; step >>= 1) {
+        const int32_t cand = lo + step;
+        lo = __shfl(x, cand, WAVE) <= f ? cand : lo;
+    }
+    return lo;
+}
+
 /* Inclusive scans over the wave's lanes, every lane calling.  The segmented
  * forms restart at lanes with head set; lanes before the chunk's first head
  * continue from carry (the previous chunk's last value). */
@@ -789,7 +802,8 @@ __device__ __forceinline__ int32_t wave_max32(int32_t v)
  *     type of the outline entry it pairs with.  Evaluated level by level,
  *     deepest first, with segmented scans (phase B).
  * Rows holding more than PAR_EVENTS events, nested deeper than PAR_LEVELS,
- * or with a dense segment, go to rows_mid. */
+ * or with a dense segment, go to rows_mid.  Split rows are read from their
+ * segments' lists directly (no gather_rows launch for a small batch). */
 template <bool LENIENT>
 __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restrict__ mode,
                                                int32_t *__restrict__ counters, int32_t *__restrict__ mid_rows)
@@ -809,30 +823,49 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
         if (lane == 0) write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
         return;
     }
-    /* the row's events: one compact list (row positions), or the one list of
-     * a row of a single segment (segment positions) */
+    /* the row's events into LDS, in position order: from its compact list (row
+     * positions), or from its segments' lists (segment positions), gathered
+     * here as gather_rows does for the per-lane kernel */
     const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
     const int64_t g = start + a.mis;
     int32_t m = 0;
-    int64_t base = 0;
-    bool listed = s1 == s0; /* no segment: an empty row, no events */
+    bool held = true;
     if (mode[r] == 1) {
         m = a.seg_count[s0];
-        listed = true;
-    } else if (s1 - s0 == 1 && a.seg_count[s0] <= EV_CAP) {
-        m = a.seg_count[s0];
-        base = 4 * row_first_vec(g) - g;
-        listed = true;
+        held = m <= PAR_EVENTS;
+        const uint32_t *list = a.events + s0 * EV_CAP;
+        for (int32_t i = lane; held && i < m; i += WAVE) {
+            const uint32_t w = list[i];
+            sP[i] = (int32_t)(w >> 4);
+            sC[i] = (int32_t)(w & 15u);
+        }
+    } else {
+        const int64_t vrow0 = row_first_vec(g);
+        for (int64_t c0 = s0; held && c0 < s1; c0 += WAVE) {
+            const int64_t s = c0 + lane;
+            const int32_t cnt = s < s1 ? a.seg_count[s] : 0;
+            const int32_t incl = wave_incl_scan32(cnt, lane);
+            const int32_t excl = incl - cnt;
+            const int32_t total = __shfl(incl, WAVE - 1, WAVE);
+            /* a dense segment (more than EV_CAP tags) or too many events: rows_mid */
+            held = __ballot(cnt > EV_CAP) == 0 && m + total <= PAR_EVENTS;
+            for (int32_t f0 = 0; held && f0 < total; f0 += WAVE) {
+                const int32_t f = f0 + lane;
+                const int32_t j = last_lane_at_most(excl, f);
+                const int32_t first = __shfl(excl, j, WAVE);
+                if (f < total) {
+                    const int64_t seg = c0 + j;
+                    const uint32_t w = a.events[seg * EV_CAP + (f - first)];
+                    sP[m + f] = (int32_t)(4 * (vrow0 + (seg - s0) * SEG_VEC) - g + (int64_t)(w >> 4));
+                    sC[m + f] = (int32_t)(w & 15u);
+                }
+            }
+            m += total;
+        }
     }
-    if (!listed || m > PAR_EVENTS) {
+    if (!held) {
         if (lane == 0) mid_rows[atomicAdd(&counters[0], 1)] = (int32_t)r;
         return;
-    }
-    const uint32_t *list = a.events + s0 * EV_CAP;
-    for (int32_t i = lane; i < m; i += WAVE) {
-        const uint32_t w = list[i];
-        sP[i] = (int32_t)(base + (int64_t)(w >> 4));
-        sC[i] = (int32_t)(w & 15u);
     }
     __syncthreads();
 
@@ -1219,19 +1252,6 @@ struct GatherArgs {
     const int32_t *split_count;
     const int32_t *split_rows;
 };
-
-/* The largest lane j with x (held by lane j) <= f, for x non-decreasing over
- * the lanes and x of lane 0 <= f (every lane must call it). */
-__device__ __forceinline__ int32_t last_lane_at_most(int32_t x, int32_t f)
-{
-    int32_t lo = 0;
-#pragma unroll
-    for (int step = WAVE / 2; step > 0; step >>= 1) {
-        const int32_t cand = lo + step;
-        lo = __shfl(x, cand, WAVE) <= f ? cand : lo;
-    }
-    return lo;
-}
 
 /* Move the events of row `row` (split between scan waves: one list per
  * segment, segment positions) into one list at the start of its slot range,
