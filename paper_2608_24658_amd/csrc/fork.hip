@@ -43,6 +43,21 @@ PackLayout pack_layout(int64_t n, int K)
 
 bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
+/* Exclusive scans of the per-row counts: one block when the rows fit one tile
+ * (pack_single; also n = 0, which only writes the zero totals), otherwise tile
+ * sums, their scan and the per-row offsets. */
+template <int K>
+void launch_pack(const pk::PackScan<K> &ps, int64_t tiles, hipStream_t stream)
+{
+    if (ps.n <= pk::PACK_TILE) {
+        pk::pack_single<K><<<dim3(1), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
+        return;
+    }
+    pk::pack_tiles<K><<<dim3((unsigned)tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
+    pk::pack_top<K><<<dim3(1), dim3(1024), 0, stream>>>(ps, tiles);
+    pk::pack_rows<K><<<dim3((unsigned)tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
+}
+
 }  // namespace
 
 extern "C" {
@@ -119,12 +134,9 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
     ps.over = (int32_t *)(ws + L.over);
 
     const unsigned wave_blocks = (unsigned)std::min<int64_t>((n_rows + 3) / 4, (int64_t)cus * 8);
-    const unsigned tiles = (unsigned)L.tiles;
     if (n_rows > 0) pk::fork_outline<false><<<dim3(wave_blocks), dim3(256), 0, stream>>>(fa);
-    if (n_rows > 0) pk::pack_tiles<2><<<dim3(tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
-    pk::pack_top<2><<<dim3(1), dim3(1024), 0, stream>>>(ps, n_rows > 0 ? L.tiles : 0);
+    launch_pack(ps, L.tiles, stream);
     if (n_rows > 0) {
-        pk::pack_rows<2><<<dim3(tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
         pk::fork_outline<true><<<dim3(wave_blocks), dim3(256), 0, stream>>>(fa);
         const unsigned copy_blocks = (unsigned)(cus * COPY_BLOCKS_PER_CU); /* persistent, tiled over the output */
         pk::fork_copy<<<dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream>>>(fa);
@@ -186,14 +198,9 @@ int parason_join(const parason_handle *h, const int32_t *tokens, const int64_t *
     ps.totals = out->totals;
     ps.over = (int32_t *)(ws + L.over);
 
-    const unsigned tiles = (unsigned)L.tiles;
+    if (n_rows > 0) pk::join_size<<<dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0, stream>>>(ja);
+    launch_pack(ps, L.tiles, stream);
     if (n_rows > 0) {
-        pk::join_size<<<dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0, stream>>>(ja);
-        pk::pack_tiles<1><<<dim3(tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
-    }
-    pk::pack_top<1><<<dim3(1), dim3(1024), 0, stream>>>(ps, n_rows > 0 ? L.tiles : 0);
-    if (n_rows > 0) {
-        pk::pack_rows<1><<<dim3(tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
         const unsigned copy_blocks = (unsigned)(cus * COPY_BLOCKS_PER_CU);
         pk::join_copy<<<dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream>>>(ja);
     }

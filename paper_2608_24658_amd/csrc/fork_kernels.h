@@ -161,6 +161,57 @@ __global__ void __launch_bounds__(PACK_THREADS) pack_rows(PackScan<K> a)
     }
 }
 
+/* The three passes in one block when the rows fit one tile (n <= PACK_TILE):
+ * every thread loads its rows' values once, then offsets, totals and the
+ * capacity check as above. */
+template <int K>
+__global__ void __launch_bounds__(PACK_THREADS) pack_single(PackScan<K> a)
+{
+    __shared__ int64_t part[K][PACK_THREADS / WAVE];
+    const int wv = threadIdx.x / WAVE;
+    const int64_t r0 = (int64_t)threadIdx.x * PACK_ROWS_PER_THREAD;
+    int64_t v[PACK_ROWS_PER_THREAD][K];
+#pragma unroll
+    for (int j = 0; j < PACK_ROWS_PER_THREAD; ++j) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) v[j][k] = r0 + j < a.n ? a.vals[(r0 + j) * K + k] : 0;
+    }
+    int64_t off[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        int64_t s = 0;
+#pragma unroll
+        for (int j = 0; j < PACK_ROWS_PER_THREAD; ++j) s += v[j][k];
+        const int64_t inc = wave_inclusive_scan(s);
+        if ((threadIdx.x & (WAVE - 1)) == WAVE - 1) part[k][wv] = inc;
+        off[k] = inc - s;
+    }
+    __syncthreads();
+    int32_t over = 0;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        int64_t total = 0;
+        for (int w = 0; w < PACK_THREADS / WAVE; ++w) {
+            if (w < wv) off[k] += part[k][w];
+            total += part[k][w];
+        }
+#pragma unroll
+        for (int j = 0; j < PACK_ROWS_PER_THREAD; ++j) {
+            if (r0 + j < a.n) a.out[k][r0 + j] = off[k];
+            off[k] += v[j][k];
+        }
+        over |= total > a.cap[k] ? 1 : 0;
+        if (threadIdx.x == 0) {
+            a.out[k][a.n] = total;
+            if (a.totals) a.totals[k] = total;
+        }
+    }
+    if (threadIdx.x == 0) {
+        if (a.totals) a.totals[K] = over;
+        a.over[0] = over;
+    }
+}
+
 /* ---- fork --------------------------------------------------------------- */
 
 struct ForkArgs {
@@ -403,26 +454,44 @@ __device__ __forceinline__ int64_t find_segment(const int64_t *offs, int64_t cou
     return s;
 }
 
-/* dst[d] = src(d) for d in [d0, d1) with the whole block, U loads in flight
- * per thread; src(d) must be a pure function of d. */
+/* dst[d] = src[idx(d)] for d in [d0, d1), except dst[d_sub] = sub, with the
+ * whole block and U loads in flight per thread.  idx(d) must be a valid index
+ * of src for every d in the range, d_sub included (its load is discarded):
+ * every load is then a plain global load from one buffer, issued before any
+ * of the U results is used. */
 #ifndef PARASON_FILL_UNROLL
-#define PARASON_FILL_UNROLL 4
+#define PARASON_FILL_UNROLL 8
 #endif
-template <class Src>
-__device__ __forceinline__ void block_fill(int32_t *__restrict__ dst, int64_t d0, int64_t d1, const Src &src)
+template <class Idx>
+__device__ __forceinline__ void block_fill(int32_t *__restrict__ dst, int64_t d0, int64_t d1,
+                                           const int32_t *__restrict__ src, const Idx &idx, int64_t d_sub = -1,
+                                           int32_t sub = 0)
 {
     constexpr int U = PARASON_FILL_UNROLL;
-    for (int64_t base = d0; base < d1; base += U * PACK_THREADS) {
+    int64_t base = d0;
+    /* whole steps: no predicates, so the U loads and stores are straight-line
+     * code and each store waits only for its own load */
+    for (; base + U * PACK_THREADS <= d1; base += U * PACK_THREADS) {
+        int32_t v[U];
+#pragma unroll
+        for (int j = 0; j < U; ++j) v[j] = src[idx(base + j * PACK_THREADS + threadIdx.x)];
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+            const int64_t d = base + j * PACK_THREADS + threadIdx.x;
+            dst[d] = d == d_sub ? sub : v[j];
+        }
+    }
+    if (base < d1) { /* the last partial step: positions past d1 load d1 - 1 and store nothing */
         int32_t v[U];
 #pragma unroll
         for (int j = 0; j < U; ++j) {
             const int64_t d = base + j * PACK_THREADS + threadIdx.x;
-            if (d < d1) v[j] = src(d);
+            v[j] = src[idx(d < d1 ? d : d1 - 1)];
         }
 #pragma unroll
         for (int j = 0; j < U; ++j) {
             const int64_t d = base + j * PACK_THREADS + threadIdx.x;
-            if (d < d1) dst[d] = v[j];
+            if (d < d1) dst[d] = d == d_sub ? sub : v[j];
         }
     }
 }
@@ -482,12 +551,15 @@ __global__ void __launch_bounds__(PACK_THREADS) fork_copy(ForkArgs a)
             const int64_t first = (a.lenient && a.seed)
                                       ? entry_text_pos(a, src, a.outl[r], k, L, &found)
                                       : a.outl[r] + 2 + 2 * k + (cs - a.tok_off[r] - k * (L + 1));
-            const int32_t thr = a.thread_id;
             const int64_t end = min(hi, cs + (int64_t)a.ctx_lengths[w]);
-            block_fill(a.ctx_tokens, max(lo, cs), end, [=](int64_t d) {
-                const int64_t off = d - cs;
-                return off < L ? src[off] : (off == L ? thr : src[first + off - L - 1]);
-            });
+            /* context offset off: the row, <Thread> at off = L, then the seed */
+            block_fill(
+                a.ctx_tokens, max(lo, cs), end, src,
+                [=](int64_t d) {
+                    const int64_t off = d - cs;
+                    return off < L ? off : (off == L ? 0 : first + off - L - 1);
+                },
+                cs + L, a.thread_id);
         }
     }
 }
@@ -565,9 +637,8 @@ __global__ void __launch_bounds__(PACK_THREADS) join_copy(JoinArgs a)
             int64_t pos = os;
             if (!a.append_only) {
                 const int32_t *src = a.tokens + a.starts[i];
-                if (pos + L > lo) block_fill(a.out_tokens, max(lo, pos), min(hi, pos + L), [=](int64_t d) {
-                    return src[d - pos];
-                });
+                if (pos + L > lo)
+                    block_fill(a.out_tokens, max(lo, pos), min(hi, pos + L), src, [=](int64_t d) { return d - pos; });
                 pos += L;
             }
             for (int64_t w = a.worker_off[i]; w < a.worker_off[i + 1] && pos < hi; ++w) {
@@ -575,9 +646,8 @@ __global__ void __launch_bounds__(PACK_THREADS) join_copy(JoinArgs a)
                 const int64_t tail = wl > L ? wl - L : 0;
                 if (pos + tail > lo) {
                     const int32_t *src = a.wtokens + a.wstarts[w] + L;
-                    block_fill(a.out_tokens, max(lo, pos), min(hi, pos + tail), [=](int64_t d) {
-                        return src[d - pos];
-                    });
+                    block_fill(a.out_tokens, max(lo, pos), min(hi, pos + tail), src,
+                               [=](int64_t d) { return d - pos; });
                 }
                 pos += tail;
             }

@@ -201,6 +201,52 @@ def test_fork_join_scattered_synthetic(dev):
     check_join(dev, px, rows, res, seqs, SCATTERED, rng, F.JOIN_CLOSE_PARALLEL | F.JOIN_APPEND_ONLY, "sc join")
 
 
+def short_rows(tags, n, rng):
+    """n short rows: well-formed outlines of 1..4 entries, malformed ones and
+    empty rows, so that many rows give few tokens."""
+    base = hand_rows(tags, [7, 8, 9, 1000, 150000])[:17]
+    rows = []
+    for i in range(n):
+        k = int(rng.integers(0, 6))
+        if k < 4:
+            names = "think t%d Par Out " % int(rng.integers(1, 9)) + " ".join(
+                ("Sub t%d /Sub" if rng.random() < 0.5 else "Tri t%d /Tri") % int(rng.integers(1, 5))
+                for _ in range(k + 1)) + " /Out"
+            rows.append([tags[c - 1] if c else 7 for c in GP.parse_names(names)])
+        else:
+            rows.append(list(base[int(rng.integers(0, len(base)))]))
+    return rows
+
+
+@pytest.mark.parametrize("seed", [True, False], ids=["seed", "noseed"])
+def test_fork_join_many_rows(dev, seed):
+    """More rows than one scan tile (4096): the scans of the worker and token
+    counts take three passes instead of one block."""
+    log("case fork many rows seed=%s" % seed)
+    rng = np.random.default_rng(12)
+    px = PX.Parason(CONTIG)
+    rows = short_rows(CONTIG, 9001, rng)
+    res, _ = check_fork(dev, px, rows, CONTIG, seed, rng, "many rows")
+    assert res["worker_off"][-1] > 9001
+    seqs = worker_sequences(res, CONTIG, rng, p_bad=0.05)
+    check_join(dev, px, rows, res, seqs, CONTIG, rng, F.JOIN_CLOSE_PARALLEL, "many rows join")
+
+
+def test_fork_join_no_rows(dev):
+    log("case fork/join of zero rows")
+    px = PX.Parason(CONTIG)
+    z32, z64 = torch.zeros(0, dtype=torch.int32, device=dev), torch.zeros(0, dtype=torch.int64, device=dev)
+    got = px.fork(torch.zeros(1, dtype=torch.int32, device=dev), z64, z32, seed=True)
+    torch.cuda.synchronize()
+    assert list(got["totals"].cpu().numpy()) == [0, 0, 0]
+    assert got["worker_off"].cpu().numpy().tolist() == [0]
+    got = px.join(torch.zeros(1, dtype=torch.int32, device=dev), z64, z32, torch.zeros(1, dtype=torch.int64, device=dev),
+                  torch.zeros(1, dtype=torch.int32, device=dev), z64, z32)
+    torch.cuda.synchronize()
+    assert list(got["totals"].cpu().numpy()) == [0, 0]
+    assert got["starts"].cpu().numpy().tolist() == [0]
+
+
 def test_fork_capacity_and_bad_rows(dev):
     log("case fork capacity / bad rows")
     px = PX.Parason(CONTIG)
