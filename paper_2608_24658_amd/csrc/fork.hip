@@ -14,9 +14,10 @@ namespace {
 
 constexpr int COPY_BLOCKS_PER_CU = 8;
 
-/* Workspace of fork (K = 2 counts per row) or join (K = 1). */
+/* Workspace of fork (K = 3 counts per row: workers, context tokens, copy
+ * units) or join (K = 1). */
 struct PackLayout {
-    size_t counts, outl, tile_sum, tile_off, tok_off, over, end;
+    size_t counts, outl, tile_sum, tile_off, tok_off, unit_off, over, end;
     int64_t tiles;
 };
 
@@ -35,6 +36,8 @@ PackLayout pack_layout(int64_t n, int K)
     o = align_up(o + (size_t)L.tiles * K * sizeof(int64_t));
     L.tok_off = o;
     o = align_up(o + (size_t)(n + 1) * sizeof(int64_t));
+    L.unit_off = o;
+    if (K == 3) o = align_up(o + (size_t)(n + 1) * sizeof(int64_t));
     L.over = o;
     o = align_up(o + sizeof(int32_t));
     L.end = o;
@@ -66,7 +69,7 @@ int parason_fork_workspace_size(int64_t n_rows, size_t *bytes)
 {
     if (!bytes) return PARASON_ERR_NULL;
     if (n_rows < 0 || n_rows > INT32_MAX) return PARASON_ERR_SIZE;
-    *bytes = pack_layout(n_rows, 2).end;
+    *bytes = pack_layout(n_rows, 3).end;
     return PARASON_OK;
 }
 
@@ -92,7 +95,7 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
         return PARASON_ERR_NULL;
     if (out->ctx_capacity > 0 && !out->ctx_tokens) return PARASON_ERR_NULL;
     if ((tokens && !aligned(tokens, 4)) || !aligned(workspace, abi::ALIGN)) return PARASON_ERR_ALIGN;
-    const PackLayout L = pack_layout(n_rows, 2);
+    const PackLayout L = pack_layout(n_rows, 3);
     if (workspace_bytes < L.end) return PARASON_ERR_WORKSPACE;
     const int cus = cu_count();
     if (cus <= 0) return PARASON_ERR_DEVICE;
@@ -113,6 +116,7 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
     fa.outl = (int32_t *)(ws + L.outl);
     fa.worker_off = out->worker_off;
     fa.tok_off = (const int64_t *)(ws + L.tok_off);
+    fa.unit_off = (const int64_t *)(ws + L.unit_off);
     fa.over = (const int32_t *)(ws + L.over);
     fa.ctx_starts = out->ctx_starts;
     fa.ctx_lengths = out->ctx_lengths;
@@ -121,16 +125,19 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
     fa.ctx_kind = out->ctx_kind;
     fa.ctx_tokens = out->ctx_tokens;
 
-    pk::PackScan<2> ps;
+    pk::PackScan<3> ps;
     ps.vals = fa.counts;
     ps.n = n_rows;
     ps.tile_sum = (int64_t *)(ws + L.tile_sum);
     ps.tile_off = (int64_t *)(ws + L.tile_off);
     ps.out[0] = out->worker_off;
     ps.out[1] = (int64_t *)(ws + L.tok_off);
+    ps.out[2] = (int64_t *)(ws + L.unit_off);
     ps.cap[0] = out->max_workers;
     ps.cap[1] = out->ctx_capacity;
+    ps.cap[2] = INT64_MAX; /* internal: never over */
     ps.totals = out->totals;
+    ps.report = 2; /* totals = workers, context tokens, over */
     ps.over = (int32_t *)(ws + L.over);
 
     const unsigned wave_blocks = (unsigned)std::min<int64_t>((n_rows + 3) / 4, (int64_t)cus * 8);
@@ -196,6 +203,7 @@ int parason_join(const parason_handle *h, const int32_t *tokens, const int64_t *
     ps.out[0] = out->starts;
     ps.cap[0] = out->capacity;
     ps.totals = out->totals;
+    ps.report = 1;
     ps.over = (int32_t *)(ws + L.over);
 
     if (n_rows > 0) pk::join_size<<<dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0, stream>>>(ja);

@@ -12,32 +12,34 @@
  *                        ballots and checking each against the one before it
  *                        (entries open, hold text, close, back to back).
  *                        Writes the row's worker and token counts.
- *   pack_tiles/top/rows  exclusive scans of those counts (worker_off and the
- *                        context token offsets), totals and the capacity check.
+ *   pack_single, or      exclusive scans of those counts (worker_off, the
+ *   pack_tiles/top/rows  context token offsets and the copy units), totals
+ *                        and the capacity check: one block up to 4096 rows.
  *   fork_outline<true>   the same walk again, now writing each worker's record
  *                        (row, entry, kind, context start and length).
- *   fork_copy            tiled over the context tokens: every block step
- *                        fills 4096 consecutive tokens; a 64-way wave search
- *                        over the context starts finds the first worker, each
- *                        token is taken from the row, the <Thread> id or the
- *                        entry's text.
+ *   fork_copy            tiled over copy units (row tokens times groups of
+ *                        up to eight workers) by waves: every wave step loads
+ *                        1024 row tokens once and stores them into the
+ *                        contexts of the group's workers, then their <Thread>
+ *                        and seeds; it finds its row by a 64-way search over
+ *                        the unit offsets.
  * join
  *   join_size            one thread per row: joined length and thread checks.
  *   pack_*               exclusive scan of the joined lengths.
  *   join_copy            tiled the same way over the joined tokens: the row,
- *                        each worker's <Thread> ... </Thread> span, and
- *                        </Parallel>.
+ *                        each worker's <Thread> ... </Thread> span (positions
+ *                        of 64 workers from one wave scan), and </Parallel>.
  *
  * With PARASON_CFG_LENIENT_GAPS Text may stand between <Parallel> and
  * <Outlines>, after <Outlines>, between entries and before </Outlines>: the
  * walk then checks only the order of the tags, takes the entry text lengths
  * from the tag positions (a wave prefix scan gives each worker's seed offset,
- * in both modes), and fork_copy finds entry k's text by a ballot search of the
- * outline.
+ * in both modes), and fork_copy finds the texts of a group's entries by one
+ * ballot scan of the outline.
  *
  * All copies are dword-granular and coalesced (rows and contexts start at any
- * element offset); they are HBM-bound.  Tiling the output keeps every block's
- * work the same size however long the rows are.
+ * element offset).  Tiling keeps every wave step's work bounded however long
+ * the rows are: at most 1024 loads and, in fork_copy, eight stores of each.
  */
 #pragma once
 #include "device_common.h"
@@ -48,6 +50,7 @@ constexpr int PACK_THREADS = 256;
 constexpr int PACK_ROWS_PER_THREAD = 16;
 constexpr int PACK_TILE = PACK_THREADS * PACK_ROWS_PER_THREAD;
 constexpr int CHUNK = 4 * WAVE; /* tokens per wave step of the outline walk */
+constexpr int COPY_GROUP = 8;   /* worker contexts fork_copy writes from one read of a row tile */
 
 /* ---- exclusive scans of K int64 values per row -------------------------- */
 
@@ -59,7 +62,8 @@ struct PackScan {
     int64_t *tile_off;     /* [tiles][K] */
     int64_t *out[K];       /* [n + 1] each: exclusive offsets, out[k][n] = total */
     int64_t cap[K];        /* totals above these set *over */
-    int64_t *totals;       /* optional: [K + 1] totals and the over flag, for the caller */
+    int64_t *totals;       /* optional: totals[0 .. report) and then the over flag, for the caller */
+    int report;            /* totals reported (the first `report` of the K) */
     int32_t *over;         /* workspace copy of the over flag */
 };
 
@@ -122,9 +126,9 @@ __global__ void __launch_bounds__(1024) pack_top(PackScan<K> a, int64_t tiles)
         for (int k = 0; k < K; ++k) {
             a.out[k][a.n] = carry[k];
             over |= carry[k] > a.cap[k] ? 1 : 0;
-            if (a.totals) a.totals[k] = carry[k];
+            if (a.totals && k < a.report) a.totals[k] = carry[k];
         }
-        if (a.totals) a.totals[K] = over;
+        if (a.totals) a.totals[a.report] = over;
         a.over[0] = over;
     }
 }
@@ -203,11 +207,11 @@ __global__ void __launch_bounds__(PACK_THREADS) pack_single(PackScan<K> a)
         over |= total > a.cap[k] ? 1 : 0;
         if (threadIdx.x == 0) {
             a.out[k][a.n] = total;
-            if (a.totals) a.totals[k] = total;
+            if (a.totals && k < a.report) a.totals[k] = total;
         }
     }
     if (threadIdx.x == 0) {
-        if (a.totals) a.totals[K] = over;
+        if (a.totals) a.totals[a.report] = over;
         a.over[0] = over;
     }
 }
@@ -224,11 +228,12 @@ struct ForkArgs {
     bool lenient;           /* PARASON_CFG_LENIENT_GAPS */
     int32_t thread_id;      /* token id of <Thread> */
     uint32_t *status;       /* [n] PARASON_PACK_* */
-    int64_t *counts;        /* [n][2]: workers, context tokens */
+    int64_t *counts;        /* [n][3]: workers, context tokens, copy units */
     int32_t *outl;          /* [n]: position of the outline's <Outlines> */
     /* filled in by the scan, read by the write pass and the copy */
     const int64_t *worker_off;
     const int64_t *tok_off;
+    const int64_t *unit_off; /* [n + 1]: scan of the copy units (fork_copy) */
     const int32_t *over;
     int64_t *ctx_starts;
     int32_t *ctx_lengths, *ctx_row, *ctx_entry, *ctx_kind;
@@ -291,7 +296,7 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
         const int32_t L = a.lengths[i];
         int64_t o;
         if (WRITE) {
-            if (a.status[i] != 0 || a.counts[2 * i] == 0) continue;
+            if (a.status[i] != 0 || a.counts[3 * i] == 0) continue;
             o = a.outl[i];
         } else {
             uint32_t st = 0;
@@ -318,8 +323,9 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
             if (st != 0) {
                 if (lane == 0) {
                     a.status[i] = st;
-                    a.counts[2 * i] = 0;
-                    a.counts[2 * i + 1] = 0;
+                    a.counts[3 * i] = 0;
+                    a.counts[3 * i + 1] = 0;
+                    a.counts[3 * i + 2] = 0;
                     a.outl[i] = -1;
                 }
                 continue;
@@ -419,8 +425,10 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
             }
             if (lane == 0) {
                 a.status[i] = st;
-                a.counts[2 * i] = st == 0 ? n_e : 0;
-                a.counts[2 * i + 1] = st == 0 ? toks : 0;
+                a.counts[3 * i] = st == 0 ? n_e : 0;
+                a.counts[3 * i + 1] = st == 0 ? toks : 0;
+                /* fork_copy reads the row once per group of COPY_GROUP workers */
+                a.counts[3 * i + 2] = st == 0 ? (n_e + COPY_GROUP - 1) / COPY_GROUP * (int64_t)L : 0;
                 a.outl[i] = (int32_t)o;
             }
         }
@@ -429,137 +437,176 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
 
 /* ---- tiled copies -------------------------------------------------------- */
 
-constexpr int64_t TILE = 16 * PACK_THREADS; /* output tokens per block step */
+/* The copies are tiled over their output by waves: each wave step covers
+ * WTILE consecutive output positions (WU per lane, all loads issued before
+ * the first store), finds the row holding the first of them by a 64-way
+ * search, and walks the pieces of that range.  Waves work independently, so
+ * the chains of dependent loads of many tiles (search, row and worker
+ * records, data) overlap on every CU. */
+#ifndef PARASON_COPY_WU
+#define PARASON_COPY_WU 16
+#endif
+constexpr int WU = PARASON_COPY_WU;      /* loads per lane per wave step */
+constexpr int64_t WTILE = WU * WAVE;     /* output positions per wave step */
+constexpr int COPY_WAVES = PACK_THREADS / WAVE;
 
 /* Largest index s in [0, count) with offs[s] <= x (offs ascending, offs[0] <= x),
- * by wave 0 in 64-way rounds; the result is returned to every thread. */
-__device__ __forceinline__ int64_t find_segment(const int64_t *offs, int64_t count, int64_t x, int64_t *lds)
+ * by one wave in 64-way rounds; the result is returned to every lane. */
+__device__ __forceinline__ int64_t wave_find(const int64_t *offs, int64_t count, int64_t x, int lane)
 {
-    if (threadIdx.x < WAVE) {
-        const int lane = threadIdx.x;
-        int64_t lo = 0, hi = count;
-        while (hi - lo > 1) {
-            const int64_t step = (hi - lo + WAVE - 1) / WAVE;
-            const int64_t idx = lo + lane * step;
-            const uint64_t m = __ballot(idx < hi && offs[idx] <= x);
-            const int64_t last = 63 - __builtin_clzll(m | 1ull);
-            lo = lo + last * step;
-            hi = min(hi, lo + step);
-        }
-        if (lane == 0) lds[0] = lo;
+    int64_t lo = 0, hi = count;
+    while (hi - lo > 1) {
+        const int64_t step = (hi - lo + WAVE - 1) / WAVE;
+        const int64_t idx = lo + lane * step;
+        const uint64_t m = __ballot(idx < hi && offs[idx] <= x);
+        const int64_t last = 63 - __builtin_clzll(m | 1ull);
+        lo = lo + last * step;
+        hi = min(hi, lo + step);
     }
-    __syncthreads();
-    const int64_t s = lds[0];
-    __syncthreads();
-    return s;
+    return lo;
 }
 
-/* dst[d] = src[idx(d)] for d in [d0, d1), except dst[d_sub] = sub, with the
- * whole block and U loads in flight per thread.  idx(d) must be a valid index
- * of src for every d in the range, d_sub included (its load is discarded):
- * every load is then a plain global load from one buffer, issued before any
- * of the U results is used. */
-#ifndef PARASON_FILL_UNROLL
-#define PARASON_FILL_UNROLL 8
-#endif
-template <class Idx>
-__device__ __forceinline__ void block_fill(int32_t *__restrict__ dst, int64_t d0, int64_t d1,
-                                           const int32_t *__restrict__ src, const Idx &idx, int64_t d_sub = -1,
-                                           int32_t sub = 0)
+/* Elements lane + j * WAVE (j < WU) of a range of n <= WTILE: how many of
+ * them this lane holds. */
+__device__ __forceinline__ int lane_count(int64_t n, int lane)
 {
-    constexpr int U = PARASON_FILL_UNROLL;
-    int64_t base = d0;
-    /* whole steps: no predicates, so the U loads and stores are straight-line
-     * code and each store waits only for its own load */
-    for (; base + U * PACK_THREADS <= d1; base += U * PACK_THREADS) {
-        int32_t v[U];
+    return n > lane ? (int)((n - lane + WAVE - 1) / WAVE) : 0;
+}
+
+/* dst[o_k + p] = src[p] for p in [p0, p1) and every k < nd, by one wave
+ * (p1 - p0 <= WTILE): each source token is loaded once and stored nd times;
+ * o_k is lane k's value of o.  One base address per lane, constant offsets. */
+__device__ __forceinline__ void wave_copy_multi(int32_t *__restrict__ dst, int64_t o, int nd, int64_t p0, int64_t p1,
+                                                const int32_t *__restrict__ src, int lane)
+{
+    const int jm = lane_count(p1 - p0, lane);
+    const int32_t *sp = src + p0 + lane;
+    int32_t v[WU];
 #pragma unroll
-        for (int j = 0; j < U; ++j) v[j] = src[idx(base + j * PACK_THREADS + threadIdx.x)];
+    for (int j = 0; j < WU; ++j) v[j] = j < jm ? sp[j * WAVE] : 0;
+    for (int k = 0; k < nd; ++k) {
+        int32_t *dp = dst + __shfl(o, k, WAVE) + p0 + lane;
 #pragma unroll
-        for (int j = 0; j < U; ++j) {
-            const int64_t d = base + j * PACK_THREADS + threadIdx.x;
-            dst[d] = d == d_sub ? sub : v[j];
-        }
-    }
-    if (base < d1) { /* the last partial step: positions past d1 load d1 - 1 and store nothing */
-        int32_t v[U];
-#pragma unroll
-        for (int j = 0; j < U; ++j) {
-            const int64_t d = base + j * PACK_THREADS + threadIdx.x;
-            v[j] = src[idx(d < d1 ? d : d1 - 1)];
-        }
-#pragma unroll
-        for (int j = 0; j < U; ++j) {
-            const int64_t d = base + j * PACK_THREADS + threadIdx.x;
-            if (d < d1) dst[d] = d == d_sub ? sub : v[j];
-        }
+        for (int j = 0; j < WU; ++j)
+            if (j < jm) dp[j * WAVE] = v[j];
     }
 }
 
-/* Position of the first text token of entry k of the outline that starts at
- * o in the row src of length L (its k-th <Subtask>/<Trial> tag, plus one), by
- * wave 0 in 64-token ballot rounds; returned to every thread.  The row's
- * outline passed the walk, so entry k exists. */
-__device__ __forceinline__ int64_t entry_text_pos(const ForkArgs &a, const int32_t *src, int64_t o, int64_t k,
-                                                  int64_t L, int64_t *lds)
+/* dst[d] = src[d - shift] for d in [d0, d1), by one wave (d1 - d0 <= WTILE). */
+__device__ __forceinline__ void wave_copy(int32_t *__restrict__ dst, int64_t d0, int64_t d1,
+                                          const int32_t *__restrict__ src, int64_t shift, int lane)
 {
-    if (threadIdx.x < WAVE) {
-        const int lane = threadIdx.x;
-        const bool contig = a.tm.contiguous != 0;
-        int64_t seen = 0, pos = -1;
-        for (int64_t lo = o + 1; lo < L - 1 && pos < 0; lo += WAVE) {
-            const int64_t p = lo + lane;
-            const uint32_t c = p < L - 1 ? classify(a.tm, src[p], contig) : C_TEXT;
-            const bool open = c == C_SUB || c == C_TRI;
-            const uint64_t b = __ballot(open);
-            const int64_t cnt = __popcll(b);
-            if (seen + cnt > k) {
-                const uint32_t rank =
-                    __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
-                const uint64_t hit = __ballot(open && (int64_t)rank == k - seen);
-                pos = lo + __builtin_ctzll(hit) + 1;
-            }
-            seen += cnt;
-        }
-        if (lane == 0) lds[0] = pos < 0 ? 0 : pos;
+    const int jm = lane_count(d1 - d0, lane);
+    const int32_t *sp = src + (d0 - shift) + lane;
+    int32_t *dp = dst + d0 + lane;
+    int32_t v[WU];
+#pragma unroll
+    for (int j = 0; j < WU; ++j) v[j] = j < jm ? sp[j * WAVE] : 0;
+#pragma unroll
+    for (int j = 0; j < WU; ++j)
+        if (j < jm) dp[j * WAVE] = v[j];
+}
+
+/* A worker context's tail at dst[d0 .. d1): sub (the <Thread> id) at d0, then
+ * src[f ..] (the entry's text), by one wave in steps of WTILE.  f >= 1: the
+ * element before the text (its opening tag) is loaded for d0 and replaced. */
+__device__ __forceinline__ void wave_tail(int32_t *__restrict__ dst, int64_t d0, int64_t d1,
+                                          const int32_t *__restrict__ src, int64_t f, int32_t sub, int lane)
+{
+    for (int64_t base = 0; base < d1 - d0; base += WTILE) {
+        const int jm = lane_count(min(d1 - d0 - base, WTILE), lane);
+        const int32_t *sp = src + (f - 1) + base + lane;
+        int32_t *dp = dst + d0 + base + lane;
+        int32_t v[WU];
+#pragma unroll
+        for (int j = 0; j < WU; ++j) v[j] = j < jm ? sp[j * WAVE] : 0;
+        if (base == 0 && lane == 0) v[0] = sub;
+#pragma unroll
+        for (int j = 0; j < WU; ++j)
+            if (j < jm) dp[j * WAVE] = v[j];
     }
-    __syncthreads();
-    const int64_t f = lds[0];
-    __syncthreads();
+}
+
+/* Positions of the first text tokens of entries ea .. ea + nd - 1 of the
+ * outline that starts at o in the row src of length L (each entry's
+ * <Subtask>/<Trial> tag plus one), found by one wave in 64-token ballot
+ * rounds; lane k < nd receives entry ea + k's.  Used with lenient gaps, where
+ * gaps break the closed form of the position.  slot: COPY_GROUP int64 of LDS
+ * owned by the wave.  The row's outline passed the walk, so the entries exist. */
+__device__ __forceinline__ int64_t group_text_pos(const ForkArgs &a, const int32_t *src, int64_t o, int64_t L,
+                                                  int64_t ea, int nd, int64_t *slot, int lane)
+{
+    const bool contig = a.tm.contiguous != 0;
+    int64_t seen = 0;
+    for (int64_t lo = o + 1; lo < L - 1 && seen < ea + nd; lo += WAVE) {
+        const int64_t p = lo + lane;
+        const uint32_t c = p < L - 1 ? classify(a.tm, src[p], contig) : C_TEXT;
+        const bool open = c == C_SUB || c == C_TRI;
+        const uint64_t b = __ballot(open);
+        const int64_t rk =
+            seen + __builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+        if (open && rk >= ea && rk < ea + nd) slot[rk - ea] = p + 1;
+        seen += __popcll(b);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int64_t f = lane < nd ? slot[lane] : 0;
+    __builtin_amdgcn_wave_barrier(); /* slot is rewritten by the next group */
     return f;
 }
 
-/* Contexts, tiled over their tokens: each block step fills TILE consecutive
- * context tokens, starting from the worker that holds the first of them. */
+/* Contexts, tiled over copy units: a forked row of length L with k workers
+ * has ceil(k / COPY_GROUP) * L units, one per row token and group of up to
+ * COPY_GROUP workers (unit_off is their scan).  A wave step takes WTILE
+ * consecutive units: it loads those row tokens once and stores them into the
+ * contexts of the group's workers; the step that reaches the end of the row
+ * also writes the group's <Thread> tokens and seeds.  The row is read from
+ * memory once per group, not once per worker. */
 __global__ void __launch_bounds__(PACK_THREADS) fork_copy(ForkArgs a)
 {
-    __shared__ int64_t found;
+    __shared__ int64_t slots[COPY_WAVES][COPY_GROUP];
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int wv = threadIdx.x / WAVE;
     if (a.over[0]) return;
-    const int64_t W = a.worker_off[a.n];
-    const int64_t T = a.tok_off[a.n];
-    for (int64_t lo = (int64_t)blockIdx.x * TILE; lo < T; lo += (int64_t)gridDim.x * TILE) {
-        const int64_t hi = min(lo + TILE, T);
-        for (int64_t w = find_segment(a.ctx_starts, W, lo, &found); w < W; ++w) {
-            const int64_t cs = a.ctx_starts[w];
-            if (cs >= hi) break;
-            const int64_t r = a.ctx_row[w];
-            const int64_t L = a.lengths[r];
-            const int32_t *src = a.tokens + a.starts[r];
-            const int64_t k = a.ctx_entry[w];
-            /* first text token of entry k: without gaps, o + 2 + 2k + the texts
-             * before it (see fork_outline); with gaps, searched */
-            const int64_t first = (a.lenient && a.seed)
-                                      ? entry_text_pos(a, src, a.outl[r], k, L, &found)
-                                      : a.outl[r] + 2 + 2 * k + (cs - a.tok_off[r] - k * (L + 1));
-            const int64_t end = min(hi, cs + (int64_t)a.ctx_lengths[w]);
-            /* context offset off: the row, <Thread> at off = L, then the seed */
-            block_fill(
-                a.ctx_tokens, max(lo, cs), end, src,
-                [=](int64_t d) {
-                    const int64_t off = d - cs;
-                    return off < L ? off : (off == L ? 0 : first + off - L - 1);
-                },
-                cs + L, a.thread_id);
+    const int64_t UT = a.unit_off[a.n];
+    const int64_t NW = (int64_t)gridDim.x * COPY_WAVES;
+    for (int64_t t = (int64_t)blockIdx.x * COPY_WAVES + wv; t * WTILE < UT; t += NW) {
+        const int64_t lo = t * WTILE, hi = min(lo + WTILE, UT);
+        for (int64_t r = wave_find(a.unit_off, a.n, lo, lane); r < a.n; ++r) {
+            /* the row's records in one round of loads, before any branch */
+            const int64_t uo = a.unit_off[r], ue = a.unit_off[r + 1];
+            const int64_t L = a.lengths[r], g0 = a.starts[r];
+            const int64_t w0 = a.worker_off[r], w1 = a.worker_off[r + 1];
+            const int64_t o = a.outl[r], to = a.tok_off[r];
+            if (uo >= hi) break;
+            if (ue <= lo) continue; /* no units (not forked), or all before the tile */
+            const int32_t *src = a.tokens + g0;
+            for (int64_t g = (max(lo, uo) - uo) / L; uo + g * L < min(hi, ue); ++g) {
+                const int64_t gs = uo + g * L;
+                const int64_t p0 = max(lo, gs) - gs, p1 = min(hi, gs + L) - gs;
+                const int64_t wa = w0 + g * COPY_GROUP;
+                const int nd = (int)min((int64_t)COPY_GROUP, w1 - wa);
+                /* lane k: worker wa + k */
+                const int64_t cs = lane < nd ? a.ctx_starts[wa + lane] : 0;
+                const int64_t len = lane < nd ? (int64_t)a.ctx_lengths[wa + lane] : 0;
+                wave_copy_multi(a.ctx_tokens, cs, nd, p0, p1, src, lane);
+                if (p1 < L) continue;
+                /* the group's tails: <Thread>, then entry e's text when seeding;
+                 * workers are numbered entry by entry, so worker wa + k runs
+                 * entry g * COPY_GROUP + k */
+                const int64_t e = g * COPY_GROUP + lane;
+                /* first text token of entry e: without gaps, o + 2 + 2e + the texts
+                 * before it (see fork_outline); with gaps, searched */
+                const int64_t ft = (a.lenient && a.seed)
+                                       ? group_text_pos(a, src, o, L, g * COPY_GROUP, nd, slots[wv], lane)
+                                       : o + 2 + 2 * e + (cs - to - e * (L + 1));
+                for (int k = 0; k < nd; ++k) {
+                    const int64_t c = __shfl(cs, k, WAVE);
+                    wave_tail(a.ctx_tokens, c + L, c + __shfl(len, k, WAVE), src, __shfl(ft, k, WAVE), a.thread_id,
+                              lane);
+                }
+            }
         }
     }
 }
@@ -620,38 +667,50 @@ __global__ void __launch_bounds__(256) join_size(JoinArgs a)
     a.out_lengths[i] = (int32_t)tot;
 }
 
-/* Joined rows, tiled over their tokens like fork_copy; inside a row the
- * pieces (the row, each worker's span, </Parallel>) are walked in order. */
+/* Joined rows, tiled over their tokens by waves like fork_copy.  Inside a
+ * row the pieces are the row, each worker's span (its sequence from the
+ * <Thread> after the row on) and </Parallel>; the span positions of 64
+ * workers at a time come from one wave prefix scan of their lengths. */
 __global__ void __launch_bounds__(PACK_THREADS) join_copy(JoinArgs a)
 {
-    __shared__ int64_t found;
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int wv = threadIdx.x / WAVE;
     if (a.over[0]) return;
     const int64_t T = a.out_starts[a.n];
-    for (int64_t lo = (int64_t)blockIdx.x * TILE; lo < T; lo += (int64_t)gridDim.x * TILE) {
-        const int64_t hi = min(lo + TILE, T);
-        for (int64_t i = find_segment(a.out_starts, a.n, lo, &found); i < a.n; ++i) {
-            const int64_t os = a.out_starts[i];
+    const int64_t NW = (int64_t)gridDim.x * COPY_WAVES;
+    for (int64_t t = (int64_t)blockIdx.x * COPY_WAVES + wv; t * WTILE < T; t += NW) {
+        const int64_t lo = t * WTILE, hi = min(lo + WTILE, T);
+        for (int64_t i = wave_find(a.out_starts, a.n, lo, lane); i < a.n; ++i) {
+            /* the row's records in one round of loads, before any branch */
+            const int64_t os = a.out_starts[i], len = a.out_len64[i];
+            const int64_t L = a.lengths[i], g0 = a.starts[i];
+            const int64_t wb = a.worker_off[i], we = a.worker_off[i + 1];
             if (os >= hi) break;
-            if (a.out_len64[i] == 0) continue;
-            const int64_t L = a.lengths[i];
+            if (len == 0) continue;
             int64_t pos = os;
             if (!a.append_only) {
-                const int32_t *src = a.tokens + a.starts[i];
-                if (pos + L > lo)
-                    block_fill(a.out_tokens, max(lo, pos), min(hi, pos + L), src, [=](int64_t d) { return d - pos; });
+                if (pos + L > lo) wave_copy(a.out_tokens, max(lo, pos), min(hi, pos + L), a.tokens + g0, pos, lane);
                 pos += L;
             }
-            for (int64_t w = a.worker_off[i]; w < a.worker_off[i + 1] && pos < hi; ++w) {
-                const int64_t wl = a.wlengths[w];
+            for (int64_t w = wb; w < we && pos < hi; w += WAVE) {
+                const bool in = w + lane < we;
+                const int64_t wl = in ? (int64_t)a.wlengths[w + lane] : 0;
+                const int64_t ws = in ? a.wstarts[w + lane] : 0;
                 const int64_t tail = wl > L ? wl - L : 0;
-                if (pos + tail > lo) {
-                    const int32_t *src = a.wtokens + a.wstarts[w] + L;
-                    block_fill(a.out_tokens, max(lo, pos), min(hi, pos + tail), src,
-                               [=](int64_t d) { return d - pos; });
+                const int64_t incl = wave_incl_scan(tail, lane);
+                const int64_t at = pos + incl - tail; /* this lane's span in the joined row */
+                uint64_t m = __ballot(in && tail > 0 && at < hi && at + tail > lo);
+                while (m) {
+                    const int k = __builtin_ctzll(m);
+                    m &= m - 1;
+                    const int64_t s0 = __shfl(at, k, WAVE);
+                    const int64_t tl = __shfl(tail, k, WAVE);
+                    wave_copy(a.out_tokens, max(lo, s0), min(hi, s0 + tl), a.wtokens + __shfl(ws, k, WAVE) + L, s0,
+                              lane);
                 }
-                pos += tail;
+                pos += __shfl(incl, WAVE - 1, WAVE);
             }
-            if (a.close && pos >= lo && pos < hi && threadIdx.x == 0) a.out_tokens[pos] = a.end_par_id;
+            if (a.close && pos >= lo && pos < hi && lane == 0) a.out_tokens[pos] = a.end_par_id;
         }
     }
 }
