@@ -141,13 +141,20 @@ struct SegCursor {
     int32_t len;
     bool loaded;
 
+    /* Called by the whole wave. */
     __device__ void seek(int64_t s, int64_t n)
     {
-        /* the row holding s: seg_off[row] <= s < seg_off[row + 1] */
+        /* the row holding s: the last row with seg_off[row] <= s, by a 64-way
+         * search (each round one load per lane), so that a wave's first load
+         * waits for log64(n) dependent loads, not log2(n) */
+        const int lane = threadIdx.x & (WAVE - 1);
         int64_t lo = 0, hi = n;
         while (hi - lo > 1) {
-            int64_t mid = (lo + hi) >> 1;
-            if (seg_off[mid] <= s) lo = mid; else hi = mid;
+            const int64_t step = (hi - lo + WAVE - 1) / WAVE;
+            const int64_t idx = lo + lane * step;
+            const uint64_t m = __ballot(idx < hi && seg_off[idx] <= s);
+            lo += (63 - __builtin_clzll(m | 1ull)) * step;
+            hi = min(hi, lo + step);
         }
         row = uniform64(lo);
         row_first = uniform64(seg_off[row]);
