@@ -49,7 +49,11 @@ namespace pk {
 constexpr int PACK_THREADS = 256;
 constexpr int PACK_ROWS_PER_THREAD = 16;
 constexpr int PACK_TILE = PACK_THREADS * PACK_ROWS_PER_THREAD;
-constexpr int CHUNK = 4 * WAVE; /* tokens per wave step of the outline walk */
+#ifndef PARASON_OUTLINE_LOADS
+#define PARASON_OUTLINE_LOADS 4
+#endif
+constexpr int CHUNK_J = PARASON_OUTLINE_LOADS; /* loads per lane per step of the outline walk */
+constexpr int CHUNK = CHUNK_J * WAVE;          /* tokens per wave step of the outline walk */
 constexpr int COPY_GROUP = 8;   /* worker contexts fork_copy writes from one read of a row tile */
 
 /* ---- exclusive scans of K int64 values per row -------------------------- */
@@ -269,7 +273,7 @@ __device__ __forceinline__ int64_t last_tag_before(const ForkArgs &a, int64_t g,
         const int64_t lo = e > CHUNK ? e - CHUNK : 0;
         int64_t best = -1;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < CHUNK_J; ++j) {
             const int64_t p = lo + lane + WAVE * j;
             if (p < e && classify(a.tm, a.tokens[g + p], contig) != C_TEXT) best = p > best ? p : best;
         }
@@ -309,7 +313,7 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
                     const int64_t lo = e > CHUNK ? e - CHUNK : 0;
                     int64_t best = -1;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
+                    for (int j = 0; j < CHUNK_J; ++j) {
                         const int64_t p = lo + lane + WAVE * j;
                         if (p < e && classify(a.tm, a.tokens[g + p], contig) == C_OUT) best = p > best ? p : best;
                     }
@@ -341,17 +345,17 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
         const int64_t w0 = WRITE ? a.worker_off[i] : 0;
         const int64_t t0 = WRITE ? a.tok_off[i] : 0;
         for (int64_t lo = o + 1; lo < end; lo += CHUNK) {
-            uint64_t b[4];
-            uint32_t c[4];
+            uint64_t b[CHUNK_J];
+            uint32_t c[CHUNK_J];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < CHUNK_J; ++j) {
                 const int64_t p = lo + lane + WAVE * j;
                 c[j] = p < end ? classify(a.tm, a.tokens[g + p], contig) : C_TEXT;
                 b[j] = __ballot(c[j] != C_TEXT);
             }
             uint32_t base = 0;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < CHUNK_J; ++j) {
                 if (c[j] != C_TEXT) {
                     const uint32_t idx = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(b[j] >> 32),
                                                                           __builtin_amdgcn_mbcnt_lo((uint32_t)b[j], 0u));
