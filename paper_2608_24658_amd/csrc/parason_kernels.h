@@ -708,15 +708,109 @@ __device__ __forceinline__ uint32_t state_after(int32_t c)
     }
 }
 
-/* Inclusive prefix sum over the wave's lanes (every lane must call it). */
-__device__ __forceinline__ int32_t wave_incl_scan32(int32_t v, int lane)
+/* Wave scans and reductions by DPP: shifts within rows of 16 lanes
+ * (row_shr), carries between the four rows from the rows' last lanes
+ * (readlane).  A chain of shuffles would go through the LDS crossbar, one
+ * round trip per step; these stay in the VALU.  Every lane must call them. */
+constexpr int DPP_ROW_SHR = 0x110; /* row_shr:n is DPP_ROW_SHR + n */
+constexpr int DPP_WAVE_SHR1 = 0x138;
+
+template <int N>
+__device__ __forceinline__ int32_t row_shr(int32_t v, int32_t ident)
 {
-#pragma unroll
-    for (int d = 1; d < WAVE; d <<= 1) {
-        const int32_t o = __shfl_up(v, (unsigned)d, WAVE);
-        v += lane >= d ? o : 0;
+    return __builtin_amdgcn_update_dpp(ident, v, DPP_ROW_SHR + N, 0xf, 0xf, false);
+}
+
+/* v of lane - 1 (ident in lane 0). */
+__device__ __forceinline__ int32_t lane_before(int32_t v, int32_t ident)
+{
+    return __builtin_amdgcn_update_dpp(ident, v, DPP_WAVE_SHR1, 0xf, 0xf, false);
+}
+
+__device__ __forceinline__ int32_t lane63(int32_t v) { return __builtin_amdgcn_readlane(v, WAVE - 1); }
+
+struct OpAdd {
+    static constexpr int32_t ident = 0;
+    __device__ static int32_t f(int32_t x, int32_t y) { return x + y; }
+};
+struct OpMax {
+    static constexpr int32_t ident = INT32_MIN;
+    __device__ static int32_t f(int32_t x, int32_t y) { return x > y ? x : y; }
+};
+struct OpMin {
+    static constexpr int32_t ident = INT32_MAX;
+    __device__ static int32_t f(int32_t x, int32_t y) { return x < y ? x : y; }
+};
+
+template <class Op>
+__device__ __forceinline__ int32_t dpp_incl_scan(int32_t v, int lane)
+{
+    v = Op::f(v, row_shr<1>(v, Op::ident));
+    v = Op::f(v, row_shr<2>(v, Op::ident));
+    v = Op::f(v, row_shr<4>(v, Op::ident));
+    v = Op::f(v, row_shr<8>(v, Op::ident));
+    const int32_t t0 = __builtin_amdgcn_readlane(v, 15), t1 = __builtin_amdgcn_readlane(v, 31),
+                  t2 = __builtin_amdgcn_readlane(v, 47);
+    const int32_t p2 = Op::f(t0, t1), p3 = Op::f(p2, t2);
+    const int row = lane >> 4;
+    return row == 0 ? v : Op::f(row == 1 ? t0 : (row == 2 ? p2 : p3), v);
+}
+
+/* Segmented form: restarts at lanes with head set; lanes before the first
+ * head continue from carry.  Row r starts from C_r: C_0 = carry, and
+ * C_{r+1} is row r's last lane if the row holds a head, else op(C_r, it). */
+template <class Op>
+__device__ __forceinline__ int32_t dpp_seg_scan(int32_t v, bool head, int32_t carry, int lane)
+{
+    int32_t f = head ? 1 : 0;
+#define PARASON_SEG_STEP(N)                          \
+    {                                                \
+        const int32_t vo = row_shr<N>(v, Op::ident); \
+        const int32_t fo = row_shr<N>(f, 0);         \
+        if (!f) {                                    \
+            v = Op::f(vo, v);                        \
+            f = fo;                                  \
+        }                                            \
     }
-    return v;
+    PARASON_SEG_STEP(1)
+    PARASON_SEG_STEP(2)
+    PARASON_SEG_STEP(4)
+    PARASON_SEG_STEP(8)
+#undef PARASON_SEG_STEP
+    const int32_t v0 = __builtin_amdgcn_readlane(v, 15), v1 = __builtin_amdgcn_readlane(v, 31),
+                  v2 = __builtin_amdgcn_readlane(v, 47);
+    const int32_t f0 = __builtin_amdgcn_readlane(f, 15), f1 = __builtin_amdgcn_readlane(f, 31),
+                  f2 = __builtin_amdgcn_readlane(f, 47);
+    const int32_t c1 = f0 ? v0 : Op::f(carry, v0);
+    const int32_t c2 = f1 ? v1 : Op::f(c1, v1);
+    const int32_t c3 = f2 ? v2 : Op::f(c2, v2);
+    const int row = lane >> 4;
+    const int32_t c = row == 0 ? carry : (row == 1 ? c1 : (row == 2 ? c2 : c3));
+    return f ? v : Op::f(c, v);
+}
+
+/* Inclusive prefix sum and running maximum over the wave's lanes. */
+__device__ __forceinline__ int32_t wave_incl_scan32(int32_t v, int lane) { return dpp_incl_scan<OpAdd>(v, lane); }
+__device__ __forceinline__ int32_t wave_incl_max32(int32_t v, int lane) { return dpp_incl_scan<OpMax>(v, lane); }
+
+template <bool MAX>
+__device__ __forceinline__ int32_t wave_seg_scan(int32_t v, bool head, int32_t carry, int lane)
+{
+    return MAX ? dpp_seg_scan<OpMax>(v, head, carry, lane) : dpp_seg_scan<OpAdd>(v, head, carry, lane);
+}
+
+/* Reductions over the wave, the result in every lane. */
+__device__ __forceinline__ int32_t wave_sum32(int32_t v)
+{
+    return lane63(dpp_incl_scan<OpAdd>(v, (int)(threadIdx.x & (WAVE - 1))));
+}
+__device__ __forceinline__ int32_t wave_min32(int32_t v)
+{
+    return lane63(dpp_incl_scan<OpMin>(v, (int)(threadIdx.x & (WAVE - 1))));
+}
+__device__ __forceinline__ int32_t wave_max32(int32_t v)
+{
+    return lane63(dpp_incl_scan<OpMax>(v, (int)(threadIdx.x & (WAVE - 1))));
 }
 
 /* The largest lane j with x (held by lane j) <= f, for x non-decreasing over
@@ -730,62 +824,6 @@ __device__ __forceinline__ int32_t last_lane_at_most(int32_t x, int32_t f)
         lo = __shfl(x, cand, WAVE) <= f ? cand : lo;
     }
     return lo;
-}
-
-/* Inclusive scans over the wave's lanes, every lane calling.  The segmented
- * forms restart at lanes with head set; lanes before the chunk's first head
- * continue from carry (the previous chunk's last value). */
-__device__ __forceinline__ int32_t wave_incl_max32(int32_t v, int lane)
-{
-#pragma unroll
-    for (int d = 1; d < WAVE; d <<= 1) {
-        const int32_t o = __shfl_up(v, (unsigned)d, WAVE);
-        v = (lane >= d && o > v) ? o : v;
-    }
-    return v;
-}
-
-template <bool MAX>
-__device__ __forceinline__ int32_t wave_seg_scan(int32_t v, bool head, int32_t carry, int lane)
-{
-    int32_t f = head ? 1 : 0;
-#pragma unroll
-    for (int d = 1; d < WAVE; d <<= 1) {
-        const int32_t vo = __shfl_up(v, (unsigned)d, WAVE);
-        const int32_t fo = __shfl_up(f, (unsigned)d, WAVE);
-        if (lane >= d && !f) {
-            v = MAX ? (vo > v ? vo : v) : v + vo;
-            f = fo;
-        }
-    }
-    return f ? v : (MAX ? (carry > v ? carry : v) : v + carry);
-}
-
-__device__ __forceinline__ int32_t wave_sum32(int32_t v)
-{
-#pragma unroll
-    for (int d = WAVE / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, WAVE);
-    return v;
-}
-
-__device__ __forceinline__ int32_t wave_min32(int32_t v)
-{
-#pragma unroll
-    for (int d = WAVE / 2; d > 0; d >>= 1) {
-        const int32_t o = __shfl_xor(v, d, WAVE);
-        v = o < v ? o : v;
-    }
-    return v;
-}
-
-__device__ __forceinline__ int32_t wave_max32(int32_t v)
-{
-#pragma unroll
-    for (int d = WAVE / 2; d > 0; d >>= 1) {
-        const int32_t o = __shfl_xor(v, d, WAVE);
-        v = o > v ? o : v;
-    }
-    return v;
 }
 
 /* One wave per row, its lanes over the row's events (a small batch).  The
@@ -846,7 +884,7 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
             const int32_t cnt = s < s1 ? a.seg_count[s] : 0;
             const int32_t incl = wave_incl_scan32(cnt, lane);
             const int32_t excl = incl - cnt;
-            const int32_t total = __shfl(incl, WAVE - 1, WAVE);
+            const int32_t total = lane63(incl);
             /* a dense segment (more than EV_CAP tags) or too many events: rows_mid */
             held = __ballot(cnt > EV_CAP) == 0 && m + total <= PAR_EVENTS;
             for (int32_t f0 = 0; held && f0 < total; f0 += WAVE) {
@@ -875,11 +913,7 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
         const int32_t i = i0 + lane;
         const bool act = i < m;
         const int32_t c = act ? sC[i] : 0, p = act ? sP[i] : 0;
-        int32_t pc = __shfl_up(c, 1u, WAVE), pp = __shfl_up(p, 1u, WAVE);
-        if (lane == 0) {
-            pc = prev_c;
-            pp = prev_p;
-        }
+        const int32_t pc = lane_before(c, prev_c), pp = lane_before(p, prev_p);
         const int32_t dd = act ? (c == C_PAR) - (c == C_END_PAR) : 0;
         const int32_t dt = act ? (c == C_THR) - (c == C_END_THR) : 0;
         const int32_t d_in = wave_incl_scan32(dd, lane), t_in = wave_incl_scan32(dt, lane);
@@ -901,10 +935,10 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
         max_depth = max(max_depth, wave_max32(open_depth));
         n_blocks += wave_sum32(act && c == C_PAR ? 1 : 0);
         const int last = min(WAVE - 1, m - 1 - i0);
-        prev_c = __shfl(c, last, WAVE);
-        prev_p = __shfl(p, last, WAVE);
-        depth += __shfl(d_in, WAVE - 1, WAVE);
-        threads += __shfl(t_in, WAVE - 1, WAVE);
+        prev_c = __builtin_amdgcn_readlane(c, last);
+        prev_p = __builtin_amdgcn_readlane(p, last);
+        depth += lane63(d_in);
+        threads += lane63(t_in);
     }
     if (err == INT32_MAX) {
         /* the end of the row: the text after the last tag, then </think> must have come */
@@ -947,9 +981,9 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
                 sLAT[i] = tok - S;
                 sOWN[i] = tok - CH;
             }
-            c_thr = __shfl(thr_idx, WAVE - 1, WAVE);
-            c_S = __shfl(S, WAVE - 1, WAVE);
-            c_CH = __shfl(CH, WAVE - 1, WAVE);
+            c_thr = lane63(thr_idx);
+            c_S = lane63(S);
+            c_CH = lane63(CH);
         }
         __syncthreads();
         /* blocks of level lev: saved tokens, thread types, count mismatch */
@@ -982,11 +1016,11 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
                 my_mismatch = my_mismatch || nt != n_e;
                 my_saved += lev == 1 ? saved : 0;
             }
-            c_sum = __shfl(sum, WAVE - 1, WAVE);
-            c_max = __shfl(mx, WAVE - 1, WAVE);
-            c_n = __shfl(nt, WAVE - 1, WAVE);
-            c_par = __shfl(par_idx, WAVE - 1, WAVE);
-            c_eout = __shfl(eout_idx, WAVE - 1, WAVE);
+            c_sum = lane63(sum);
+            c_max = lane63(mx);
+            c_n = lane63(nt);
+            c_par = lane63(par_idx);
+            c_eout = lane63(eout_idx);
         }
         __syncthreads();
     }
