@@ -139,14 +139,16 @@ void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, const
     }
     const unsigned row_blocks = (unsigned)((ra.n + per_wave - 1) / per_wave);
     if (per_wave == 1) {
-        pk::rows_par<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows);
+        /* rows_par runs the rows it does not hold through the automaton
+         * itself (the second tier), so rows_mid has nothing to do */
+        pk::rows_par<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows);
     } else {
         /* the per-lane automaton reads split rows best as compact lists */
         pk::gather_rows<<<dim3((unsigned)(cus * GATHER_BLOCKS_PER_CU)), dim3(256), 0, stream>>>(ga);
         pk::rows_fast<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows, lane_shift);
+        pk::rows_mid<LENIENT><<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(
+            ra, mode, counters, mid_rows, deep_rows);
     }
-    pk::rows_mid<LENIENT><<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(ra, mode, counters,
-                                                                                              mid_rows, deep_rows);
     pk::rows_deep<LENIENT><<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);
 }
 

@@ -21,18 +21,20 @@
  *        one compact list with row positions (mode[i] = 1).
  *   rows_par  (small batches: one wave per row, lanes over its events)
  *        Validity from local checks and a depth prefix sum; latency and branch
- *        tokens level by level with segmented scans.  Rows it cannot hold go
- *        to rows_mid.
+ *        tokens level by level with segmented scans (DPP).  A row it cannot
+ *        hold runs through the automaton on one lane, with MID_DEPTH frames in
+ *        LDS, as in rows_mid.
  *   rows_fast  (larger batches: one thread per row)
  *        The grammar's pushdown automaton over the row's events; Text runs are
  *        the gaps between event positions.  A segment holding more than EV_CAP
  *        tags, or marked DENSE by the scan, is classified again token by token.
  *        Frames of open blocks in LDS (FAST_DEPTH per row, 64 outline entries
  *        per block); a row that needs more is handed to rows_mid.
- *   rows_mid  (one thread per handed-over row, MID_DEPTH frames in LDS)
+ *   rows_mid  (after rows_fast: one thread per handed-over row, MID_DEPTH
+ *        frames in LDS)
  *        The same automaton for deeper rows; a row that needs more still is
  *        handed to rows_deep.
- *   rows_deep  (one thread, only rows rows_mid handed over)
+ *   rows_deep  (one thread, only rows rows_mid or rows_par handed over)
  *        The same automaton with frames and entry types in global workspace.
  *   group_reward  (one thread per row)
  *        Statistics and Definition 3.1 in IEEE double, fixed order.
@@ -840,11 +842,12 @@ __device__ __forceinline__ int32_t last_lane_at_most(int32_t x, int32_t f)
  *     type of the outline entry it pairs with.  Evaluated level by level,
  *     deepest first, with segmented scans (phase B).
  * Rows holding more than PAR_EVENTS events, nested deeper than PAR_LEVELS,
- * or with a dense segment, go to rows_mid.  Split rows are read from their
+ * or with a dense segment, run through the automaton on lane 0 (the single
+ * automaton call site of this kernel).  Split rows are read from their
  * segments' lists directly (no gather_rows launch for a small batch). */
 template <bool LENIENT>
 __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restrict__ mode,
-                                               int32_t *__restrict__ counters, int32_t *__restrict__ mid_rows)
+                                               int32_t *__restrict__ counters, int32_t *__restrict__ deep_rows)
 {
     __shared__ int32_t sP[PAR_EVENTS], sC[PAR_EVENTS], sD[PAR_EVENTS], sT[PAR_EVENTS];
     __shared__ int32_t sTOK[PAR_EVENTS], sLAT[PAR_EVENTS], sOWN[PAR_EVENTS], sSAV[PAR_EVENTS];
@@ -901,59 +904,72 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
             m += total;
         }
     }
-    if (!held) {
-        if (lane == 0) mid_rows[atomicAdd(&counters[0], 1)] = (int32_t)r;
-        return;
-    }
-    __syncthreads();
-
     /* phase A: validity, first error, depth and open threads before each event */
     int32_t prev_c = -1, prev_p = -1, depth = 0, threads = 0, err = INT32_MAX, max_depth = 0, n_blocks = 0;
-    for (int32_t i0 = 0; i0 < m && err == INT32_MAX; i0 += WAVE) {
-        const int32_t i = i0 + lane;
-        const bool act = i < m;
-        const int32_t c = act ? sC[i] : 0, p = act ? sP[i] : 0;
-        const int32_t pc = lane_before(c, prev_c), pp = lane_before(p, prev_p);
-        const int32_t dd = act ? (c == C_PAR) - (c == C_END_PAR) : 0;
-        const int32_t dt = act ? (c == C_THR) - (c == C_END_THR) : 0;
-        const int32_t d_in = wave_incl_scan32(dd, lane), t_in = wave_incl_scan32(dt, lane);
-        const int32_t db = depth + d_in - dd, tb = threads + t_in - dt;
-        int32_t e = INT32_MAX, open_depth = 0;
-        if (act) {
-            const uint32_t st = pc < 0 ? (uint32_t)S_START : state_after(pc);
-            const int32_t gap = p - pp - 1;
-            const bool text_ok = gap == 0 || st == S_BODY || st == S_TRAIL || st == S_ENTRY || (LENIENT && st != S_START);
-            const bool tag_ok = ((allowed_classes(st) >> c) & 1u) && !(c == C_END_THINK && db != 0) &&
-                                !(c == C_END_THR && db == 0) &&
-                                !((c == C_END_SUB || c == C_END_TRI) && (c != pc + 1 || gap == 0));
-            e = !text_ok ? pp + 1 : (!tag_ok ? p : INT32_MAX);
-            sD[i] = db;
-            sT[i] = tb;
-            open_depth = c == C_PAR ? db + 1 : 0;
+    bool fallback = !held; /* the row goes to the automaton below */
+    do {
+        if (fallback) break;
+        __syncthreads();
+        for (int32_t i0 = 0; i0 < m && err == INT32_MAX; i0 += WAVE) {
+            const int32_t i = i0 + lane;
+            const bool act = i < m;
+            const int32_t c = act ? sC[i] : 0, p = act ? sP[i] : 0;
+            const int32_t pc = lane_before(c, prev_c), pp = lane_before(p, prev_p);
+            const int32_t dd = act ? (c == C_PAR) - (c == C_END_PAR) : 0;
+            const int32_t dt = act ? (c == C_THR) - (c == C_END_THR) : 0;
+            const int32_t d_in = wave_incl_scan32(dd, lane), t_in = wave_incl_scan32(dt, lane);
+            const int32_t db = depth + d_in - dd, tb = threads + t_in - dt;
+            int32_t e = INT32_MAX, open_depth = 0;
+            if (act) {
+                const uint32_t st = pc < 0 ? (uint32_t)S_START : state_after(pc);
+                const int32_t gap = p - pp - 1;
+                const bool text_ok = gap == 0 || st == S_BODY || st == S_TRAIL || st == S_ENTRY || (LENIENT && st != S_START);
+                const bool tag_ok = ((allowed_classes(st) >> c) & 1u) && !(c == C_END_THINK && db != 0) &&
+                                    !(c == C_END_THR && db == 0) &&
+                                    !((c == C_END_SUB || c == C_END_TRI) && (c != pc + 1 || gap == 0));
+                e = !text_ok ? pp + 1 : (!tag_ok ? p : INT32_MAX);
+                sD[i] = db;
+                sT[i] = tb;
+                open_depth = c == C_PAR ? db + 1 : 0;
+            }
+            err = wave_min32(e);
+            max_depth = max(max_depth, wave_max32(open_depth));
+            n_blocks += wave_sum32(act && c == C_PAR ? 1 : 0);
+            const int last = min(WAVE - 1, m - 1 - i0);
+            prev_c = __builtin_amdgcn_readlane(c, last);
+            prev_p = __builtin_amdgcn_readlane(p, last);
+            depth += lane63(d_in);
+            threads += lane63(t_in);
         }
-        err = wave_min32(e);
-        max_depth = max(max_depth, wave_max32(open_depth));
-        n_blocks += wave_sum32(act && c == C_PAR ? 1 : 0);
-        const int last = min(WAVE - 1, m - 1 - i0);
-        prev_c = __builtin_amdgcn_readlane(c, last);
-        prev_p = __builtin_amdgcn_readlane(p, last);
-        depth += lane63(d_in);
-        threads += lane63(t_in);
-    }
-    if (err == INT32_MAX) {
-        /* the end of the row: the text after the last tag, then </think> must have come */
-        const uint32_t st = prev_c < 0 ? (uint32_t)S_START : state_after(prev_c);
-        const int32_t gap = len - prev_p - 1;
-        const bool text_ok = gap == 0 || st == S_BODY || st == S_TRAIL || st == S_ENTRY || (LENIENT && st != S_START);
-        if (!text_ok) err = prev_p + 1;
-        else if (st != S_TRAIL) err = len;
-    }
-    if (err != INT32_MAX) {
-        if (lane == 0) write_row(a.out, r, len, len, 0, 0, 0, 0, err, err == len ? PARASON_FLAG_TRUNCATED : 0u);
-        return;
-    }
-    if (max_depth > PAR_LEVELS) {
-        if (lane == 0) mid_rows[atomicAdd(&counters[0], 1)] = (int32_t)r;
+        if (err == INT32_MAX) {
+            /* the end of the row: the text after the last tag, then </think> must have come */
+            const uint32_t st = prev_c < 0 ? (uint32_t)S_START : state_after(prev_c);
+            const int32_t gap = len - prev_p - 1;
+            const bool text_ok = gap == 0 || st == S_BODY || st == S_TRAIL || st == S_ENTRY || (LENIENT && st != S_START);
+            if (!text_ok) err = prev_p + 1;
+            else if (st != S_TRAIL) err = len;
+        }
+        if (err != INT32_MAX) {
+            if (lane == 0) write_row(a.out, r, len, len, 0, 0, 0, 0, err, err == len ? PARASON_FLAG_TRUNCATED : 0u);
+            return;
+        }
+        fallback = max_depth > PAR_LEVELS;
+    } while (0);
+    if (fallback) {
+        /* a row this kernel does not hold (more than PAR_EVENTS events, a dense
+         * segment, nesting deeper than PAR_LEVELS): the automaton on one lane
+         * with MID_DEPTH frames in LDS (sTOK, unused on this path), as rows_mid
+         * would; a row that needs still more is listed for rows_deep */
+        if (lane == 0) {
+            Automaton<LdsStore<MID_DEPTH>, LENIENT> A;
+            A.st.lds = sTOK;
+            A.st.tid = 0;
+            A.st.nt = 1;
+            A.init();
+            if (drive_row(a, r, g, len, mode[r] == 1, A)) A.finish(len);
+            if (A.overflow) deep_rows[atomicAdd(&counters[1], 1)] = (int32_t)r;
+            else write_result(a.out, r, len, A);
+        }
         return;
     }
     __syncthreads();
