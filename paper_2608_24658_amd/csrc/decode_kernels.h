@@ -187,18 +187,32 @@ __global__ void __launch_bounds__(DECODE_THREADS) decode_step(DecodeArgs a)
         const uint32_t w = a.elem == 2 ? (a.ninf | (a.ninf << 16)) : a.ninf;
         const uint4 ninf4 = make_uint4(w, w, w, w);
         uint4 *vrow = reinterpret_cast<uint4 *>(row + head * a.elem);
+        /* the (at most three) vectors that hold a kept logit are written
+         * elementwise below; every other vector is one 16-byte store */
+        const int32_t nv = (int32_t)n_vec;
+        const int32_t kv0 = keep0 >= head && keep0 < tail0 ? (int32_t)((keep0 - head) / per) : -1;
+        const int32_t kv1 = keep1 >= head && keep1 < tail0 ? (int32_t)((keep1 - head) / per) : -1;
+        const int32_t kv2 = keep2 >= head && keep2 < tail0 ? (int32_t)((keep2 - head) / per) : -1;
 #ifndef PARASON_DECODE_UNROLL
-#define PARASON_DECODE_UNROLL 1
+#define PARASON_DECODE_UNROLL 4
 #endif
-#pragma unroll PARASON_DECODE_UNROLL
-        for (int64_t v = threadIdx.x; v < n_vec; v += DECODE_THREADS) {
-            const int64_t e0 = head + v * per;
-            const bool clean = (uint64_t)(keep0 - e0) >= (uint64_t)per && (uint64_t)(keep1 - e0) >= (uint64_t)per &&
-                               (uint64_t)(keep2 - e0) >= (uint64_t)per;
-            if (clean) {
-                vrow[v] = ninf4;
-            } else {
-                for (int64_t e = e0; e < e0 + per; ++e)
+        constexpr int U = PARASON_DECODE_UNROLL;
+        int32_t v = (int32_t)threadIdx.x;
+        for (; v + (U - 1) * DECODE_THREADS < nv; v += U * DECODE_THREADS) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t vv = v + u * DECODE_THREADS;
+                if (vv != kv0 && vv != kv1 && vv != kv2) vrow[vv] = ninf4;
+            }
+        }
+        for (; v < nv; v += DECODE_THREADS)
+            if (v != kv0 && v != kv1 && v != kv2) vrow[v] = ninf4;
+        if (threadIdx.x < 3) {
+            const int32_t kv = threadIdx.x == 0 ? kv0 : (threadIdx.x == 1 ? kv1 : kv2);
+            /* a vector holding two kept logits is listed twice: only its first listing writes it */
+            const bool first = kv >= 0 && !(threadIdx.x >= 1 && kv == kv0) && !(threadIdx.x == 2 && kv == kv1);
+            if (first) {
+                for (int64_t e = head + (int64_t)kv * per; e < head + (int64_t)(kv + 1) * per; ++e)
                     if (e != keep0 && e != keep1 && e != keep2) store_ninf(row, e, a);
             }
         }
