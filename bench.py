@@ -100,7 +100,28 @@ def cpu_baseline(tokens_d, starts_h, lengths_h, correct_h, tag_ids, coef, budget
         "sample": "first %d groups (%d rows, %d tokens) of the same workload, copied to the host; %.1f s "
                   "single-threaded" % (n_groups, n_groups * G, toks.size, dt),
         "rows_per_s": n_groups * G / dt,
+        "host": host_cpu(),
     }
+
+
+def host_cpu():
+    """The host's CPU model and the threads this process may run on."""
+    import os
+
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        threads = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        threads = os.cpu_count()
+    return {"cpu_model": model, "threads_available": threads}
 
 
 def main():
