@@ -854,31 +854,44 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
     const int lane = threadIdx.x;
     const int64_t r = blockIdx.x;
     if (r >= a.n) return;
+    /* the row's records in one round of loads, before any branch */
     const int64_t start = a.starts[r];
     const int32_t len = a.lengths[r];
+    const int64_t S = a.seg_off[a.n], s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
+    const uint8_t md = mode[r];
     if (start < 0 || len < 0) {
         if (lane == 0) write_row(a.out, r, 0, 0, 0, 0, 0, 0, 0, PARASON_FLAG_BAD_ROW);
         return;
     }
-    if (a.seg_off[a.n] > a.seg_cap) {
+    if (S > a.seg_cap) {
         if (lane == 0) write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_WS_OVERFLOW);
         return;
     }
     /* the row's events into LDS, in position order: from its compact list (row
      * positions), or from its segments' lists (segment positions), gathered
      * here as gather_rows does for the per-lane kernel */
-    const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
     const int64_t g = start + a.mis;
     int32_t m = 0;
     bool held = true;
-    if (mode[r] == 1) {
+    if (md == 1) {
         m = a.seg_count[s0];
         held = m <= PAR_EVENTS;
         const uint32_t *list = a.events + s0 * EV_CAP;
-        for (int32_t i = lane; held && i < m; i += WAVE) {
-            const uint32_t w = list[i];
-            sP[i] = (int32_t)(w >> 4);
-            sC[i] = (int32_t)(w & 15u);
+        for (int32_t i0 = 0; held && i0 < m; i0 += 4 * WAVE) { /* four loads per lane in flight */
+            uint32_t w[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int32_t i = i0 + u * WAVE + lane;
+                w[u] = i < m ? list[i] : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int32_t i = i0 + u * WAVE + lane;
+                if (i < m) {
+                    sP[i] = (int32_t)(w[u] >> 4);
+                    sC[i] = (int32_t)(w[u] & 15u);
+                }
+            }
         }
     } else {
         const int64_t vrow0 = row_first_vec(g);
@@ -888,17 +901,27 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
             const int32_t incl = wave_incl_scan32(cnt, lane);
             const int32_t excl = incl - cnt;
             const int32_t total = lane63(incl);
-            /* a dense segment (more than EV_CAP tags) or too many events: rows_mid */
+            /* a dense segment (more than EV_CAP tags) or too many events: the
+             * automaton below */
             held = __ballot(cnt > EV_CAP) == 0 && m + total <= PAR_EVENTS;
-            for (int32_t f0 = 0; held && f0 < total; f0 += WAVE) {
-                const int32_t f = f0 + lane;
-                const int32_t j = last_lane_at_most(excl, f);
-                const int32_t first = __shfl(excl, j, WAVE);
-                if (f < total) {
-                    const int64_t seg = c0 + j;
-                    const uint32_t w = a.events[seg * EV_CAP + (f - first)];
-                    sP[m + f] = (int32_t)(4 * (vrow0 + (seg - s0) * SEG_VEC) - g + (int64_t)(w >> 4));
-                    sC[m + f] = (int32_t)(w & 15u);
+            for (int32_t f0 = 0; held && f0 < total; f0 += 2 * WAVE) { /* two loads per lane in flight */
+                int32_t j[2];
+                uint32_t w[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int32_t f = f0 + u * WAVE + lane;
+                    j[u] = last_lane_at_most(excl, f);
+                    const int32_t first = __shfl(excl, j[u], WAVE);
+                    w[u] = f < total ? a.events[(c0 + j[u]) * EV_CAP + (f - first)] : 0u;
+                }
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int32_t f = f0 + u * WAVE + lane;
+                    if (f < total) {
+                        const int64_t seg = c0 + j[u];
+                        sP[m + f] = (int32_t)(4 * (vrow0 + (seg - s0) * SEG_VEC) - g + (int64_t)(w[u] >> 4));
+                        sC[m + f] = (int32_t)(w[u] & 15u);
+                    }
                 }
             }
             m += total;
@@ -966,7 +989,7 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
             A.st.tid = 0;
             A.st.nt = 1;
             A.init();
-            if (drive_row(a, r, g, len, mode[r] == 1, A)) A.finish(len);
+            if (drive_row(a, r, g, len, md == 1, A)) A.finish(len);
             if (A.overflow) deep_rows[atomicAdd(&counters[1], 1)] = (int32_t)r;
             else write_result(a.out, r, len, A);
         }
