@@ -576,6 +576,13 @@ def bench_fork(args):
     assert not jfirst["row_status"].any().item()
     join_ms = timed(lambda: px.join(tokens, starts, lengths, first["worker_off"], wtokens, wstarts, wl32,
                                     capacity=JT))
+    # references at the same sizes: torch's copy_ of T int32 (the contexts' bytes, read and written) and of
+    # JT int32 (the joined rows' bytes)
+    ref_src = torch.empty(T, dtype=torch.int32, device=dev)
+    ref_dst = torch.empty_like(ref_src)
+    copy_ms = timed(lambda: ref_dst.copy_(ref_src))
+    jcopy_ms = timed(lambda: ref_dst[:JT].copy_(ref_src[:JT]))
+    del ref_src, ref_dst
     rows_read = int(cut.astype(np.int64).sum())
     tail = JT - rows_read - B  # each worker's <Thread> ... </Thread> span
     # fork: rows read once, contexts written, 24 B of record per worker, 28 B of offsets/status per row
@@ -607,6 +614,10 @@ def bench_fork(args):
                      "kernel_ms": fork_ms, "algorithmic_bytes": fork_bytes},
         "join_roofline": {"achieved": join_bytes / (join_ms * 1e-3) / 1e9, "unit": "GB/s",
                           "frac": join_bytes / (join_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "algorithmic_bytes": join_bytes},
+        "reference": {"what": "torch copy_ of the context tokens (T int32 read and written, one kernel)",
+                      "ms": copy_ms, "GB/s": 8 * T / (copy_ms * 1e-3) / 1e9},
+        "join_reference": {"what": "torch copy_ of the joined tokens (JT int32 read and written, one kernel)",
+                           "ms": jcopy_ms, "GB/s": 8 * JT / (jcopy_ms * 1e-3) / 1e9},
     }
     print(json.dumps(res), flush=True)
 

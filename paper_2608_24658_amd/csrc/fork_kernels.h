@@ -28,7 +28,9 @@
  *   pack_*               exclusive scan of the joined lengths.
  *   join_copy            tiled the same way over the joined tokens: the row,
  *                        each worker's <Thread> ... </Thread> span (positions
- *                        of 64 workers from one wave scan), and </Parallel>.
+ *                        of 64 workers from one wave scan), and </Parallel>;
+ *                        16-byte stores aligned on the output, 16-byte loads
+ *                        at dword alignment.
  *
  * With PARASON_CFG_LENIENT_GAPS Text may stand between <Parallel> and
  * <Outlines>, after <Outlines>, between entries and before </Outlines>: the
@@ -37,9 +39,11 @@
  * in both modes), and fork_copy finds the texts of a group's entries by one
  * ballot scan of the outline.
  *
- * All copies are dword-granular and coalesced (rows and contexts start at any
- * element offset).  Tiling keeps every wave step's work bounded however long
- * the rows are: at most 1024 loads and, in fork_copy, eight stores of each.
+ * Rows, contexts and joined rows start at any element offset.  fork_copy
+ * moves dwords (the contexts of a group start at unrelated alignments, and
+ * the loads are shared between them); join_copy moves 16-byte vectors.
+ * Tiling keeps every wave step's work bounded however long the rows are: 1024
+ * positions and, in fork_copy, eight stores of each.
  */
 #pragma once
 #include "device_common.h"
@@ -442,17 +446,29 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
 /* ---- tiled copies -------------------------------------------------------- */
 
 /* The copies are tiled over their output by waves: each wave step covers
- * WTILE consecutive output positions (WU per lane, all loads issued before
- * the first store), finds the row holding the first of them by a 64-way
- * search, and walks the pieces of that range.  Waves work independently, so
- * the chains of dependent loads of many tiles (search, row and worker
- * records, data) overlap on every CU. */
-#ifndef PARASON_COPY_WU
-#define PARASON_COPY_WU 16
+ * WTILE consecutive output positions (WV 16-byte vectors per lane, all loads
+ * issued before the first store), finds the row holding the first of them by
+ * a 64-way search, and walks the pieces of that range.  Waves work
+ * independently, so the chains of dependent loads of many tiles (search, row
+ * and worker records, data) overlap on every CU. */
+#ifndef PARASON_COPY_WV
+#define PARASON_COPY_WV 4
 #endif
-constexpr int WU = PARASON_COPY_WU;      /* loads per lane per wave step */
-constexpr int64_t WTILE = WU * WAVE;     /* output positions per wave step */
+constexpr int WV = PARASON_COPY_WV;      /* 16-byte vectors per lane per wave step */
+constexpr int64_t WTILE = 4 * WV * WAVE; /* output positions per wave step */
+constexpr int TAIL_U = 16;               /* elements per lane per step of a context's tail */
 constexpr int COPY_WAVES = PACK_THREADS / WAVE;
+
+typedef int v4i_t __attribute__((ext_vector_type(4)));
+
+/* 16 bytes from a 4-byte aligned address (global memory takes unaligned
+ * 16-byte loads at dword granularity). */
+__device__ __forceinline__ v4i_t load16(const int32_t *p)
+{
+    v4i_t v;
+    __builtin_memcpy(&v, p, 16);
+    return v;
+}
 
 /* Largest index s in [0, count) with offs[s] <= x (offs ascending, offs[0] <= x),
  * by one wave in 64-way rounds; the result is returned to every lane. */
@@ -470,63 +486,79 @@ __device__ __forceinline__ int64_t wave_find(const int64_t *offs, int64_t count,
     return lo;
 }
 
-/* Elements lane + j * WAVE (j < WU) of a range of n <= WTILE: how many of
- * them this lane holds. */
+/* Elements lane + j * WAVE of a range of n: how many of them this lane holds. */
 __device__ __forceinline__ int lane_count(int64_t n, int lane)
 {
     return n > lane ? (int)((n - lane + WAVE - 1) / WAVE) : 0;
 }
 
 /* dst[o_k + p] = src[p] for p in [p0, p1) and every k < nd, by one wave
- * (p1 - p0 <= WTILE): each source token is loaded once and stored nd times;
- * o_k is lane k's value of o.  One base address per lane, constant offsets. */
+ * (p1 - p0 <= WTILE): each source token is loaded once (dword loads, 4 * WV
+ * per lane) and stored nd times; o_k is lane k's value of o.  Sharing the
+ * loads beats per-destination 16-byte copies here: the contexts of a group
+ * start at unrelated alignments. */
 __device__ __forceinline__ void wave_copy_multi(int32_t *__restrict__ dst, int64_t o, int nd, int64_t p0, int64_t p1,
                                                 const int32_t *__restrict__ src, int lane)
 {
+    constexpr int U = 4 * WV;
     const int jm = lane_count(p1 - p0, lane);
     const int32_t *sp = src + p0 + lane;
-    int32_t v[WU];
+    int32_t v[U];
 #pragma unroll
-    for (int j = 0; j < WU; ++j) v[j] = j < jm ? sp[j * WAVE] : 0;
+    for (int j = 0; j < U; ++j) v[j] = j < jm ? sp[j * WAVE] : 0;
     for (int k = 0; k < nd; ++k) {
         int32_t *dp = dst + __shfl(o, k, WAVE) + p0 + lane;
 #pragma unroll
-        for (int j = 0; j < WU; ++j)
+        for (int j = 0; j < U; ++j)
             if (j < jm) dp[j * WAVE] = v[j];
     }
 }
 
-/* dst[d] = src[d - shift] for d in [d0, d1), by one wave (d1 - d0 <= WTILE). */
+/* dst[d] = src[d - shift] for d in [d0, d1), by one wave (d1 - d0 <= WTILE):
+ * 16-byte stores aligned on dst and 16-byte loads from src at whatever dword
+ * alignment that gives; the at most three elements before dst's first 16-byte
+ * boundary and the at most three after the last one are copied singly. */
 __device__ __forceinline__ void wave_copy(int32_t *__restrict__ dst, int64_t d0, int64_t d1,
                                           const int32_t *__restrict__ src, int64_t shift, int lane)
 {
-    const int jm = lane_count(d1 - d0, lane);
-    const int32_t *sp = src + (d0 - shift) + lane;
-    int32_t *dp = dst + d0 + lane;
-    int32_t v[WU];
+    if (d0 >= d1) return;
+    const int64_t b0 = min(d0 + (int64_t)(((16u - ((uint32_t)(uintptr_t)(dst + d0) & 15u)) & 15u) >> 2), d1);
+    const int64_t nvec = (d1 - b0) >> 2;
+    const int64_t b1 = b0 + 4 * nvec;
+    if (lane < 6) { /* lanes 0-2: the head, lanes 3-5: the tail */
+        const int64_t d = lane < 3 ? d0 + lane : b1 + (lane - 3);
+        if (lane < 3 ? d < b0 : d < d1) dst[d] = src[d - shift];
+    }
+    if (nvec == 0) return;
+    /* every lane loads WV vectors (beyond the range: the last one again), so
+     * that the loads are unconditional and issue back to back */
+    const int32_t *sp = src + (b0 - shift);
+    v4i_t *dp = reinterpret_cast<v4i_t *>(dst + b0);
+    v4i_t v[WV];
 #pragma unroll
-    for (int j = 0; j < WU; ++j) v[j] = j < jm ? sp[j * WAVE] : 0;
+    for (int j = 0; j < WV; ++j) v[j] = load16(sp + 4 * min((int64_t)(lane + WAVE * j), nvec - 1));
 #pragma unroll
-    for (int j = 0; j < WU; ++j)
-        if (j < jm) dp[j * WAVE] = v[j];
+    for (int j = 0; j < WV; ++j)
+        if (lane + WAVE * j < nvec) dp[lane + WAVE * j] = v[j];
 }
 
 /* A worker context's tail at dst[d0 .. d1): sub (the <Thread> id) at d0, then
- * src[f ..] (the entry's text), by one wave in steps of WTILE.  f >= 1: the
- * element before the text (its opening tag) is loaded for d0 and replaced. */
+ * src[f ..] (the entry's text), by one wave in steps of TAIL_U per lane.
+ * f >= 1: the element before the text (its opening tag) is loaded for d0 and
+ * replaced. */
 __device__ __forceinline__ void wave_tail(int32_t *__restrict__ dst, int64_t d0, int64_t d1,
                                           const int32_t *__restrict__ src, int64_t f, int32_t sub, int lane)
 {
-    for (int64_t base = 0; base < d1 - d0; base += WTILE) {
-        const int jm = lane_count(min(d1 - d0 - base, WTILE), lane);
+    for (int64_t base = 0; base < d1 - d0; base += TAIL_U * WAVE) {
+        const int jm = lane_count(min(d1 - d0 - base, (int64_t)TAIL_U * WAVE), lane);
         const int32_t *sp = src + (f - 1) + base + lane;
         int32_t *dp = dst + d0 + base + lane;
-        int32_t v[WU];
+        int32_t v[TAIL_U];
 #pragma unroll
-        for (int j = 0; j < WU; ++j) v[j] = j < jm ? sp[j * WAVE] : 0;
+        for (int j = 0; j < TAIL_U; ++j) v[j] = j < jm ? sp[j * WAVE] : 0;
         if (base == 0 && lane == 0) v[0] = sub;
 #pragma unroll
-        for (int j = 0; j < WU; ++j)
+        for (int j = 0; j < TAIL_U; ++j)
             if (j < jm) dp[j * WAVE] = v[j];
     }
 }
