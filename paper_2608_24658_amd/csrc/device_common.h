@@ -118,6 +118,87 @@ __device__ __forceinline__ int64_t wave_inclusive_scan(int64_t v)
     return v;
 }
 
+/* Wave scans and reductions by DPP: shifts within rows of 16 lanes
+ * (row_shr), carries between the four rows from the rows' last lanes
+ * (readlane).  A chain of shuffles would go through the LDS crossbar, one
+ * round trip per step; these stay in the VALU.  Every lane must call them. */
+constexpr int DPP_ROW_SHR = 0x110; /* row_shr:n is DPP_ROW_SHR + n */
+constexpr int DPP_WAVE_SHR1 = 0x138;
+
+template <int N>
+__device__ __forceinline__ int32_t row_shr(int32_t v, int32_t ident)
+{
+    return __builtin_amdgcn_update_dpp(ident, v, DPP_ROW_SHR + N, 0xf, 0xf, false);
+}
+
+/* v of lane - 1 (ident in lane 0). */
+__device__ __forceinline__ int32_t lane_before(int32_t v, int32_t ident)
+{
+    return __builtin_amdgcn_update_dpp(ident, v, DPP_WAVE_SHR1, 0xf, 0xf, false);
+}
+
+__device__ __forceinline__ int32_t lane63(int32_t v) { return __builtin_amdgcn_readlane(v, WAVE - 1); }
+
+struct OpAdd {
+    static constexpr int32_t ident = 0;
+    __device__ static int32_t f(int32_t x, int32_t y) { return x + y; }
+};
+struct OpMax {
+    static constexpr int32_t ident = INT32_MIN;
+    __device__ static int32_t f(int32_t x, int32_t y) { return x > y ? x : y; }
+};
+struct OpMin {
+    static constexpr int32_t ident = INT32_MAX;
+    __device__ static int32_t f(int32_t x, int32_t y) { return x < y ? x : y; }
+};
+
+template <class Op>
+__device__ __forceinline__ int32_t dpp_incl_scan(int32_t v, int lane)
+{
+    v = Op::f(v, row_shr<1>(v, Op::ident));
+    v = Op::f(v, row_shr<2>(v, Op::ident));
+    v = Op::f(v, row_shr<4>(v, Op::ident));
+    v = Op::f(v, row_shr<8>(v, Op::ident));
+    const int32_t t0 = __builtin_amdgcn_readlane(v, 15), t1 = __builtin_amdgcn_readlane(v, 31),
+                  t2 = __builtin_amdgcn_readlane(v, 47);
+    const int32_t p2 = Op::f(t0, t1), p3 = Op::f(p2, t2);
+    const int row = lane >> 4;
+    return row == 0 ? v : Op::f(row == 1 ? t0 : (row == 2 ? p2 : p3), v);
+}
+
+/* Segmented form: restarts at lanes with head set; lanes before the first
+ * head continue from carry.  Row r starts from C_r: C_0 = carry, and
+ * C_{r+1} is row r's last lane if the row holds a head, else op(C_r, it). */
+template <class Op>
+__device__ __forceinline__ int32_t dpp_seg_scan(int32_t v, bool head, int32_t carry, int lane)
+{
+    int32_t f = head ? 1 : 0;
+#define PARASON_SEG_STEP(N)                          \
+    {                                                \
+        const int32_t vo = row_shr<N>(v, Op::ident); \
+        const int32_t fo = row_shr<N>(f, 0);         \
+        if (!f) {                                    \
+            v = Op::f(vo, v);                        \
+            f = fo;                                  \
+        }                                            \
+    }
+    PARASON_SEG_STEP(1)
+    PARASON_SEG_STEP(2)
+    PARASON_SEG_STEP(4)
+    PARASON_SEG_STEP(8)
+#undef PARASON_SEG_STEP
+    const int32_t v0 = __builtin_amdgcn_readlane(v, 15), v1 = __builtin_amdgcn_readlane(v, 31),
+                  v2 = __builtin_amdgcn_readlane(v, 47);
+    const int32_t f0 = __builtin_amdgcn_readlane(f, 15), f1 = __builtin_amdgcn_readlane(f, 31),
+                  f2 = __builtin_amdgcn_readlane(f, 47);
+    const int32_t c1 = f0 ? v0 : Op::f(carry, v0);
+    const int32_t c2 = f1 ? v1 : Op::f(c1, v1);
+    const int32_t c3 = f2 ? v2 : Op::f(c2, v2);
+    const int row = lane >> 4;
+    const int32_t c = row == 0 ? carry : (row == 1 ? c1 : (row == 2 ? c2 : c3));
+    return f ? v : Op::f(c, v);
+}
+
 /* A segment as the scan wave sees it (all fields wave-uniform). */
 struct SegView {
     int64_t s;                  /* segment id */

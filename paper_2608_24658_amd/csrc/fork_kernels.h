@@ -248,15 +248,8 @@ struct ForkArgs {
     int32_t *ctx_tokens;
 };
 
-__device__ __forceinline__ int64_t wave_max(int64_t v)
-{
-#pragma unroll
-    for (int d = WAVE / 2; d > 0; d >>= 1) {
-        const int64_t o = __shfl_xor(v, d, WAVE);
-        v = o > v ? o : v;
-    }
-    return v;
-}
+/* Largest value over the wave (positions, so int32), in every lane. */
+__device__ __forceinline__ int32_t wave_max_pos(int32_t v, int lane) { return lane63(dpp_incl_scan<OpMax>(v, lane)); }
 
 /* Inclusive prefix sum over the wave's lanes (every lane must call it). */
 __device__ __forceinline__ int64_t wave_incl_scan(int64_t v, int lane)
@@ -275,13 +268,13 @@ __device__ __forceinline__ int64_t last_tag_before(const ForkArgs &a, int64_t g,
 {
     for (int64_t e = o; e > 0; e -= CHUNK) {
         const int64_t lo = e > CHUNK ? e - CHUNK : 0;
-        int64_t best = -1;
+        int32_t best = -1;
 #pragma unroll
         for (int j = 0; j < CHUNK_J; ++j) {
             const int64_t p = lo + lane + WAVE * j;
-            if (p < e && classify(a.tm, a.tokens[g + p], contig) != C_TEXT) best = p > best ? p : best;
+            if (p < e && classify(a.tm, a.tokens[g + p], contig) != C_TEXT) best = (int32_t)p > best ? (int32_t)p : best;
         }
-        best = uniform64(wave_max(best));
+        best = wave_max_pos(best, lane);
         if (best >= 0) return best;
     }
     return -1;
@@ -308,25 +301,50 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
             o = a.outl[i];
         } else {
             uint32_t st = 0;
-            if (L < 0 || g < 0) st = PARASON_PACK_BAD_ROW;
-            else if (L == 0 || classify(a.tm, a.tokens[g + L - 1], contig) != C_END_OUT) st = PARASON_PACK_NO_OUTLINE_END;
             o = -1;
-            if (st == 0) {
-                /* the last <Outlines> before the final </Outlines> */
-                for (int64_t e = (int64_t)L - 1; e > 0 && o < 0; e -= CHUNK) {
-                    const int64_t lo = e > CHUNK ? e - CHUNK : 0;
-                    int64_t best = -1;
+            if (L < 0 || g < 0) st = PARASON_PACK_BAD_ROW;
+            else if (L == 0) st = PARASON_PACK_NO_OUTLINE_END;
+            /* backwards from the row's end in chunks: the first chunk holds the
+             * last token, which must be </Outlines>; then the last <Outlines>
+             * before it, and the class of the token right before that when it
+             * is in the same chunk (1: <Parallel>, 0: not, -1: not seen) */
+            int32_t par_before = -1;
+            for (int64_t e = (int64_t)L; st == 0 && e > 0 && o < 0; e -= CHUNK) {
+                const int64_t lo = e > CHUNK ? e - CHUNK : 0;
+                uint32_t c[CHUNK_J];
+                int32_t best = -1;
+                bool end_mine = false;
 #pragma unroll
-                    for (int j = 0; j < CHUNK_J; ++j) {
-                        const int64_t p = lo + lane + WAVE * j;
-                        if (p < e && classify(a.tm, a.tokens[g + p], contig) == C_OUT) best = p > best ? p : best;
-                    }
-                    o = uniform64(wave_max(best));
+                for (int j = 0; j < CHUNK_J; ++j) {
+                    const int64_t p = lo + lane + WAVE * j;
+                    c[j] = p < e ? classify(a.tm, a.tokens[g + p], contig) : C_TEXT;
+                    if (p < (int64_t)L - 1 && c[j] == C_OUT) best = (int32_t)p > best ? (int32_t)p : best;
+                    end_mine = end_mine || (p == (int64_t)L - 1 && c[j] == C_END_OUT);
                 }
+                if (e == (int64_t)L && __ballot(end_mine) == 0) {
+                    st = PARASON_PACK_NO_OUTLINE_END;
+                    break;
+                }
+                o = wave_max_pos(best, lane);
+                if (o >= 1 && o - 1 >= lo) {
+                    bool par_mine = false;
+#pragma unroll
+                    for (int j = 0; j < CHUNK_J; ++j) par_mine = par_mine || (lo + lane + WAVE * j == o - 1 && c[j] == C_PAR);
+                    par_before = __ballot(par_mine) != 0 ? 1 : 0;
+                }
+            }
+            if (st == 0) {
                 /* the tag before <Outlines> must be <Parallel>: right before it,
                  * or with only Text between when lenient */
-                const int64_t q = (a.lenient && o >= 1) ? last_tag_before(a, g, o, lane, contig) : o - 1;
-                if (o < 0 || q < 0 || classify(a.tm, a.tokens[g + q], contig) != C_PAR) st = PARASON_PACK_NO_OUTLINE;
+                bool par_ok;
+                if (a.lenient) {
+                    const int64_t q = o >= 1 ? last_tag_before(a, g, o, lane, contig) : -1;
+                    par_ok = q >= 0 && classify(a.tm, a.tokens[g + q], contig) == C_PAR;
+                } else {
+                    par_ok = o >= 1 && (par_before >= 0 ? par_before == 1
+                                                        : classify(a.tm, a.tokens[g + o - 1], contig) == C_PAR);
+                }
+                if (o < 0 || !par_ok) st = PARASON_PACK_NO_OUTLINE;
             }
             if (st != 0) {
                 if (lane == 0) {
@@ -398,7 +416,8 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
                         len = P - pp - 1;
                     }
                 }
-                const int64_t incl = wave_incl_scan(len, lane);
+                /* entry text lengths and their sums within a chunk are below L */
+                const int64_t incl = dpp_incl_scan<OpAdd>((int32_t)len, lane);
                 if (WRITE && act && (J & 1)) {
                     const int64_t k = J >> 1;
                     const int64_t w = w0 + k;
@@ -409,7 +428,7 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
                     a.ctx_entry[w] = (int32_t)k;
                     a.ctx_kind[w] = pc == C_SUB ? (int32_t)T_SUB : (int32_t)T_TRI;
                 }
-                text += __shfl(incl, WAVE - 1, WAVE);
+                text += lane63((int32_t)incl);
             }
             if (base > 0) {
                 const uint32_t y = ev[base - 1];
