@@ -17,7 +17,7 @@ constexpr int COPY_BLOCKS_PER_CU = 8;
 /* Workspace of fork (K = 3 counts per row: workers, context tokens, copy
  * units) or join (K = 1). */
 struct PackLayout {
-    size_t counts, outl, tile_sum, tile_off, tok_off, unit_off, over, end;
+    size_t counts, outl, tile_sum, tile_off, tok_off, unit_off, summ, over, end;
     int64_t tiles;
 };
 
@@ -38,6 +38,8 @@ PackLayout pack_layout(int64_t n, int K)
     o = align_up(o + (size_t)(n + 1) * sizeof(int64_t));
     L.unit_off = o;
     if (K == 3) o = align_up(o + (size_t)(n + 1) * sizeof(int64_t));
+    L.summ = o;
+    if (K == 3) o = align_up(o + (size_t)(n > 0 ? n : 1) * pk::SUMM_ENTRIES * sizeof(uint64_t));
     L.over = o;
     o = align_up(o + sizeof(int32_t));
     L.end = o;
@@ -117,6 +119,7 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
     fa.worker_off = out->worker_off;
     fa.tok_off = (const int64_t *)(ws + L.tok_off);
     fa.unit_off = (const int64_t *)(ws + L.unit_off);
+    fa.summ = (uint64_t *)(ws + L.summ);
     fa.over = (const int32_t *)(ws + L.over);
     fa.ctx_starts = out->ctx_starts;
     fa.ctx_lengths = out->ctx_lengths;

@@ -59,6 +59,7 @@ constexpr int PACK_TILE = PACK_THREADS * PACK_ROWS_PER_THREAD;
 constexpr int CHUNK_J = PARASON_OUTLINE_LOADS; /* loads per lane per step of the outline walk */
 constexpr int CHUNK = CHUNK_J * WAVE;          /* tokens per wave step of the outline walk */
 constexpr int COPY_GROUP = 8;   /* worker contexts fork_copy writes from one read of a row tile */
+constexpr int SUMM_ENTRIES = 8; /* outline entries per row the first walk keeps for the second */
 
 /* ---- exclusive scans of K int64 values per row -------------------------- */
 
@@ -242,6 +243,8 @@ struct ForkArgs {
     const int64_t *worker_off;
     const int64_t *tok_off;
     const int64_t *unit_off; /* [n + 1]: scan of the copy units (fork_copy) */
+    uint64_t *summ;          /* [n][SUMM_ENTRIES]: the row's first entries, text start | length << 32 |
+                                (Trial) << 63, written by the first walk */
     const int32_t *over;
     int64_t *ctx_starts;
     int32_t *ctx_lengths, *ctx_row, *ctx_entry, *ctx_kind;
@@ -297,7 +300,24 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
         const int32_t L = a.lengths[i];
         int64_t o;
         if (WRITE) {
-            if (a.status[i] != 0 || a.counts[3 * i] == 0) continue;
+            const int64_t n_e = a.counts[3 * i];
+            if (a.status[i] != 0 || n_e == 0) continue;
+            if (n_e <= SUMM_ENTRIES) {
+                /* the first walk kept every entry of this outline: the records
+                 * without a second walk (lane k: entry k) */
+                const uint64_t x = lane < n_e ? a.summ[i * SUMM_ENTRIES + lane] : 0ull;
+                const int32_t sl = a.seed ? (int32_t)((x >> 32) & 0x7fffffffu) : 0;
+                const int64_t before = dpp_incl_scan<OpAdd>(sl, lane) - sl; /* seeds of entries 0 .. k-1 */
+                if (lane < n_e) {
+                    const int64_t w = a.worker_off[i] + lane;
+                    a.ctx_starts[w] = a.tok_off[i] + lane * ((int64_t)L + 1) + before;
+                    a.ctx_lengths[w] = (int32_t)((int64_t)L + 1 + sl);
+                    a.ctx_row[w] = (int32_t)i;
+                    a.ctx_entry[w] = lane;
+                    a.ctx_kind[w] = (x >> 63) ? (int32_t)T_TRI : (int32_t)T_SUB;
+                }
+                continue;
+            }
             o = a.outl[i];
         } else {
             uint32_t st = 0;
@@ -392,7 +412,7 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
                 const uint32_t e = e0 + (uint32_t)lane;
                 const bool act = e < base;
                 int64_t len = 0; /* text tokens of the entry this lane closes */
-                int64_t J = 0;
+                int64_t J = 0, tstart = 0;
                 uint32_t pc = 0;
                 if (act) {
                     const uint32_t x = ev[e];
@@ -414,8 +434,13 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
                         /* and closes with its own tag after at least one text token */
                         ok = ok && (pc == C_SUB || pc == C_TRI) && cl == pc + 1 && P >= pp + 2;
                         len = P - pp - 1;
+                        tstart = pp + 1;
                     }
                 }
+                if (!WRITE && act && (J & 1) && (J >> 1) < SUMM_ENTRIES)
+                    a.summ[i * SUMM_ENTRIES + (J >> 1)] = (uint64_t)(uint32_t)tstart |
+                                                         ((uint64_t)(uint32_t)len << 32) |
+                                                         ((uint64_t)(pc == C_TRI) << 63);
                 /* entry text lengths and their sums within a chunk are below L */
                 const int64_t incl = dpp_incl_scan<OpAdd>((int32_t)len, lane);
                 if (WRITE && act && (J & 1)) {
@@ -653,9 +678,10 @@ __global__ void __launch_bounds__(PACK_THREADS) fork_copy(ForkArgs a)
                 const int64_t e = g * COPY_GROUP + lane;
                 /* first text token of entry e: without gaps, o + 2 + 2e + the texts
                  * before it (see fork_outline); with gaps, searched */
-                const int64_t ft = (a.lenient && a.seed)
-                                       ? group_text_pos(a, src, o, L, g * COPY_GROUP, nd, slots[wv], lane)
-                                       : o + 2 + 2 * e + (cs - to - e * (L + 1));
+                int64_t ft;
+                if (!(a.lenient && a.seed)) ft = o + 2 + 2 * e + (cs - to - e * (L + 1));
+                else if (w1 - w0 <= SUMM_ENTRIES) ft = lane < nd ? (int64_t)(uint32_t)a.summ[r * SUMM_ENTRIES + lane] : 0;
+                else ft = group_text_pos(a, src, o, L, g * COPY_GROUP, nd, slots[wv], lane);
                 for (int k = 0; k < nd; ++k) {
                     const int64_t c = __shfl(cs, k, WAVE);
                     wave_tail(a.ctx_tokens, c + L, c + __shfl(len, k, WAVE), src, __shfl(ft, k, WAVE), a.thread_id,
