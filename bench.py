@@ -145,8 +145,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(groups shard across GPUs with no exchange; see the design notes). Use --gpus 1.",
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(groups would shard across GPUs with no exchange). Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 
