@@ -1034,6 +1034,14 @@ __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_l
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
         const int32_t t[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
+        if (MODE == TM_CONTIG) {
+            /* Contiguous ids are base .. base + 11 with base >= 0: a vector
+             * holds a tag only if its largest (signed) token reaches base.
+             * Three VALU operations per lane instead of eight settle the
+             * vectors without a tag (about four in five at 0.1 % tags). */
+            const int32_t hi = max(max(t[0], t[1]), max(t[2], t[3]));
+            if (__ballot(hi >= tm.base) == 0) continue; /* wave-uniform */
+        }
         const int32_t q0 = 4 * (i * WAVE + lane);
         uint64_t b[4];
 #pragma unroll
