@@ -120,11 +120,13 @@ void find_tag_hash(pk::TagMatch &tm)
     }
 }
 
-/* The three tiers of the row automaton, in the grammar's strict or lenient
- * form. */
+/* The tiers of the row automaton, in the grammar's strict or lenient form.
+ * The deep tier is a launch of its own only when deep_launch is set (the
+ * batch-wide statistics need every row first); otherwise group_reward runs
+ * it. */
 template <bool LENIENT>
-void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, const uint8_t *mode, int32_t *counters,
-                 int32_t *mid_rows, int32_t *deep_rows, int32_t *deep_frames, uint32_t *deep_bits,
+void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, uint8_t *mode, int32_t *counters,
+                 int32_t *mid_rows, int32_t *deep_rows, int32_t *deep_frames, uint32_t *deep_bits, bool deep_launch,
                  hipStream_t stream)
 {
     /* A small batch (fewer rows than ROWS_WAVES_PER_CU waves on every CU):
@@ -149,7 +151,9 @@ void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, const
         pk::rows_mid<LENIENT><<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(
             ra, mode, counters, mid_rows, deep_rows);
     }
-    pk::rows_deep<LENIENT><<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames, deep_bits);
+    if (deep_launch)
+        pk::rows_deep<LENIENT><<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames,
+                                                                 deep_bits);
 }
 
 }  // namespace
@@ -327,10 +331,14 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.tm = h->tm;
     ra.out = row_out;
     const pk::GatherArgs ga{starts, n_traj, mis, seg_off, cap, seg_count, events, mode, counters + 2, split_rows};
-    if (h->cfg.flags & PARASON_CFG_LENIENT_GAPS)
-        launch_rows<true>(ra, ga, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
+    const bool lenient = (h->cfg.flags & PARASON_CFG_LENIENT_GAPS) != 0;
+    const bool batch_stats = (h->cfg.flags & PARASON_CFG_BATCH_STATS) != 0;
+    if (lenient)
+        launch_rows<true>(ra, ga, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, batch_stats,
+                          stream);
     else
-        launch_rows<false>(ra, ga, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, stream);
+        launch_rows<false>(ra, ga, cus, mode, counters, mid_rows, deep_rows, deep_frames, deep_bits, batch_stats,
+                           stream);
 
     pk::RewardArgs rw;
     rw.total = out->total;
@@ -355,7 +363,7 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     rw.saved = out->saved;
     rw.batch = nullptr;
     rw.n = n_traj;
-    if (h->cfg.flags & PARASON_CFG_BATCH_STATS) {
+    if (batch_stats) {
         pk::StatsArgs st{out->total, out->latency, out->n_subtask, out->n_trial, out->flags, n_traj, red_d, red_i, stats};
         pk::batch_stats_tiles<1><<<dim3(tiles), dim3(pk::RED_THREADS), 0, stream>>>(st);
         pk::batch_stats_final<1><<<dim3(1), dim3(pk::RED_THREADS), 0, stream>>>(st, L.n_tiles);
@@ -364,7 +372,10 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
         rw.batch = stats;
         pk::batch_reward<<<dim3((unsigned)((n_traj + 255) / 256)), dim3(256), 0, stream>>>(rw);
     } else {
-        pk::group_reward<<<dim3((unsigned)((n_traj + 255) / 256)), dim3(256), 0, stream>>>(rw);
+        const pk::DeepArgs da{ra, mode, counters, deep_rows, deep_frames, deep_bits};
+        const dim3 grid((unsigned)((n_traj + 255) / 256));
+        if (lenient) pk::group_reward<true><<<grid, dim3(256), 0, stream>>>(rw, da);
+        else pk::group_reward<false><<<grid, dim3(256), 0, stream>>>(rw, da);
     }
     if (out->metrics) {
         pk::MetricsArgs ma{out->total, out->latency, out->n_subtask, out->n_trial, out->flags, correct,

@@ -36,6 +36,10 @@
  *        handed to rows_deep.
  *   rows_deep  (one thread, only rows rows_mid or rows_par handed over)
  *        The same automaton with frames and entry types in global workspace.
+ *        Only with batch-wide statistics is this a launch of its own; with
+ *        per-group statistics the first block of group_reward runs these rows
+ *        and then the rewards of their groups (mode[i] bit MODE_DEEP marks
+ *        them, so every other block skips those groups).
  *   group_reward  (one thread per row)
  *        Statistics and Definition 3.1 in IEEE double, fixed order.
  *
@@ -50,6 +54,11 @@
 #include "device_common.h"
 
 namespace pk {
+
+/* mode[i], one byte per row: where its events are, and whether the deep tier
+ * evaluates it. */
+constexpr uint8_t MODE_COMPACT = 1; /* one compact list with row positions (else per-segment slots) */
+constexpr uint8_t MODE_DEEP = 2;    /* listed for the single-thread tier with global frames */
 
 /* ------------------------------------------------------------------ plan */
 
@@ -577,7 +586,7 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
     return true;
 }
 
-/* One thread per row.  mode[r] == 1: the scan left the row's events as one
+/* One thread per row.  mode[r] == MODE_COMPACT: the scan left the row's events as one
  * compact list; 0: per-segment slots.  A row that needs more than FAST_DEPTH
  * frames (or more than 64 entries in an open block) is listed for rows_mid.
  * Few frames keep the LDS per block small, so that many waves hide the
@@ -607,7 +616,7 @@ __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__rest
     A.st.tid = threadIdx.x;
     A.st.nt = blockDim.x;
     A.init();
-    if (drive_row(a, r, start + a.mis, len, mode[r] == 1, A)) A.finish(len);
+    if (drive_row(a, r, start + a.mis, len, (mode[r] & MODE_COMPACT) != 0, A)) A.finish(len);
     if (A.overflow) {
         mid_rows[atomicAdd(&counters[0], 1)] = (int32_t)r;
         return; /* rows_mid writes this row */
@@ -619,7 +628,7 @@ __global__ void __launch_bounds__(64) rows_fast(RowArgs a, const uint8_t *__rest
  * MID_DEPTH frames per row in LDS; rows that need still more are listed for
  * rows_deep. */
 template <bool LENIENT>
-__global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restrict__ mode,
+__global__ void __launch_bounds__(64) rows_mid(RowArgs a, uint8_t *__restrict__ mode,
                                                int32_t *__restrict__ counters, const int32_t *__restrict__ mid_rows,
                                                int32_t *__restrict__ deep_rows)
 {
@@ -634,8 +643,9 @@ __global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restr
         A.st.tid = threadIdx.x;
         A.st.nt = blockDim.x;
         A.init();
-        if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
+        if (drive_row(a, r, a.starts[r] + a.mis, len, (mode[r] & MODE_COMPACT) != 0, A)) A.finish(len);
         if (A.overflow) {
+            mode[r] |= MODE_DEEP;
             int32_t slot = atomicAdd(&counters[1], 1);
             deep_rows[slot] = (int32_t)r;
         } else {
@@ -645,15 +655,12 @@ __global__ void __launch_bounds__(64) rows_mid(RowArgs a, const uint8_t *__restr
 }
 
 /* Rows whose nesting or entry count exceeded the LDS stores, one after the
- * other, on a single thread with frames in global workspace. */
+ * other, on the calling thread with frames in global workspace. */
 template <bool LENIENT>
-__global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__restrict__ mode,
-                                                const int32_t *__restrict__ counters,
-                                                const int32_t *__restrict__ deep_rows, int32_t *__restrict__ frames,
-                                                uint32_t *__restrict__ bits)
+__device__ void run_deep_rows(const RowArgs &a, const uint8_t *__restrict__ mode, int32_t n_deep,
+                              const int32_t *__restrict__ deep_rows, int32_t *__restrict__ frames,
+                              uint32_t *__restrict__ bits)
 {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    const int32_t n_deep = counters[1];
     for (int32_t i = 0; i < n_deep; ++i) {
         const int64_t r = deep_rows[i];
         const int32_t len = a.lengths[r];
@@ -662,12 +669,24 @@ __global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__rest
         A.st.bits = bits;
         A.st.esp = 0;
         A.init();
-        if (drive_row(a, r, a.starts[r] + a.mis, len, mode[r] == 1, A)) A.finish(len);
+        if (drive_row(a, r, a.starts[r] + a.mis, len, (mode[r] & MODE_COMPACT) != 0, A)) A.finish(len);
         if (A.overflow)
             write_row(a.out, r, len, 0, 0, 0, 0, 0, 0, PARASON_FLAG_DEPTH_LIMIT);
         else
             write_result(a.out, r, len, A);
     }
+}
+
+/* The deep rows on a single thread, as a launch of its own: used when the
+ * batch-wide statistics need every row before the reward. */
+template <bool LENIENT>
+__global__ void __launch_bounds__(64) rows_deep(RowArgs a, const uint8_t *__restrict__ mode,
+                                                const int32_t *__restrict__ counters,
+                                                const int32_t *__restrict__ deep_rows, int32_t *__restrict__ frames,
+                                                uint32_t *__restrict__ bits)
+{
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    run_deep_rows<LENIENT>(a, mode, counters[1], deep_rows, frames, bits);
 }
 
 /* ------------------------------------------------------------------ rows_par */
@@ -765,7 +784,7 @@ __device__ __forceinline__ int32_t last_lane_at_most(int32_t x, int32_t f)
  * automaton call site of this kernel).  Split rows are read from their
  * segments' lists directly (no gather_rows launch for a small batch). */
 template <bool LENIENT>
-__global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restrict__ mode,
+__global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ mode,
                                                int32_t *__restrict__ counters, int32_t *__restrict__ deep_rows)
 {
     __shared__ int32_t sP[PAR_EVENTS], sC[PAR_EVENTS], sD[PAR_EVENTS], sT[PAR_EVENTS];
@@ -792,7 +811,7 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
     const int64_t g = start + a.mis;
     int32_t m = 0;
     bool held = true;
-    if (md == 1) {
+    if (md & MODE_COMPACT) {
         m = a.seg_count[s0];
         held = m <= PAR_EVENTS;
         const uint32_t *list = a.events + s0 * EV_CAP;
@@ -908,8 +927,11 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, const uint8_t *__restr
             A.st.tid = 0;
             A.st.nt = 1;
             A.init();
-            if (drive_row(a, r, g, len, md == 1, A)) A.finish(len);
-            if (A.overflow) deep_rows[atomicAdd(&counters[1], 1)] = (int32_t)r;
+            if (drive_row(a, r, g, len, (md & MODE_COMPACT) != 0, A)) A.finish(len);
+            if (A.overflow) {
+                mode[r] = md | MODE_DEEP;
+                deep_rows[atomicAdd(&counters[1], 1)] = (int32_t)r;
+            }
             else write_result(a.out, r, len, A);
         }
         return;
@@ -1133,7 +1155,7 @@ __device__ __forceinline__ void flush_row(const ScanArgs &a, int64_t row, int64_
     for (uint32_t i = lane; i < lcnt; i += WAVE) dst[i] = lev[i];
     if (lane == 0) {
         a.seg_count[first] = (int32_t)lcnt;
-        a.mode[row] = 1;
+        a.mode[row] = MODE_COMPACT;
     }
 }
 
@@ -1297,7 +1319,7 @@ __device__ __forceinline__ void gather_row(const GatherArgs &a, int64_t row, int
     }
     if (lane == 0) {
         a.seg_count[s0] = (int32_t)carry;
-        a.mode[row] = 1;
+        a.mode[row] = MODE_COMPACT;
     }
 }
 
@@ -1443,23 +1465,12 @@ __device__ __forceinline__ void group_reward_lanes(const RewardArgs &a, int64_t 
     write_reward(a, r, zscore(xT, mT, lat_equal), zscore(xs, ms, sub_equal), zscore(xr, mr, tri_equal), xs, xr);
 }
 
-/* One thread per row.  A group within one wave shares its values by shuffles
- * (group_reward_lanes); otherwise every thread of a group computes the group's
- * moments itself from memory.  Either way the sums run in the group's row
- * order, so every thread of a group holds the same values; a group takes G
- * threads instead of one, which keeps the GPU busy when a batch has few
- * groups (an RL step has 128). */
-__global__ void __launch_bounds__(256) group_reward(RewardArgs a)
+/* Row r's reward from its group's values in memory, in the group's row order
+ * (any group size, any thread layout). */
+__device__ __forceinline__ void group_reward_memory(const RewardArgs &a, int64_t r)
 {
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= a.n) return; /* n is a multiple of G: whole groups only */
     const int32_t G = a.G;
-    if (G <= WAVE && (G & (G - 1)) == 0) {
-        group_reward_lanes(a, r, G);
-        return;
-    }
     const int64_t r0 = r - r % G;
-
     bool evaluated = true;
     bool lat_equal = true;
     for (int32_t i = 0; i < G; ++i) {
@@ -1479,6 +1490,55 @@ __global__ void __launch_bounds__(256) group_reward(RewardArgs a)
     const int32_t i = (int32_t)(r - r0);
     write_reward(a, r, zscore(xT(i), mT, lat_equal), zscore(xs(i), ms, sub_equal), zscore(xr(i), mr, tri_equal),
                  xs(i), xr(i));
+}
+
+/* The deep tier's rows (listed by rows_par or rows_mid), run by the first
+ * block of group_reward instead of a launch of their own. */
+struct DeepArgs {
+    RowArgs rows;
+    const uint8_t *mode;
+    const int32_t *counters; /* counters[1]: rows in deep_rows */
+    const int32_t *deep_rows;
+    int32_t *frames;
+    uint32_t *bits;
+};
+
+/* One thread per row.  A group within one wave shares its values by shuffles
+ * (group_reward_lanes); otherwise every thread of a group computes the group's
+ * moments itself from memory.  Either way the sums run in the group's row
+ * order, so every thread of a group holds the same values; a group takes G
+ * threads instead of one, which keeps the GPU busy when a batch has few
+ * groups (an RL step has 128).
+ *
+ * Rows listed for the deep tier (normally none) are evaluated here first, by
+ * thread 0 of block 0; after a barrier that block computes the rewards of the
+ * groups holding them (a group listed twice is written twice, with the same
+ * values).  Every block skips those groups: it tells them by the MODE_DEEP
+ * mark, which nothing writes during this launch, so no block reads a row
+ * another block is writing. */
+template <bool LENIENT>
+__global__ void __launch_bounds__(256) group_reward(RewardArgs a, DeepArgs d)
+{
+    const int32_t G = a.G;
+    const int32_t n_deep = d.counters[1]; /* the same for every thread */
+    if (n_deep > 0 && blockIdx.x == 0) {
+        if (threadIdx.x == 0) run_deep_rows<LENIENT>(d.rows, d.mode, n_deep, d.deep_rows, d.frames, d.bits);
+        __syncthreads();
+        for (int64_t k = threadIdx.x; k < (int64_t)n_deep * G; k += blockDim.x) {
+            const int64_t rd = d.deep_rows[k / G];
+            group_reward_memory(a, rd - rd % G + k % G);
+        }
+    }
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= a.n) return; /* n is a multiple of G: whole groups only */
+    if (n_deep > 0) {
+        const int64_t r0 = r - r % G;
+        bool deep = false;
+        for (int32_t i = 0; i < G; ++i) deep = deep || (d.mode[r0 + i] & MODE_DEEP) != 0;
+        if (deep) return; /* the whole group returns here */
+    }
+    if (G <= WAVE && (G & (G - 1)) == 0) group_reward_lanes(a, r, G);
+    else group_reward_memory(a, r);
 }
 
 /* One thread per row; mu, sigma of the whole batch from batch_stats. */
