@@ -142,7 +142,14 @@ def main():
     ap.add_argument("--decode-batch", type=int, default=1024)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device-to-device copy of 4 GiB (HBM counter calibration)")
+    ap.add_argument("--traffic-summary", metavar="DIR",
+                    help="only summarise the four rocprofv3 --pmc runs under DIR (prof_fetch, prof_write, "
+                         "prof_copy_fetch, prof_copy_write) into the scan's traffic record under profiles/")
     args = ap.parse_args()
+
+    if args.traffic_summary:
+        traffic_summary(args.traffic_summary)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
@@ -620,6 +627,49 @@ def bench_fork(args):
                            "ms": jcopy_ms, "GB/s": 8 * JT / (jcopy_ms * 1e-3) / 1e9},
     }
     print(json.dumps(res), flush=True)
+
+
+def traffic_summary(d):
+    """HBM bytes per scan_rows launch from FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch), each scaled by what the same counter reads for a plain 4 GiB
+    device-to-device copy; the algorithmic bytes come from the JSON line the
+    profiled FETCH_SIZE run printed."""
+    import csv
+    import glob
+
+    def per_kernel(sub, counter):
+        acc = {}
+        for r in csv.DictReader(open(glob.glob(os.path.join(d, sub, "*counter_collection.csv"))[0])):
+            if r["Counter_Name"] == counter:
+                acc.setdefault(r["Kernel_Name"].split("(")[0].replace("void ", ""), []).append(
+                    float(r["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in acc.items()}, {k: len(v) for k, v in acc.items()}
+
+    cf, _ = per_kernel("prof_copy_fetch", "FETCH_SIZE")
+    cw, _ = per_kernel("prof_copy_write", "WRITE_SIZE")
+    copy = next(k for k in cf if "copyBuffer" in k)
+    fetch_factor = cf[copy] * 1024 / (4 << 30)
+    write_factor = cw[copy] * 1024 / (4 << 30)
+    f, nf = per_kernel("prof_fetch", "FETCH_SIZE")
+    w, _ = per_kernel("prof_write", "WRITE_SIZE")
+    scan = next(k for k in f if "scan_rows" in k)
+    line = [ln for ln in open(os.path.join(d, "prof_fetch.log")) if ln.startswith("{")][-1]
+    run = json.loads(line)
+    alg = run["roofline"]["algorithmic_bytes"]
+    traffic = f[scan] * 1024 / fetch_factor + w[scan] * 1024 / write_factor
+    rec = {"kernel": "scan_rows", "workload": run["config"]["workload"].split(":")[0],
+           "kernel_source_sha": kernel_sha(), "fetch_kib_per_launch": f[scan], "write_kib_per_launch": w[scan],
+           "launches": nf[scan],
+           "copy_calibration": {"kernel": copy, "bytes_read": 4 << 30, "bytes_written": 4 << 30,
+                                "fetch_kib": cf[copy], "write_kib": cw[copy], "fetch_factor": fetch_factor,
+                                "write_factor": write_factor},
+           "bytes_per_launch": traffic, "algorithmic_bytes_per_launch": alg,
+           "traffic_over_algorithmic": traffic / alg,
+           "other_kernels_gb_per_launch": {k: [f[k] * 1024 / fetch_factor / 1e9, w.get(k, 0.0) * 1024 / write_factor / 1e9]
+                                           for k in f if k.startswith("pk::") or "pk::" in k}}
+    with open(PROFILE_TRAFFIC, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec, indent=1))
 
 
 def kernel_sha():
