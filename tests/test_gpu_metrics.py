@@ -135,3 +135,36 @@ def test_metrics_on_large_workload_properties(dev):
     assert 0 <= m["trigger_ratio"] <= 1 and 0 <= m["accuracy"] <= 1
     del tok_d, out
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("n_rows", [64, 12288])
+@pytest.mark.parametrize("batch_stats", [False, True])
+def test_deep_rows_with_metrics(dev, n_rows, batch_stats):
+    """Rows nested beyond the LDS tiers (34-60 deep) mixed with shallow ones,
+    under both normalisations and with the batch metrics: the deep tier runs
+    inside the per-group reward launch, or as a launch of its own before the
+    batch-wide statistics.  64 rows take the one-wave row kernel, 12,288 the
+    per-lane one."""
+    from test_gpu_parity import deep_stream, pack
+    import grammar_pins as GP
+
+    log("case deep rows n=%d batch_stats=%s" % (n_rows, batch_stats))
+    rng = np.random.default_rng(n_rows + batch_stats)
+    depths = np.concatenate([rng.integers(34, 61, size=6), rng.integers(6, 34, size=n_rows // 4),
+                             rng.integers(1, 6, size=n_rows - 6 - n_rows // 4)])
+    rng.shuffle(depths)
+    streams = [deep_stream(int(d), GP.TRI if d % 2 else GP.SUB) for d in depths]
+    tokens, starts, lengths = pack(streams, TAGS)
+    n = lengths.size
+    co = (np.arange(n) % 4 != 0).astype(np.uint8)
+    flags = PX.CFG_BATCH_STATS if batch_stats else 0
+    px = PX.Parason(TAGS, group_size=G, flags=flags, **DEFAULT_COEF)
+    out = px.run(to_dev(tokens, torch.int32, dev), to_dev(starts, torch.int64, dev), to_dev(lengths, torch.int32, dev),
+                 to_dev(co, torch.uint8, dev), metrics=True)
+    torch.cuda.synchronize()
+    got = fetch(out)
+    rows, R, rs, rt, eta = oracle_expect(tokens, starts, lengths, co, TAGS, G, DEFAULT_COEF,
+                                         O.CFG_BATCH_STATS if batch_stats else 0)
+    compare(got, rows, R, rs, rt, eta, what="deep rows")
+    check_metrics(got["metrics"], rows, co, R)
+    assert int(np.max(got["max_depth"])) >= 34

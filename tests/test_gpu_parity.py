@@ -78,7 +78,10 @@ def pack(streams, tags, text_ids=None):
     toks = []
     for s in streams:
         t = np.array(GP.to_tokens(s, tags), dtype=np.int32) if len(s) else np.zeros(0, np.int32)
-        text = rng.integers(0, 150000, size=t.size).astype(np.int32)
+        if text_ids is None:
+            text = rng.integers(0, 150000, size=t.size).astype(np.int32)
+        else:
+            text = rng.choice(np.asarray(text_ids, np.int32), size=t.size)
         text = np.where(np.isin(text, tags), 7, text)
         is_text = np.array([c == GP.TEXT for c in s], dtype=bool) if len(s) else np.zeros(0, bool)
         toks.append(np.where(is_text, text, t))
@@ -167,6 +170,31 @@ def test_adversarial_streams(dev, tags):
     compare(got, *oracle_expect(tokens, starts, lengths, correct, tag_ids, G, coef), what="adversarial")
     assert int(np.sum(got["max_depth"] == 1000)) == 1
     log("adversarial: %d rows ok" % n)
+
+
+@pytest.mark.parametrize("tags", ["contiguous", "scattered", "scattered-compare", "low-ids"])
+def test_text_ids_over_the_whole_int32_range(dev, tags):
+    """Every id that is not one of the twelve tags is Text: negative ids, ids
+    just outside a contiguous tag range and the int32 extremes, mixed with
+    ids drawn from the whole int32 range (the contiguous scan first compares
+    each vector's largest signed token with the first tag id)."""
+    log("case text ids over int32 tags=%s" % tags)
+    tag_ids = {"contiguous": TAGS, "low-ids": LOW_IDS}.get(tags, S.SCATTERED_TAGS)
+    lo, hi = min(tag_ids), max(tag_ids)
+    i32 = np.iinfo(np.int32)
+    edges = [i32.min, i32.min + 1, -(1 << 24), -2, -1, 0, 1, lo - 1, hi + 1, hi + 2, i32.max - 1, i32.max]
+    wide = np.random.default_rng(5).integers(i32.min, i32.max, size=4096, endpoint=True)
+    text_ids = np.array([e for e in edges if i32.min <= e <= i32.max] * 64 + list(wide), dtype=np.int64)
+    text_ids = text_ids[~np.isin(text_ids, tag_ids)].astype(np.int32)
+    tokens, starts, lengths = pack(adversarial_streams(), tag_ids, text_ids=text_ids)
+    assert np.any(tokens < 0) and np.any(tokens == i32.max)
+    n = lengths.size
+    correct = (np.arange(n) % 3 != 1).astype(np.uint8)
+    px, coef = px_for(tag_ids, flags=PX.CFG_TAG_COMPARE if tags == "scattered-compare" else 0)
+    got = run_gpu(px, to_dev(tokens, torch.int32, dev), to_dev(starts, torch.int64, dev),
+                  to_dev(lengths, torch.int32, dev), to_dev(correct, torch.uint8, dev))
+    compare(got, *oracle_expect(tokens, starts, lengths, correct, tag_ids, G, coef), what="int32 text ids")
+    log("int32 text ids: %d rows ok" % n)
 
 
 def test_many_rows_beyond_the_first_tier(dev):
