@@ -3,8 +3,8 @@
 TEST INFRASTRUCTURE.  Only the tests and the smoke check may import this
 module; the product path never does.  Plain numpy in float64.
 
-The paper trains with GRPO in VeRL using "lower clip ratio 0.2, and upper clip
-ratio 0.28" and 8 rollouts per prompt (Sec. 4, "Training Framework"); it does
+The paper trains with GRPO in VeRL, 8 rollouts per prompt, and separate lower
+and upper clip ratios of 0.2 and 0.28 (Sec. 4, "Training Framework"); it does
 not write the objective out.  This oracle therefore follows the textbook
 definitions, each a reading listed in the design notes:
 
@@ -19,23 +19,19 @@ definitions, each a reading listed in the design notes:
 * token-level mean over every generated token of the batch:
   J = sum_t L_t / N_tokens; the loss is -J; no KL or entropy term.
 
-The clip decision is taken on the float32 log-ratio d = logp - logp_old
-(computed in float32, as the kernel does) against the float32 thresholds
-ln(1 + eps_high) and ln(1 - eps_low): rho > 1 + eps_high exactly when
-d > ln(1 + eps_high).  Values (rho, L, gradient) are evaluated in float64.
+Everything is float64 from the float32 inputs: d = logp - logp_old (exact in
+float64 for log-probabilities of similar magnitude), rho = exp(d), and the clip
+decision is the definition itself: for A > 0 the clipped term is the minimum
+exactly when rho > 1 + eps_high, for A < 0 exactly when rho < 1 - eps_low (at
+equality both terms are equal; the unclipped one is taken).
 
 Gradient of the loss with respect to logp_t:
-  d(-J)/d logp_t = -A rho_t / N_tokens where the unclipped term is the minimum
-  (A > 0 and d <= thr_high, or A < 0 and d >= thr_low), else 0.
+  d(-J)/d logp_t = -A rho_t / N_tokens where the unclipped term is the minimum,
+  else 0.
 """
 from __future__ import annotations
 
 import numpy as np
-
-
-def thresholds(eps_low: float, eps_high: float):
-    """float32 ln(1 - eps_low), ln(1 + eps_high)."""
-    return np.float32(np.log1p(-np.float64(eps_low))), np.float32(np.log1p(np.float64(eps_high)))
 
 
 def advantages(reward, group_size: int) -> np.ndarray:
@@ -68,13 +64,16 @@ def surrogate(logp, logp_old, starts, lengths, adv, eps_low: float, eps_high: fl
     n_tokens: N of the token-level mean, the generated tokens of the whole
     batch; by default the tokens of the rows given (pass the batch's N when
     the rows are a sample of a larger batch).
-    Returns dict(loss, tokens, clip_high, clip_low, grad) where grad is float64
-    with NaN outside the rows."""
+    Returns dict(loss, tokens, clip_high, clip_low, grad, clipped, d): grad is
+    float64 with NaN outside the rows; clipped (bool) marks the tokens whose
+    clipped term is the minimum; d is the float64 log-ratio (NaN outside)."""
     logp = np.asarray(logp, np.float32)
     logp_old = np.asarray(logp_old, np.float32)
-    thr_low, thr_high = thresholds(eps_low, eps_high)
     grad = np.full(logp.size, np.nan)
+    dd = np.full(logp.size, np.nan)
+    clipped_all = np.zeros(logp.size, bool)
     n_tok = int(np.sum(np.maximum(lengths, 0))) if n_tokens is None else int(n_tokens)
+    hi, lo = 1.0 + float(eps_high), 1.0 - float(eps_low)
     total = 0.0
     clip_hi = clip_lo = 0
     for i in range(len(starts)):
@@ -82,20 +81,21 @@ def surrogate(logp, logp_old, starts, lengths, adv, eps_low: float, eps_high: fl
         s, n = int(starts[i]), int(lengths[i])
         if n <= 0:
             continue
-        d32 = (logp[s: s + n] - logp_old[s: s + n]).astype(np.float32)  # float32 subtraction
-        rho = np.exp(d32.astype(np.float64))
+        d = logp[s: s + n].astype(np.float64) - logp_old[s: s + n].astype(np.float64)
+        rho = np.exp(d)
         if a > 0:
-            unclipped = d32 <= thr_high
-            clip_hi += int(np.sum(~unclipped))
+            clipped = rho > hi
+            clip_hi += int(np.sum(clipped))
         elif a < 0:
-            unclipped = d32 >= thr_low
-            clip_lo += int(np.sum(~unclipped))
+            clipped = rho < lo
+            clip_lo += int(np.sum(clipped))
         else:
-            unclipped = np.ones(n, bool)
-        # min(rho A, clip(rho) A): the unclipped term where the decision says
-        # so, else the bound the clip holds rho at
-        L = np.where(unclipped, rho * a, np.where(a > 0, (1.0 + eps_high) * a, (1.0 - eps_low) * a))
+            clipped = np.zeros(n, bool)
+        # min(rho A, clip(rho) A): the clip bound where the decision says so
+        L = np.where(clipped, (hi if a > 0 else lo) * a, rho * a)
         total += float(np.sum(L))
-        grad[s: s + n] = np.where(unclipped, -a * rho / n_tok, 0.0) if n_tok else 0.0
+        grad[s: s + n] = np.where(clipped, 0.0, -a * rho / n_tok) if n_tok else 0.0
+        clipped_all[s: s + n] = clipped
+        dd[s: s + n] = d
     loss = -total / n_tok if n_tok else 0.0
-    return dict(loss=loss, tokens=n_tok, clip_high=clip_hi, clip_low=clip_lo, grad=grad)
+    return dict(loss=loss, tokens=n_tok, clip_high=clip_hi, clip_low=clip_lo, grad=grad, clipped=clipped_all, d=dd)

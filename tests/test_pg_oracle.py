@@ -50,8 +50,8 @@ def test_surrogate_matches_textbook_objective():
         adv = PG.advantages(reward, 8).astype(np.float32)
         res = PG.surrogate(new, old, starts, lengths, adv, EPS_LO, EPS_HI)
         ref = textbook_loss(new.astype(np.float64), old.astype(np.float64), starts, lengths, adv.astype(np.float64))
-        # differences only from the float32 log-ratio used for rho in the oracle
-        assert abs(res["loss"] - ref) <= 1e-6 * max(1.0, abs(ref))
+        # both in float64 from the same inputs: summation order only
+        assert abs(res["loss"] - ref) <= 1e-13 * max(1.0, abs(ref))
         assert res["tokens"] == lengths.sum()
 
 
@@ -61,8 +61,8 @@ def test_gradient_matches_finite_differences():
     res = PG.surrogate(new, old, starts, lengths, adv, EPS_LO, EPS_HI)
     lp = new.astype(np.float64)
     lo = old.astype(np.float64)
-    thr_lo, thr_hi = PG.thresholds(EPS_LO, EPS_HI)
-    d = (new - old).astype(np.float32)
+    thr_lo, thr_hi = np.log(1 - EPS_LO), np.log(1 + EPS_HI)
+    d = lp - old.astype(np.float64)
     h = 1e-6
     checked = 0
     for t in range(0, lp.size, 3):
@@ -92,6 +92,22 @@ def test_closed_forms():
     assert res["loss"] == 0 and np.all(res["grad"] == 0) and res["clip_high"] == res["clip_low"] == 0
 
 
-def test_thresholds_are_the_clip_bounds():
-    lo, hi = PG.thresholds(EPS_LO, EPS_HI)
-    assert abs(np.exp(np.float64(hi)) - 1.28) < 1e-7 and abs(np.exp(np.float64(lo)) - 0.8) < 1e-7
+def test_clip_decision_at_the_bounds():
+    """Tokens placed just inside and just outside rho = 1 + eps_high and
+    rho = 1 - eps_low: the decision follows the clip bounds of the objective,
+    and matches the textbook min/clip form token by token."""
+    rng = np.random.default_rng(7)
+    n = 4000
+    old = (-rng.random(n) * 4).astype(np.float32)
+    off = rng.choice([np.log(1 + EPS_HI), np.log(1 - EPS_LO)], n) + rng.uniform(-1e-5, 1e-5, n)
+    new = (old.astype(np.float64) + off).astype(np.float32)
+    d = new.astype(np.float64) - old.astype(np.float64)
+    for a in (1.5, -0.75):
+        res = PG.surrogate(new, old, np.array([0]), np.array([n]), np.array([a], np.float32), EPS_LO, EPS_HI)
+        rho = np.exp(d)
+        want = rho > 1 + EPS_HI if a > 0 else rho < 1 - EPS_LO
+        assert np.array_equal(res["clipped"], want)
+        assert 100 < want.sum() < n - 100  # both sides of the bound are exercised
+        # the textbook form picks the clipped term exactly where it is strictly smaller
+        terms = np.minimum(rho * a, np.clip(rho, 1 - EPS_LO, 1 + EPS_HI) * a)
+        assert np.array_equal(terms < rho * a, want)
