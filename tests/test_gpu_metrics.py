@@ -76,7 +76,7 @@ def test_batch_stats_parity(dev, workload):
     torch.cuda.synchronize()
     got = fetch(out)
     rows, R, rs, rt, eta = oracle_expect(tok_h, st_h, ln_h, co_h, TAGS, G, coef, O.CFG_BATCH_STATS)
-    compare(got, rows, R, rs, rt, eta, what="batch " + workload)
+    compare(got, rows, R, rs, rt, eta, what="batch " + workload, exact_reward=False)
     check_metrics(got["metrics"], rows, co_h, R)
 
 
@@ -165,6 +165,6 @@ def test_deep_rows_with_metrics(dev, n_rows, batch_stats):
     got = fetch(out)
     rows, R, rs, rt, eta = oracle_expect(tokens, starts, lengths, co, TAGS, G, DEFAULT_COEF,
                                          O.CFG_BATCH_STATS if batch_stats else 0)
-    compare(got, rows, R, rs, rt, eta, what="deep rows")
+    compare(got, rows, R, rs, rt, eta, what="deep rows", exact_reward=not batch_stats)
     check_metrics(got["metrics"], rows, co, R)
     assert int(np.max(got["max_depth"])) >= 34
