@@ -61,7 +61,8 @@ extern "C" {
 #define PARASON_ERR_PARAM (-6)     /* a reward parameter is not finite */
 #define PARASON_ERR_ALIGN (-7)     /* tokens not 4-byte aligned or workspace not 256-byte aligned */
 #define PARASON_ERR_HIP (-8)       /* a HIP call or kernel launch failed */
-#define PARASON_ERR_DEVICE (-9)    /* the current device is not gfx950 or cannot be queried */
+#define PARASON_ERR_DEVICE (-9)    /* the current device is not gfx950 or cannot be queried (checked by
+                                      every call that launches, before its first launch) */
 
 /* ---- per-row flag bits (parason_outputs.flags) ------------------------- */
 #define PARASON_FLAG_VALID (1u << 0)          /* the stream is in the language */
@@ -170,8 +171,11 @@ typedef struct parason_outputs {
 
 typedef struct parason_handle parason_handle;
 
-/* Validate *cfg and create a handle (host memory only; the current HIP device
- * must be a gfx950 GPU).  On success *out receives the handle. */
+/* Validate *cfg and create a handle (host memory only; no HIP call, so a
+ * handle can be made and workspaces sized without a GPU).  On success *out
+ * receives the handle.  Every call that launches kernels (parason_run and the
+ * other steps below) first checks that the current HIP device is a gfx950 GPU
+ * and returns PARASON_ERR_DEVICE, before any launch, when it is not. */
 int parason_create(const parason_config *cfg, parason_handle **out);
 
 /* Bytes of device workspace parason_run needs for n_traj rows whose lengths
@@ -206,6 +210,16 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
                       size_t workspace_bytes, void *stream, void *const *scan_events);
 
 void parason_destroy(parason_handle *h);
+
+/* Measurement aid, not an operation of the paper: a plain streaming read of
+ * data[0 .. bytes) with the token scan's loads and grid and nothing else, the
+ * ceiling that a read of every token once reaches on this GPU (the scan's
+ * roofline is reported against it and against the HBM peak).  data: device
+ * memory, 16-byte aligned, bytes a multiple of 4.  sink: device uint32[sink_len],
+ * sink_len >= 1; each wave stores a checksum of what it read to
+ * sink[wave % sink_len].  Asynchronous on `stream`; host-side argument errors
+ * return a negative status before any launch. */
+int parason_read_probe(const void *data, size_t bytes, uint32_t *sink, int64_t sink_len, void *stream);
 
 /* ---- policy-gradient step ------------------------------------------------
  * The update that consumes the rewards in PA-GRPO (Sec. 4 "Training

@@ -8,6 +8,7 @@
 #include <atomic>
 #include <cmath>
 #include <cstdint>
+#include <cstring>
 
 #include "parason.h"
 #include "device_common.h"
@@ -23,7 +24,9 @@ constexpr size_t ALIGN = 256;
 
 inline size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
-/* Compute units of the current device (cached per device), or -1. */
+/* Compute units of the current device (cached per device) when it is a
+ * gfx950 GPU, the only target the kernels are built for; -1 when no device
+ * can be queried, -2 when the current device is another GPU. */
 inline int cu_count()
 {
     static std::atomic<int> cached[64];
@@ -31,10 +34,19 @@ inline int cu_count()
     if (hipGetDevice(&dev) != hipSuccess) return -1;
     if (dev >= 0 && dev < 64) {
         int c = cached[dev].load(std::memory_order_relaxed);
-        if (c > 0) return c;
+        if (c != 0) return c;
     }
-    int cus = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return -1;
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return -1;
+    /* gcnArchName is "gfx950" followed by nothing or by ":feature" suffixes */
+    const bool gfx950 = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 &&
+                        (prop.gcnArchName[6] == '\0' || prop.gcnArchName[6] == ':');
+    int cus = -2;
+    if (gfx950) {
+        cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            return -1;
+    }
     if (dev >= 0 && dev < 64) cached[dev].store(cus, std::memory_order_relaxed);
     return cus;
 }

@@ -25,6 +25,7 @@ int parason_decode_init(parason_decode_state *states, int64_t batch, void *strea
     if (batch == 0) return PARASON_OK;
     if (!states) return PARASON_ERR_NULL;
     if (((uintptr_t)states & 15u) != 0) return PARASON_ERR_ALIGN;
+    if (cu_count() <= 0) return PARASON_ERR_DEVICE;
     hipStream_t stream = (hipStream_t)stream_ptr;
     pk::decode_init<<<dim3((unsigned)((batch + 255) / 256)), dim3(256), 0, stream>>>(
         reinterpret_cast<pk::DecodeState *>(states), batch);

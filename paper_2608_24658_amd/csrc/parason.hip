@@ -188,7 +188,7 @@ const char *parason_strerror(int status)
     case PARASON_ERR_PARAM: return "a reward parameter is not finite";
     case PARASON_ERR_ALIGN: return "tokens must be 4-byte aligned and the workspace 256-byte aligned";
     case PARASON_ERR_HIP: return "a HIP call or kernel launch failed";
-    case PARASON_ERR_DEVICE: return "no usable HIP device";
+    case PARASON_ERR_DEVICE: return "the current HIP device is not a gfx950 GPU or cannot be queried";
     default: return "unknown status";
     }
 }
@@ -393,6 +393,22 @@ int parason_run(const parason_handle *h, const int32_t *tokens, const int64_t *s
 {
     return parason_run_timed(h, tokens, starts, lengths, correct, n_traj, out, workspace, workspace_bytes, stream,
                              nullptr);
+}
+
+int parason_read_probe(const void *data, size_t bytes, uint32_t *sink, int64_t sink_len, void *stream_ptr)
+{
+    if (bytes == 0) return PARASON_OK;
+    if (!data || !sink) return PARASON_ERR_NULL;
+    if (sink_len < 1 || (bytes & 3u) != 0) return PARASON_ERR_SIZE;
+    if (((uintptr_t)data & 15u) != 0 || ((uintptr_t)sink & 3u) != 0) return PARASON_ERR_ALIGN;
+    const int cus = cu_count();
+    if (cus <= 0) return PARASON_ERR_DEVICE;
+    const int64_t n_vec = (int64_t)(bytes / 16);
+    const int32_t n_tail = (int32_t)((bytes % 16) / 4);
+    const int32_t *tail = (const int32_t *)((const char *)data + (size_t)n_vec * 16);
+    pk::read_probe<<<dim3((unsigned)(cus * SCAN_BLOCKS_PER_CU)), dim3(pk::WAVE * pk::SCAN_WAVES), 0,
+                     (hipStream_t)stream_ptr>>>((const int4 *)data, n_vec, tail, n_tail, sink, sink_len);
+    return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
 }
 
 }  // extern "C"

@@ -176,3 +176,51 @@ def test_fork_join_reject_bad_arguments_before_launch():
     assert join(FAKE, FAKE, FAKE, 16, FAKE, FAKE, FAKE, FAKE, 32, 0, jo, FAKE, 64, None) == P.ERR_WORKSPACE
     bad = P.JoinOutputs(100, None, FAKE, FAKE, FAKE, FAKE)
     assert join(FAKE, FAKE, FAKE, 16, FAKE, FAKE, FAKE, FAKE, 32, 0, bad, FAKE, W, None) == P.ERR_NULL
+
+
+def _gpu_visible():
+    """True when a HIP device is visible (counting devices does not initialise one)."""
+    try:
+        import torch
+
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return False
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="with a GPU these calls would pass the device check and launch")
+def test_launching_calls_check_the_device_first():
+    """With no gfx950 device current, every call that launches returns
+    PARASON_ERR_DEVICE after its argument checks and before any launch (the
+    fake pointers are never dereferenced)."""
+    px = P.Parason(TAGS, group_size=8)
+    out = _FakeOut()
+    ws = px.workspace_size(16, 1000)
+    assert px.run_raw(FAKE, FAKE, FAKE, FAKE, 16, out, FAKE, ws, None) == P.ERR_DEVICE
+    assert P.lib().parason_decode_init(FAKE, 4, None) == P.ERR_DEVICE
+    V = 151936
+    assert px.decode_step_raw(FAKE, FAKE, 4, FAKE, V, V, P.DTYPE_BF16, 0, None) == P.ERR_DEVICE
+    pw = ctypes.c_size_t()
+    assert P.lib().parason_pg_workspace_size(16, ctypes.byref(pw)) == P.OK
+    cfg = P.PgConfig(8, 0.2, 0.28)
+    assert P.pg_run_raw(cfg, FAKE, FAKE, FAKE, FAKE, FAKE, 16, FAKE, FAKE, FAKE, FAKE, pw.value, None) == P.ERR_DEVICE
+    fw = ctypes.c_size_t()
+    P.lib().parason_fork_workspace_size(16, ctypes.byref(fw))
+    fo = P.ForkOutputs(4, 100, *([FAKE] * 9))
+    assert px.fork_raw(FAKE, FAKE, FAKE, 16, 0, fo, FAKE, fw.value, None) == P.ERR_DEVICE
+    jw = ctypes.c_size_t()
+    P.lib().parason_join_workspace_size(16, ctypes.byref(jw))
+    jo = P.JoinOutputs(100, *([FAKE] * 5))
+    assert px.join_raw(FAKE, FAKE, FAKE, 16, FAKE, FAKE, FAKE, FAKE, 32, 0, jo, FAKE, jw.value, None) == P.ERR_DEVICE
+    assert P.read_probe_raw(FAKE, 4096, FAKE, 1, None) == P.ERR_DEVICE
+
+
+def test_read_probe_rejects_bad_arguments_before_launch():
+    rp = P.read_probe_raw
+    assert rp(0, 0, 0, 0, None) == P.OK  # nothing to read
+    assert rp(0, 4096, FAKE, 1, None) == P.ERR_NULL
+    assert rp(FAKE, 4096, 0, 1, None) == P.ERR_NULL
+    assert rp(FAKE, 4096, FAKE, 0, None) == P.ERR_SIZE
+    assert rp(FAKE, 4095, FAKE, 1, None) == P.ERR_SIZE
+    assert rp(FAKE + 4, 4096, FAKE, 1, None) == P.ERR_ALIGN
+    assert rp(FAKE, 4096, FAKE + 2, 1, None) == P.ERR_ALIGN
