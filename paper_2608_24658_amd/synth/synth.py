@@ -33,8 +33,8 @@ typical 256 groups; total uniform in [13400, 40200] (mean 26.8k:        2
         latency 15.7k at 1.71x, Table 4); 1% of thread bodies x100
 large   89,000 groups; total uniform in [25150, 75450] (mean 50.3k,     3
         the hard rows of Table 5); about 3.6e10 tokens, 143 GB
-ragged  128 groups; total octave-uniform over [1, 50300]; 5% of rows    4
-        truncated at a uniform position
+ragged  128 groups; total log-uniform over [1, 50300]               4
+        (P(L) ~ 1/L); 5% of rows truncated at a uniform position
 ======  ===========================================================  ====
 """
 from __future__ import annotations

@@ -34,7 +34,7 @@ enum {
 
 /* Draw purposes (top byte of counter word 2). */
 enum {
-    D_LEN = 1, D_LEN2, D_CORRECT, D_TRUNC, D_TRUNC_POS, D_TRIGGER, D_NBLOCKS,
+    D_LEN = 1, D_LEN2 /* unused */, D_CORRECT, D_TRUNC, D_TRUNC_POS, D_TRIGGER, D_NBLOCKS,
     D_KIND, D_K, D_NEST, D_NK, D_WEIGHT, D_OUTLIER, D_TEXT, D_LOGP
 };
 
@@ -43,7 +43,7 @@ typedef struct synth_params {
     int32_t vocab;           /* V: token ids are in [0, V) */
     int32_t tag_ids[12];     /* in SY_* order */
     int32_t sorted_tags[12]; /* tag_ids ascending (text ids skip them) */
-    int32_t len_kind;        /* 0: uniform in [len_lo, len_hi]; 1: octave-uniform */
+    int32_t len_kind;        /* 0: uniform in [len_lo, len_hi]; 1: log-uniform (P(x) ~ 1/x) */
     int32_t len_lo, len_hi;
     uint32_t p_trigger;      /* probabilities in units of 2^-32 */
     uint32_t p_trial;
@@ -128,17 +128,26 @@ __host__ __device__ static inline int64_t sy_block_fixed(const sy_shape *s, int 
 
 __host__ __device__ static inline int64_t sy_target_len(const synth_params *P, uint64_t row)
 {
-    uint32_t u = sy_draw(P, row, D_LEN, 0);
     if (P->len_kind == 0)
-        return (int64_t)P->len_lo + sy_below(u, (uint32_t)(P->len_hi - P->len_lo + 1));
-    /* octave-uniform: pick an octave [2^j, 2^(j+1)) of [len_lo, len_hi], then uniform in it */
-    int oct = 0;
-    while (((int64_t)P->len_lo << (oct + 1)) <= P->len_hi) ++oct;
-    uint32_t j = sy_below(u, (uint32_t)(oct + 1));
-    int64_t lo = (int64_t)P->len_lo << j;
-    int64_t hi = (lo << 1) - 1;
-    if (hi > P->len_hi) hi = P->len_hi;
-    return lo + sy_below(sy_draw(P, row, D_LEN2, 0), (uint32_t)(hi - lo + 1));
+        return (int64_t)P->len_lo + sy_below(sy_draw(P, row, D_LEN, 0), (uint32_t)(P->len_hi - P->len_lo + 1));
+    /* Log-uniform: P(L = x) proportional to 1/x on [len_lo, len_hi], by
+     * rejection in integer arithmetic.  Draw one of the J octaves
+     * [lo 2^j, lo 2^(j+1)) that start inside the range, uniformly (the last
+     * one as a whole octave), then x uniform in it; keep x when x <= len_hi,
+     * with probability lo 2^j / x (u / 2^32 < lo 2^j / x).  A kept x has
+     * probability (1/J) (1/(lo 2^j)) (lo 2^j / x) = 1/(J x) per attempt, for
+     * every x of the range; about two attempts in three keep theirs. */
+    const int64_t lo = P->len_lo, hi = P->len_hi;
+    uint32_t J = 1;
+    while ((lo << J) <= hi) ++J;
+    for (uint32_t a = 0; a < 1024; ++a) {
+        const int64_t base = lo << sy_below(sy_draw(P, row, D_LEN, 3 * a), J);
+        const int64_t x = base + (int64_t)sy_below(sy_draw(P, row, D_LEN, 3 * a + 1), (uint32_t)base);
+        if (x > hi) continue;
+        const uint32_t u = sy_draw(P, row, D_LEN, 3 * a + 2);
+        if ((uint64_t)u * (uint64_t)x < ((uint64_t)base << 32)) return x;
+    }
+    return lo; /* 1024 rejections in a row: probability below 2^-1500 */
 }
 
 __host__ __device__ static inline void sy_shape_of(const synth_params *P, uint64_t row, int64_t L, sy_shape *s)
