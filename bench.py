@@ -45,6 +45,12 @@ class HipEvents:
         self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
         self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
         self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+
+    def record(self, e, stream):
+        rc = self.hip.hipEventRecord(e, ctypes.c_void_p(stream))
+        if rc != 0:
+            raise RuntimeError("hipEventRecord failed: %d" % rc)
 
     def create(self):
         e = ctypes.c_void_p()
@@ -64,7 +70,9 @@ class HipEvents:
 
 def cpu_baseline(tokens_d, starts_h, lengths_h, correct_h, tag_ids, coef, budget_s=12.0):
     """Time the CPU oracle on the first groups of the batch (copied to the host
-    outside the timed region), sized for about budget_s seconds of CPU work."""
+    outside the timed region), sized for about budget_s seconds of CPU work.
+    Returns the baseline record and the oracle's results on those rows (for
+    the parity check against the GPU outputs)."""
     import numpy as np
 
     from oracle import oracle as O
@@ -80,19 +88,20 @@ def cpu_baseline(tokens_d, starts_h, lengths_h, correct_h, tag_ids, coef, budget
     def timed(toks, st, ln, co):
         t0 = time.perf_counter()
         rows = O.eval_rows(toks, st, ln, tag_ids)
-        O.group_reward(rows, co, G, coef["alpha"], coef["beta_subtask"], coef["beta_trial"], coef["rho"],
-                       coef["rho_clip"])
-        return time.perf_counter() - t0
+        res = O.group_reward(rows, co, G, coef["alpha"], coef["beta_subtask"], coef["beta_trial"], coef["rho"],
+                             coef["rho_clip"])
+        return time.perf_counter() - t0, rows, res
 
     probe = sample(4)
-    dt = timed(*probe)
+    dt, _, _ = timed(*probe)
     rate = probe[0].size / max(dt, 1e-6)
     want = budget_s * rate
     per_group = probe[0].size / 4
     n_groups = int(max(4, min(len(starts_h) // G, want / per_group)))
     toks, st, ln, co = sample(n_groups)
-    dt = timed(toks, st, ln, co)
-    return {
+    dt, rows, (R, rs, rt, eta) = timed(toks, st, ln, co)
+    accel, saved = O.row_acceleration(rows)
+    rec = {
         "value": toks.size / dt,
         "unit": "tokens/s",
         "cores": 1,
@@ -102,6 +111,31 @@ def cpu_baseline(tokens_d, starts_h, lengths_h, correct_h, tag_ids, coef, budget
         "rows_per_s": n_groups * G / dt,
         "host": host_cpu(),
     }
+    return rec, dict(rows=rows, reward=R, r_subtask=rs, r_trial=rt, eta=eta, accel=accel, saved=saved)
+
+
+def parity_of(out, ref):
+    """Rows of the GPU outputs `out` (device tensors of the last timed step)
+    that differ from the oracle's results `ref` on the rows ref covers (the
+    first rows of the batch): integers and flags exactly, float outputs as the
+    float rounding of the oracle's double values."""
+    import numpy as np
+
+    from paper_2608_24658_amd import parason as PX
+
+    rows = ref["rows"]
+    m = rows.size
+    bad = np.zeros(m, bool)
+    for k in PX.INT_FIELDS:
+        bad |= out[k][:m].cpu().numpy() != rows[k]
+    bad |= out["flags"][:m].cpu().numpy().view(np.uint32) != rows["flags"]
+    for k in ("reward", "r_subtask", "r_trial", "eta", "accel"):
+        bad |= out[k][:m].cpu().numpy() != ref[k].astype(np.float32)
+    bad |= out["saved"][:m].cpu().numpy() != ref["saved"]
+    return {"rows_checked": int(m), "mismatches": int(bad.sum()),
+            "compared": "every integer output and flag exactly; reward, R_subtask, R_trial, eta, acceleration as "
+                        "the float rounding of the oracle's double values; the cpu_baseline sample's rows against "
+                        "the last timed step"}
 
 
 def host_cpu():
@@ -228,6 +262,21 @@ def main():
     torch.cuda.synchronize()
     scan_avg = float(np.mean(scan_ms))
 
+    # the measured ceiling: a plain streaming read of the same token buffer,
+    # timed the same way on the same stream
+    sink = torch.empty(1, dtype=torch.int32, device=dev)
+    probe_ms = []
+    for i in range(args.warmup + args.steps):
+        hev.record(ev[0], stream)
+        rc = PX.read_probe_raw(tokens.data_ptr(), 4 * n_tok, sink.data_ptr(), 1, stream)
+        if rc != PX.OK:
+            raise PX.ParasonError(rc, "parason_read_probe")
+        hev.record(ev[1], stream)
+        if i >= args.warmup:
+            probe_ms.append(hev.elapsed_ms(ev[0], ev[1]))
+    torch.cuda.synchronize()
+    probe_avg = float(np.mean(probe_ms))
+
     # sanity of the last step
     fl = out["flags"].cpu().numpy().view(np.uint32)
     n_valid = int(np.sum(fl & PX.FLAG_VALID))
@@ -276,12 +325,20 @@ def main():
             "traffic": traffic,
             "kernel_ms": scan_avg,
             "algorithmic_bytes": alg_bytes,
+            "read_ceiling_ms": probe_avg,
+            "read_ceiling_gbs": 4.0 * n_tok / (probe_avg * 1e-3) / 1e9,
+            "scan_over_ceiling": scan_avg / probe_avg,
+            "read_ceiling": "parason_read_probe: plain streaming read of the same token buffer (the scan's "
+                            "16-byte nontemporal loads and grid, 8 loads per lane in flight, no work), timed "
+                            "with HIP events on the same stream in the same run",
         },
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
-        res["cpu_baseline"] = cpu_baseline(tokens, starts.cpu().numpy(), lengths.cpu().numpy(),
-                                           correct.cpu().numpy(), S.CONTIGUOUS_TAGS, coef, args.cpu_budget)
+        res["cpu_baseline"], ref = cpu_baseline(tokens, starts.cpu().numpy(), lengths.cpu().numpy(),
+                                                correct.cpu().numpy(), S.CONTIGUOUS_TAGS, coef, args.cpu_budget)
+        res["parity"] = parity_of(out, ref)
+        log("parity: %s" % json.dumps(res["parity"]))
     if args.workload == "large" and not args.no_typical_batch:
         # the same step on a batch of the size of one training step (latency-bound, not HBM-bound)
         del tokens, starts, lengths, correct, out, ws

@@ -2,8 +2,8 @@
 
 Inputs are the seeded synthetic workloads (generated on the device and
 regenerated bit-identically by the host mirror) and hand-built adversarial
-batches.  Integer outputs must be bit-exact; float outputs within the bound
-stated in gpu_util.
+batches.  Integer outputs must be bit-exact; float outputs the float rounding
+of the oracle's double values (see gpu_util).
 """
 import numpy as np
 import pytest
@@ -313,3 +313,38 @@ def test_repeatable(dev):
     for k in a:
         assert np.array_equal(a[k].view(np.uint32) if a[k].dtype == np.float32 else a[k],
                               b[k].view(np.uint32) if b[k].dtype == np.float32 else b[k]), k
+
+
+def test_device_is_gfx950_and_accepted(dev):
+    """The library's device check (every launching call returns
+    PARASON_ERR_DEVICE unless the current device is gfx950) passes here."""
+    log("case device check")
+    arch = torch.cuda.get_device_properties(dev).gcnArchName
+    assert arch.split(":")[0] == "gfx950", arch
+    px, _ = px_for()
+    P = S.make_params("tiny")
+    tok, st, ln, co = S.device_batch(P, G, device=dev)
+    out = px.alloc_outputs(G, dev)
+    ws = px.alloc_workspace(G, int(tok.numel()), dev)
+    rc = px.run_raw(tok.data_ptr(), st.data_ptr(), ln.data_ptr(), co.data_ptr(), G, out, ws.data_ptr(), ws.numel(),
+                    torch.cuda.current_stream(dev).cuda_stream)
+    assert rc == PX.OK
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("n_elem", [0, 1, 3, 4, 515, 1 << 20, (1 << 22) + 4096 * 3 + 7])
+def test_read_probe_reads_every_word(dev, n_elem):
+    """The streaming-read ceiling probe reads every word once: with one sink
+    word per wave, the XOR of the sink is the XOR of the buffer."""
+    log("case read probe %d" % n_elem)
+    rng = np.random.default_rng(n_elem)
+    buf = rng.integers(-2 ** 31, 2 ** 31, size=n_elem + 8, dtype=np.int64).astype(np.int32)
+    d = to_dev(buf, torch.int32, dev)
+    waves = torch.cuda.get_device_properties(dev).multi_processor_count * 16
+    sink = torch.zeros(waves, dtype=torch.int32, device=dev)
+    rc = PX.read_probe_raw(d.data_ptr(), 4 * n_elem, sink.data_ptr(), waves, torch.cuda.current_stream(dev).cuda_stream)
+    assert rc == PX.OK
+    torch.cuda.synchronize()
+    want = np.bitwise_xor.reduce(buf[:n_elem].view(np.uint32)) if n_elem else np.uint32(0)
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    assert got == want
