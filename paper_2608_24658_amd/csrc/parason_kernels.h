@@ -1261,6 +1261,52 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
     }
 }
 
+/* The ceiling the token scan is measured against: a plain streaming read of
+ * the same buffer with the scan's 16-byte nontemporal loads and persistent
+ * grid, each wave over a contiguous range of 8 KB chunks whose eight loads per
+ * lane are all issued before any is used, and no other work.  Each wave stores
+ * the XOR of what it read to sink[wave % sink_len] (so the loads are kept). */
+constexpr int PROBE_LOADS = 8;
+constexpr int PROBE_CHUNK = PROBE_LOADS * WAVE; /* 16-byte vectors per chunk */
+
+__global__ void __launch_bounds__(WAVE * SCAN_WAVES) read_probe(const int4 *__restrict__ src, int64_t n_vec,
+                                                                const int32_t *__restrict__ tail, int32_t n_tail,
+                                                                uint32_t *__restrict__ sink, int64_t sink_len)
+{
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int64_t wave = uniform64((int64_t)blockIdx.x * SCAN_WAVES + threadIdx.x / WAVE);
+    const int64_t n_waves = (int64_t)gridDim.x * SCAN_WAVES;
+    const int64_t n_chunks = n_vec / PROBE_CHUNK;
+    const int64_t c0 = uniform64(n_chunks * wave / n_waves), c1 = uniform64(n_chunks * (wave + 1) / n_waves);
+    uint32_t acc = 0;
+    for (int64_t c = c0; c < c1; ++c) {
+        int4 x[PROBE_LOADS];
+        const int4 *p = src + c * PROBE_CHUNK + lane;
+#pragma unroll
+        for (int i = 0; i < PROBE_LOADS; ++i) x[i] = load_vec(p + i * WAVE);
+#pragma unroll
+        for (int i = 0; i < PROBE_LOADS; ++i) acc ^= (uint32_t)(x[i].x ^ x[i].y ^ x[i].z ^ x[i].w);
+    }
+    if (wave == n_waves - 1) {
+        /* the vectors after the last whole chunk, then the last 0-3 elements */
+        for (int64_t v = n_chunks * PROBE_CHUNK + lane; v < n_vec; v += WAVE) {
+            const int4 x = load_vec(src + v);
+            acc ^= (uint32_t)(x.x ^ x.y ^ x.z ^ x.w);
+        }
+        if (lane < n_tail) acc ^= (uint32_t)tail[lane];
+    }
+    /* XOR over the wave by DPP (row_shr) and readlane, as the scans do */
+    uint32_t v = acc;
+    v ^= (uint32_t)row_shr<1>((int32_t)v, 0);
+    v ^= (uint32_t)row_shr<2>((int32_t)v, 0);
+    v ^= (uint32_t)row_shr<4>((int32_t)v, 0);
+    v ^= (uint32_t)row_shr<8>((int32_t)v, 0);
+    const uint32_t w = (uint32_t)__builtin_amdgcn_readlane((int32_t)v, 15) ^
+                       (uint32_t)__builtin_amdgcn_readlane((int32_t)v, 31) ^
+                       (uint32_t)__builtin_amdgcn_readlane((int32_t)v, 47) ^ (uint32_t)lane63((int32_t)v);
+    if (lane == 0) sink[wave % sink_len] = w;
+}
+
 /* ------------------------------------------------------------------ gather */
 
 struct GatherArgs {

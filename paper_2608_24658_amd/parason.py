@@ -42,7 +42,7 @@ MAX_OPEN_ENTRIES = 1 << 24
 EXPORTED = ("parason_create", "parason_workspace_size", "parason_run", "parason_run_timed", "parason_destroy",
             "parason_strerror", "parason_pg_workspace_size", "parason_pg_run", "parason_decode_init",
             "parason_decode_step", "parason_fork_workspace_size", "parason_join_workspace_size", "parason_fork",
-            "parason_join")
+            "parason_join", "parason_read_probe")
 
 FORK_SEED_ENTRY = 1 << 0
 JOIN_CLOSE_PARALLEL = 1 << 0
@@ -188,6 +188,9 @@ def lib():
             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32,
             ctypes.POINTER(JoinOutputs), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
         ]
+        L.parason_read_probe.restype = ctypes.c_int
+        L.parason_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64,
+                                         ctypes.c_void_p]
         L.parason_strerror.restype = ctypes.c_char_p
         L.parason_strerror.argtypes = [ctypes.c_int]
         _lib = L
@@ -421,6 +424,11 @@ class Parason:
         if rc != OK:
             raise ParasonError(rc, "parason_run")
         return out
+
+
+def read_probe_raw(data_ptr, nbytes, sink_ptr, sink_len, stream) -> int:
+    """parason_read_probe: streaming read of nbytes at data_ptr (measurement)."""
+    return lib().parason_read_probe(data_ptr, int(nbytes), sink_ptr, int(sink_len), stream)
 
 
 def _check_rows(tokens, starts, lengths):
