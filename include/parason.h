@@ -63,6 +63,7 @@ extern "C" {
 #define PARASON_ERR_HIP (-8)       /* a HIP call or kernel launch failed */
 #define PARASON_ERR_DEVICE (-9)    /* the current device is not gfx950 or cannot be queried (checked by
                                       every call that launches, before its first launch) */
+#define PARASON_ERR_SCRATCH (-10)  /* parason_run_noalloc: the batch needs more than its static scratch */
 
 /* ---- per-row flag bits (parason_outputs.flags) ------------------------- */
 #define PARASON_FLAG_VALID (1u << 0)          /* the stream is in the language */
@@ -208,6 +209,26 @@ int parason_run(const parason_handle *h, const int32_t *tokens, const int64_t *s
 int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
                       const uint8_t *correct, int64_t n_traj, const parason_outputs *out, void *workspace,
                       size_t workspace_bytes, void *stream, void *const *scan_events);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): parason_run
+ * with no workspace argument.  Its scratch is one static device array of
+ * PARASON_NOALLOC_SCRATCH_BYTES per GPU the library runs on, held until the
+ * process ends; nothing is allocated by this call, and nothing is freed.
+ *   total_tokens: an upper bound of the sum of the row lengths, known on the
+ *            host; a batch whose parason_workspace_size(h, n_traj,
+ *            total_tokens) exceeds the scratch returns PARASON_ERR_SCRATCH
+ *            before any launch (lengths beyond the bound are reported per row
+ *            as PARASON_FLAG_WS_OVERFLOW, as for parason_run).
+ * Every other argument and every result is as for parason_run.  All calls on
+ * one GPU share that GPU's scratch, which keeps the last call's contents (no
+ * call relies on them): calls that overlap on one GPU (on two streams, or from
+ * two threads without ordering between them) race and give wrong results.
+ * Serialise them, e.g. on one stream. */
+#define PARASON_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+int parason_run_noalloc(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                        const uint8_t *correct, int64_t n_traj, int64_t total_tokens, const parason_outputs *out,
+                        void *stream);
 
 void parason_destroy(parason_handle *h);
 

@@ -189,6 +189,9 @@ const char *parason_strerror(int status)
     case PARASON_ERR_ALIGN: return "tokens must be 4-byte aligned and the workspace 256-byte aligned";
     case PARASON_ERR_HIP: return "a HIP call or kernel launch failed";
     case PARASON_ERR_DEVICE: return "the current HIP device is not a gfx950 GPU or cannot be queried";
+    case PARASON_ERR_SCRATCH:
+        return "the batch needs more scratch than parason_run_noalloc's static buffer holds "
+               "(PARASON_NOALLOC_SCRATCH_BYTES); use parason_run with a workspace";
     default: return "unknown status";
     }
 }
@@ -393,6 +396,49 @@ int parason_run(const parason_handle *h, const int32_t *tokens, const int64_t *s
 {
     return parason_run_timed(h, tokens, starts, lengths, correct, n_traj, out, workspace, workspace_bytes, stream,
                              nullptr);
+}
+
+/* The scratch of parason_run_noalloc: one static array per GPU the library
+ * runs on, held until the process ends.  Host code never uses its name as an
+ * address (on the host it is a stand-in symbol); each device's address comes
+ * from hipGetSymbolAddress, once per device, with that device current. */
+static __device__ __align__(256) unsigned char scratch[PARASON_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+std::atomic<void *> scratch_ptr[64];
+
+/* This device's address of `scratch`, or nullptr if it cannot be had. */
+void *scratch_for_current_device()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    void *p = scratch_ptr[dev].load(std::memory_order_acquire);
+    if (p) return p;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    scratch_ptr[dev].store(p, std::memory_order_release);
+    return p;
+}
+}  // namespace
+
+int parason_run_noalloc(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
+                        const uint8_t *correct, int64_t n_traj, int64_t total_tokens, const parason_outputs *out,
+                        void *stream)
+{
+    if (!h || !out) return PARASON_ERR_NULL;
+    if (n_traj < 0 || n_traj > INT32_MAX || total_tokens < 0) return PARASON_ERR_SIZE;
+    if (n_traj % h->cfg.group_size != 0) return PARASON_ERR_GROUP;
+    if (n_traj == 0) return PARASON_OK;
+    size_t need = 0;
+    const int rc = parason_workspace_size(h, n_traj, total_tokens, &need);
+    if (rc != PARASON_OK) return rc;
+    if (need > (size_t)PARASON_NOALLOC_SCRATCH_BYTES) return PARASON_ERR_SCRATCH;
+    if (cu_count() <= 0) return PARASON_ERR_DEVICE;
+    void *ws = scratch_for_current_device();
+    if (!ws) return PARASON_ERR_HIP;
+    /* parason_run needs no initialised workspace: its first launch clears
+     * what must start at zero, so nothing here writes to the scratch */
+    return parason_run_timed(h, tokens, starts, lengths, correct, n_traj, out, ws,
+                             (size_t)PARASON_NOALLOC_SCRATCH_BYTES, stream, nullptr);
 }
 
 int parason_read_probe(const void *data, size_t bytes, uint32_t *sink, int64_t sink_len, void *stream_ptr)

@@ -14,7 +14,9 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libparason.so")
 
 OK = 0
-ERR_NULL, ERR_SIZE, ERR_GROUP, ERR_WORKSPACE, ERR_TAGS, ERR_PARAM, ERR_ALIGN, ERR_HIP, ERR_DEVICE = range(-1, -10, -1)
+ERR_NULL, ERR_SIZE, ERR_GROUP, ERR_WORKSPACE, ERR_TAGS, ERR_PARAM, ERR_ALIGN, ERR_HIP, ERR_DEVICE, ERR_SCRATCH = \
+    range(-1, -11, -1)
+NOALLOC_SCRATCH_BYTES = 128 << 20
 
 FLAG_VALID = 1 << 0
 FLAG_TRUNCATED = 1 << 1
@@ -42,7 +44,7 @@ MAX_OPEN_ENTRIES = 1 << 24
 EXPORTED = ("parason_create", "parason_workspace_size", "parason_run", "parason_run_timed", "parason_destroy",
             "parason_strerror", "parason_pg_workspace_size", "parason_pg_run", "parason_decode_init",
             "parason_decode_step", "parason_fork_workspace_size", "parason_join_workspace_size", "parason_fork",
-            "parason_join", "parason_read_probe")
+            "parason_join", "parason_read_probe", "parason_run_noalloc")
 
 FORK_SEED_ENTRY = 1 << 0
 JOIN_CLOSE_PARALLEL = 1 << 0
@@ -154,6 +156,11 @@ def lib():
         L.parason_run.argtypes = [
             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
             ctypes.POINTER(Outputs), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+        ]
+        L.parason_run_noalloc.restype = ctypes.c_int
+        L.parason_run_noalloc.argtypes = [
+            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+            ctypes.c_int64, ctypes.POINTER(Outputs), ctypes.c_void_p,
         ]
         L.parason_run_timed.restype = ctypes.c_int
         L.parason_run_timed.argtypes = L.parason_run.argtypes + [ctypes.c_void_p]
@@ -279,6 +286,17 @@ class Parason:
             setattr(o, k, out[k].data_ptr() if k in out and out[k] is not None else None)
         return lib().parason_run(self._h, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, int(n_traj),
                                  ctypes.byref(o), ws_ptr, int(ws_bytes), stream)
+
+    def run_noalloc_raw(self, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, n_traj, total_tokens, out: dict,
+                        stream) -> int:
+        """parason_run_noalloc (no workspace: the library's static scratch); returns the status."""
+        o = Outputs()
+        for k in INT_FIELDS + ("flags", "reward"):
+            setattr(o, k, out[k].data_ptr())
+        for k in OPTIONAL_FIELDS:
+            setattr(o, k, out[k].data_ptr() if k in out and out[k] is not None else None)
+        return lib().parason_run_noalloc(self._h, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, int(n_traj),
+                                         int(total_tokens), ctypes.byref(o), stream)
 
     def run_timed_raw(self, tokens_ptr, starts_ptr, lengths_ptr, correct_ptr, n_traj, out: dict, ws_ptr, ws_bytes,
                       stream, scan_events) -> int:

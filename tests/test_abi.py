@@ -33,7 +33,7 @@ def test_exports_every_declared_function():
 
 
 def test_strerror_covers_codes():
-    for rc in range(0, -10, -1):
+    for rc in range(0, -11, -1):
         assert P.strerror(rc) != "unknown status"
     assert P.strerror(-99) == "unknown status"
 
@@ -213,6 +213,7 @@ def test_launching_calls_check_the_device_first():
     jo = P.JoinOutputs(100, *([FAKE] * 5))
     assert px.join_raw(FAKE, FAKE, FAKE, 16, FAKE, FAKE, FAKE, FAKE, 32, 0, jo, FAKE, jw.value, None) == P.ERR_DEVICE
     assert P.read_probe_raw(FAKE, 4096, FAKE, 1, None) == P.ERR_DEVICE
+    assert px.run_noalloc_raw(FAKE, FAKE, FAKE, FAKE, 16, 1000, out, None) == P.ERR_DEVICE
 
 
 def test_read_probe_rejects_bad_arguments_before_launch():
@@ -224,3 +225,25 @@ def test_read_probe_rejects_bad_arguments_before_launch():
     assert rp(FAKE, 4095, FAKE, 1, None) == P.ERR_SIZE
     assert rp(FAKE + 4, 4096, FAKE, 1, None) == P.ERR_ALIGN
     assert rp(FAKE, 4096, FAKE + 2, 1, None) == P.ERR_ALIGN
+
+
+def test_run_noalloc_rejects_bad_arguments_before_launch():
+    """parason_run_noalloc: argument errors, and a batch whose workspace would
+    exceed the static scratch, are refused on the host."""
+    px = P.Parason(TAGS, group_size=8)
+    out = _FakeOut()
+    run = px.run_noalloc_raw
+    assert run(0, 0, 0, 0, 0, 0, out, None) == P.OK  # nothing to do
+    assert run(FAKE, FAKE, FAKE, FAKE, 12, 1000, out, None) == P.ERR_GROUP
+    assert run(FAKE, FAKE, FAKE, FAKE, -8, 1000, out, None) == P.ERR_SIZE
+    assert run(FAKE, FAKE, FAKE, FAKE, 16, -1, out, None) == P.ERR_SIZE
+    assert P.lib().parason_run_noalloc(None, FAKE, FAKE, FAKE, FAKE, 16, 1000, None, None) == P.ERR_NULL
+    # the largest token count whose workspace fits, and one segment's worth more
+    lo, hi = 0, 1 << 40
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        lo, hi = (mid, hi) if px.workspace_size(16, mid) <= P.NOALLOC_SCRATCH_BYTES else (lo, mid)
+    assert px.workspace_size(16, lo) <= P.NOALLOC_SCRATCH_BYTES < px.workspace_size(16, lo + 4096)
+    assert run(FAKE, FAKE, FAKE, FAKE, 16, lo + 4096, out, None) == P.ERR_SCRATCH
+    assert run(FAKE, FAKE, FAKE, FAKE, 16, 10 ** 12, out, None) == P.ERR_SCRATCH
+    assert "scratch" in P.strerror(P.ERR_SCRATCH)
