@@ -4,6 +4,10 @@
  * out the caller's workspace and enqueues the launches on the caller's stream.
  * The policy-gradient step (pg.hip) and the decode step (decode.hip) are
  * further entry points of the same library.
+ *
+ * Launches are written with HIP's hipLaunchKernelGGL rather than the triple
+ * chevron, so that this file also compiles as plain C++ against the CPU
+ * emulation of the HIP runtime that the tests run the kernels on.
  */
 #include <cstring>
 #include <new>
@@ -143,17 +147,18 @@ void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, uint8
     if (per_wave == 1) {
         /* rows_par runs the rows it does not hold through the automaton
          * itself (the second tier), so rows_mid has nothing to do */
-        pk::rows_par<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows);
+        hipLaunchKernelGGL(pk::rows_par<LENIENT>, dim3(row_blocks), dim3(64), 0, stream, ra, mode, counters, deep_rows);
     } else {
         /* the per-lane automaton reads split rows best as compact lists */
-        pk::gather_rows<<<dim3((unsigned)(cus * GATHER_BLOCKS_PER_CU)), dim3(256), 0, stream>>>(ga);
-        pk::rows_fast<LENIENT><<<dim3(row_blocks), dim3(64), 0, stream>>>(ra, mode, counters, mid_rows, lane_shift);
-        pk::rows_mid<LENIENT><<<dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream>>>(
-            ra, mode, counters, mid_rows, deep_rows);
+        hipLaunchKernelGGL(pk::gather_rows, dim3((unsigned)(cus * GATHER_BLOCKS_PER_CU)), dim3(256), 0, stream, ga);
+        hipLaunchKernelGGL(pk::rows_fast<LENIENT>, dim3(row_blocks), dim3(64), 0, stream, ra, mode, counters, mid_rows,
+                           lane_shift);
+        hipLaunchKernelGGL(pk::rows_mid<LENIENT>, dim3((unsigned)(cus * MID_BLOCKS_PER_CU)), dim3(64), 0, stream, ra,
+                           mode, counters, mid_rows, deep_rows);
     }
     if (deep_launch)
-        pk::rows_deep<LENIENT><<<dim3(1), dim3(64), 0, stream>>>(ra, mode, counters, deep_rows, deep_frames,
-                                                                 deep_bits);
+        hipLaunchKernelGGL(pk::rows_deep<LENIENT>, dim3(1), dim3(64), 0, stream, ra, mode, counters, deep_rows,
+                           deep_frames, deep_bits);
 }
 
 }  // namespace
@@ -164,14 +169,15 @@ void abi::launch_plan(const int64_t *starts, const int32_t *lengths, int64_t n, 
 {
     const unsigned tiles = (unsigned)n_tiles;
     if (n_tiles == 1) {
-        pk::plan_rows<true><<<dim3(1), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n, mis, nullptr, seg_off,
-                                                                          mode, counters);
+        hipLaunchKernelGGL(pk::plan_rows<true>, dim3(1), dim3(pk::PLAN_THREADS), 0, stream, starts, lengths, n, mis,
+                           nullptr, seg_off, mode, counters);
         return;
     }
-    pk::plan_tiles<<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n, mis, tile_sum);
-    pk::plan_top<<<dim3(1), dim3(1024), 0, stream>>>(tile_sum, n_tiles, tile_off, seg_off, n, counters);
-    pk::plan_rows<false><<<dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream>>>(starts, lengths, n, mis, tile_off,
-                                                                           seg_off, mode, counters);
+    hipLaunchKernelGGL(pk::plan_tiles, dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream, starts, lengths, n, mis,
+                       tile_sum);
+    hipLaunchKernelGGL(pk::plan_top, dim3(1), dim3(1024), 0, stream, tile_sum, n_tiles, tile_off, seg_off, n, counters);
+    hipLaunchKernelGGL(pk::plan_rows<false>, dim3(tiles), dim3(pk::PLAN_THREADS), 0, stream, starts, lengths, n, mis,
+                       tile_off, seg_off, mode, counters);
 }
 
 extern "C" {
@@ -314,11 +320,14 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     const unsigned scan_blocks = (unsigned)(cus * SCAN_BLOCKS_PER_CU);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[0], stream) != hipSuccess) return PARASON_ERR_HIP;
     if (h->tm.contiguous)
-        pk::scan_rows<pk::TM_CONTIG><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
+        hipLaunchKernelGGL(pk::scan_rows<pk::TM_CONTIG>, dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream,
+                           sa);
     else if (h->tm.hashed)
-        pk::scan_rows<pk::TM_HASH><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
+        hipLaunchKernelGGL(pk::scan_rows<pk::TM_HASH>, dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream,
+                           sa);
     else
-        pk::scan_rows<pk::TM_LINEAR><<<dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream>>>(sa);
+        hipLaunchKernelGGL(pk::scan_rows<pk::TM_LINEAR>, dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream,
+                           sa);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[1], stream) != hipSuccess) return PARASON_ERR_HIP;
 
     pk::RowArgs ra;
@@ -368,23 +377,23 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     rw.n = n_traj;
     if (batch_stats) {
         pk::StatsArgs st{out->total, out->latency, out->n_subtask, out->n_trial, out->flags, n_traj, red_d, red_i, stats};
-        pk::batch_stats_tiles<1><<<dim3(tiles), dim3(pk::RED_THREADS), 0, stream>>>(st);
-        pk::batch_stats_final<1><<<dim3(1), dim3(pk::RED_THREADS), 0, stream>>>(st, L.n_tiles);
-        pk::batch_stats_tiles<2><<<dim3(tiles), dim3(pk::RED_THREADS), 0, stream>>>(st);
-        pk::batch_stats_final<2><<<dim3(1), dim3(pk::RED_THREADS), 0, stream>>>(st, L.n_tiles);
+        hipLaunchKernelGGL(pk::batch_stats_tiles<1>, dim3(tiles), dim3(pk::RED_THREADS), 0, stream, st);
+        hipLaunchKernelGGL(pk::batch_stats_final<1>, dim3(1), dim3(pk::RED_THREADS), 0, stream, st, L.n_tiles);
+        hipLaunchKernelGGL(pk::batch_stats_tiles<2>, dim3(tiles), dim3(pk::RED_THREADS), 0, stream, st);
+        hipLaunchKernelGGL(pk::batch_stats_final<2>, dim3(1), dim3(pk::RED_THREADS), 0, stream, st, L.n_tiles);
         rw.batch = stats;
-        pk::batch_reward<<<dim3((unsigned)((n_traj + 255) / 256)), dim3(256), 0, stream>>>(rw);
+        hipLaunchKernelGGL(pk::batch_reward, dim3((unsigned)((n_traj + 255) / 256)), dim3(256), 0, stream, rw);
     } else {
         const pk::DeepArgs da{ra, mode, counters, deep_rows, deep_frames, deep_bits};
         const dim3 grid((unsigned)((n_traj + 255) / 256));
-        if (lenient) pk::group_reward<true><<<grid, dim3(256), 0, stream>>>(rw, da);
-        else pk::group_reward<false><<<grid, dim3(256), 0, stream>>>(rw, da);
+        if (lenient) hipLaunchKernelGGL(pk::group_reward<true>, grid, dim3(256), 0, stream, rw, da);
+        else hipLaunchKernelGGL(pk::group_reward<false>, grid, dim3(256), 0, stream, rw, da);
     }
     if (out->metrics) {
         pk::MetricsArgs ma{out->total, out->latency, out->n_subtask, out->n_trial, out->flags, correct,
                            out->reward, n_traj, red_i, red_d, out->metrics};
-        pk::metrics_tiles<<<dim3(tiles), dim3(pk::RED_THREADS), 0, stream>>>(ma);
-        pk::metrics_final<<<dim3(1), dim3(pk::RED_THREADS), 0, stream>>>(ma, L.n_tiles);
+        hipLaunchKernelGGL(pk::metrics_tiles, dim3(tiles), dim3(pk::RED_THREADS), 0, stream, ma);
+        hipLaunchKernelGGL(pk::metrics_final, dim3(1), dim3(pk::RED_THREADS), 0, stream, ma, L.n_tiles);
     }
 
     return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
@@ -452,8 +461,8 @@ int parason_read_probe(const void *data, size_t bytes, uint32_t *sink, int64_t s
     const int64_t n_vec = (int64_t)(bytes / 16);
     const int32_t n_tail = (int32_t)((bytes % 16) / 4);
     const int32_t *tail = (const int32_t *)((const char *)data + (size_t)n_vec * 16);
-    pk::read_probe<<<dim3((unsigned)(cus * SCAN_BLOCKS_PER_CU)), dim3(pk::WAVE * pk::SCAN_WAVES), 0,
-                     (hipStream_t)stream_ptr>>>((const int4 *)data, n_vec, tail, n_tail, sink, sink_len);
+    hipLaunchKernelGGL(pk::read_probe, dim3((unsigned)(cus * SCAN_BLOCKS_PER_CU)), dim3(pk::WAVE * pk::SCAN_WAVES), 0,
+                       (hipStream_t)stream_ptr, (const int4 *)data, n_vec, tail, n_tail, sink, sink_len);
     return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
 }
 

@@ -1152,6 +1152,10 @@ __device__ __forceinline__ void flush_row(const ScanArgs &a, int64_t row, int64_
         return;
     }
     uint32_t *dst = a.events + first * EV_CAP;
+    /* lane i copies events other lanes wrote: the wave's LDS stores above
+     * come first (a wave's LDS accesses are performed in program order; this
+     * keeps the compiler from moving them across) */
+    __builtin_amdgcn_wave_barrier();
     for (uint32_t i = lane; i < lcnt; i += WAVE) dst[i] = lev[i];
     if (lane == 0) {
         a.seg_count[first] = (int32_t)lcnt;
@@ -1352,9 +1356,12 @@ __device__ __forceinline__ void gather_row(const GatherArgs &a, int64_t row, int
             const int32_t f = f0 + lane; /* the chunk's f-th event, of segment c0 + j */
             const int32_t j = last_lane_at_most(excl, f);
             const int32_t first = __shfl(excl, j, WAVE);
+            const int64_t seg = c0 + j;
+            const uint32_t w = f < total ? a.events[seg * EV_CAP + (f - first)] : 0u;
+            /* every lane's load of this round before any lane's store (the
+             * stores may overwrite slots other lanes read) */
+            __builtin_amdgcn_wave_barrier();
             if (f < total) {
-                const int64_t seg = c0 + j;
-                const uint32_t w = a.events[seg * EV_CAP + (f - first)];
                 /* row position of segment position 0 */
                 const int64_t base = 4 * (vrow0 + (seg - s0) * SEG_VEC) - g;
                 const uint32_t pos = (uint32_t)(base + (int64_t)(w >> 4));

@@ -145,7 +145,7 @@ def test_deep_rows_with_metrics(dev, n_rows, batch_stats):
     inside the per-group reward launch, or as a launch of its own before the
     batch-wide statistics.  64 rows take the one-wave row kernel, 12,288 the
     per-lane one."""
-    from test_gpu_parity import deep_stream, pack
+    from adversarial import deep_stream, pack
     import grammar_pins as GP
 
     log("case deep rows n=%d batch_stats=%s" % (n_rows, batch_stats))

@@ -1,0 +1,219 @@
+"""The accounting kernels run on the CPU, under AddressSanitizer and
+UndefinedBehaviorSanitizer, against the oracle.
+
+tests/simt/hip/hip_runtime.h emulates the HIP subset the kernels use (lanes as
+fibers meeting at every wave operation: ballot, shuffles, readlane,
+readfirstlane, DPP row shifts, ds_bpermute; blocks run one after the other).
+The library's own csrc/parason.hip is compiled with it for the host, and the
+driver tests/simt/emu_main.cpp runs batches through the C-ABI (parason_run and
+parason_run_noalloc) with host memory as device memory.  The emulated device
+reports a chosen number of compute units, which picks the kernels a batch
+takes: with many units every batch here is small (plan, scan_rows, rows_par,
+group_reward); with one or two, rows_fast after gather_rows, then rows_mid and
+the single-thread deep tier.  The workspace is handed over filled with a byte
+pattern and sized exactly, so reliance on its contents or reads past it fail.
+
+Planted mistakes in copies of the kernel sources (an off-by-one in a DPP
+segmented scan, a lost carry in the scan's compaction, a dropped row-edge
+mask) must each be caught by these comparisons."""
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+from adversarial import adversarial_streams, pack
+from gpu_util import DEFAULT_COEF, compare, insert_gaps, oracle_expect
+from oracle import oracle as O
+from paper_2608_24658_amd import parason as PX
+from paper_2608_24658_amd.synth import synth as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2608_24658_amd", "csrc")
+SIMT = os.path.join(ROOT, "tests", "simt")
+CLANG = "/opt/rocm/llvm/bin/clang++"
+TAGS = S.CONTIGUOUS_TAGS
+LOW_IDS = np.array([3, 9, 4, 11, 0, 13, 1, 6, 15, 2, 10, 8], dtype=np.int32)
+G = 8
+INT_OUT = ("total", "latency", "n_subtask", "n_trial", "n_blocks", "max_depth", "first_error_pos", "flags")
+FLOAT_OUT = ("reward", "r_subtask", "r_trial", "eta", "accel")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(CLANG), reason="no host clang++ with the sanitizers")
+
+
+def build(out, csrc=CSRC):
+    cmd = [CLANG, "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+           "-ffp-contract=off", "-I", SIMT, "-I", os.path.join(ROOT, "include"), "-I", csrc, "-x", "c++",
+           os.path.join(csrc, "parason.hip"), os.path.join(SIMT, "emu_main.cpp"), "-o", out]
+    subprocess.check_call(cmd)
+    return out
+
+
+@pytest.fixture(scope="module")
+def emu(tmp_path_factory):
+    return build(str(tmp_path_factory.mktemp("simt") / "emu"))
+
+
+def run_emu(binary, tokens, starts, lengths, correct, tags=TAGS, flags=0, cus=2, shift=0, noalloc=False,
+            ws_tokens=None, coef=DEFAULT_COEF, tmp="/tmp"):
+    n = len(starts)
+    tokens = np.ascontiguousarray(tokens, np.int32)
+    if ws_tokens is None:
+        ws_tokens = int(np.maximum(np.asarray(lengths), 0).astype(np.int64).sum())
+    hdr = (np.array([n, tokens.size, ws_tokens], np.int64).tobytes() + np.asarray(tags, np.int32).tobytes()
+           + np.array([G], np.int32).tobytes() + np.array([flags], np.uint32).tobytes()
+           + np.array([cus, shift, int(noalloc)], np.int32).tobytes()
+           + np.array([coef[k] for k in ("alpha", "beta_subtask", "beta_trial", "rho", "rho_clip")],
+                      np.float64).tobytes())
+    body = (tokens.tobytes() + np.asarray(starts, np.int64).tobytes() + np.asarray(lengths, np.int32).tobytes()
+            + np.asarray(correct, np.uint8).tobytes())
+    fin = os.path.join(tmp, "emu_in_%d.bin" % os.getpid())
+    fout = os.path.join(tmp, "emu_out_%d.bin" % os.getpid())
+    with open(fin, "wb") as f:
+        f.write(hdr + body)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:halt_on_error=1:abort_on_error=1",
+               UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    r = subprocess.run([binary, fin, fout], env=env, capture_output=True, text=True, timeout=600)
+    if r.returncode != 0:
+        raise RuntimeError("emulation failed (%d):\n%s" % (r.returncode, r.stderr[-4000:]))
+    b = open(fout, "rb").read()
+    os.unlink(fin)
+    os.unlink(fout)
+    out, off = {}, 0
+    for k in INT_OUT:
+        out[k] = np.frombuffer(b, np.int32, n, off).copy()
+        off += 4 * n
+    out["flags"] = out["flags"].view(np.uint32)
+    for k in FLOAT_OUT:
+        out[k] = np.frombuffer(b, np.float32, n, off).copy()
+        off += 4 * n
+    out["saved"] = np.frombuffer(b, np.int32, n, off).copy()
+    off += 4 * n
+    return out, int(np.frombuffer(b, np.int32, 1, off)[0])
+
+
+def check(binary, tokens, starts, lengths, correct, tags=TAGS, flags=0, cus=2, what="", **kw):
+    got, rc = run_emu(binary, tokens, starts, lengths, correct, tags, flags, cus, **kw)
+    assert rc == PX.OK, (what, rc)
+    exp = oracle_expect(tokens, starts, lengths, correct, tags, G, DEFAULT_COEF, flags & ~PX.CFG_TAG_COMPARE)
+    compare(got, *exp, what=what, exact_reward=not (flags & PX.CFG_BATCH_STATS))
+    return got
+
+
+# rows_par for every batch here (fewer rows than 20 waves per emulated unit x 2)
+MANY = 64
+# rows_fast (one row per lane), gather_rows, rows_mid, deep tier
+FEW = 1
+
+
+@pytest.mark.parametrize("workload", ["tiny", "small", "ragged"])
+@pytest.mark.parametrize("cus", [MANY, FEW])
+def test_emulated_workloads(emu, workload, cus):
+    P = S.make_params(workload)
+    n = S.n_rows_of(workload)
+    tok, st, ln, co = S.host_batch(P, n)
+    check(emu, tok, st, ln, co, cus=cus, what="%s cus %d" % (workload, cus))
+
+
+@pytest.mark.parametrize("tags", ["contiguous", "scattered", "scattered-compare", "low-ids"])
+@pytest.mark.parametrize("cus", [16, FEW])
+def test_emulated_adversarial(emu, tags, cus):
+    """Every short valid string and mutations, nesting to depth 1000, outlines
+    beyond 64 entries, all-tag rows whose segments overflow their event
+    storage (the dense path, classified again token by token)."""
+    tag_ids = {"contiguous": TAGS, "low-ids": LOW_IDS}.get(tags, S.SCATTERED_TAGS)
+    tokens, starts, lengths = pack(adversarial_streams(), tag_ids)
+    n = lengths.size
+    correct = (np.arange(n) % 3 != 0).astype(np.uint8)
+    flags = PX.CFG_TAG_COMPARE if tags == "scattered-compare" else 0
+    got = check(emu, tokens, starts, lengths, correct, tag_ids, flags, cus, what="adversarial %s" % tags)
+    assert int(np.sum(got["max_depth"] == 1000)) == 1
+
+
+def test_emulated_lenient_gaps(emu):
+    rng = np.random.default_rng(21)
+    P = S.make_params("small")
+    tok, st, ln, co = S.host_batch(P, 64)
+    rows = [insert_gaps(tok[st[i]: st[i] + ln[i]], TAGS, rng) for i in range(64)]
+    lengths = np.array([r.size for r in rows], np.int32)
+    starts = np.zeros(64, np.int64)
+    starts[1:] = np.cumsum(lengths[:-1])
+    tokens = np.concatenate(rows)
+    for cus in (MANY, FEW):
+        check(emu, tokens, starts, lengths, co, flags=PX.CFG_LENIENT_GAPS, cus=cus, what="lenient cus %d" % cus)
+
+
+def test_emulated_layouts_noalloc_batch_stats(emu):
+    P = S.make_params("small")
+    tok, st, ln, co = S.host_batch(P, 64)
+    for shift in (1, 2, 3):
+        check(emu, tok, st, ln, co, cus=MANY, shift=shift, what="shift %d" % shift)
+    lmax = int(ln.max()) + 3
+    padded = np.full((64, lmax), 11, np.int32)
+    for i in range(64):
+        padded[i, : ln[i]] = tok[st[i]: st[i] + ln[i]]
+    check(emu, padded.ravel(), (np.arange(64) * lmax).astype(np.int64), ln, co, cus=FEW, what="padded")
+    check(emu, tok, st, ln, co, cus=MANY, noalloc=True, what="noalloc")
+    check(emu, tok, st, ln, co, flags=PX.CFG_BATCH_STATS, cus=FEW, what="batch stats")
+
+
+def test_emulated_bad_rows_and_workspace_overflow(emu):
+    P = S.make_params("typical")
+    tok, st, ln, co = S.host_batch(P, 16)
+    got, rc = run_emu(emu, tok, st, ln, co, cus=MANY, ws_tokens=0)
+    assert rc == PX.OK and np.all(got["flags"] == PX.FLAG_WS_OVERFLOW) and np.all(np.isnan(got["reward"]))
+    bad = ln.copy()
+    bad[3] = -4
+    got, rc = run_emu(emu, tok, st, bad, co, cus=MANY)
+    assert rc == PX.OK and got["flags"][3] == PX.FLAG_BAD_ROW and np.all(np.isnan(got["reward"][:8]))
+    keep = np.r_[8:16]
+    exp = oracle_expect(tok, st[keep], ln[keep], co[keep], TAGS, G, DEFAULT_COEF)
+    compare({k: v[keep] for k, v in got.items()}, *exp, what="bad-row rest")
+
+
+MUTANTS = {
+    # a DPP segmented scan whose carry out of the first row of 16 lanes is read one lane early
+    "seg-scan-off-by-one": ("device_common.h",
+                            "const int32_t v0 = __builtin_amdgcn_readlane(v, 15), v1",
+                            "const int32_t v0 = __builtin_amdgcn_readlane(v, 14), v1"),
+    # the scan's compaction forgets the count of tags of the vector's first token column
+    "compaction-carry": ("parason_kernels.h",
+                         "cnt += (uint32_t)(__popcll(b[0]) + __popcll(b[1])",
+                         "cnt += (uint32_t)(0 + __popcll(b[1])"),
+    # a row's edge segments keep tags of the neighbouring rows
+    "edge-mask": ("parason_kernels.h",
+                  "if (EDGE) hit = hit && q0 + j >= q_lo && q0 + j < q_hi;",
+                  "if (EDGE) hit = hit && q0 + j < q_hi;"),
+}
+
+
+def test_planted_mistakes_are_caught(tmp_path):
+    """Each mutant (built in parallel) must fail at least one comparison."""
+    procs = {}
+    for name, (f, old, new) in sorted(MUTANTS.items()):
+        d = tmp_path / name
+        shutil.copytree(CSRC, d)
+        src = (d / f).read_text()
+        assert src.count(old) == 1, "the planted line of %s is not in %s" % (name, f)
+        (d / f).write_text(src.replace(old, new))
+        out = str(tmp_path / (name + ".emu"))
+        cmd = [CLANG, "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+               "-ffp-contract=off", "-I", SIMT, "-I", os.path.join(ROOT, "include"), "-I", str(d), "-x", "c++",
+               str(d / "parason.hip"), os.path.join(SIMT, "emu_main.cpp"), "-o", out]
+        procs[name] = (subprocess.Popen(cmd), out)
+    for name, (p, _) in procs.items():
+        assert p.wait() == 0, name
+    P = S.make_params("small")
+    tok, st, ln, co = S.host_batch(P, 64)
+    tokens, starts, lengths = pack(adversarial_streams(), TAGS)
+    correct = (np.arange(lengths.size) % 3 != 0).astype(np.uint8)
+    for name, (_, binary) in sorted(procs.items()):
+        caught = 0
+        for args, cus in (((tok, st, ln, co), MANY), ((tokens, starts, lengths, correct), 16),
+                          ((tok, st, ln, co), FEW)):
+            try:
+                check(binary, *args, cus=cus, what=name)
+            except (AssertionError, RuntimeError):
+                caught += 1
+        assert caught > 0, "planted mistake %s went unnoticed" % name
