@@ -23,9 +23,21 @@ constexpr int WAVE = 64;
 constexpr int SEG_VEC = PARASON_SEG_VEC; /* 16-byte vectors per segment (1024 tokens) */
 constexpr int SEG_TOK = 4 * SEG_VEC;     /* tokens per segment */
 constexpr int LOADS = SEG_VEC / WAVE;    /* vector loads per lane per segment */
-constexpr int EV_CAP = 128;              /* events stored per segment (12.5 % of its tokens) */
+/* Where the scan leaves the tag events of a segment (or of a whole row):
+ * EV_INLINE slots in the segment's own record, and the rest in a pool that is
+ * cut into one region per scan wave, the same number of slots for each
+ * segment of the wave's range: POOL_PER_SEG, or more when the batch is small
+ * enough for the pool to hold POOL_MIN slots.  A wave fills its region in
+ * order, so no atomics are needed, and tags, which are rare, use about 1.5 %
+ * of the token bytes in all. */
+constexpr int EV_INLINE = 4;
+constexpr int POOL_PER_SEG = 8;
+constexpr int64_t POOL_MIN = (int64_t)1 << 18;
+/* seg_count of a segment whose events were not stored: the row kernels
+ * classify its tokens again (counts of stored lists are at most 2048) */
+constexpr int32_t DENSE = 1 << 20;
 static_assert(SEG_VEC % WAVE == 0, "a segment is a whole number of wave-wide loads");
-static_assert(EV_CAP % 4 == 0, "stored events are read 16 bytes at a time");
+static_assert(EV_INLINE % 4 == 0 && POOL_PER_SEG % 4 == 0, "stored events are read 16 bytes at a time");
 constexpr int PLAN_TILE = 4096;          /* rows per plan tile */
 constexpr int PLAN_THREADS = 256;
 constexpr int ROWS_PER_THREAD = PLAN_TILE / PLAN_THREADS;
@@ -38,6 +50,11 @@ constexpr int FAST_ENTRIES = 64;         /* entries per open block on the fast p
 constexpr int FRAME_WORDS = 8;
 constexpr int64_t DEEP_FRAMES = PARASON_MAX_DEPTH;
 constexpr int64_t DEEP_ENTRY_BITS = PARASON_MAX_OPEN_ENTRIES;
+/* A row nests at most one level per 6 tokens and opens at most one outline
+ * entry per 3, so a store of these per 1024-token segment of the batch holds
+ * any row (up to DEEP_FRAMES and DEEP_ENTRY_BITS). */
+constexpr int64_t DEEP_FRAMES_PER_SEG = 1024 / 6 + 1;
+constexpr int64_t DEEP_BITS_PER_SEG = 1024 / 3 + 1;
 
 /* Token classes: 0 = Text, 1..12 = tags in tag_ids order. */
 enum : uint32_t {

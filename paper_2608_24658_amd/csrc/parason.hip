@@ -9,6 +9,7 @@
  * chevron, so that this file also compiles as plain C++ against the CPU
  * emulation of the HIP runtime that the tests run the kernels on.
  */
+#include <algorithm>
 #include <cstring>
 #include <new>
 
@@ -33,8 +34,7 @@ constexpr int ROWS_WAVES_PER_CU = 20;   /* rows_fast waves a CU holds (8 KB of L
 
 /* Byte offsets of the workspace sections for n rows. */
 struct Layout {
-    size_t seg_off, tile_sum, tile_off, counters, mode, mid_rows, deep_rows, split_rows, deep_frames, deep_bits,
-        seg_count, events;
+    size_t seg_off, tile_sum, tile_off, counters, mode, mid_rows, deep_rows, split_rows;
     size_t red_d, red_i, stats;
     size_t fixed;  /* bytes before the per-segment sections */
     int64_t n_tiles;
@@ -61,10 +61,6 @@ Layout layout_for(int64_t n)
     o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
     L.split_rows = o;
     o = align_up(o + (size_t)(n > 0 ? n : 1) * sizeof(int32_t));
-    L.deep_frames = o;
-    o = align_up(o + (size_t)pk::DEEP_FRAMES * pk::FRAME_WORDS * sizeof(int32_t));
-    L.deep_bits = o;
-    o = align_up(o + (size_t)(pk::DEEP_ENTRY_BITS / 32) * sizeof(uint32_t));
     /* partial sums of the batch reductions (one record per 4096 rows) */
     L.red_d = o;
     o = align_up(o + (size_t)L.n_tiles * 3 * sizeof(double));
@@ -73,20 +69,56 @@ Layout layout_for(int64_t n)
     L.stats = o;
     o = align_up(o + sizeof(pk::BatchStats));
     L.fixed = o;
-    L.seg_count = o;
-    L.events = 0; /* depends on the capacity */
     return L;
 }
 
-constexpr size_t PER_SEGMENT = sizeof(int32_t) + (size_t)pk::EV_CAP * sizeof(uint32_t);
+/* The sections after the fixed ones, for a capacity of cap segments: the
+ * deep tier's frames and entry bits (sized for any row that fits in cap
+ * segments), seg_count (int32), seg_ovf (int64) and EV_INLINE inline event
+ * slots per segment, then the event pool.  About 60 bytes per 1024-token
+ * segment once the deep store reaches its maximum (2^20 frames, 32 MiB, from
+ * about 6,100 segments on). */
+struct CapSections {
+    size_t frames, bits, seg_count, seg_ovf, events, pool, end; /* byte offsets; end = bytes needed */
+    int64_t n_frames, n_bits, pool_per_seg;
+};
 
-/* Segments a workspace of `bytes` can hold for n rows. */
+CapSections cap_sections(const Layout &L, int64_t cap)
+{
+    CapSections q;
+    q.n_frames = std::min(pk::DEEP_FRAMES, pk::DEEP_FRAMES_PER_SEG * cap + 1);
+    q.n_bits = std::min(pk::DEEP_ENTRY_BITS, (pk::DEEP_BITS_PER_SEG * cap + 32 + 31) / 32 * 32);
+    const int64_t pool_slots = std::max((int64_t)pk::POOL_PER_SEG * cap, pk::POOL_MIN);
+    q.pool_per_seg = cap > 0 ? (pool_slots / cap) & ~(int64_t)3 : pk::POOL_PER_SEG; /* >= POOL_PER_SEG */
+    size_t o = L.fixed;
+    q.frames = o;
+    o = align_up(o + (size_t)q.n_frames * pk::FRAME_WORDS * sizeof(int32_t));
+    q.bits = o;
+    o = align_up(o + (size_t)(q.n_bits / 32) * sizeof(uint32_t));
+    q.seg_count = o;
+    o = align_up(o + (size_t)cap * sizeof(int32_t));
+    q.seg_ovf = o;
+    o = align_up(o + (size_t)cap * sizeof(int64_t));
+    q.events = o;
+    o = align_up(o + (size_t)cap * pk::EV_INLINE * sizeof(uint32_t));
+    q.pool = o;
+    q.end = o + (size_t)pool_slots * sizeof(uint32_t);
+    return q;
+}
+
+/* Segments a workspace of `bytes` can hold for n rows (the bytes needed grow
+ * with the capacity, so the largest one that fits is found by bisection). */
 int64_t capacity_for(int64_t n, size_t bytes)
 {
-    Layout L = layout_for(n);
-    if (bytes < L.fixed + 2 * ALIGN) return 0;
-    int64_t cap = (int64_t)((bytes - L.fixed - 2 * ALIGN) / PER_SEGMENT);
-    return cap < MAX_SEGMENTS ? cap : MAX_SEGMENTS;
+    const Layout L = layout_for(n);
+    if (cap_sections(L, 1).end > bytes) return 0;
+    int64_t lo = 1, hi = MAX_SEGMENTS + 1; /* cap_sections(lo) fits, hi does not (or is past the maximum) */
+    while (hi - lo > 1) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (cap_sections(L, mid).end <= bytes) lo = mid;
+        else hi = mid;
+    }
+    return lo;
 }
 
 /* Upper bound of the number of segments of rows whose lengths add up to total. */
@@ -250,8 +282,7 @@ int parason_workspace_size(const parason_handle *h, int64_t n_traj, int64_t tota
     if (n_traj < 0 || total_tokens < 0 || n_traj > INT32_MAX) return PARASON_ERR_SIZE;
     int64_t segs = segment_bound(n_traj, total_tokens);
     if (segs > MAX_SEGMENTS) return PARASON_ERR_SIZE;
-    Layout L = layout_for(n_traj);
-    *bytes = L.fixed + 2 * ALIGN + (size_t)segs * PER_SEGMENT;
+    *bytes = cap_sections(layout_for(n_traj), segs).end;
     return PARASON_OK;
 }
 
@@ -290,13 +321,16 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     int32_t *mid_rows = (int32_t *)(ws + L.mid_rows);
     int32_t *deep_rows = (int32_t *)(ws + L.deep_rows);
     int32_t *split_rows = (int32_t *)(ws + L.split_rows);
-    int32_t *deep_frames = (int32_t *)(ws + L.deep_frames);
-    uint32_t *deep_bits = (uint32_t *)(ws + L.deep_bits);
-    int32_t *seg_count = (int32_t *)(ws + L.seg_count);
     double *red_d = (double *)(ws + L.red_d);
     int64_t *red_i = (int64_t *)(ws + L.red_i);
     pk::BatchStats *stats = (pk::BatchStats *)(ws + L.stats);
-    uint32_t *events = (uint32_t *)(ws + align_up(L.seg_count + (size_t)cap * sizeof(int32_t)));
+    const CapSections q = cap_sections(L, cap);
+    int32_t *deep_frames = (int32_t *)(ws + q.frames);
+    uint32_t *deep_bits = (uint32_t *)(ws + q.bits);
+    int32_t *seg_count = (int32_t *)(ws + q.seg_count);
+    int64_t *seg_ovf = (int64_t *)(ws + q.seg_ovf);
+    uint32_t *events = (uint32_t *)(ws + q.events);
+    uint32_t *pool = (uint32_t *)(ws + q.pool);
 
     const unsigned tiles = (unsigned)L.n_tiles;
     abi::launch_plan(starts, lengths, n_traj, mis, L.n_tiles, tile_sum, tile_off, seg_off, counters, mode, stream);
@@ -312,7 +346,10 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     sa.seg_off = seg_off;
     sa.seg_cap = cap;
     sa.seg_count = seg_count;
+    sa.seg_ovf = seg_ovf;
     sa.events = events;
+    sa.pool = pool;
+    sa.pool_per_seg = q.pool_per_seg;
     sa.mode = mode;
     sa.tm = h->tm;
     sa.split_count = counters + 2;
@@ -339,10 +376,15 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.seg_off = seg_off;
     ra.seg_cap = cap;
     ra.seg_count = seg_count;
+    ra.seg_ovf = seg_ovf;
     ra.events = events;
+    ra.pool = pool;
+    ra.deep_frames = q.n_frames;
+    ra.deep_bits = q.n_bits;
     ra.tm = h->tm;
     ra.out = row_out;
-    const pk::GatherArgs ga{starts, n_traj, mis, seg_off, cap, seg_count, events, mode, counters + 2, split_rows};
+    const pk::GatherArgs ga{starts, n_traj, mis,  seg_off,      cap,       seg_count,
+                            seg_ovf, events, pool, mode, counters + 2, split_rows};
     const bool lenient = (h->cfg.flags & PARASON_CFG_LENIENT_GAPS) != 0;
     const bool batch_stats = (h->cfg.flags & PARASON_CFG_BATCH_STATS) != 0;
     if (lenient)

@@ -14,11 +14,13 @@
  *        0.1-1% of tokens) in position order.  A row whose segments all fall in
  *        one wave's range collects its events in that wave's LDS buffer and is
  *        written out, coalesced, as one compact list (mode[i] = 1).  Other rows
- *        leave their events in per-segment global slots (mode[i] = 0) and are
- *        listed as split.
+ *        leave their events in per-segment lists (mode[i] = 0) and are listed
+ *        as split.  A list's first slots are inline in its first segment's
+ *        record (EV_INLINE per segment of the list); the others are in the
+ *        scan wave's region of the pool.
  *   gather_rows  (one wave per split row)
- *        Moves a split row's per-segment events, in place and in order, into
- *        one compact list with row positions (mode[i] = 1).
+ *        Gathers a split row's per-segment events through LDS into one compact
+ *        list with row positions in the row's inline slots (mode[i] = 1).
  *   rows_par  (small batches: one wave per row, lanes over its events)
  *        Validity from local checks and a depth prefix sum; latency and branch
  *        tokens level by level with segmented scans (DPP).  A row it cannot
@@ -26,8 +28,8 @@
  *        LDS, as in rows_mid.
  *   rows_fast  (larger batches: one thread per row)
  *        The grammar's pushdown automaton over the row's events; Text runs are
- *        the gaps between event positions.  A segment holding more than EV_CAP
- *        tags, or marked DENSE by the scan, is classified again token by token.
+ *        the gaps between event positions.  A segment whose events the scan
+ *        could not store (marked DENSE) is classified again token by token.
  *        Frames of open blocks in LDS (FAST_DEPTH per row, 64 outline entries
  *        per block); a row that needs more is handed to rows_mid.
  *   rows_mid  (after rows_fast: one thread per handed-over row, MID_DEPTH
@@ -57,7 +59,7 @@ namespace pk {
 
 /* mode[i], one byte per row: where its events are, and whether the deep tier
  * evaluates it. */
-constexpr uint8_t MODE_COMPACT = 1; /* one compact list with row positions (else per-segment slots) */
+constexpr uint8_t MODE_COMPACT = 1; /* one compact list with row positions (else per-segment lists) */
 constexpr uint8_t MODE_DEEP = 2;    /* listed for the single-thread tier with global frames */
 
 /* ------------------------------------------------------------------ plan */
@@ -114,7 +116,7 @@ __global__ void __launch_bounds__(1024) plan_top(const int64_t *__restrict__ til
     if (threadIdx.x == 0) seg_off[n] = carry_s;
 }
 
-/* seg_off[i] = first segment of row i; mode[i] = 0 (events in per-segment slots). */
+/* seg_off[i] = first segment of row i; mode[i] = 0 (events in per-segment lists). */
 /* SINGLE: the batch is one tile, and this one block also does plan_top's
  * work (seg_off[n], clearing the counters), so a small batch is planned with
  * one launch instead of three. */
@@ -209,12 +211,14 @@ struct LdsStore {
 
 /* Deep store: frames and entry bits in global workspace (single thread). */
 struct GlobalStore {
-    int32_t *frames;  /* [DEEP_FRAMES][FRAME_WORDS] */
-    uint32_t *bits;   /* DEEP_ENTRY_BITS bits */
+    int32_t *frames;    /* [max_frames][FRAME_WORDS] */
+    uint32_t *bits;     /* max_bits bits */
+    int64_t max_frames; /* at most DEEP_FRAMES */
+    int64_t max_bits;   /* at most DEEP_ENTRY_BITS */
     int64_t esp;      /* next free entry bit */
     __device__ bool push(const Top &t, int d)
     {
-        if ((int64_t)d > DEEP_FRAMES) return false;
+        if ((int64_t)d > max_frames) return false;
         int32_t *f = frames + (int64_t)(d - 1) * FRAME_WORDS;
         f[0] = t.saved_acc;
         f[1] = t.block_main;
@@ -242,7 +246,7 @@ struct GlobalStore {
     __device__ bool add_entry(Top &t, bool trial)
     {
         int64_t b = (int64_t)t.ent + t.n_e;
-        if (b >= DEEP_ENTRY_BITS) return false;
+        if (b >= max_bits) return false;
         uint32_t w = bits[b >> 5], m = 1u << (b & 31);
         bits[b >> 5] = trial ? (w | m) : (w & ~m);
         esp = b + 1;
@@ -500,7 +504,11 @@ struct RowArgs {
     const int64_t *seg_off;
     int64_t seg_cap;
     const int32_t *seg_count;
-    const uint32_t *events;
+    const int64_t *seg_ovf; /* pool slot of a list's events beyond its inline ones */
+    const uint32_t *events; /* EV_INLINE inline slots per segment */
+    const uint32_t *pool;
+    int64_t deep_frames;    /* frames of the deep tier's store in workspace ... */
+    int64_t deep_bits;      /* ... and its entry bits */
     TagMatch tm;
     RowOut out;
 };
@@ -508,13 +516,14 @@ struct RowArgs {
 /* Feed row r's events to A.  Returns false when A stopped early.
  *
  * Three sources, all feeding the one call of A.event below: a compact list
- * (the scan collected the whole row: events[first*EV_CAP ..], row positions,
- * count in seg_count[first]), or per segment its stored events (segment
- * positions) or, for a segment holding more than EV_CAP tags or marked DENSE,
- * its tokens classified again one by one.  With two inlined copies of the
- * automaton (one per source) the gfx950 build returned wrong results for dense
- * segments although the same source is correct when compiled for the CPU, so
- * the sources are merged into one fetch loop. */
+ * (the whole row: count in seg_count[first], row positions), or per segment
+ * its stored list (segment positions) or, for a segment marked DENSE, its
+ * tokens classified again one by one.  A list's first events are inline
+ * (EV_INLINE slots per segment it covers), the others in the pool at
+ * seg_ovf.  With two inlined copies of the automaton (one per source) the
+ * gfx950 build returned wrong results for dense segments although the same
+ * source is correct when compiled for the CPU, so the sources are merged into
+ * one fetch loop. */
 template <class Store, bool LENIENT>
 __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, bool compact,
                           Automaton<Store, LENIENT> &A)
@@ -522,15 +531,17 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
     const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
     const int64_t vrow0 = row_first_vec(g), vend = row_end_vec(g, len);
     int64_t s = s0;              /* next segment to open */
-    const uint32_t *ev = nullptr;
-    int32_t e = 0, cnt = 0;      /* stored-event cursor */
+    const uint32_t *ev = nullptr, *ovf = nullptr;
+    int32_t e = 0, cnt = 0, cap_in = 0; /* stored-event cursor, list length, inline slots */
     int64_t base = 0;            /* row position of stored position 0 */
     bool dense = false;
     int64_t q = 0, q_end = 0;    /* dense cursor (element index on the token grid) */
     uint4 quad = make_uint4(0u, 0u, 0u, 0u);
     if (compact) {
-        ev = a.events + s0 * EV_CAP;
+        ev = a.events + s0 * EV_INLINE;
         cnt = a.seg_count[s0];
+        cap_in = (int32_t)min((int64_t)cnt, (s1 - s0) * EV_INLINE);
+        if (cnt > cap_in) ovf = a.pool + a.seg_ovf[s0];
         s = s1;
     }
     for (;;) {
@@ -538,9 +549,10 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
         uint32_t c = 0;
         for (;;) {
             if (!dense && e < cnt) {
-                /* stored lists start 256-byte aligned and their slots are
+                /* inline slots and pool parts start 16-byte aligned and hold
                  * multiples of 4 events: read them 16 bytes at a time */
-                if ((e & 3) == 0) quad = *reinterpret_cast<const uint4 *>(ev + e);
+                if ((e & 3) == 0)
+                    quad = *reinterpret_cast<const uint4 *>(e < cap_in ? ev + e : ovf + (e - cap_in));
                 const uint32_t k = (uint32_t)e & 3u;
                 const uint32_t w = k == 0 ? quad.x : k == 1 ? quad.y : k == 2 ? quad.z : quad.w;
                 ++e;
@@ -569,9 +581,11 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
             const int32_t n_s = a.seg_count[s];
             base = 4 * v0 - g;
             e = 0;
-            if (n_s <= EV_CAP) {
-                ev = a.events + s * EV_CAP;
+            if (n_s != DENSE) {
+                ev = a.events + s * EV_INLINE;
                 cnt = n_s;
+                cap_in = min(n_s, EV_INLINE);
+                ovf = n_s > EV_INLINE ? a.pool + a.seg_ovf[s] : nullptr;
             } else {
                 cnt = 0;
                 dense = true;
@@ -587,7 +601,7 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
 }
 
 /* One thread per row.  mode[r] == MODE_COMPACT: the scan left the row's events as one
- * compact list; 0: per-segment slots.  A row that needs more than FAST_DEPTH
+ * compact list; 0: per-segment lists.  A row that needs more than FAST_DEPTH
  * frames (or more than 64 entries in an open block) is listed for rows_mid.
  * Few frames keep the LDS per block small, so that many waves hide the
  * latency of the branchy automaton. */
@@ -667,6 +681,8 @@ __device__ void run_deep_rows(const RowArgs &a, const uint8_t *__restrict__ mode
         Automaton<GlobalStore, LENIENT> A;
         A.st.frames = frames;
         A.st.bits = bits;
+        A.st.max_frames = a.deep_frames;
+        A.st.max_bits = a.deep_bits;
         A.st.esp = 0;
         A.init();
         if (drive_row(a, r, a.starts[r] + a.mis, len, (mode[r] & MODE_COMPACT) != 0, A)) A.finish(len);
@@ -814,13 +830,16 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
     if (md & MODE_COMPACT) {
         m = a.seg_count[s0];
         held = m <= PAR_EVENTS;
-        const uint32_t *list = a.events + s0 * EV_CAP;
+        /* the list's first slots inline (EV_INLINE per segment), the rest in the pool */
+        const uint32_t *list = a.events + s0 * EV_INLINE;
+        const int32_t cap_in = (int32_t)min((int64_t)m, (s1 - s0) * EV_INLINE);
+        const int64_t ovf = m > cap_in ? a.seg_ovf[s0] : 0;
         for (int32_t i0 = 0; held && i0 < m; i0 += 4 * WAVE) { /* four loads per lane in flight */
             uint32_t w[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int32_t i = i0 + u * WAVE + lane;
-                w[u] = i < m ? list[i] : 0u;
+                w[u] = i < m ? (i < cap_in ? list[i] : a.pool[ovf + (i - cap_in)]) : 0u;
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
@@ -836,12 +855,14 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
         for (int64_t c0 = s0; held && c0 < s1; c0 += WAVE) {
             const int64_t s = c0 + lane;
             const int32_t cnt = s < s1 ? a.seg_count[s] : 0;
-            const int32_t incl = wave_incl_scan32(cnt, lane);
+            /* where the segment's events beyond its inline slots are (loaded
+             * with the count; meaningless unless cnt > EV_INLINE) */
+            const int64_t ovf = s < s1 ? a.seg_ovf[s] - EV_INLINE : 0;
+            const int32_t incl = wave_incl_scan32(cnt, lane); /* DENSE counts cannot overflow it */
             const int32_t excl = incl - cnt;
             const int32_t total = lane63(incl);
-            /* a dense segment (more than EV_CAP tags) or too many events: the
-             * automaton below */
-            held = __ballot(cnt > EV_CAP) == 0 && m + total <= PAR_EVENTS;
+            /* a dense segment or too many events: the automaton below */
+            held = __ballot(cnt == DENSE) == 0 && m + total <= PAR_EVENTS;
             for (int32_t f0 = 0; held && f0 < total; f0 += 2 * WAVE) { /* two loads per lane in flight */
                 int32_t j[2];
                 uint32_t w[2];
@@ -850,7 +871,9 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
                     const int32_t f = f0 + u * WAVE + lane;
                     j[u] = last_lane_at_most(excl, f);
                     const int32_t first = __shfl(excl, j[u], WAVE);
-                    w[u] = f < total ? a.events[(c0 + j[u]) * EV_CAP + (f - first)] : 0u;
+                    const int64_t ov = __shfl(ovf, j[u], WAVE);
+                    const int32_t e = f - first; /* the event's index in its segment's list */
+                    w[u] = f < total ? (e < EV_INLINE ? a.events[(c0 + j[u]) * EV_INLINE + e] : a.pool[ov + e]) : 0u;
                 }
 #pragma unroll
                 for (int u = 0; u < 2; ++u) {
@@ -1044,14 +1067,16 @@ __device__ __forceinline__ bool is_tag(const TagMatch &tm, int32_t t, int32_t ta
 __device__ __forceinline__ uint32_t lane_bit(uint64_t mask, int lane) { return (uint32_t)(mask >> lane) & 1u; }
 
 /* Tags of the LOADS vectors x[i] (vector v0 + i*WAVE + lane of this lane) are
- * appended to dst[0 .. cap) in position order as (q + bias) << 4 | class, where
- * q = 4*(i*WAVE + lane) + j is the position in the segment; cnt counts all of
- * them, stored or not.  EDGE: the segment holds the first or last vector of its
- * row, so only positions q_lo <= q < q_hi belong to the row. */
+ * appended in position order as (q + bias) << 4 | class, where
+ * q = 4*(i*WAVE + lane) + j is the position in the segment: the first cap to
+ * dst[0 .. cap), the next cap2 to dst2[0 .. cap2); cnt counts all of them,
+ * stored or not.  EDGE: the segment holds the first or last vector of its row,
+ * so only positions q_lo <= q < q_hi belong to the row. */
 template <int MODE, bool EDGE>
 __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_lo, int32_t q_hi,
-                                             uint32_t *__restrict__ dst, uint32_t cap, int32_t bias, uint32_t &cnt,
-                                             const TagMatch &tm, int32_t tab, int lane)
+                                             uint32_t *__restrict__ dst, uint32_t cap, uint32_t *__restrict__ dst2,
+                                             uint32_t cap2, int32_t bias, uint32_t &cnt, const TagMatch &tm,
+                                             int32_t tab, int lane)
 {
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
@@ -1084,7 +1109,9 @@ __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_l
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 if (mine & (1u << j)) {
-                    if (idx < cap) dst[idx] = ((uint32_t)(q0 + j + bias) << 4) | classify(tm, t[j], MODE == TM_CONTIG);
+                    const uint32_t v = ((uint32_t)(q0 + j + bias) << 4) | classify(tm, t[j], MODE == TM_CONTIG);
+                    if (idx < cap) dst[idx] = v;
+                    else if (idx - cap < cap2) dst2[idx - cap] = v;
                     ++idx;
                 }
             }
@@ -1106,9 +1133,8 @@ __device__ __forceinline__ void issue_loads(int4 (&x)[LOADS], const int4 *src, c
     }
 }
 
-/* seg_count[s] = DENSE for s in [a, b): the row kernel classifies those
+/* seg_count[s] = DENSE for s in [a, b): the row kernels classify those
  * segments' tokens again. */
-constexpr int32_t DENSE = EV_CAP + 1;
 
 __device__ __forceinline__ void mark_dense(int32_t *seg_count, int64_t a, int64_t b, int lane)
 {
@@ -1124,7 +1150,11 @@ struct ScanArgs {
     const int64_t *seg_off;
     int64_t seg_cap;
     int32_t *seg_count;
-    uint32_t *events;
+    int64_t *seg_ovf;   /* pool slot of a list's events beyond its inline ones */
+    uint32_t *events;   /* EV_INLINE inline slots per segment */
+    uint32_t *pool;     /* wave w's region: pool_per_seg slots per segment of its
+                           range [s_begin, s_end), from pool_per_seg * s_begin */
+    int64_t pool_per_seg; /* a multiple of 4, at least POOL_PER_SEG */
     uint8_t *mode;
     TagMatch tm;
     int32_t *split_count; /* rows of more than one segment that no scan wave owns ... */
@@ -1134,38 +1164,50 @@ struct ScanArgs {
 /* Row being collected by a scan wave, in processing order. */
 struct RowCollect {
     uint32_t lcnt; /* events in the wave's LDS buffer */
-    bool global;   /* events go to the segments' global slots; the row kernel evaluates the row */
+    bool global;   /* events go to per-segment lists; the row kernel evaluates the row */
+    int64_t pc;    /* next free slot of the wave's pool region (a multiple of 4) ... */
+    int64_t p_end; /* ... and its end */
 };
 
 constexpr int EVL = 1024;                 /* LDS events per wave */
 constexpr int SCAN_WAVES = 4;             /* waves per scan block */
 
 /* The whole of row `row` is in the wave's LDS buffer lev[0 .. lcnt): copy it,
- * coalesced, to the row's own slot range events[first*EV_CAP ..] as one
- * compact list for the row kernel (mode 1).  A list longer than the row's
- * slots makes the row kernel classify its segments again. */
+ * coalesced, as one compact list for the row kernel (mode 1): its first
+ * events to the row's inline slots (EV_INLINE per segment), the rest to the
+ * wave's pool region.  A list that does not fit makes the row kernel classify
+ * the row's segments again. */
 __device__ __forceinline__ void flush_row(const ScanArgs &a, int64_t row, int64_t first, int64_t last, uint32_t lcnt,
-                                          const uint32_t *lev, int lane)
+                                          const uint32_t *lev, RowCollect &rc, int lane)
 {
-    if ((int64_t)lcnt > (last - first + 1) * EV_CAP) {
+    const int64_t cap_in = (last - first + 1) * EV_INLINE;
+    const int64_t rest = (int64_t)lcnt > cap_in ? (int64_t)lcnt - cap_in : 0;
+    const int64_t need = (rest + 3) & ~(int64_t)3;
+    if (need > rc.p_end - rc.pc) {
         mark_dense(a.seg_count, first, last + 1, lane);
         return;
     }
-    uint32_t *dst = a.events + first * EV_CAP;
+    uint32_t *in = a.events + first * EV_INLINE;
+    uint32_t *ovf = a.pool + rc.pc;
     /* lane i copies events other lanes wrote: the wave's LDS stores above
      * come first (a wave's LDS accesses are performed in program order; this
      * keeps the compiler from moving them across) */
     __builtin_amdgcn_wave_barrier();
-    for (uint32_t i = lane; i < lcnt; i += WAVE) dst[i] = lev[i];
+    for (uint32_t i = lane; i < lcnt; i += WAVE) {
+        if ((int64_t)i < cap_in) in[i] = lev[i];
+        else ovf[i - cap_in] = lev[i];
+    }
     if (lane == 0) {
         a.seg_count[first] = (int32_t)lcnt;
+        if (rest > 0) a.seg_ovf[first] = rc.pc;
         a.mode[row] = MODE_COMPACT;
     }
+    rc.pc += need;
 }
 
 /* Scan one segment whose loads are in x.  A row owned by the wave collects
  * its events in the wave's LDS buffer; any other row leaves its events in the
- * global per-segment slots for rows_fast.  Returns true when this segment
+ * per-segment lists for the row kernels.  Returns true when this segment
  * completes a row whose events are all in the LDS buffer (rc.lcnt of them). */
 template <int MODE>
 __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&x)[LOADS], const SegView &w,
@@ -1183,22 +1225,33 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
     if (!rc.global) {
         const int32_t bias = (int32_t)(4 * w.v0 - w.g); /* row position of segment position 0 */
         const uint32_t cap = (uint32_t)EVL - rc.lcnt;
-        if (!w.edge) scan_vectors<MODE, false>(x, 0, SEG_TOK, lev + rc.lcnt, cap, bias, cnt, a.tm, tab, lane);
-        else scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, lev + rc.lcnt, cap, bias, cnt, a.tm, tab, lane);
+        if (!w.edge)
+            scan_vectors<MODE, false>(x, 0, SEG_TOK, lev + rc.lcnt, cap, nullptr, 0, bias, cnt, a.tm, tab, lane);
+        else
+            scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, lev + rc.lcnt, cap, nullptr, 0, bias, cnt, a.tm, tab, lane);
         if (cnt > cap) {
             /* the row's events overflow the LDS buffer: its segments so far are
-             * classified again by the row kernel, the rest use global slots */
+             * classified again by the row kernel, the rest use per-segment lists */
             mark_dense(a.seg_count, w.first, w.s + 1, lane);
             rc.global = true;
         } else {
             rc.lcnt += cnt;
         }
     } else {
+        /* the segment's own list: EV_INLINE slots inline, the rest in the pool */
+        uint32_t *in = a.events + w.s * EV_INLINE, *ovf = a.pool + rc.pc;
+        const uint32_t room = (uint32_t)min(rc.p_end - rc.pc, (int64_t)SEG_TOK);
         if (!w.edge)
-            scan_vectors<MODE, false>(x, 0, SEG_TOK, a.events + w.s * EV_CAP, EV_CAP, 0, cnt, a.tm, tab, lane);
+            scan_vectors<MODE, false>(x, 0, SEG_TOK, in, EV_INLINE, ovf, room, 0, cnt, a.tm, tab, lane);
         else
-            scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, a.events + w.s * EV_CAP, EV_CAP, 0, cnt, a.tm, tab, lane);
-        if (lane == 0) a.seg_count[w.s] = (int32_t)cnt;
+            scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, in, EV_INLINE, ovf, room, 0, cnt, a.tm, tab, lane);
+        const int64_t need = cnt > (uint32_t)EV_INLINE ? ((int64_t)cnt - EV_INLINE + 3) & ~(int64_t)3 : 0;
+        const bool stored = need <= (int64_t)room; /* room is a multiple of 4 */
+        if (lane == 0) {
+            a.seg_count[w.s] = stored ? (int32_t)cnt : DENSE;
+            if (stored && need > 0) a.seg_ovf[w.s] = rc.pc;
+        }
+        if (stored) rc.pc += need;
     }
     return w.s == w.last && !rc.global;
 }
@@ -1237,6 +1290,8 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
     RowCollect rc;
     rc.lcnt = 0;
     rc.global = true; /* a row already begun in the previous wave's range */
+    rc.pc = uniform64(a.pool_per_seg * s_begin);
+    rc.p_end = uniform64(a.pool_per_seg * s_end);
     SegView w = cur.view(s_begin);
     /* two register buffers: segment s + 1 is in flight while s is compacted */
     int4 xa[LOADS], xb[LOADS];
@@ -1249,7 +1304,7 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
             wn = cur.view(s + 1);
             issue_loads(xb, src, wn, lane);
         }
-        if (collect_segment<MODE>(a, xa, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, lane);
+        if (collect_segment<MODE>(a, xa, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
         if (!more) break;
         ++s;
         w = wn;
@@ -1258,7 +1313,7 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
             wn = cur.view(s + 1);
             issue_loads(xa, src, wn, lane);
         }
-        if (collect_segment<MODE>(a, xb, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, lane);
+        if (collect_segment<MODE>(a, xb, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
         if (!more) break;
         ++s;
         w = wn;
@@ -1319,74 +1374,83 @@ struct GatherArgs {
     const int64_t *seg_off;
     int64_t seg_cap;
     int32_t *seg_count;
+    const int64_t *seg_ovf;
     uint32_t *events;
+    const uint32_t *pool;
     uint8_t *mode;
     const int32_t *split_count;
     const int32_t *split_rows;
 };
 
-/* Move the events of row `row` (split between scan waves: one list per
- * segment, segment positions) into one list at the start of its slot range,
- * in position order, with row positions (the compact form, mode 1).  The move
- * is in place: the k-th event of the row goes to slot k, which is never later
- * than the slot it comes from (a segment holds at most EV_CAP events), and
- * each wave-wide round loads all of its events before it stores any.  Rows
- * with a segment of more than EV_CAP events (or marked DENSE) are left as
- * they are; the whole wave calls this. */
-__device__ __forceinline__ void gather_row(const GatherArgs &a, int64_t row, int lane)
+constexpr int GATHER_EVENTS = 1024; /* LDS events per gather wave */
+
+/* Gather the events of row `row` (split between scan waves: one list per
+ * segment, segment positions) into one list in the row's inline slots, in
+ * position order, with row positions (the compact form, mode 1).  Every event
+ * is first loaded into the wave's LDS buffer lds[0 .. GATHER_EVENTS), then
+ * stored, so the inline slots can be overwritten.  A row with a DENSE segment,
+ * or with more events than its inline slots or the buffer hold, is left as it
+ * is; the whole wave calls this. */
+__device__ __forceinline__ void gather_row(const GatherArgs &a, int64_t row, uint32_t *lds, int lane)
 {
     const int64_t s0 = uniform64(a.seg_off[row]), s1 = uniform64(a.seg_off[row + 1]);
     const int64_t g = uniform64(a.starts[row] + a.mis);
     const int64_t vrow0 = row_first_vec(g);
     bool dense = false;
+    int64_t total = 0;
     for (int64_t c0 = s0; c0 < s1; c0 += WAVE) {
         const int64_t s = c0 + lane;
-        dense = dense || (s < s1 && a.seg_count[s] > EV_CAP);
+        const int32_t cnt = s < s1 ? a.seg_count[s] : 0;
+        dense = dense || cnt == DENSE;
+        total += lane63(wave_incl_scan32(cnt, lane)); /* DENSE counts cannot overflow it */
     }
-    if (__ballot(dense) != 0) return;
-    uint32_t *list = a.events + s0 * EV_CAP;
+    if (__ballot(dense) != 0 || total > GATHER_EVENTS || total > (s1 - s0) * EV_INLINE) return;
     int64_t carry = 0; /* events of the segments before this chunk */
     for (int64_t c0 = s0; c0 < s1; c0 += WAVE) {
         const int64_t s = c0 + lane;
         const int32_t cnt = s < s1 ? a.seg_count[s] : 0;
+        const int64_t ovf = s < s1 ? a.seg_ovf[s] - EV_INLINE : 0; /* used only when cnt > EV_INLINE */
         const int32_t incl = wave_incl_scan32(cnt, lane);
         const int32_t excl = incl - cnt;
-        const int32_t total = __shfl(incl, WAVE - 1, WAVE);
-        for (int32_t f0 = 0; f0 < total; f0 += WAVE) {
+        const int32_t n_c = lane63(incl);
+        for (int32_t f0 = 0; f0 < n_c; f0 += WAVE) {
             const int32_t f = f0 + lane; /* the chunk's f-th event, of segment c0 + j */
             const int32_t j = last_lane_at_most(excl, f);
             const int32_t first = __shfl(excl, j, WAVE);
-            const int64_t seg = c0 + j;
-            const uint32_t w = f < total ? a.events[seg * EV_CAP + (f - first)] : 0u;
-            /* every lane's load of this round before any lane's store (the
-             * stores may overwrite slots other lanes read) */
-            __builtin_amdgcn_wave_barrier();
-            if (f < total) {
+            const int64_t ov = __shfl(ovf, j, WAVE);
+            if (f < n_c) {
+                const int64_t seg = c0 + j;
+                const int32_t e = f - first;
+                const uint32_t w = e < EV_INLINE ? a.events[seg * EV_INLINE + e] : a.pool[ov + e];
                 /* row position of segment position 0 */
                 const int64_t base = 4 * (vrow0 + (seg - s0) * SEG_VEC) - g;
-                const uint32_t pos = (uint32_t)(base + (int64_t)(w >> 4));
-                list[carry + f] = (pos << 4) | (w & 15u);
+                lds[carry + f] = ((uint32_t)(base + (int64_t)(w >> 4)) << 4) | (w & 15u);
             }
         }
-        carry += total;
+        carry += n_c;
     }
+    /* lanes store what other lanes loaded: every load above first */
+    __builtin_amdgcn_wave_barrier();
+    uint32_t *list = a.events + s0 * EV_INLINE;
+    for (int64_t i = lane; i < carry; i += WAVE) list[i] = lds[i];
     if (lane == 0) {
         a.seg_count[s0] = (int32_t)carry;
         a.mode[row] = MODE_COMPACT;
     }
 }
 
-/* The rows the scan listed as split between its waves: when a batch holds
- * few rows, as an RL step does, that is nearly every row.  One wave per
- * listed row (grid-stride over the list). */
+/* The rows the scan listed as split between its waves, for the per-lane row
+ * kernel: one wave per listed row (grid-stride over the list). */
 __global__ void __launch_bounds__(256) gather_rows(GatherArgs a)
 {
+    __shared__ uint32_t lds[256 / WAVE][GATHER_EVENTS];
     const int lane = threadIdx.x & (WAVE - 1);
+    const int wib = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
     const int64_t wave = uniform64(((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / WAVE);
     const int64_t n_waves = (int64_t)gridDim.x * (blockDim.x / WAVE);
     if (a.seg_off[a.n] > a.seg_cap) return; /* the scan wrote nothing: the row kernel reports it */
     const int32_t n_split = __builtin_amdgcn_readfirstlane(*a.split_count);
-    for (int64_t i = wave; i < n_split; i += n_waves) gather_row(a, uniform64(a.split_rows[i]), lane);
+    for (int64_t i = wave; i < n_split; i += n_waves) gather_row(a, uniform64(a.split_rows[i]), lds[wib], lane);
 }
 
 /* ------------------------------------------------------------------ reward */

@@ -15,7 +15,7 @@ pattern and sized exactly, so reliance on its contents or reads past it fail.
 
 Planted mistakes in copies of the kernel sources (an off-by-one in a DPP
 segmented scan, a lost carry in the scan's compaction, a dropped row-edge
-mask) must each be caught by these comparisons."""
+mask, an unreserved pool part) must each be caught by these comparisons."""
 import os
 import shutil
 import subprocess
@@ -185,6 +185,8 @@ MUTANTS = {
     "edge-mask": ("parason_kernels.h",
                   "if (EDGE) hit = hit && q0 + j >= q_lo && q0 + j < q_hi;",
                   "if (EDGE) hit = hit && q0 + j < q_hi;"),
+    # a compact list's pool part is not reserved, so the next list overwrites it
+    "pool-cursor": ("parason_kernels.h", "    rc.pc += need;\n}", "    rc.pc += 0 * need;\n}"),
 }
 
 
