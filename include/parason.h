@@ -180,7 +180,9 @@ typedef struct parason_handle parason_handle;
 int parason_create(const parason_config *cfg, parason_handle **out);
 
 /* Bytes of device workspace parason_run needs for n_traj rows whose lengths
- * add up to at most total_tokens. */
+ * add up to at most total_tokens: about 1.4 % of the token bytes for large
+ * batches.  Batches beyond about 3.6e11 tokens (far more than one GPU holds)
+ * return PARASON_ERR_SIZE. */
 int parason_workspace_size(const parason_handle *h, int64_t n_traj, int64_t total_tokens, size_t *bytes);
 
 /* Evaluate a batch, asynchronously on `stream` (a hipStream_t; NULL is the

@@ -23,21 +23,33 @@ constexpr int WAVE = 64;
 constexpr int SEG_VEC = PARASON_SEG_VEC; /* 16-byte vectors per segment (1024 tokens) */
 constexpr int SEG_TOK = 4 * SEG_VEC;     /* tokens per segment */
 constexpr int LOADS = SEG_VEC / WAVE;    /* vector loads per lane per segment */
-/* Where the scan leaves the tag events of a segment (or of a whole row):
- * EV_INLINE slots in the segment's own record, and the rest in a pool that is
- * cut into one region per scan wave, the same number of slots for each
- * segment of the wave's range: POOL_PER_SEG, or more when the batch is small
- * enough for the pool to hold POOL_MIN slots.  A wave fills its region in
- * order, so no atomics are needed, and tags, which are rare, use about 1.5 %
- * of the token bytes in all. */
-constexpr int EV_INLINE = 4;
+/* Where the tag events of a segment (or of a whole row) are kept: one array
+ * of 4-byte slots, a list being a run of slots starting at a multiple of 4.
+ * The first GATHER_SLOTS per segment are a per-row area (the segments of a
+ * row are consecutive) that gather_rows writes compact lists into; the rest is
+ * the pool the scan writes into, cut into one region per scan wave:
+ * POOL_PER_SEG slots for each segment of the wave's range, plus an equal
+ * share of what the batch's segments leave of the pool (at least POOL_MIN
+ * slots), so that a wave with one or two segments of a small batch can still
+ * hold an outline-heavy segment.  A wave fills its region in order, so no
+ * atomics are needed, and tags, which are rare, use about 1.5 % of the token
+ * bytes in all. */
+constexpr int GATHER_SLOTS = 4;
 constexpr int POOL_PER_SEG = 8;
-constexpr int64_t POOL_MIN = (int64_t)1 << 18;
-/* seg_count of a segment whose events were not stored: the row kernels
+constexpr int64_t POOL_MIN = (int64_t)1 << 20;
+/* A segment's event list (or, in its first segment, a compact row's): its
+ * length and its first slot.  Slot indices fit 32 bits for any batch one GPU
+ * holds (the host refuses larger ones). */
+struct SegRec {
+    int32_t count;
+    uint32_t list;
+};
+
+/* seg count of a segment whose events were not stored: the row kernels
  * classify its tokens again (counts of stored lists are at most 2048) */
 constexpr int32_t DENSE = 1 << 20;
 static_assert(SEG_VEC % WAVE == 0, "a segment is a whole number of wave-wide loads");
-static_assert(EV_INLINE % 4 == 0 && POOL_PER_SEG % 4 == 0, "stored events are read 16 bytes at a time");
+static_assert(GATHER_SLOTS % 4 == 0 && POOL_PER_SEG % 4 == 0, "stored events are read 16 bytes at a time");
 constexpr int PLAN_TILE = 4096;          /* rows per plan tile */
 constexpr int PLAN_THREADS = 256;
 constexpr int ROWS_PER_THREAD = PLAN_TILE / PLAN_THREADS;

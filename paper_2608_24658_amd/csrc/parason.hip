@@ -27,7 +27,11 @@ namespace {
 #define PARASON_SCAN_BLOCKS_PER_CU 4
 #endif
 constexpr int SCAN_BLOCKS_PER_CU = PARASON_SCAN_BLOCKS_PER_CU; /* persistent grid of 4-wave blocks */
-constexpr int64_t MAX_SEGMENTS = (int64_t)1 << 40;
+/* slot indices are 32-bit: GATHER_SLOTS + POOL_PER_SEG slots per segment and
+ * POOL_MIN more must stay below 2^32 (about 3.6e11 tokens, far beyond what
+ * one GPU holds) */
+constexpr int64_t MAX_SEGMENTS =
+    (((int64_t)1 << 32) - 1 - pk::POOL_MIN) / (pk::GATHER_SLOTS + pk::POOL_PER_SEG);
 constexpr int MID_BLOCKS_PER_CU = 2; /* rows_mid blocks hold 64 KB of LDS frames each */
 constexpr int GATHER_BLOCKS_PER_CU = 8; /* 4-wave blocks of gather_rows */
 constexpr int ROWS_WAVES_PER_CU = 20;   /* rows_fast waves a CU holds (8 KB of LDS frames each) */
@@ -74,13 +78,13 @@ Layout layout_for(int64_t n)
 
 /* The sections after the fixed ones, for a capacity of cap segments: the
  * deep tier's frames and entry bits (sized for any row that fits in cap
- * segments), seg_count (int32), seg_ovf (int64) and EV_INLINE inline event
- * slots per segment, then the event pool.  About 60 bytes per 1024-token
- * segment once the deep store reaches its maximum (2^20 frames, 32 MiB, from
- * about 6,100 segments on). */
+ * segments), one SegRec per segment, then the event slots: GATHER_SLOTS per
+ * segment, then the pool (POOL_PER_SEG slots per segment, at least
+ * POOL_MIN).  About 56 bytes per 1024-token segment once the deep store
+ * reaches its maximum (2^20 frames, 32 MiB, from about 6,100 segments on). */
 struct CapSections {
-    size_t frames, bits, seg_count, seg_ovf, events, pool, end; /* byte offsets; end = bytes needed */
-    int64_t n_frames, n_bits, pool_per_seg;
+    size_t frames, bits, seg, slots, end;            /* byte offsets; end = bytes needed */
+    int64_t n_frames, n_bits, pool_base, pool_slots; /* the pool in slots */
 };
 
 CapSections cap_sections(const Layout &L, int64_t cap)
@@ -88,21 +92,17 @@ CapSections cap_sections(const Layout &L, int64_t cap)
     CapSections q;
     q.n_frames = std::min(pk::DEEP_FRAMES, pk::DEEP_FRAMES_PER_SEG * cap + 1);
     q.n_bits = std::min(pk::DEEP_ENTRY_BITS, (pk::DEEP_BITS_PER_SEG * cap + 32 + 31) / 32 * 32);
-    const int64_t pool_slots = std::max((int64_t)pk::POOL_PER_SEG * cap, pk::POOL_MIN);
-    q.pool_per_seg = cap > 0 ? (pool_slots / cap) & ~(int64_t)3 : pk::POOL_PER_SEG; /* >= POOL_PER_SEG */
+    q.pool_slots = std::max((int64_t)pk::POOL_PER_SEG * cap, pk::POOL_MIN);
     size_t o = L.fixed;
     q.frames = o;
     o = align_up(o + (size_t)q.n_frames * pk::FRAME_WORDS * sizeof(int32_t));
     q.bits = o;
     o = align_up(o + (size_t)(q.n_bits / 32) * sizeof(uint32_t));
-    q.seg_count = o;
-    o = align_up(o + (size_t)cap * sizeof(int32_t));
-    q.seg_ovf = o;
-    o = align_up(o + (size_t)cap * sizeof(int64_t));
-    q.events = o;
-    o = align_up(o + (size_t)cap * pk::EV_INLINE * sizeof(uint32_t));
-    q.pool = o;
-    q.end = o + (size_t)pool_slots * sizeof(uint32_t);
+    q.seg = o;
+    o = align_up(o + (size_t)cap * sizeof(pk::SegRec));
+    q.slots = o;
+    q.pool_base = (int64_t)pk::GATHER_SLOTS * cap;
+    q.end = o + (size_t)(q.pool_base + q.pool_slots) * sizeof(uint32_t);
     return q;
 }
 
@@ -327,10 +327,8 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     const CapSections q = cap_sections(L, cap);
     int32_t *deep_frames = (int32_t *)(ws + q.frames);
     uint32_t *deep_bits = (uint32_t *)(ws + q.bits);
-    int32_t *seg_count = (int32_t *)(ws + q.seg_count);
-    int64_t *seg_ovf = (int64_t *)(ws + q.seg_ovf);
-    uint32_t *events = (uint32_t *)(ws + q.events);
-    uint32_t *pool = (uint32_t *)(ws + q.pool);
+    pk::SegRec *seg = (pk::SegRec *)(ws + q.seg);
+    uint32_t *slots = (uint32_t *)(ws + q.slots);
 
     const unsigned tiles = (unsigned)L.n_tiles;
     abi::launch_plan(starts, lengths, n_traj, mis, L.n_tiles, tile_sum, tile_off, seg_off, counters, mode, stream);
@@ -345,11 +343,10 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     sa.n = n_traj;
     sa.seg_off = seg_off;
     sa.seg_cap = cap;
-    sa.seg_count = seg_count;
-    sa.seg_ovf = seg_ovf;
-    sa.events = events;
-    sa.pool = pool;
-    sa.pool_per_seg = q.pool_per_seg;
+    sa.seg = seg;
+    sa.slots = slots;
+    sa.pool_base = (uint32_t)q.pool_base;
+    sa.pool_slots = (uint32_t)q.pool_slots;
     sa.mode = mode;
     sa.tm = h->tm;
     sa.split_count = counters + 2;
@@ -375,16 +372,13 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     ra.n = n_traj;
     ra.seg_off = seg_off;
     ra.seg_cap = cap;
-    ra.seg_count = seg_count;
-    ra.seg_ovf = seg_ovf;
-    ra.events = events;
-    ra.pool = pool;
+    ra.seg = seg;
+    ra.slots = slots;
     ra.deep_frames = q.n_frames;
     ra.deep_bits = q.n_bits;
     ra.tm = h->tm;
     ra.out = row_out;
-    const pk::GatherArgs ga{starts, n_traj, mis,  seg_off,      cap,       seg_count,
-                            seg_ovf, events, pool, mode, counters + 2, split_rows};
+    const pk::GatherArgs ga{starts, n_traj, mis, seg_off, cap, seg, slots, mode, counters + 2, split_rows};
     const bool lenient = (h->cfg.flags & PARASON_CFG_LENIENT_GAPS) != 0;
     const bool batch_stats = (h->cfg.flags & PARASON_CFG_BATCH_STATS) != 0;
     if (lenient)

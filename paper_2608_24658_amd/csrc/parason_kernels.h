@@ -15,12 +15,11 @@
  *        one wave's range collects its events in that wave's LDS buffer and is
  *        written out, coalesced, as one compact list (mode[i] = 1).  Other rows
  *        leave their events in per-segment lists (mode[i] = 0) and are listed
- *        as split.  A list's first slots are inline in its first segment's
- *        record (EV_INLINE per segment of the list); the others are in the
- *        scan wave's region of the pool.
+ *        as split.  Every list the scan writes is in the wave's region of the
+ *        slot pool; seg[s] holds its length and first slot.
  *   gather_rows  (one wave per split row)
  *        Gathers a split row's per-segment events through LDS into one compact
- *        list with row positions in the row's inline slots (mode[i] = 1).
+ *        list with row positions in the row's gather slots (mode[i] = 1).
  *   rows_par  (small batches: one wave per row, lanes over its events)
  *        Validity from local checks and a depth prefix sum; latency and branch
  *        tokens level by level with segmented scans (DPP).  A row it cannot
@@ -503,10 +502,8 @@ struct RowArgs {
     int64_t n;
     const int64_t *seg_off;
     int64_t seg_cap;
-    const int32_t *seg_count;
-    const int64_t *seg_ovf; /* pool slot of a list's events beyond its inline ones */
-    const uint32_t *events; /* EV_INLINE inline slots per segment */
-    const uint32_t *pool;
+    const SegRec *seg;
+    const uint32_t *slots;
     int64_t deep_frames;    /* frames of the deep tier's store in workspace ... */
     int64_t deep_bits;      /* ... and its entry bits */
     TagMatch tm;
@@ -516,11 +513,10 @@ struct RowArgs {
 /* Feed row r's events to A.  Returns false when A stopped early.
  *
  * Three sources, all feeding the one call of A.event below: a compact list
- * (the whole row: count in seg_count[first], row positions), or per segment
+ * (the whole row: seg[first], row positions), or per segment
  * its stored list (segment positions) or, for a segment marked DENSE, its
- * tokens classified again one by one.  A list's first events are inline
- * (EV_INLINE slots per segment it covers), the others in the pool at
- * seg_ovf.  With two inlined copies of the automaton (one per source) the
+ * tokens classified again one by one.  Lists start at slots + seg[s].list.
+ * With two inlined copies of the automaton (one per source) the
  * gfx950 build returned wrong results for dense segments although the same
  * source is correct when compiled for the CPU, so the sources are merged into
  * one fetch loop. */
@@ -531,17 +527,16 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
     const int64_t s0 = a.seg_off[r], s1 = a.seg_off[r + 1];
     const int64_t vrow0 = row_first_vec(g), vend = row_end_vec(g, len);
     int64_t s = s0;              /* next segment to open */
-    const uint32_t *ev = nullptr, *ovf = nullptr;
-    int32_t e = 0, cnt = 0, cap_in = 0; /* stored-event cursor, list length, inline slots */
+    const uint32_t *ev = nullptr;
+    int32_t e = 0, cnt = 0;      /* stored-event cursor and list length */
     int64_t base = 0;            /* row position of stored position 0 */
     bool dense = false;
     int64_t q = 0, q_end = 0;    /* dense cursor (element index on the token grid) */
     uint4 quad = make_uint4(0u, 0u, 0u, 0u);
     if (compact) {
-        ev = a.events + s0 * EV_INLINE;
-        cnt = a.seg_count[s0];
-        cap_in = (int32_t)min((int64_t)cnt, (s1 - s0) * EV_INLINE);
-        if (cnt > cap_in) ovf = a.pool + a.seg_ovf[s0];
+        const SegRec rec = a.seg[s0];
+        ev = a.slots + rec.list;
+        cnt = rec.count;
         s = s1;
     }
     for (;;) {
@@ -549,10 +544,9 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
         uint32_t c = 0;
         for (;;) {
             if (!dense && e < cnt) {
-                /* inline slots and pool parts start 16-byte aligned and hold
-                 * multiples of 4 events: read them 16 bytes at a time */
-                if ((e & 3) == 0)
-                    quad = *reinterpret_cast<const uint4 *>(e < cap_in ? ev + e : ovf + (e - cap_in));
+                /* lists start 16-byte aligned and take multiples of 4 slots:
+                 * read them 16 bytes at a time */
+                if ((e & 3) == 0) quad = *reinterpret_cast<const uint4 *>(ev + e);
                 const uint32_t k = (uint32_t)e & 3u;
                 const uint32_t w = k == 0 ? quad.x : k == 1 ? quad.y : k == 2 ? quad.z : quad.w;
                 ++e;
@@ -578,14 +572,13 @@ __device__ bool drive_row(const RowArgs &a, int64_t r, int64_t g, int32_t len, b
             if (s >= s1) break;
             /* open segment s */
             const int64_t v0 = vrow0 + (s - s0) * SEG_VEC;
-            const int32_t n_s = a.seg_count[s];
+            const SegRec rec = a.seg[s];
+            const int32_t n_s = rec.count;
             base = 4 * v0 - g;
             e = 0;
             if (n_s != DENSE) {
-                ev = a.events + s * EV_INLINE;
                 cnt = n_s;
-                cap_in = min(n_s, EV_INLINE);
-                ovf = n_s > EV_INLINE ? a.pool + a.seg_ovf[s] : nullptr;
+                ev = a.slots + rec.list; /* not read when n_s is 0 */
             } else {
                 cnt = 0;
                 dense = true;
@@ -828,18 +821,16 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
     int32_t m = 0;
     bool held = true;
     if (md & MODE_COMPACT) {
-        m = a.seg_count[s0];
+        const SegRec rec = a.seg[s0];
+        m = rec.count;
         held = m <= PAR_EVENTS;
-        /* the list's first slots inline (EV_INLINE per segment), the rest in the pool */
-        const uint32_t *list = a.events + s0 * EV_INLINE;
-        const int32_t cap_in = (int32_t)min((int64_t)m, (s1 - s0) * EV_INLINE);
-        const int64_t ovf = m > cap_in ? a.seg_ovf[s0] : 0;
+        const uint32_t *list = a.slots + rec.list;
         for (int32_t i0 = 0; held && i0 < m; i0 += 4 * WAVE) { /* four loads per lane in flight */
             uint32_t w[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int32_t i = i0 + u * WAVE + lane;
-                w[u] = i < m ? (i < cap_in ? list[i] : a.pool[ovf + (i - cap_in)]) : 0u;
+                w[u] = i < m ? list[i] : 0u;
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
@@ -854,10 +845,9 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
         const int64_t vrow0 = row_first_vec(g);
         for (int64_t c0 = s0; held && c0 < s1; c0 += WAVE) {
             const int64_t s = c0 + lane;
-            const int32_t cnt = s < s1 ? a.seg_count[s] : 0;
-            /* where the segment's events beyond its inline slots are (loaded
-             * with the count; meaningless unless cnt > EV_INLINE) */
-            const int64_t ovf = s < s1 ? a.seg_ovf[s] - EV_INLINE : 0;
+            const SegRec rec = s < s1 ? a.seg[s] : SegRec{0, 0u};
+            const int32_t cnt = rec.count;
+            const uint32_t list = rec.list; /* meaningless for a segment without events */
             const int32_t incl = wave_incl_scan32(cnt, lane); /* DENSE counts cannot overflow it */
             const int32_t excl = incl - cnt;
             const int32_t total = lane63(incl);
@@ -871,9 +861,8 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
                     const int32_t f = f0 + u * WAVE + lane;
                     j[u] = last_lane_at_most(excl, f);
                     const int32_t first = __shfl(excl, j[u], WAVE);
-                    const int64_t ov = __shfl(ovf, j[u], WAVE);
-                    const int32_t e = f - first; /* the event's index in its segment's list */
-                    w[u] = f < total ? (e < EV_INLINE ? a.events[(c0 + j[u]) * EV_INLINE + e] : a.pool[ov + e]) : 0u;
+                    const uint32_t lj = __shfl(list, j[u], WAVE);
+                    w[u] = f < total ? a.slots[(int64_t)lj + (f - first)] : 0u;
                 }
 #pragma unroll
                 for (int u = 0; u < 2; ++u) {
@@ -1067,16 +1056,14 @@ __device__ __forceinline__ bool is_tag(const TagMatch &tm, int32_t t, int32_t ta
 __device__ __forceinline__ uint32_t lane_bit(uint64_t mask, int lane) { return (uint32_t)(mask >> lane) & 1u; }
 
 /* Tags of the LOADS vectors x[i] (vector v0 + i*WAVE + lane of this lane) are
- * appended in position order as (q + bias) << 4 | class, where
- * q = 4*(i*WAVE + lane) + j is the position in the segment: the first cap to
- * dst[0 .. cap), the next cap2 to dst2[0 .. cap2); cnt counts all of them,
- * stored or not.  EDGE: the segment holds the first or last vector of its row,
- * so only positions q_lo <= q < q_hi belong to the row. */
+ * appended to dst[0 .. cap) in position order as (q + bias) << 4 | class, where
+ * q = 4*(i*WAVE + lane) + j is the position in the segment; cnt counts all of
+ * them, stored or not.  EDGE: the segment holds the first or last vector of its
+ * row, so only positions q_lo <= q < q_hi belong to the row. */
 template <int MODE, bool EDGE>
 __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_lo, int32_t q_hi,
-                                             uint32_t *__restrict__ dst, uint32_t cap, uint32_t *__restrict__ dst2,
-                                             uint32_t cap2, int32_t bias, uint32_t &cnt, const TagMatch &tm,
-                                             int32_t tab, int lane)
+                                             uint32_t *__restrict__ dst, uint32_t cap, int32_t bias, uint32_t &cnt,
+                                             const TagMatch &tm, int32_t tab, int lane)
 {
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
@@ -1109,9 +1096,7 @@ __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_l
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 if (mine & (1u << j)) {
-                    const uint32_t v = ((uint32_t)(q0 + j + bias) << 4) | classify(tm, t[j], MODE == TM_CONTIG);
-                    if (idx < cap) dst[idx] = v;
-                    else if (idx - cap < cap2) dst2[idx - cap] = v;
+                    if (idx < cap) dst[idx] = ((uint32_t)(q0 + j + bias) << 4) | classify(tm, t[j], MODE == TM_CONTIG);
                     ++idx;
                 }
             }
@@ -1133,12 +1118,12 @@ __device__ __forceinline__ void issue_loads(int4 (&x)[LOADS], const int4 *src, c
     }
 }
 
-/* seg_count[s] = DENSE for s in [a, b): the row kernels classify those
+/* seg[s].count = DENSE for s in [a, b): the row kernels classify those
  * segments' tokens again. */
 
-__device__ __forceinline__ void mark_dense(int32_t *seg_count, int64_t a, int64_t b, int lane)
+__device__ __forceinline__ void mark_dense(SegRec *seg, int64_t a, int64_t b, int lane)
 {
-    for (int64_t s = a + lane; s < b; s += WAVE) seg_count[s] = DENSE;
+    for (int64_t s = a + lane; s < b; s += WAVE) seg[s].count = DENSE;
 }
 
 struct ScanArgs {
@@ -1149,12 +1134,12 @@ struct ScanArgs {
     int64_t n;
     const int64_t *seg_off;
     int64_t seg_cap;
-    int32_t *seg_count;
-    int64_t *seg_ovf;   /* pool slot of a list's events beyond its inline ones */
-    uint32_t *events;   /* EV_INLINE inline slots per segment */
-    uint32_t *pool;     /* wave w's region: pool_per_seg slots per segment of its
-                           range [s_begin, s_end), from pool_per_seg * s_begin */
-    int64_t pool_per_seg; /* a multiple of 4, at least POOL_PER_SEG */
+    SegRec *seg;
+    uint32_t *slots;
+    uint32_t pool_base;  /* the pool: slots [pool_base, pool_base + pool_slots); wave w's */
+    uint32_t pool_slots; /* region starts at pool_base + POOL_PER_SEG * s_begin + x * w and ends at
+                            pool_base + POOL_PER_SEG * s_end + x * (w + 1), with
+                            x = (pool_slots - POOL_PER_SEG * S) / W rounded down to 4 */
     uint8_t *mode;
     TagMatch tm;
     int32_t *split_count; /* rows of more than one segment that no scan wave owns ... */
@@ -1165,41 +1150,33 @@ struct ScanArgs {
 struct RowCollect {
     uint32_t lcnt; /* events in the wave's LDS buffer */
     bool global;   /* events go to per-segment lists; the row kernel evaluates the row */
-    int64_t pc;    /* next free slot of the wave's pool region (a multiple of 4) ... */
-    int64_t p_end; /* ... and its end */
+    uint32_t pc;    /* next free slot of the wave's pool region (a multiple of 4) ... */
+    uint32_t p_end; /* ... and its end */
 };
 
 constexpr int EVL = 1024;                 /* LDS events per wave */
 constexpr int SCAN_WAVES = 4;             /* waves per scan block */
 
 /* The whole of row `row` is in the wave's LDS buffer lev[0 .. lcnt): copy it,
- * coalesced, as one compact list for the row kernel (mode 1): its first
- * events to the row's inline slots (EV_INLINE per segment), the rest to the
- * wave's pool region.  A list that does not fit makes the row kernel classify
- * the row's segments again. */
+ * coalesced, to the wave's pool region as one compact list for the row kernel
+ * (mode 1).  A list that does not fit makes the row kernel classify the row's
+ * segments again. */
 __device__ __forceinline__ void flush_row(const ScanArgs &a, int64_t row, int64_t first, int64_t last, uint32_t lcnt,
                                           const uint32_t *lev, RowCollect &rc, int lane)
 {
-    const int64_t cap_in = (last - first + 1) * EV_INLINE;
-    const int64_t rest = (int64_t)lcnt > cap_in ? (int64_t)lcnt - cap_in : 0;
-    const int64_t need = (rest + 3) & ~(int64_t)3;
+    const uint32_t need = (lcnt + 3u) & ~3u;
     if (need > rc.p_end - rc.pc) {
-        mark_dense(a.seg_count, first, last + 1, lane);
+        mark_dense(a.seg, first, last + 1, lane);
         return;
     }
-    uint32_t *in = a.events + first * EV_INLINE;
-    uint32_t *ovf = a.pool + rc.pc;
+    uint32_t *dst = a.slots + rc.pc;
     /* lane i copies events other lanes wrote: the wave's LDS stores above
      * come first (a wave's LDS accesses are performed in program order; this
      * keeps the compiler from moving them across) */
     __builtin_amdgcn_wave_barrier();
-    for (uint32_t i = lane; i < lcnt; i += WAVE) {
-        if ((int64_t)i < cap_in) in[i] = lev[i];
-        else ovf[i - cap_in] = lev[i];
-    }
+    for (uint32_t i = lane; i < lcnt; i += WAVE) dst[i] = lev[i];
     if (lane == 0) {
-        a.seg_count[first] = (int32_t)lcnt;
-        if (rest > 0) a.seg_ovf[first] = rc.pc;
+        a.seg[first] = SegRec{(int32_t)lcnt, rc.pc};
         a.mode[row] = MODE_COMPACT;
     }
     rc.pc += need;
@@ -1225,33 +1202,25 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
     if (!rc.global) {
         const int32_t bias = (int32_t)(4 * w.v0 - w.g); /* row position of segment position 0 */
         const uint32_t cap = (uint32_t)EVL - rc.lcnt;
-        if (!w.edge)
-            scan_vectors<MODE, false>(x, 0, SEG_TOK, lev + rc.lcnt, cap, nullptr, 0, bias, cnt, a.tm, tab, lane);
-        else
-            scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, lev + rc.lcnt, cap, nullptr, 0, bias, cnt, a.tm, tab, lane);
+        if (!w.edge) scan_vectors<MODE, false>(x, 0, SEG_TOK, lev + rc.lcnt, cap, bias, cnt, a.tm, tab, lane);
+        else scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, lev + rc.lcnt, cap, bias, cnt, a.tm, tab, lane);
         if (cnt > cap) {
             /* the row's events overflow the LDS buffer: its segments so far are
              * classified again by the row kernel, the rest use per-segment lists */
-            mark_dense(a.seg_count, w.first, w.s + 1, lane);
+            mark_dense(a.seg, w.first, w.s + 1, lane);
             rc.global = true;
         } else {
             rc.lcnt += cnt;
         }
     } else {
-        /* the segment's own list: EV_INLINE slots inline, the rest in the pool */
-        uint32_t *in = a.events + w.s * EV_INLINE, *ovf = a.pool + rc.pc;
-        const uint32_t room = (uint32_t)min(rc.p_end - rc.pc, (int64_t)SEG_TOK);
-        if (!w.edge)
-            scan_vectors<MODE, false>(x, 0, SEG_TOK, in, EV_INLINE, ovf, room, 0, cnt, a.tm, tab, lane);
-        else
-            scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, in, EV_INLINE, ovf, room, 0, cnt, a.tm, tab, lane);
-        const int64_t need = cnt > (uint32_t)EV_INLINE ? ((int64_t)cnt - EV_INLINE + 3) & ~(int64_t)3 : 0;
-        const bool stored = need <= (int64_t)room; /* room is a multiple of 4 */
-        if (lane == 0) {
-            a.seg_count[w.s] = stored ? (int32_t)cnt : DENSE;
-            if (stored && need > 0) a.seg_ovf[w.s] = rc.pc;
-        }
-        if (stored) rc.pc += need;
+        /* the segment's own list, in the wave's pool region */
+        const uint32_t room = min(rc.p_end - rc.pc, (uint32_t)SEG_TOK); /* a multiple of 4 */
+        uint32_t *dst = a.slots + rc.pc;
+        if (!w.edge) scan_vectors<MODE, false>(x, 0, SEG_TOK, dst, room, 0, cnt, a.tm, tab, lane);
+        else scan_vectors<MODE, true>(x, w.q_lo, w.q_hi, dst, room, 0, cnt, a.tm, tab, lane);
+        const bool stored = cnt <= room;
+        if (lane == 0) a.seg[w.s] = SegRec{stored ? (int32_t)cnt : DENSE, rc.pc};
+        if (stored) rc.pc += (cnt + 3u) & ~3u;
     }
     return w.s == w.last && !rc.global;
 }
@@ -1290,8 +1259,12 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
     RowCollect rc;
     rc.lcnt = 0;
     rc.global = true; /* a row already begun in the previous wave's range */
-    rc.pc = uniform64(a.pool_per_seg * s_begin);
-    rc.p_end = uniform64(a.pool_per_seg * s_end);
+    /* the slots the segments leave, shared equally (slot indices fit 32 bits,
+     * which the host checks) */
+    const uint32_t extra = ((a.pool_slots - POOL_PER_SEG * (uint32_t)S) / (uint32_t)n_waves) & ~3u;
+    rc.pc = __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)s_begin + extra * (uint32_t)wave);
+    rc.p_end =
+        __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)s_end + extra * (uint32_t)(wave + 1));
     SegView w = cur.view(s_begin);
     /* two register buffers: segment s + 1 is in flight while s is compacted */
     int4 xa[LOADS], xb[LOADS];
@@ -1373,10 +1346,8 @@ struct GatherArgs {
     int64_t n, mis;
     const int64_t *seg_off;
     int64_t seg_cap;
-    int32_t *seg_count;
-    const int64_t *seg_ovf;
-    uint32_t *events;
-    const uint32_t *pool;
+    SegRec *seg;
+    uint32_t *slots;
     uint8_t *mode;
     const int32_t *split_count;
     const int32_t *split_rows;
@@ -1385,11 +1356,11 @@ struct GatherArgs {
 constexpr int GATHER_EVENTS = 1024; /* LDS events per gather wave */
 
 /* Gather the events of row `row` (split between scan waves: one list per
- * segment, segment positions) into one list in the row's inline slots, in
- * position order, with row positions (the compact form, mode 1).  Every event
- * is first loaded into the wave's LDS buffer lds[0 .. GATHER_EVENTS), then
- * stored, so the inline slots can be overwritten.  A row with a DENSE segment,
- * or with more events than its inline slots or the buffer hold, is left as it
+ * segment, segment positions) into one list in the row's gather slots
+ * (GATHER_SLOTS per segment of the row, from slot GATHER_SLOTS * seg_off[row]),
+ * in position order, with row positions (the compact form, mode 1), through
+ * the wave's LDS buffer lds[0 .. GATHER_EVENTS).  A row with a DENSE segment,
+ * or with more events than its gather slots or the buffer hold, is left as it
  * is; the whole wave calls this. */
 __device__ __forceinline__ void gather_row(const GatherArgs &a, int64_t row, uint32_t *lds, int lane)
 {
@@ -1400,16 +1371,17 @@ __device__ __forceinline__ void gather_row(const GatherArgs &a, int64_t row, uin
     int64_t total = 0;
     for (int64_t c0 = s0; c0 < s1; c0 += WAVE) {
         const int64_t s = c0 + lane;
-        const int32_t cnt = s < s1 ? a.seg_count[s] : 0;
+        const int32_t cnt = s < s1 ? a.seg[s].count : 0;
         dense = dense || cnt == DENSE;
         total += lane63(wave_incl_scan32(cnt, lane)); /* DENSE counts cannot overflow it */
     }
-    if (__ballot(dense) != 0 || total > GATHER_EVENTS || total > (s1 - s0) * EV_INLINE) return;
+    if (__ballot(dense) != 0 || total > GATHER_EVENTS || total > (s1 - s0) * GATHER_SLOTS) return;
     int64_t carry = 0; /* events of the segments before this chunk */
     for (int64_t c0 = s0; c0 < s1; c0 += WAVE) {
         const int64_t s = c0 + lane;
-        const int32_t cnt = s < s1 ? a.seg_count[s] : 0;
-        const int64_t ovf = s < s1 ? a.seg_ovf[s] - EV_INLINE : 0; /* used only when cnt > EV_INLINE */
+        const SegRec rec = s < s1 ? a.seg[s] : SegRec{0, 0u};
+        const int32_t cnt = rec.count;
+        const uint32_t list = rec.list; /* meaningless for a segment without events */
         const int32_t incl = wave_incl_scan32(cnt, lane);
         const int32_t excl = incl - cnt;
         const int32_t n_c = lane63(incl);
@@ -1417,11 +1389,10 @@ __device__ __forceinline__ void gather_row(const GatherArgs &a, int64_t row, uin
             const int32_t f = f0 + lane; /* the chunk's f-th event, of segment c0 + j */
             const int32_t j = last_lane_at_most(excl, f);
             const int32_t first = __shfl(excl, j, WAVE);
-            const int64_t ov = __shfl(ovf, j, WAVE);
+            const uint32_t lj = __shfl(list, j, WAVE);
             if (f < n_c) {
                 const int64_t seg = c0 + j;
-                const int32_t e = f - first;
-                const uint32_t w = e < EV_INLINE ? a.events[seg * EV_INLINE + e] : a.pool[ov + e];
+                const uint32_t w = a.slots[(int64_t)lj + (f - first)];
                 /* row position of segment position 0 */
                 const int64_t base = 4 * (vrow0 + (seg - s0) * SEG_VEC) - g;
                 lds[carry + f] = ((uint32_t)(base + (int64_t)(w >> 4)) << 4) | (w & 15u);
@@ -1431,10 +1402,10 @@ __device__ __forceinline__ void gather_row(const GatherArgs &a, int64_t row, uin
     }
     /* lanes store what other lanes loaded: every load above first */
     __builtin_amdgcn_wave_barrier();
-    uint32_t *list = a.events + s0 * EV_INLINE;
-    for (int64_t i = lane; i < carry; i += WAVE) list[i] = lds[i];
+    uint32_t *dst = a.slots + s0 * GATHER_SLOTS;
+    for (int64_t i = lane; i < carry; i += WAVE) dst[i] = lds[i];
     if (lane == 0) {
-        a.seg_count[s0] = (int32_t)carry;
+        a.seg[s0] = SegRec{(int32_t)carry, (uint32_t)(s0 * GATHER_SLOTS)};
         a.mode[row] = MODE_COMPACT;
     }
 }

@@ -65,6 +65,13 @@ def test_workspace_size_validates_and_grows():
     b = px.workspace_size(8, 10 ** 6)
     c = px.workspace_size(800, 10 ** 6)
     assert 0 < a < b < c
+    # about 56 bytes per 1024-token segment for a large batch (1.4 % of the token bytes)
+    big = px.workspace_size(712000, 35825658097)
+    assert big < 0.015 * 4 * 35825658097
+    # slot indices are 32-bit: beyond about 3.6e11 tokens the size is refused
+    assert px.workspace_size(8, 3 * 10 ** 11) > 0
+    with pytest.raises(P.ParasonError):
+        px.workspace_size(8, 4 * 10 ** 11)
     with pytest.raises(P.ParasonError):
         px.workspace_size(-1, 10)
     with pytest.raises(P.ParasonError):
@@ -239,11 +246,13 @@ def test_run_noalloc_rejects_bad_arguments_before_launch():
     assert run(FAKE, FAKE, FAKE, FAKE, 16, -1, out, None) == P.ERR_SIZE
     assert P.lib().parason_run_noalloc(None, FAKE, FAKE, FAKE, FAKE, 16, 1000, None, None) == P.ERR_NULL
     # the largest token count whose workspace fits, and one segment's worth more
-    lo, hi = 0, 1 << 40
+    lo, hi = 0, 1 << 36
     while hi - lo > 1:
         mid = (lo + hi) // 2
         lo, hi = (mid, hi) if px.workspace_size(16, mid) <= P.NOALLOC_SCRATCH_BYTES else (lo, mid)
     assert px.workspace_size(16, lo) <= P.NOALLOC_SCRATCH_BYTES < px.workspace_size(16, lo + 4096)
     assert run(FAKE, FAKE, FAKE, FAKE, 16, lo + 4096, out, None) == P.ERR_SCRATCH
-    assert run(FAKE, FAKE, FAKE, FAKE, 16, 10 ** 12, out, None) == P.ERR_SCRATCH
+    assert run(FAKE, FAKE, FAKE, FAKE, 16, 10 ** 11, out, None) == P.ERR_SCRATCH
+    # beyond what any workspace can index (3.6e11 tokens): a size error
+    assert run(FAKE, FAKE, FAKE, FAKE, 16, 10 ** 12, out, None) == P.ERR_SIZE
     assert "scratch" in P.strerror(P.ERR_SCRATCH)
