@@ -1,6 +1,9 @@
 /*
  * fork.hip -- C-ABI of fork/join packing for tool-call execution (kernels in
  * fork_kernels.h).
+ *
+ * Launches use hipLaunchKernelGGL, as in parason.hip, so that the same source
+ * also compiles against a host-side stand-in for the HIP runtime.
  */
 #include <algorithm>
 
@@ -55,12 +58,12 @@ template <int K>
 void launch_pack(const pk::PackScan<K> &ps, int64_t tiles, hipStream_t stream)
 {
     if (ps.n <= pk::PACK_TILE) {
-        pk::pack_single<K><<<dim3(1), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
+        hipLaunchKernelGGL(pk::pack_single<K>, dim3(1), dim3(pk::PACK_THREADS), 0, stream, ps);
         return;
     }
-    pk::pack_tiles<K><<<dim3((unsigned)tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
-    pk::pack_top<K><<<dim3(1), dim3(1024), 0, stream>>>(ps, tiles);
-    pk::pack_rows<K><<<dim3((unsigned)tiles), dim3(pk::PACK_THREADS), 0, stream>>>(ps);
+    hipLaunchKernelGGL(pk::pack_tiles<K>, dim3((unsigned)tiles), dim3(pk::PACK_THREADS), 0, stream, ps);
+    hipLaunchKernelGGL(pk::pack_top<K>, dim3(1), dim3(1024), 0, stream, ps, tiles);
+    hipLaunchKernelGGL(pk::pack_rows<K>, dim3((unsigned)tiles), dim3(pk::PACK_THREADS), 0, stream, ps);
 }
 
 }  // namespace
@@ -144,12 +147,12 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
     ps.over = (int32_t *)(ws + L.over);
 
     const unsigned wave_blocks = (unsigned)std::min<int64_t>((n_rows + 3) / 4, (int64_t)cus * 8);
-    if (n_rows > 0) pk::fork_outline<false><<<dim3(wave_blocks), dim3(256), 0, stream>>>(fa);
+    if (n_rows > 0) hipLaunchKernelGGL(pk::fork_outline<false>, dim3(wave_blocks), dim3(256), 0, stream, fa);
     launch_pack(ps, L.tiles, stream);
     if (n_rows > 0) {
-        pk::fork_outline<true><<<dim3(wave_blocks), dim3(256), 0, stream>>>(fa);
+        hipLaunchKernelGGL(pk::fork_outline<true>, dim3(wave_blocks), dim3(256), 0, stream, fa);
         const unsigned copy_blocks = (unsigned)(cus * COPY_BLOCKS_PER_CU); /* persistent, tiled over the output */
-        pk::fork_copy<<<dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream>>>(fa);
+        hipLaunchKernelGGL(pk::fork_copy, dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream, fa);
     }
     return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
 }
@@ -209,11 +212,11 @@ int parason_join(const parason_handle *h, const int32_t *tokens, const int64_t *
     ps.report = 1;
     ps.over = (int32_t *)(ws + L.over);
 
-    if (n_rows > 0) pk::join_size<<<dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0, stream>>>(ja);
+    if (n_rows > 0) hipLaunchKernelGGL(pk::join_size, dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0, stream, ja);
     launch_pack(ps, L.tiles, stream);
     if (n_rows > 0) {
         const unsigned copy_blocks = (unsigned)(cus * COPY_BLOCKS_PER_CU);
-        pk::join_copy<<<dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream>>>(ja);
+        hipLaunchKernelGGL(pk::join_copy, dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream, ja);
     }
     return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
 }

@@ -660,7 +660,7 @@ __global__ void __launch_bounds__(PACK_THREADS) fork_copy(ForkArgs a)
             const int64_t w0 = a.worker_off[r], w1 = a.worker_off[r + 1];
             const int64_t o = a.outl[r], to = a.tok_off[r];
             if (uo >= hi) break;
-            if (ue <= lo) continue; /* no units (not forked), or all before the tile */
+            if (ue <= max(lo, uo)) continue; /* no units (not forked), or all before the tile */
             const int32_t *src = a.tokens + g0;
             for (int64_t g = (max(lo, uo) - uo) / L; uo + g * L < min(hi, ue); ++g) {
                 const int64_t gs = uo + g * L;

@@ -418,6 +418,9 @@ inline uint32_t mbcnt_hi(uint32_t m, uint32_t acc)
 #define __builtin_amdgcn_update_dpp(o, s, c, r, b, bc) simt::update_dpp((o), (s), (c), (r), (b), (bc), SIMT_SITE)
 #define __builtin_amdgcn_ds_bpermute(a, v) simt::bpermute((a), (v), SIMT_SITE)
 #define __builtin_amdgcn_wave_barrier() ((void)simt::meet(simt::OP_WAVE_BARRIER, SIMT_SITE, 0, 0))
+/* the lanes of a wave meet only at wave operations, which the kernels place
+ * next to each fence that orders memory within a wave */
+#define __builtin_amdgcn_fence(order, scope) ((void)0)
 #define __builtin_amdgcn_mbcnt_lo(m, a) simt::mbcnt_lo((m), (a))
 #define __builtin_amdgcn_mbcnt_hi(m, a) simt::mbcnt_hi((m), (a))
 
