@@ -148,9 +148,15 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
 
     const unsigned wave_blocks = (unsigned)std::min<int64_t>((n_rows + 3) / 4, (int64_t)cus * 8);
     if (n_rows > 0) hipLaunchKernelGGL(pk::fork_outline<false>, dim3(wave_blocks), dim3(256), 0, stream, fa);
-    launch_pack(ps, L.tiles, stream);
-    if (n_rows > 0) {
+    if (n_rows <= pk::FORK_SINGLE) {
+        /* scans and records in one launch (at least one block: it writes the totals) */
+        const unsigned blocks = (unsigned)std::max<int64_t>(1, (n_rows + pk::FORK_SINGLE_WAVES - 1) / pk::FORK_SINGLE_WAVES);
+        hipLaunchKernelGGL(pk::fork_records, dim3(blocks), dim3(pk::FORK_SINGLE), 0, stream, fa, ps);
+    } else {
+        launch_pack(ps, L.tiles, stream);
         hipLaunchKernelGGL(pk::fork_outline<true>, dim3(wave_blocks), dim3(256), 0, stream, fa);
+    }
+    if (n_rows > 0) {
         const unsigned copy_blocks = (unsigned)(cus * COPY_BLOCKS_PER_CU); /* persistent, tiled over the output */
         hipLaunchKernelGGL(pk::fork_copy, dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream, fa);
     }
@@ -213,10 +219,13 @@ int parason_join(const parason_handle *h, const int32_t *tokens, const int64_t *
     ps.over = (int32_t *)(ws + L.over);
 
     if (n_rows > 0) hipLaunchKernelGGL(pk::join_size, dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0, stream, ja);
-    launch_pack(ps, L.tiles, stream);
-    if (n_rows > 0) {
-        const unsigned copy_blocks = (unsigned)(cus * COPY_BLOCKS_PER_CU);
-        hipLaunchKernelGGL(pk::join_copy, dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream, ja);
+    const unsigned copy_blocks = n_rows > 0 ? (unsigned)(cus * COPY_BLOCKS_PER_CU) : 1u;
+    if (n_rows <= pk::JOIN_SINGLE) {
+        /* the scan inside the copy (no rows: one block, which writes the zero totals) */
+        hipLaunchKernelGGL(pk::join_copy<true>, dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream, ja, ps);
+    } else {
+        launch_pack(ps, L.tiles, stream);
+        hipLaunchKernelGGL(pk::join_copy<false>, dim3(copy_blocks), dim3(pk::PACK_THREADS), 0, stream, ja, ps);
     }
     return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
 }

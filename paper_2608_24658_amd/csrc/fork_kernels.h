@@ -60,6 +60,17 @@ constexpr int CHUNK_J = PARASON_OUTLINE_LOADS; /* loads per lane per step of the
 constexpr int CHUNK = CHUNK_J * WAVE;          /* tokens per wave step of the outline walk */
 constexpr int COPY_GROUP = 8;   /* worker contexts fork_copy writes from one read of a row tile */
 constexpr int SUMM_ENTRIES = 8; /* outline entries per row the first walk keeps for the second */
+constexpr int JOIN_UNROLL = 4;  /* workers of a row whose records join_size loads together */
+constexpr int JOIN_SINGLE = 1024; /* rows up to which join_copy scans the joined lengths itself */
+
+/* Orders the LDS accesses of a wave's lanes: what one lane wrote before it is
+ * visible to every lane of the wave after it. */
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 /* ---- exclusive scans of K int64 values per row -------------------------- */
 
@@ -283,6 +294,201 @@ __device__ __forceinline__ int64_t last_tag_before(const ForkArgs &a, int64_t g,
     return -1;
 }
 
+/* One row's outline, by one wave.  WRITE = false: status and counts (the
+ * first walk); WRITE = true: the worker records of a row whose outline is well
+ * formed, its first worker w0 and first context token t0 given.  ev: the
+ * wave's CHUNK entries of LDS. */
+template <bool WRITE>
+__device__ __forceinline__ void outline_row(const ForkArgs &a, int64_t i, int64_t w0, int64_t t0, uint32_t *ev,
+                                            int lane)
+{
+    const bool contig = a.tm.contiguous != 0;
+    const int64_t g = a.starts[i];
+    const int32_t L = a.lengths[i];
+    int64_t o;
+    if (WRITE) {
+        const int64_t n_e = a.counts[3 * i];
+        if (a.status[i] != 0 || n_e == 0) return;
+        if (n_e <= SUMM_ENTRIES) {
+            /* the first walk kept every entry of this outline: the records
+             * without a second walk (lane k: entry k) */
+            const uint64_t x = lane < n_e ? a.summ[i * SUMM_ENTRIES + lane] : 0ull;
+            const int32_t sl = a.seed ? (int32_t)((x >> 32) & 0x7fffffffu) : 0;
+            const int64_t before = dpp_incl_scan<OpAdd>(sl, lane) - sl; /* seeds of entries 0 .. k-1 */
+            if (lane < n_e) {
+                const int64_t w = w0 + lane;
+                a.ctx_starts[w] = t0 + lane * ((int64_t)L + 1) + before;
+                a.ctx_lengths[w] = (int32_t)((int64_t)L + 1 + sl);
+                a.ctx_row[w] = (int32_t)i;
+                a.ctx_entry[w] = lane;
+                a.ctx_kind[w] = (x >> 63) ? (int32_t)T_TRI : (int32_t)T_SUB;
+            }
+            return;
+        }
+        o = a.outl[i];
+    } else {
+        uint32_t st = 0;
+        o = -1;
+        if (L < 0 || g < 0) st = PARASON_PACK_BAD_ROW;
+        else if (L == 0) st = PARASON_PACK_NO_OUTLINE_END;
+        /* backwards from the row's end in chunks: the first chunk holds the
+         * last token, which must be </Outlines>; then the last <Outlines>
+         * before it, and the class of the token right before that when it
+         * is in the same chunk (1: <Parallel>, 0: not, -1: not seen) */
+        int32_t par_before = -1;
+        for (int64_t e = (int64_t)L; st == 0 && e > 0 && o < 0; e -= CHUNK) {
+            const int64_t lo = e > CHUNK ? e - CHUNK : 0;
+            uint32_t c[CHUNK_J];
+            int32_t best = -1;
+            bool end_mine = false;
+#pragma unroll
+            for (int j = 0; j < CHUNK_J; ++j) {
+                const int64_t p = lo + lane + WAVE * j;
+                c[j] = p < e ? classify(a.tm, a.tokens[g + p], contig) : C_TEXT;
+                if (p < (int64_t)L - 1 && c[j] == C_OUT) best = (int32_t)p > best ? (int32_t)p : best;
+                end_mine = end_mine || (p == (int64_t)L - 1 && c[j] == C_END_OUT);
+            }
+            if (e == (int64_t)L && __ballot(end_mine) == 0) {
+                st = PARASON_PACK_NO_OUTLINE_END;
+                break;
+            }
+            o = wave_max_pos(best, lane);
+            if (o >= 1 && o - 1 >= lo) {
+                bool par_mine = false;
+#pragma unroll
+                for (int j = 0; j < CHUNK_J; ++j) par_mine = par_mine || (lo + lane + WAVE * j == o - 1 && c[j] == C_PAR);
+                par_before = __ballot(par_mine) != 0 ? 1 : 0;
+            }
+        }
+        if (st == 0) {
+            /* the tag before <Outlines> must be <Parallel>: right before it,
+             * or with only Text between when lenient */
+            bool par_ok;
+            if (a.lenient) {
+                const int64_t q = o >= 1 ? last_tag_before(a, g, o, lane, contig) : -1;
+                par_ok = q >= 0 && classify(a.tm, a.tokens[g + q], contig) == C_PAR;
+            } else {
+                par_ok = o >= 1 && (par_before >= 0 ? par_before == 1
+                                                    : classify(a.tm, a.tokens[g + o - 1], contig) == C_PAR);
+            }
+            if (o < 0 || !par_ok) st = PARASON_PACK_NO_OUTLINE;
+        }
+        if (st != 0) {
+            if (lane == 0) {
+                a.status[i] = st;
+                a.counts[3 * i] = 0;
+                a.counts[3 * i + 1] = 0;
+                a.counts[3 * i + 2] = 0;
+                a.outl[i] = -1;
+            }
+            return;
+        }
+    }
+    /* walk the outline [o + 1, L - 1) in chunks; events are its tags */
+    const int64_t end = (int64_t)L - 1;
+    int64_t m = 0;                       /* tags before this chunk */
+    int64_t prev_pos = o;                /* the tag before the current one */
+    uint32_t prev_cls = C_OUT;
+    int64_t text = 0;                    /* entry text tokens so far (the same in every lane) */
+    bool ok = true;
+    for (int64_t lo = o + 1; lo < end; lo += CHUNK) {
+        uint64_t b[CHUNK_J];
+        uint32_t c[CHUNK_J];
+#pragma unroll
+        for (int j = 0; j < CHUNK_J; ++j) {
+            const int64_t p = lo + lane + WAVE * j;
+            c[j] = p < end ? classify(a.tm, a.tokens[g + p], contig) : C_TEXT;
+            b[j] = __ballot(c[j] != C_TEXT);
+        }
+        uint32_t base = 0;
+#pragma unroll
+        for (int j = 0; j < CHUNK_J; ++j) {
+            if (c[j] != C_TEXT) {
+                const uint32_t idx = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(b[j] >> 32),
+                                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)b[j], 0u));
+                ev[idx] = ((uint32_t)(lane + WAVE * j) << 4) | c[j];
+            }
+            base += (uint32_t)__popcll(b[j]);
+        }
+        wave_lds_sync();
+        for (uint32_t e0 = 0; e0 < base; e0 += WAVE) { /* the same trip count in every lane */
+            const uint32_t e = e0 + (uint32_t)lane;
+            const bool act = e < base;
+            int64_t len = 0; /* text tokens of the entry this lane closes */
+            int64_t J = 0, tstart = 0;
+            uint32_t pc = 0;
+            if (act) {
+                const uint32_t x = ev[e];
+                const int64_t P = lo + (x >> 4);
+                const uint32_t cl = x & 15u;
+                int64_t pp = prev_pos;
+                pc = prev_cls;
+                if (e > 0) {
+                    const uint32_t y = ev[e - 1];
+                    pp = lo + (y >> 4);
+                    pc = y & 15u;
+                }
+                J = m + e;
+                if ((J & 1) == 0) {
+                    /* an entry opens after <Outlines> or the previous entry:
+                     * right after it, or after a gap when lenient */
+                    ok = ok && (cl == C_SUB || cl == C_TRI) && (a.lenient || P == pp + 1);
+                } else {
+                    /* and closes with its own tag after at least one text token */
+                    ok = ok && (pc == C_SUB || pc == C_TRI) && cl == pc + 1 && P >= pp + 2;
+                    len = P - pp - 1;
+                    tstart = pp + 1;
+                }
+            }
+            if (!WRITE && act && (J & 1) && (J >> 1) < SUMM_ENTRIES)
+                a.summ[i * SUMM_ENTRIES + (J >> 1)] = (uint64_t)(uint32_t)tstart |
+                                                     ((uint64_t)(uint32_t)len << 32) |
+                                                     ((uint64_t)(pc == C_TRI) << 63);
+            /* entry text lengths and their sums within a chunk are below L */
+            const int64_t incl = dpp_incl_scan<OpAdd>((int32_t)len, lane);
+            if (WRITE && act && (J & 1)) {
+                const int64_t k = J >> 1;
+                const int64_t w = w0 + k;
+                const int64_t seed_before = text + incl - len; /* texts of entries 0 .. k-1 */
+                a.ctx_starts[w] = t0 + k * ((int64_t)L + 1) + (a.seed ? seed_before : 0);
+                a.ctx_lengths[w] = (int32_t)((int64_t)L + 1 + (a.seed ? len : 0));
+                a.ctx_row[w] = (int32_t)i;
+                a.ctx_entry[w] = (int32_t)k;
+                a.ctx_kind[w] = pc == C_SUB ? (int32_t)T_SUB : (int32_t)T_TRI;
+            }
+            text += lane63((int32_t)incl);
+        }
+        if (base > 0) {
+            const uint32_t y = ev[base - 1];
+            prev_pos = lo + (y >> 4);
+            prev_cls = y & 15u;
+        }
+        m += base;
+        __builtin_amdgcn_wave_barrier(); /* ev is rewritten by the next chunk */
+    }
+    if (!WRITE) {
+        ok = __ballot(!ok) == 0;
+        /* an even, non-zero number of tags, the last one right before
+         * </Outlines> (or followed by a gap when lenient) */
+        ok = ok && m >= 2 && (m & 1) == 0 && (a.lenient || prev_pos == end - 1);
+        const int64_t n_e = ok ? m / 2 : 0;
+        int64_t toks = n_e * ((int64_t)L + 1) + (a.seed ? text : 0);
+        uint32_t st = ok ? 0u : (uint32_t)PARASON_PACK_BAD_ENTRY;
+        if (ok && (int64_t)L + 1 + (a.seed ? text : 0) > (int64_t)INT32_MAX) {
+            st = PARASON_PACK_TOO_LONG;
+            toks = 0;
+        }
+        if (lane == 0) {
+            a.status[i] = st;
+            a.counts[3 * i] = st == 0 ? n_e : 0;
+            a.counts[3 * i + 1] = st == 0 ? toks : 0;
+            /* fork_copy reads the row once per group of COPY_GROUP workers */
+            a.counts[3 * i + 2] = st == 0 ? (n_e + COPY_GROUP - 1) / COPY_GROUP * (int64_t)L : 0;
+            a.outl[i] = (int32_t)o;
+        }
+    }
+}
+
 /* One wave per row (grid-stride).  WRITE = false: status and counts;
  * WRITE = true: the worker records of rows whose outline is well formed. */
 template <bool WRITE>
@@ -291,200 +497,67 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
     __shared__ uint32_t ev_all[4][CHUNK]; /* per wave: (offset in chunk << 4) | class, in position order */
     const int lane = threadIdx.x & (WAVE - 1);
     const int wv = threadIdx.x / WAVE;
-    uint32_t *ev = ev_all[wv];
-    const bool contig = a.tm.contiguous != 0;
     if (WRITE && a.over[0]) return;
     const int64_t n_waves = (int64_t)gridDim.x * 4;
-    for (int64_t i = uniform64((int64_t)blockIdx.x * 4 + wv); i < a.n; i += n_waves) {
-        const int64_t g = a.starts[i];
-        const int32_t L = a.lengths[i];
-        int64_t o;
-        if (WRITE) {
-            const int64_t n_e = a.counts[3 * i];
-            if (a.status[i] != 0 || n_e == 0) continue;
-            if (n_e <= SUMM_ENTRIES) {
-                /* the first walk kept every entry of this outline: the records
-                 * without a second walk (lane k: entry k) */
-                const uint64_t x = lane < n_e ? a.summ[i * SUMM_ENTRIES + lane] : 0ull;
-                const int32_t sl = a.seed ? (int32_t)((x >> 32) & 0x7fffffffu) : 0;
-                const int64_t before = dpp_incl_scan<OpAdd>(sl, lane) - sl; /* seeds of entries 0 .. k-1 */
-                if (lane < n_e) {
-                    const int64_t w = a.worker_off[i] + lane;
-                    a.ctx_starts[w] = a.tok_off[i] + lane * ((int64_t)L + 1) + before;
-                    a.ctx_lengths[w] = (int32_t)((int64_t)L + 1 + sl);
-                    a.ctx_row[w] = (int32_t)i;
-                    a.ctx_entry[w] = lane;
-                    a.ctx_kind[w] = (x >> 63) ? (int32_t)T_TRI : (int32_t)T_SUB;
-                }
-                continue;
-            }
-            o = a.outl[i];
-        } else {
-            uint32_t st = 0;
-            o = -1;
-            if (L < 0 || g < 0) st = PARASON_PACK_BAD_ROW;
-            else if (L == 0) st = PARASON_PACK_NO_OUTLINE_END;
-            /* backwards from the row's end in chunks: the first chunk holds the
-             * last token, which must be </Outlines>; then the last <Outlines>
-             * before it, and the class of the token right before that when it
-             * is in the same chunk (1: <Parallel>, 0: not, -1: not seen) */
-            int32_t par_before = -1;
-            for (int64_t e = (int64_t)L; st == 0 && e > 0 && o < 0; e -= CHUNK) {
-                const int64_t lo = e > CHUNK ? e - CHUNK : 0;
-                uint32_t c[CHUNK_J];
-                int32_t best = -1;
-                bool end_mine = false;
+    for (int64_t i = uniform64((int64_t)blockIdx.x * 4 + wv); i < a.n; i += n_waves)
+        outline_row<WRITE>(a, i, WRITE ? a.worker_off[i] : 0, WRITE ? a.tok_off[i] : 0, ev_all[wv], lane);
+}
+
+/* Up to FORK_SINGLE rows: the scans of the three counts and the worker
+ * records in one launch instead of pack_single and fork_outline<true>.  Every
+ * block scans the counts of all rows, one row per thread (24 bytes per row,
+ * read from L2), then its FORK_SINGLE_WAVES waves write the records of the
+ * block's rows, one row per wave.  Each block writes the offsets of its own
+ * rows; the block holding the last row writes the totals and the capacity
+ * flag, which every block computes alike. */
+constexpr int FORK_SINGLE = 1024;
+constexpr int FORK_SINGLE_WAVES = FORK_SINGLE / WAVE;
+
+__global__ void __launch_bounds__(FORK_SINGLE) fork_records(ForkArgs a, PackScan<3> ps)
+{
+    __shared__ int64_t part[3][FORK_SINGLE_WAVES];
+    __shared__ int64_t offs[2][FORK_SINGLE_WAVES]; /* first worker and first context token of the block's rows */
+    __shared__ uint32_t ev_all[FORK_SINGLE_WAVES][CHUNK];
+    const int t = (int)threadIdx.x, lane = t & (WAVE - 1), wv = t / WAVE;
+    int64_t v[3], off[3], total[3];
 #pragma unroll
-                for (int j = 0; j < CHUNK_J; ++j) {
-                    const int64_t p = lo + lane + WAVE * j;
-                    c[j] = p < e ? classify(a.tm, a.tokens[g + p], contig) : C_TEXT;
-                    if (p < (int64_t)L - 1 && c[j] == C_OUT) best = (int32_t)p > best ? (int32_t)p : best;
-                    end_mine = end_mine || (p == (int64_t)L - 1 && c[j] == C_END_OUT);
-                }
-                if (e == (int64_t)L && __ballot(end_mine) == 0) {
-                    st = PARASON_PACK_NO_OUTLINE_END;
-                    break;
-                }
-                o = wave_max_pos(best, lane);
-                if (o >= 1 && o - 1 >= lo) {
-                    bool par_mine = false;
+    for (int k = 0; k < 3; ++k) v[k] = t < a.n ? a.counts[3 * t + k] : 0;
 #pragma unroll
-                    for (int j = 0; j < CHUNK_J; ++j) par_mine = par_mine || (lo + lane + WAVE * j == o - 1 && c[j] == C_PAR);
-                    par_before = __ballot(par_mine) != 0 ? 1 : 0;
-                }
-            }
-            if (st == 0) {
-                /* the tag before <Outlines> must be <Parallel>: right before it,
-                 * or with only Text between when lenient */
-                bool par_ok;
-                if (a.lenient) {
-                    const int64_t q = o >= 1 ? last_tag_before(a, g, o, lane, contig) : -1;
-                    par_ok = q >= 0 && classify(a.tm, a.tokens[g + q], contig) == C_PAR;
-                } else {
-                    par_ok = o >= 1 && (par_before >= 0 ? par_before == 1
-                                                        : classify(a.tm, a.tokens[g + o - 1], contig) == C_PAR);
-                }
-                if (o < 0 || !par_ok) st = PARASON_PACK_NO_OUTLINE;
-            }
-            if (st != 0) {
-                if (lane == 0) {
-                    a.status[i] = st;
-                    a.counts[3 * i] = 0;
-                    a.counts[3 * i + 1] = 0;
-                    a.counts[3 * i + 2] = 0;
-                    a.outl[i] = -1;
-                }
-                continue;
-            }
-        }
-        /* walk the outline [o + 1, L - 1) in chunks; events are its tags */
-        const int64_t end = (int64_t)L - 1;
-        int64_t m = 0;                       /* tags before this chunk */
-        int64_t prev_pos = o;                /* the tag before the current one */
-        uint32_t prev_cls = C_OUT;
-        int64_t text = 0;                    /* entry text tokens so far (the same in every lane) */
-        bool ok = true;
-        const int64_t w0 = WRITE ? a.worker_off[i] : 0;
-        const int64_t t0 = WRITE ? a.tok_off[i] : 0;
-        for (int64_t lo = o + 1; lo < end; lo += CHUNK) {
-            uint64_t b[CHUNK_J];
-            uint32_t c[CHUNK_J];
-#pragma unroll
-            for (int j = 0; j < CHUNK_J; ++j) {
-                const int64_t p = lo + lane + WAVE * j;
-                c[j] = p < end ? classify(a.tm, a.tokens[g + p], contig) : C_TEXT;
-                b[j] = __ballot(c[j] != C_TEXT);
-            }
-            uint32_t base = 0;
-#pragma unroll
-            for (int j = 0; j < CHUNK_J; ++j) {
-                if (c[j] != C_TEXT) {
-                    const uint32_t idx = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(b[j] >> 32),
-                                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)b[j], 0u));
-                    ev[idx] = ((uint32_t)(lane + WAVE * j) << 4) | c[j];
-                }
-                base += (uint32_t)__popcll(b[j]);
-            }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            for (uint32_t e0 = 0; e0 < base; e0 += WAVE) { /* the same trip count in every lane */
-                const uint32_t e = e0 + (uint32_t)lane;
-                const bool act = e < base;
-                int64_t len = 0; /* text tokens of the entry this lane closes */
-                int64_t J = 0, tstart = 0;
-                uint32_t pc = 0;
-                if (act) {
-                    const uint32_t x = ev[e];
-                    const int64_t P = lo + (x >> 4);
-                    const uint32_t cl = x & 15u;
-                    int64_t pp = prev_pos;
-                    pc = prev_cls;
-                    if (e > 0) {
-                        const uint32_t y = ev[e - 1];
-                        pp = lo + (y >> 4);
-                        pc = y & 15u;
-                    }
-                    J = m + e;
-                    if ((J & 1) == 0) {
-                        /* an entry opens after <Outlines> or the previous entry:
-                         * right after it, or after a gap when lenient */
-                        ok = ok && (cl == C_SUB || cl == C_TRI) && (a.lenient || P == pp + 1);
-                    } else {
-                        /* and closes with its own tag after at least one text token */
-                        ok = ok && (pc == C_SUB || pc == C_TRI) && cl == pc + 1 && P >= pp + 2;
-                        len = P - pp - 1;
-                        tstart = pp + 1;
-                    }
-                }
-                if (!WRITE && act && (J & 1) && (J >> 1) < SUMM_ENTRIES)
-                    a.summ[i * SUMM_ENTRIES + (J >> 1)] = (uint64_t)(uint32_t)tstart |
-                                                         ((uint64_t)(uint32_t)len << 32) |
-                                                         ((uint64_t)(pc == C_TRI) << 63);
-                /* entry text lengths and their sums within a chunk are below L */
-                const int64_t incl = dpp_incl_scan<OpAdd>((int32_t)len, lane);
-                if (WRITE && act && (J & 1)) {
-                    const int64_t k = J >> 1;
-                    const int64_t w = w0 + k;
-                    const int64_t seed_before = text + incl - len; /* texts of entries 0 .. k-1 */
-                    a.ctx_starts[w] = t0 + k * ((int64_t)L + 1) + (a.seed ? seed_before : 0);
-                    a.ctx_lengths[w] = (int32_t)((int64_t)L + 1 + (a.seed ? len : 0));
-                    a.ctx_row[w] = (int32_t)i;
-                    a.ctx_entry[w] = (int32_t)k;
-                    a.ctx_kind[w] = pc == C_SUB ? (int32_t)T_SUB : (int32_t)T_TRI;
-                }
-                text += lane63((int32_t)incl);
-            }
-            if (base > 0) {
-                const uint32_t y = ev[base - 1];
-                prev_pos = lo + (y >> 4);
-                prev_cls = y & 15u;
-            }
-            m += base;
-            __builtin_amdgcn_wave_barrier(); /* ev is rewritten by the next chunk */
-        }
-        if (!WRITE) {
-            ok = __ballot(!ok) == 0;
-            /* an even, non-zero number of tags, the last one right before
-             * </Outlines> (or followed by a gap when lenient) */
-            ok = ok && m >= 2 && (m & 1) == 0 && (a.lenient || prev_pos == end - 1);
-            const int64_t n_e = ok ? m / 2 : 0;
-            int64_t toks = n_e * ((int64_t)L + 1) + (a.seed ? text : 0);
-            uint32_t st = ok ? 0u : (uint32_t)PARASON_PACK_BAD_ENTRY;
-            if (ok && (int64_t)L + 1 + (a.seed ? text : 0) > (int64_t)INT32_MAX) {
-                st = PARASON_PACK_TOO_LONG;
-                toks = 0;
-            }
-            if (lane == 0) {
-                a.status[i] = st;
-                a.counts[3 * i] = st == 0 ? n_e : 0;
-                a.counts[3 * i + 1] = st == 0 ? toks : 0;
-                /* fork_copy reads the row once per group of COPY_GROUP workers */
-                a.counts[3 * i + 2] = st == 0 ? (n_e + COPY_GROUP - 1) / COPY_GROUP * (int64_t)L : 0;
-                a.outl[i] = (int32_t)o;
-            }
-        }
+    for (int k = 0; k < 3; ++k) {
+        const int64_t inc = wave_inclusive_scan(v[k]);
+        if (lane == WAVE - 1) part[k][wv] = inc;
+        off[k] = inc - v[k];
     }
+    __syncthreads();
+    int32_t over = 0;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        total[k] = 0;
+        for (int w = 0; w < FORK_SINGLE_WAVES; ++w) {
+            off[k] += w < wv ? part[k][w] : 0;
+            total[k] += part[k][w];
+        }
+        over |= total[k] > ps.cap[k] ? 1 : 0;
+    }
+    const int64_t r0 = (int64_t)blockIdx.x * FORK_SINGLE_WAVES; /* the block's rows */
+    if (t >= r0 && t < r0 + FORK_SINGLE_WAVES && t < a.n) {
+#pragma unroll
+        for (int k = 0; k < 3; ++k) ps.out[k][t] = off[k];
+        offs[0][t - r0] = off[0];
+        offs[1][t - r0] = off[1];
+    }
+    if (blockIdx.x == gridDim.x - 1 && t == 0) {
+#pragma unroll
+        for (int k = 0; k < 3; ++k) ps.out[k][a.n] = total[k];
+        ps.totals[0] = total[0];
+        ps.totals[1] = total[1];
+        ps.totals[2] = over;
+        ps.over[0] = over;
+    }
+    __syncthreads();
+    const int64_t i = r0 + wv;
+    if (over || i >= a.n) return;
+    outline_row<true>(a, i, offs[0][wv], offs[1][wv], ev_all[wv], lane);
 }
 
 /* ---- tiled copies -------------------------------------------------------- */
@@ -581,9 +654,11 @@ __device__ __forceinline__ void wave_copy(int32_t *__restrict__ dst, int64_t d0,
     v4i_t v[WV];
 #pragma unroll
     for (int j = 0; j < WV; ++j) v[j] = load16(sp + 4 * min((int64_t)(lane + WAVE * j), nvec - 1));
+    /* streaming stores: the joined rows are not read again by this call
+     * (dword stores of fork_copy's contexts measured slower this way) */
 #pragma unroll
     for (int j = 0; j < WV; ++j)
-        if (lane + WAVE * j < nvec) dp[lane + WAVE * j] = v[j];
+        if (lane + WAVE * j < nvec) __builtin_nontemporal_store(v[j], dp + lane + WAVE * j);
 }
 
 /* A worker context's tail at dst[d0 .. d1): sub (the <Thread> id) at d0, then
@@ -628,9 +703,7 @@ __device__ __forceinline__ int64_t group_text_pos(const ForkArgs &a, const int32
         if (open && rk >= ea && rk < ea + nd) slot[rk - ea] = p + 1;
         seen += __popcll(b);
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    wave_lds_sync();
     const int64_t f = lane < nd ? slot[lane] : 0;
     __builtin_amdgcn_wave_barrier(); /* slot is rewritten by the next group */
     return f;
@@ -714,10 +787,10 @@ struct JoinArgs {
     int32_t *out_tokens;
 };
 
-__global__ void __launch_bounds__(256) join_size(JoinArgs a)
+/* Joined length and status of row i (the checks of its worker sequences);
+ * writes status, out_len64 and out_lengths and returns the length. */
+__device__ __forceinline__ int64_t join_row(const JoinArgs &a, int64_t i)
 {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= a.n) return;
     const int64_t L = a.lengths[i], g = a.starts[i];
     const int64_t w0 = a.worker_off[i], w1 = a.worker_off[i + 1];
     uint32_t st = 0;
@@ -726,16 +799,35 @@ __global__ void __launch_bounds__(256) join_size(JoinArgs a)
         st = PARASON_PACK_BAD_ROW;
     } else {
         tot = (a.append_only ? 0 : L) + (a.close ? 1 : 0);
-        for (int64_t w = w0; w < w1; ++w) {
-            const int64_t wl = a.wlengths[w], ws = a.wstarts[w];
-            if (wl < 0 || ws < 0) {
-                st |= PARASON_PACK_BAD_ROW;
-                continue;
+        /* JOIN_UNROLL workers at a time: their records in one round of loads,
+         * then the tokens after the row and at the end in one more */
+        for (int64_t wb = w0; wb < w1; wb += JOIN_UNROLL) {
+            int64_t wl[JOIN_UNROLL], ws[JOIN_UNROLL];
+#pragma unroll
+            for (int u = 0; u < JOIN_UNROLL; ++u) {
+                const bool in = wb + u < w1;
+                wl[u] = in ? (int64_t)a.wlengths[wb + u] : 0;
+                ws[u] = in ? a.wstarts[wb + u] : 0;
             }
-            const int64_t tail = wl > L ? wl - L : 0;
-            if (tail < 2 || a.wtokens[ws + L] != a.thread_id || a.wtokens[ws + wl - 1] != a.end_thread_id)
-                st |= PARASON_PACK_BAD_THREAD;
-            tot += tail;
+            int32_t first[JOIN_UNROLL], last[JOIN_UNROLL];
+            bool chk[JOIN_UNROLL];
+#pragma unroll
+            for (int u = 0; u < JOIN_UNROLL; ++u) {
+                const int64_t tail = wl[u] > L ? wl[u] - L : 0;
+                chk[u] = wb + u < w1 && wl[u] >= 0 && ws[u] >= 0 && tail >= 2;
+                first[u] = chk[u] ? a.wtokens[ws[u] + L] : 0;
+                last[u] = chk[u] ? a.wtokens[ws[u] + wl[u] - 1] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < JOIN_UNROLL; ++u) {
+                if (wb + u >= w1) break;
+                if (wl[u] < 0 || ws[u] < 0) {
+                    st |= PARASON_PACK_BAD_ROW;
+                    continue;
+                }
+                if (!chk[u] || first[u] != a.thread_id || last[u] != a.end_thread_id) st |= PARASON_PACK_BAD_THREAD;
+                tot += wl[u] > L ? wl[u] - L : 0;
+            }
         }
         if (st & PARASON_PACK_BAD_ROW) tot = 0;
         else if (tot > (int64_t)INT32_MAX) {
@@ -746,24 +838,79 @@ __global__ void __launch_bounds__(256) join_size(JoinArgs a)
     a.status[i] = st;
     a.out_len64[i] = tot;
     a.out_lengths[i] = (int32_t)tot;
+    return tot;
+}
+
+__global__ void __launch_bounds__(256) join_size(JoinArgs a)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < a.n) join_row(a, i);
 }
 
 /* Joined rows, tiled over their tokens by waves like fork_copy.  Inside a
  * row the pieces are the row, each worker's span (its sequence from the
  * <Thread> after the row on) and </Parallel>; the span positions of 64
- * workers at a time come from one wave prefix scan of their lengths. */
-__global__ void __launch_bounds__(PACK_THREADS) join_copy(JoinArgs a)
+ * workers at a time come from one wave prefix scan of their lengths.
+ * SCAN (up to JOIN_SINGLE rows): every block first scans the joined lengths
+ * itself into LDS, where its waves then search the rows (block 0 also writes
+ * the offsets, the total and the capacity flag), in place of the separate
+ * scan launch and the searches in global memory. */
+template <bool SCAN>
+__global__ void __launch_bounds__(PACK_THREADS) join_copy(JoinArgs a, PackScan<1> ps)
 {
+    constexpr int RPT = JOIN_SINGLE / PACK_THREADS; /* rows per thread of the scan */
+    __shared__ int64_t soff[SCAN ? JOIN_SINGLE + 1 : 1];
+    __shared__ int64_t part[PACK_THREADS / WAVE];
     const int lane = threadIdx.x & (WAVE - 1);
     const int wv = threadIdx.x / WAVE;
-    if (a.over[0]) return;
-    const int64_t T = a.out_starts[a.n];
+    const int64_t *out_starts = a.out_starts;
+    if (SCAN) {
+        const int64_t r0 = (int64_t)threadIdx.x * RPT;
+        int64_t v[RPT], sum = 0;
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            v[j] = r0 + j < a.n ? a.out_len64[r0 + j] : 0;
+            sum += v[j];
+        }
+        const int64_t inc = wave_inclusive_scan(sum);
+        if (lane == WAVE - 1) part[wv] = inc;
+        __syncthreads();
+        int64_t off = inc - sum, total = 0;
+        for (int w = 0; w < PACK_THREADS / WAVE; ++w) {
+            off += w < wv ? part[w] : 0;
+            total += part[w];
+        }
+        const int32_t over = total > ps.cap[0] ? 1 : 0;
+#pragma unroll
+        for (int j = 0; j < RPT; ++j) {
+            if (r0 + j < a.n) {
+                soff[r0 + j] = off;
+                if (blockIdx.x == 0) ps.out[0][r0 + j] = off;
+            }
+            off += v[j];
+        }
+        if (threadIdx.x == 0) {
+            soff[a.n] = total;
+            if (blockIdx.x == 0) {
+                ps.out[0][a.n] = total;
+                ps.totals[0] = total;
+                ps.totals[1] = over;
+                ps.over[0] = over;
+            }
+        }
+        __syncthreads();
+        if (over) return;
+        out_starts = soff;
+    } else if (a.over[0]) {
+        return;
+    }
+    const int64_t T = out_starts[a.n];
     const int64_t NW = (int64_t)gridDim.x * COPY_WAVES;
     for (int64_t t = (int64_t)blockIdx.x * COPY_WAVES + wv; t * WTILE < T; t += NW) {
         const int64_t lo = t * WTILE, hi = min(lo + WTILE, T);
-        for (int64_t i = wave_find(a.out_starts, a.n, lo, lane); i < a.n; ++i) {
+        for (int64_t i = wave_find(out_starts, a.n, lo, lane); i < a.n; ++i) {
             /* the row's records in one round of loads, before any branch */
-            const int64_t os = a.out_starts[i], len = a.out_len64[i];
+            const int64_t os = out_starts[i], len = a.out_len64[i];
             const int64_t L = a.lengths[i], g0 = a.starts[i];
             const int64_t wb = a.worker_off[i], we = a.worker_off[i + 1];
             if (os >= hi) break;
