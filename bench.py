@@ -344,6 +344,9 @@ def main():
         del tokens, starts, lengths, correct, out, ws
         torch.cuda.empty_cache()
         res["typical_batch"] = time_small_batch("typical", coef, args.steps * 5, args.warmup)
+        # and the other small workloads: one group, 32 groups, and 128 groups of log-uniform lengths
+        res["small_batches"] = {wl: time_small_batch(wl, coef, args.steps * 10, args.warmup)
+                                for wl in ("tiny", "small", "ragged")}
     print(json.dumps(res), flush=True)
 
 
