@@ -160,6 +160,10 @@ void find_tag_hash(pk::TagMatch &tm)
  * The deep tier is a launch of its own only when deep_launch is set (the
  * batch-wide statistics need every row first); otherwise group_reward runs
  * it. */
+/* A small batch (fewer rows than ROWS_WAVES_PER_CU waves on every CU, with
+ * two rows per wave) takes rows_par, one wave per row. */
+bool rows_par_batch(int64_t n, int cus) { return n / 2 < (int64_t)cus * ROWS_WAVES_PER_CU; }
+
 template <bool LENIENT>
 void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, uint8_t *mode, int32_t *counters,
                  int32_t *mid_rows, int32_t *deep_rows, int32_t *deep_frames, uint32_t *deep_bits, bool deep_launch,
@@ -171,6 +175,7 @@ void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, uint8
      * ROWS_WAVES_PER_CU waves on every CU (64 once the batch is large). */
     int64_t per_wave = 1;
     int32_t lane_shift = 6; /* log2(64 / per_wave) */
+    /* per_wave stays 1 exactly when rows_par_batch(ra.n, cus) */
     while (per_wave < 64 && ra.n / (per_wave * 2) >= (int64_t)cus * ROWS_WAVES_PER_CU) {
         per_wave *= 2;
         --lane_shift;
@@ -191,6 +196,20 @@ void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, uint8
     if (deep_launch)
         hipLaunchKernelGGL(pk::rows_deep<LENIENT>, dim3(1), dim3(64), 0, stream, ra, mode, counters, deep_rows,
                            deep_frames, deep_bits);
+}
+
+template <bool PLAN>
+void launch_scan(const pk::TagMatch &tm, const pk::ScanArgs &sa, unsigned scan_blocks, hipStream_t stream)
+{
+    if (tm.contiguous)
+        hipLaunchKernelGGL((pk::scan_rows<pk::TM_CONTIG, PLAN>), dim3(scan_blocks), dim3(pk::SCAN_THREADS), 0, stream,
+                           sa);
+    else if (tm.hashed)
+        hipLaunchKernelGGL((pk::scan_rows<pk::TM_HASH, PLAN>), dim3(scan_blocks), dim3(pk::SCAN_THREADS), 0, stream,
+                           sa);
+    else
+        hipLaunchKernelGGL((pk::scan_rows<pk::TM_LINEAR, PLAN>), dim3(scan_blocks), dim3(pk::SCAN_THREADS), 0, stream,
+                           sa);
 }
 
 }  // namespace
@@ -331,7 +350,12 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     uint32_t *slots = (uint32_t *)(ws + q.slots);
 
     const unsigned tiles = (unsigned)L.n_tiles;
-    abi::launch_plan(starts, lengths, n_traj, mis, L.n_tiles, tile_sum, tile_off, seg_off, counters, mode, stream);
+    /* a batch that takes rows_par and fits one scan block's plan is planned
+     * by the scan blocks themselves (one launch less, and the scan waves find
+     * their rows in LDS) */
+    const bool plan_in_scan = n_traj <= pk::SCAN_PLAN_ROWS && rows_par_batch(n_traj, cus);
+    if (!plan_in_scan)
+        abi::launch_plan(starts, lengths, n_traj, mis, L.n_tiles, tile_sum, tile_off, seg_off, counters, mode, stream);
 
     const pk::RowOut row_out{out->total,    out->latency,   out->n_subtask,       out->n_trial,
                              out->n_blocks, out->max_depth, out->first_error_pos, out->flags};
@@ -351,17 +375,13 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     sa.tm = h->tm;
     sa.split_count = counters + 2;
     sa.split_rows = split_rows;
+    sa.counters = counters;
     const unsigned scan_blocks = (unsigned)(cus * SCAN_BLOCKS_PER_CU);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[0], stream) != hipSuccess) return PARASON_ERR_HIP;
-    if (h->tm.contiguous)
-        hipLaunchKernelGGL(pk::scan_rows<pk::TM_CONTIG>, dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream,
-                           sa);
-    else if (h->tm.hashed)
-        hipLaunchKernelGGL(pk::scan_rows<pk::TM_HASH>, dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream,
-                           sa);
+    if (plan_in_scan)
+        launch_scan<true>(h->tm, sa, scan_blocks, stream);
     else
-        hipLaunchKernelGGL(pk::scan_rows<pk::TM_LINEAR>, dim3(scan_blocks), dim3(pk::WAVE * pk::SCAN_WAVES), 0, stream,
-                           sa);
+        launch_scan<false>(h->tm, sa, scan_blocks, stream);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[1], stream) != hipSuccess) return PARASON_ERR_HIP;
 
     pk::RowArgs ra;

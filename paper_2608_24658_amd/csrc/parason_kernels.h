@@ -7,7 +7,9 @@
  *        Each row is cut into segments of SEG_VEC 16-byte vectors, starting at
  *        the 128-byte line that holds its first token.  A three-pass exclusive
  *        scan gives seg_off[i] (first segment of row i) and the segment count
- *        seg_off[n]; mode[i] is cleared.
+ *        seg_off[n]; mode[i] is cleared.  A batch that takes rows_par and has
+ *        at most SCAN_PLAN_ROWS rows skips these launches: every scan block
+ *        makes the plan in LDS itself (scan_plan).
  *   scan_rows  (HBM-bound; one wave per segment, persistent grid)
  *        Streams every token once with 16-byte loads, tests it against the
  *        twelve tag ids with a wave ballot and compacts the rare tags (about
@@ -1144,6 +1146,7 @@ struct ScanArgs {
     TagMatch tm;
     int32_t *split_count; /* rows of more than one segment that no scan wave owns ... */
     int32_t *split_rows;  /* ... listed here for gather_rows */
+    int32_t *counters;    /* cleared by a scan that plans the batch itself */
 };
 
 /* Row being collected by a scan wave, in processing order. */
@@ -1156,6 +1159,8 @@ struct RowCollect {
 
 constexpr int EVL = 1024;                 /* LDS events per wave */
 constexpr int SCAN_WAVES = 4;             /* waves per scan block */
+constexpr int SCAN_THREADS = WAVE * SCAN_WAVES;
+constexpr int SCAN_PLAN_ROWS = 2048;      /* rows up to which a scan block plans the batch itself */
 
 /* The whole of row `row` is in the wave's LDS buffer lev[0 .. lcnt): copy it,
  * coalesced, to the wave's pool region as one compact list for the row kernel
@@ -1186,17 +1191,22 @@ __device__ __forceinline__ void flush_row(const ScanArgs &a, int64_t row, int64_
  * its events in the wave's LDS buffer; any other row leaves its events in the
  * per-segment lists for the row kernels.  Returns true when this segment
  * completes a row whose events are all in the LDS buffer (rc.lcnt of them). */
-template <int MODE>
+template <int MODE, bool PLAN>
 __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&x)[LOADS], const SegView &w,
                                                 RowCollect &rc, uint32_t *lev, int32_t tab, int lane)
 {
     if (w.s == w.first) {
         rc.lcnt = 0;
         rc.global = !w.owned;
-        /* the wave holding the first segment of a split row lists it for
-         * gather_rows (rows of 2^27 tokens or more stay per segment) */
-        if (!w.owned && w.last > w.first && w.len < (1 << 27) && lane == 0)
+        if (PLAN) {
+            /* the scan planned the batch itself: the wave holding a row's first
+             * segment clears its mode (flush_row may set it again below) */
+            if (lane == 0) a.mode[w.row] = 0;
+        } else if (!w.owned && w.last > w.first && w.len < (1 << 27) && lane == 0) {
+            /* the wave holding the first segment of a split row lists it for
+             * gather_rows (rows of 2^27 tokens or more stay per segment) */
             a.split_rows[atomicAdd(a.split_count, 1)] = (int32_t)w.row;
+        }
     }
     uint32_t cnt = 0; /* wave-uniform */
     if (!rc.global) {
@@ -1229,15 +1239,71 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
  * register buffers alternate: the loads of segment s + 1 are issued before
  * segment s is compacted (and a finished row's events flushed), so a wave
  * always has a segment in flight. */
-template <int MODE>
+/* The segment plan of a batch of at most SCAN_PLAN_ROWS rows, made by one
+ * scan block in LDS (off[r] = first segment of row r, off[n] = the total):
+ * the segment counts with coalesced loads (row t + SCAN_THREADS * j for thread
+ * t), then an exclusive scan with each thread over SCAN_PLAN_ROWS /
+ * SCAN_THREADS consecutive rows.  Block 0 also writes the plan to seg_off for
+ * the row kernels, clears the mode of rows without segments (no scan wave
+ * sees them) and the counters; every other row's mode is cleared by the wave
+ * holding its first segment. */
+__device__ __forceinline__ void scan_plan(const ScanArgs &a, int64_t *off, int64_t *part)
+{
+    constexpr int RPT = SCAN_PLAN_ROWS / SCAN_THREADS;
+    const int t = (int)threadIdx.x, lane = t & (WAVE - 1), wv = t / WAVE;
+#pragma unroll
+    for (int j = 0; j < RPT; ++j) {
+        const int64_t r = t + (int64_t)SCAN_THREADS * j;
+        off[r] = r < a.n ? row_segments(a.starts[r], a.lengths[r], a.mis) : 0;
+    }
+    __syncthreads();
+    int64_t c[RPT], sum = 0;
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+        c[k] = off[t * RPT + k];
+        sum += c[k];
+    }
+    const int64_t inc = wave_inclusive_scan(sum);
+    if (lane == WAVE - 1) part[wv] = inc;
+    __syncthreads();
+    int64_t run = inc - sum, total = 0;
+    for (int w = 0; w < SCAN_WAVES; ++w) {
+        run += w < wv ? part[w] : 0;
+        total += part[w];
+    }
+#pragma unroll
+    for (int k = 0; k < RPT; ++k) {
+        if (t * RPT + k < a.n) off[t * RPT + k] = run;
+        run += c[k];
+    }
+    if (t == 0) off[a.n] = total; /* rows beyond n are not rewritten, so no other thread writes off[n] */
+    __syncthreads();
+    if (blockIdx.x == 0) {
+        int64_t *seg_off = const_cast<int64_t *>(a.seg_off);
+        for (int64_t r = t; r <= a.n; r += SCAN_THREADS) {
+            seg_off[r] = off[r];
+            if (r < a.n && off[r + 1] == off[r]) a.mode[r] = 0;
+        }
+        if (t < 4) a.counters[t] = 0;
+    }
+}
+
+template <int MODE, bool PLAN>
 __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD) scan_rows(ScanArgs a)
 {
     __shared__ uint32_t lds_ev[SCAN_WAVES][EVL];
+    __shared__ int64_t plan_off[PLAN ? SCAN_PLAN_ROWS + 1 : 1];
+    __shared__ int64_t plan_part[SCAN_WAVES];
     const int lane = threadIdx.x & (WAVE - 1);
     const int wib = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
     const int64_t wave = uniform64((int64_t)blockIdx.x * SCAN_WAVES + wib);
     const int64_t n_waves = (int64_t)gridDim.x * SCAN_WAVES;
-    const int64_t S = a.seg_off[a.n];
+    const int64_t *seg_off = a.seg_off;
+    if (PLAN) {
+        scan_plan(a, plan_off, plan_part);
+        seg_off = plan_off;
+    }
+    const int64_t S = uniform64(seg_off[a.n]);
     if (S > a.seg_cap) return; /* the row kernel reports PARASON_FLAG_WS_OVERFLOW */
     /* S < 2^40 and n_waves < 2^20 (checked on the host), so S * wave fits */
     const int64_t s_begin = uniform64(S * wave / n_waves);
@@ -1246,7 +1312,7 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
 
     const int4 *src = reinterpret_cast<const int4 *>(a.tok_base);
     SegCursor cur;
-    cur.seg_off = a.seg_off;
+    cur.seg_off = seg_off;
     cur.starts = a.starts;
     cur.lengths = a.lengths;
     cur.mis = a.mis;
@@ -1277,7 +1343,7 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
             wn = cur.view(s + 1);
             issue_loads(xb, src, wn, lane);
         }
-        if (collect_segment<MODE>(a, xa, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
+        if (collect_segment<MODE, PLAN>(a, xa, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
         if (!more) break;
         ++s;
         w = wn;
@@ -1286,7 +1352,7 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
             wn = cur.view(s + 1);
             issue_loads(xa, src, wn, lane);
         }
-        if (collect_segment<MODE>(a, xb, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
+        if (collect_segment<MODE, PLAN>(a, xb, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
         if (!more) break;
         ++s;
         w = wn;
