@@ -150,8 +150,8 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
     if (n_rows > 0) hipLaunchKernelGGL(pk::fork_outline<false>, dim3(wave_blocks), dim3(256), 0, stream, fa);
     if (n_rows <= pk::FORK_SINGLE) {
         /* scans and records in one launch (at least one block: it writes the totals) */
-        const unsigned blocks = (unsigned)std::max<int64_t>(1, (n_rows + pk::FORK_SINGLE_WAVES - 1) / pk::FORK_SINGLE_WAVES);
-        hipLaunchKernelGGL(pk::fork_records, dim3(blocks), dim3(pk::FORK_SINGLE), 0, stream, fa, ps);
+        const unsigned blocks = (unsigned)std::max<int64_t>(1, (n_rows + pk::FORK_REC_WAVES - 1) / pk::FORK_REC_WAVES);
+        hipLaunchKernelGGL(pk::fork_records, dim3(blocks), dim3(pk::FORK_REC_THREADS), 0, stream, fa, ps);
     } else {
         launch_pack(ps, L.tiles, stream);
         hipLaunchKernelGGL(pk::fork_outline<true>, dim3(wave_blocks), dim3(256), 0, stream, fa);
@@ -218,7 +218,8 @@ int parason_join(const parason_handle *h, const int32_t *tokens, const int64_t *
     ps.report = 1;
     ps.over = (int32_t *)(ws + L.over);
 
-    if (n_rows > 0) hipLaunchKernelGGL(pk::join_size, dim3((unsigned)((n_rows + 255) / 256)), dim3(256), 0, stream, ja);
+    if (n_rows > 0) hipLaunchKernelGGL(pk::join_size, dim3((unsigned)((n_rows + pk::JOIN_SIZE_THREADS - 1) / pk::JOIN_SIZE_THREADS)),
+                                       dim3(pk::JOIN_SIZE_THREADS), 0, stream, ja);
     const unsigned copy_blocks = n_rows > 0 ? (unsigned)(cus * COPY_BLOCKS_PER_CU) : 1u;
     if (n_rows <= pk::JOIN_SINGLE) {
         /* the scan inside the copy (no rows: one block, which writes the zero totals) */

@@ -62,6 +62,9 @@ constexpr int COPY_GROUP = 8;   /* worker contexts fork_copy writes from one rea
 constexpr int SUMM_ENTRIES = 8; /* outline entries per row the first walk keeps for the second */
 constexpr int JOIN_UNROLL = 4;  /* workers of a row whose records join_size loads together */
 constexpr int JOIN_SINGLE = 1024; /* rows up to which join_copy scans the joined lengths itself */
+/* join_size: small blocks spread its scattered loads of worker tokens over
+ * many compute units (256-thread blocks measured 0.9 us slower at 1,024 rows) */
+constexpr int JOIN_SIZE_THREADS = 64;
 
 /* Orders the LDS accesses of a wave's lanes: what one lane wrote before it is
  * visible to every lane of the wave after it. */
@@ -505,46 +508,62 @@ __global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
 
 /* Up to FORK_SINGLE rows: the scans of the three counts and the worker
  * records in one launch instead of pack_single and fork_outline<true>.  Every
- * block scans the counts of all rows, one row per thread (24 bytes per row,
- * read from L2), then its FORK_SINGLE_WAVES waves write the records of the
- * block's rows, one row per wave.  Each block writes the offsets of its own
- * rows; the block holding the last row writes the totals and the capacity
- * flag, which every block computes alike. */
+ * block scans the counts of all rows (24 bytes per row, read from L2; each
+ * thread FORK_REC_RPT consecutive rows), then its FORK_REC_WAVES waves write
+ * the records of the block's rows, one row per wave.  The thread holding a
+ * row in the scan writes its offsets (in the row's own block); the block
+ * holding the last row writes the totals and the capacity flag, which every
+ * block computes alike. */
 constexpr int FORK_SINGLE = 1024;
-constexpr int FORK_SINGLE_WAVES = FORK_SINGLE / WAVE;
+constexpr int FORK_REC_WAVES = 8; /* 16: 1.3 us slower at 1,024 rows; 4: as fast */
+constexpr int FORK_REC_THREADS = FORK_REC_WAVES * WAVE;
+constexpr int FORK_REC_RPT = FORK_SINGLE / FORK_REC_THREADS;
 
-__global__ void __launch_bounds__(FORK_SINGLE) fork_records(ForkArgs a, PackScan<3> ps)
+__global__ void __launch_bounds__(FORK_REC_THREADS) fork_records(ForkArgs a, PackScan<3> ps)
 {
-    __shared__ int64_t part[3][FORK_SINGLE_WAVES];
-    __shared__ int64_t offs[2][FORK_SINGLE_WAVES]; /* first worker and first context token of the block's rows */
-    __shared__ uint32_t ev_all[FORK_SINGLE_WAVES][CHUNK];
+    __shared__ int64_t part[3][FORK_REC_WAVES];
+    __shared__ int64_t offs[2][FORK_REC_WAVES]; /* first worker and first context token of the block's rows */
+    __shared__ uint32_t ev_all[FORK_REC_WAVES][CHUNK];
     const int t = (int)threadIdx.x, lane = t & (WAVE - 1), wv = t / WAVE;
-    int64_t v[3], off[3], total[3];
+    const int64_t q0 = (int64_t)t * FORK_REC_RPT; /* this thread's rows in the scan */
+    int64_t v[FORK_REC_RPT][3], off[3], total[3];
 #pragma unroll
-    for (int k = 0; k < 3; ++k) v[k] = t < a.n ? a.counts[3 * t + k] : 0;
+    for (int j = 0; j < FORK_REC_RPT; ++j) {
+#pragma unroll
+        for (int k = 0; k < 3; ++k) v[j][k] = q0 + j < a.n ? a.counts[3 * (q0 + j) + k] : 0;
+    }
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
-        const int64_t inc = wave_inclusive_scan(v[k]);
+        int64_t sum = 0;
+#pragma unroll
+        for (int j = 0; j < FORK_REC_RPT; ++j) sum += v[j][k];
+        const int64_t inc = wave_inclusive_scan(sum);
         if (lane == WAVE - 1) part[k][wv] = inc;
-        off[k] = inc - v[k];
+        off[k] = inc - sum;
     }
     __syncthreads();
     int32_t over = 0;
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
         total[k] = 0;
-        for (int w = 0; w < FORK_SINGLE_WAVES; ++w) {
+        for (int w = 0; w < FORK_REC_WAVES; ++w) {
             off[k] += w < wv ? part[k][w] : 0;
             total[k] += part[k][w];
         }
         over |= total[k] > ps.cap[k] ? 1 : 0;
     }
-    const int64_t r0 = (int64_t)blockIdx.x * FORK_SINGLE_WAVES; /* the block's rows */
-    if (t >= r0 && t < r0 + FORK_SINGLE_WAVES && t < a.n) {
+    const int64_t r0 = (int64_t)blockIdx.x * FORK_REC_WAVES; /* the block's rows */
 #pragma unroll
-        for (int k = 0; k < 3; ++k) ps.out[k][t] = off[k];
-        offs[0][t - r0] = off[0];
-        offs[1][t - r0] = off[1];
+    for (int j = 0; j < FORK_REC_RPT; ++j) {
+        const int64_t r = q0 + j;
+        if (r >= r0 && r < r0 + FORK_REC_WAVES && r < a.n) {
+#pragma unroll
+            for (int k = 0; k < 3; ++k) ps.out[k][r] = off[k];
+            offs[0][r - r0] = off[0];
+            offs[1][r - r0] = off[1];
+        }
+#pragma unroll
+        for (int k = 0; k < 3; ++k) off[k] += v[j][k];
     }
     if (blockIdx.x == gridDim.x - 1 && t == 0) {
 #pragma unroll
@@ -841,7 +860,7 @@ __device__ __forceinline__ int64_t join_row(const JoinArgs &a, int64_t i)
     return tot;
 }
 
-__global__ void __launch_bounds__(256) join_size(JoinArgs a)
+__global__ void __launch_bounds__(JOIN_SIZE_THREADS) join_size(JoinArgs a)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < a.n) join_row(a, i);
