@@ -113,6 +113,21 @@ def test_text_ids_over_the_whole_int32_range(dev, tags):
     log("int32 text ids: %d rows ok" % n)
 
 
+@pytest.mark.parametrize("n", [2040, 2048, 2056, 4104])
+def test_plan_boundaries(dev, n):
+    """Around the batch sizes where the plan changes: up to 2,048 rows (that
+    take rows_par) the scan blocks plan the batch themselves; 2,056 rows take
+    the one-block plan launch; 4,104 rows two plan tiles.  Rows of the small
+    workload, every output compared with the oracle."""
+    log("case plan boundary n=%d" % n)
+    P = S.make_params("small")
+    tok_h, st_h, ln_h, co_h = S.host_batch(P, n)
+    px, coef = px_for()
+    got = run_gpu(px, to_dev(tok_h, torch.int32, dev), to_dev(st_h, torch.int64, dev),
+                  to_dev(ln_h, torch.int32, dev), to_dev(co_h, torch.uint8, dev))
+    compare(got, *oracle_expect(tok_h, st_h, ln_h, co_h, TAGS, G, coef), what="plan boundary %d" % n)
+
+
 def test_many_rows_beyond_the_first_tier(dev):
     """40,000 rows nested 6-33 deep (more than the second tier has threads, so
     its threads stride over the handed-over list) and 48 rows nested 34-60

@@ -116,6 +116,18 @@ def test_emulated_workloads(emu, workload, cus):
     check(emu, tok, st, ln, co, cus=cus, what="%s cus %d" % (workload, cus))
 
 
+@pytest.mark.parametrize("n", [2048, 2056])
+def test_emulated_plan_boundary(emu, n):
+    """With 64 emulated units a batch of 2,048 rows takes rows_par with the
+    plan made by the scan blocks, one of 2,056 rows takes rows_par after the
+    plan launch (short rows, so the batch stays small)."""
+    streams = adversarial_streams()
+    streams = [streams[i % len(streams)] for i in range(n)]
+    tokens, starts, lengths = pack(streams, TAGS)
+    correct = (np.arange(n) % 3 != 0).astype(np.uint8)
+    check(emu, tokens, starts, lengths, correct, cus=MANY, what="plan boundary %d" % n)
+
+
 @pytest.mark.parametrize("tags", ["contiguous", "scattered", "scattered-compare", "low-ids"])
 @pytest.mark.parametrize("cus", [16, FEW])
 def test_emulated_adversarial(emu, tags, cus):
