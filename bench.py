@@ -350,6 +350,9 @@ def main():
     print(json.dumps(res), flush=True)
 
 
+GRAPH_CALLS = 8  # accounting calls per captured graph in time_small_batch
+
+
 def time_small_batch(workload, coef, steps, warmup):
     """Whole-step time of the accounting path on a small batch (wall clock
     around `steps` calls, inputs resident)."""
@@ -369,22 +372,43 @@ def time_small_batch(workload, coef, steps, warmup):
     ws = px.alloc_workspace(n, n_tok, dev)
     stream = torch.cuda.current_stream(dev).cuda_stream
 
-    def step():
+    def step(stream):
         rc = px.run_raw(tokens.data_ptr(), starts.data_ptr(), lengths.data_ptr(), correct.data_ptr(), n, out,
                         ws.data_ptr(), ws.numel(), stream)
         if rc != PX.OK:
             raise PX.ParasonError(rc, "parason_run")
 
     for _ in range(warmup):
-        step()
+        step(stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
-        step()
+        step(stream)
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
+    eager = {k: out[k].clone() for k in ("reward", "flags", "latency", "total")}
+    # the same call inside a HIP graph, as in a trainer that captures its whole
+    # step (the call allocates nothing and records no memset): GRAPH_CALLS calls
+    # captured in one graph and replayed, checked against the eager outputs
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(GRAPH_CALLS):
+            step(torch.cuda.current_stream(dev).cuda_stream)
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    reps = max(1, steps // GRAPH_CALLS)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        graph.replay()
+    torch.cuda.synchronize()
+    graph_ms = (time.perf_counter() - t0) * 1e3 / (reps * GRAPH_CALLS)
+    for k, v in eager.items():
+        if not torch.equal(out[k], v):
+            raise RuntimeError("graph replay of the %s step differs from the eager step in %s" % (workload, k))
     return {"workload": "%s: %d groups x %d rollouts, %d rows, %d tokens" % (workload, n // G, G, n, n_tok),
-            "ms_per_step": ms, "tokens_per_s": n_tok / (ms * 1e-3), "rows_per_s": n / (ms * 1e-3)}
+            "ms_per_step": ms, "tokens_per_s": n_tok / (ms * 1e-3), "rows_per_s": n / (ms * 1e-3),
+            "hip_graph_ms_per_call": graph_ms, "hip_graph_calls_per_replay": GRAPH_CALLS}
 
 
 def bench_pg(args):
