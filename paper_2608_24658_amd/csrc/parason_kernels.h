@@ -1245,8 +1245,9 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
  * t), then an exclusive scan with each thread over SCAN_PLAN_ROWS /
  * SCAN_THREADS consecutive rows.  Block 0 also writes the plan to seg_off for
  * the row kernels, clears the mode of rows without segments (no scan wave
- * sees them) and the counters; every other row's mode is cleared by the wave
- * holding its first segment. */
+ * sees them; all rows when the batch overflows the workspace) and the
+ * counters; every other row's mode is cleared by the wave holding its first
+ * segment. */
 __device__ __forceinline__ void scan_plan(const ScanArgs &a, int64_t *off, int64_t *part)
 {
     constexpr int RPT = SCAN_PLAN_ROWS / SCAN_THREADS;
@@ -1279,10 +1280,13 @@ __device__ __forceinline__ void scan_plan(const ScanArgs &a, int64_t *off, int64
     if (t == 0) off[a.n] = total; /* rows beyond n are not rewritten, so no other thread writes off[n] */
     __syncthreads();
     if (blockIdx.x == 0) {
+        /* when the batch overflows the workspace no scan wave runs, so every
+         * mode byte is cleared here */
+        const bool overflow = off[a.n] > a.seg_cap;
         int64_t *seg_off = const_cast<int64_t *>(a.seg_off);
         for (int64_t r = t; r <= a.n; r += SCAN_THREADS) {
             seg_off[r] = off[r];
-            if (r < a.n && off[r + 1] == off[r]) a.mode[r] = 0;
+            if (r < a.n && (overflow || off[r + 1] == off[r])) a.mode[r] = 0;
         }
         if (t < 4) a.counters[t] = 0;
     }
