@@ -146,15 +146,16 @@ int parason_fork(const parason_handle *h, const int32_t *tokens, const int64_t *
     ps.report = 2; /* totals = workers, context tokens, over */
     ps.over = (int32_t *)(ws + L.over);
 
-    const unsigned wave_blocks = (unsigned)std::min<int64_t>((n_rows + 3) / 4, (int64_t)cus * 8);
-    if (n_rows > 0) hipLaunchKernelGGL(pk::fork_outline<false>, dim3(wave_blocks), dim3(256), 0, stream, fa);
+    const unsigned wave_blocks = (unsigned)std::min<int64_t>((n_rows + pk::OUTLINE_WAVES - 1) / pk::OUTLINE_WAVES,
+                                                             (int64_t)cus * (32 / pk::OUTLINE_WAVES));
+    if (n_rows > 0) hipLaunchKernelGGL(pk::fork_outline<false>, dim3(wave_blocks), dim3(pk::OUTLINE_WAVES * pk::WAVE), 0, stream, fa);
     if (n_rows <= pk::FORK_SINGLE) {
         /* scans and records in one launch (at least one block: it writes the totals) */
         const unsigned blocks = (unsigned)std::max<int64_t>(1, (n_rows + pk::FORK_REC_WAVES - 1) / pk::FORK_REC_WAVES);
         hipLaunchKernelGGL(pk::fork_records, dim3(blocks), dim3(pk::FORK_REC_THREADS), 0, stream, fa, ps);
     } else {
         launch_pack(ps, L.tiles, stream);
-        hipLaunchKernelGGL(pk::fork_outline<true>, dim3(wave_blocks), dim3(256), 0, stream, fa);
+        hipLaunchKernelGGL(pk::fork_outline<true>, dim3(wave_blocks), dim3(pk::OUTLINE_WAVES * pk::WAVE), 0, stream, fa);
     }
     if (n_rows > 0) {
         const unsigned copy_blocks = (unsigned)(cus * COPY_BLOCKS_PER_CU); /* persistent, tiled over the output */

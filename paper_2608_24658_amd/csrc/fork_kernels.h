@@ -60,6 +60,10 @@ constexpr int CHUNK_J = PARASON_OUTLINE_LOADS; /* loads per lane per step of the
 constexpr int CHUNK = CHUNK_J * WAVE;          /* tokens per wave step of the outline walk */
 constexpr int COPY_GROUP = 8;   /* worker contexts fork_copy writes from one read of a row tile */
 constexpr int SUMM_ENTRIES = 8; /* outline entries per row the first walk keeps for the second */
+#ifndef PARASON_OUTLINE_WAVES
+#define PARASON_OUTLINE_WAVES 4
+#endif
+constexpr int OUTLINE_WAVES = PARASON_OUTLINE_WAVES; /* waves (rows at a time) per fork_outline block */
 constexpr int JOIN_UNROLL = 4;  /* workers of a row whose records join_size loads together */
 constexpr int JOIN_SINGLE = 1024; /* rows up to which join_copy scans the joined lengths itself */
 /* join_size: small blocks spread its scattered loads of worker tokens over
@@ -495,14 +499,14 @@ __device__ __forceinline__ void outline_row(const ForkArgs &a, int64_t i, int64_
 /* One wave per row (grid-stride).  WRITE = false: status and counts;
  * WRITE = true: the worker records of rows whose outline is well formed. */
 template <bool WRITE>
-__global__ void __launch_bounds__(256) fork_outline(ForkArgs a)
+__global__ void __launch_bounds__(OUTLINE_WAVES * WAVE) fork_outline(ForkArgs a)
 {
-    __shared__ uint32_t ev_all[4][CHUNK]; /* per wave: (offset in chunk << 4) | class, in position order */
+    __shared__ uint32_t ev_all[OUTLINE_WAVES][CHUNK]; /* per wave: (offset in chunk << 4) | class, in position order */
     const int lane = threadIdx.x & (WAVE - 1);
     const int wv = threadIdx.x / WAVE;
     if (WRITE && a.over[0]) return;
-    const int64_t n_waves = (int64_t)gridDim.x * 4;
-    for (int64_t i = uniform64((int64_t)blockIdx.x * 4 + wv); i < a.n; i += n_waves)
+    const int64_t n_waves = (int64_t)gridDim.x * OUTLINE_WAVES;
+    for (int64_t i = uniform64((int64_t)blockIdx.x * OUTLINE_WAVES + wv); i < a.n; i += n_waves)
         outline_row<WRITE>(a, i, WRITE ? a.worker_off[i] : 0, WRITE ? a.tok_off[i] : 0, ev_all[wv], lane);
 }
 
