@@ -249,6 +249,9 @@ struct SegCursor {
     int64_t row, row_first, row_next;
     int64_t g, vrow0, vend;
     int32_t len;
+    int32_t nvec;  /* vectors of the row: vend - vrow0 (rows are shorter than 2^31 tokens) */
+    int32_t head;  /* row position 0 relative to the row's first vector element: 0 .. 31 */
+    bool owned_row;
     bool loaded;
 
     /* Called by the whole wave. */
@@ -285,8 +288,17 @@ struct SegCursor {
             len = __builtin_amdgcn_readfirstlane(lengths[row]);
             vrow0 = row_first_vec(g);
             vend = row_end_vec(g, len);
+            nvec = (int32_t)(vend - vrow0);
+            head = (int32_t)(g - 4 * vrow0);
+            /* LDS events hold (position << 4 | class) in 32 bits */
+            owned_row = row_first >= s_begin && row_next <= s_end && len < (1 << 27);
             loaded = true;
         }
+        /* the segment relative to the row, in 32 bits (a row has fewer than
+         * 2^21 segments); only the absolute vector indices are 64-bit */
+        const int32_t k = (int32_t)(s - row_first);
+        const int32_t v0r = k * SEG_VEC;
+        const int32_t v1r = min(v0r + SEG_VEC, nvec);
         SegView w;
         w.s = s;
         w.row = row;
@@ -294,15 +306,15 @@ struct SegCursor {
         w.last = row_next - 1;
         w.g = g;
         w.len = len;
-        w.v0 = vrow0 + (s - row_first) * SEG_VEC;
-        w.v1 = min(w.v0 + (int64_t)SEG_VEC, vend);
-        w.edge = w.v0 == vrow0 || w.v1 == vend;
-        /* row positions g .. g+len-1 relative to the segment's first element */
-        const int64_t lo = g - 4 * w.v0, hi = g + (int64_t)len - 4 * w.v0;
-        w.q_lo = (int32_t)max((int64_t)0, lo);
-        w.q_hi = (int32_t)min((int64_t)4 * (w.v1 - w.v0), hi);
-        /* LDS events hold (position << 4 | class) in 32 bits */
-        w.owned = row_first >= s_begin && row_next <= s_end && len < (1 << 27);
+        w.v0 = vrow0 + v0r;
+        w.v1 = vrow0 + v1r;
+        w.edge = k == 0 || v1r == nvec;
+        /* row positions 0 .. len-1 relative to the segment's first element:
+         * they start inside the first segment only (head < 32) and end inside
+         * the last one only, so every other segment is whole */
+        w.q_lo = k == 0 ? head : 0;
+        w.q_hi = v1r == nvec ? (int32_t)((int64_t)head + len - 4 * (int64_t)v0r) : 4 * (v1r - v0r);
+        w.owned = owned_row;
         return w;
     }
 };
