@@ -1107,16 +1107,17 @@ __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_l
     }
 }
 
-__device__ __forceinline__ void issue_loads(int4 (&x)[LOADS], const int4 *src, const SegView &w, int lane)
+__device__ __forceinline__ void issue_loads(int4 (&x)[LOADS], const int4 *src, int64_t v0, int64_t v1, bool edge,
+                                            int lane)
 {
-    const int4 *p = src + w.v0 + lane;
-    if (!w.edge) {
+    const int4 *p = src + v0 + lane;
+    if (!edge) {
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) x[i] = load_vec(p + i * WAVE);
     } else {
 #pragma unroll
         for (int i = 0; i < LOADS; ++i)
-            x[i] = (w.v0 + i * WAVE + lane < w.v1) ? load_vec(p + i * WAVE) : make_int4(-1, -1, -1, -1);
+            x[i] = (v0 + i * WAVE + lane < v1) ? load_vec(p + i * WAVE) : make_int4(-1, -1, -1, -1);
     }
 }
 
@@ -1335,28 +1336,30 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES, PARASON_SCAN_WAVES_PER_SIMD
     rc.pc = __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)s_begin + extra * (uint32_t)wave);
     rc.p_end =
         __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)s_end + extra * (uint32_t)(wave + 1));
-    SegView w = cur.view(s_begin);
     /* two register buffers: segment s + 1 is in flight while s is compacted */
+    SegView w = cur.view(s_begin);
     int4 xa[LOADS], xb[LOADS];
-    issue_loads(xa, src, w, lane);
+    issue_loads(xa, src, w.v0, w.v1, w.edge, lane);
     int64_t s = s_begin;
     while (true) {
         SegView wn;
         bool more = s + 1 < s_end;
         if (more) {
             wn = cur.view(s + 1);
-            issue_loads(xb, src, wn, lane);
+            issue_loads(xb, src, wn.v0, wn.v1, wn.edge, lane);
         }
-        if (collect_segment<MODE, PLAN>(a, xa, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
+        if (collect_segment<MODE, PLAN>(a, xa, w, rc, lev, tab, lane))
+            flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
         if (!more) break;
         ++s;
         w = wn;
         more = s + 1 < s_end;
         if (more) {
             wn = cur.view(s + 1);
-            issue_loads(xa, src, wn, lane);
+            issue_loads(xa, src, wn.v0, wn.v1, wn.edge, lane);
         }
-        if (collect_segment<MODE, PLAN>(a, xb, w, rc, lev, tab, lane)) flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
+        if (collect_segment<MODE, PLAN>(a, xb, w, rc, lev, tab, lane))
+            flush_row(a, w.row, w.first, w.last, rc.lcnt, lev, rc, lane);
         if (!more) break;
         ++s;
         w = wn;
