@@ -65,8 +65,8 @@ constexpr int64_t DEEP_ENTRY_BITS = PARASON_MAX_OPEN_ENTRIES;
 /* A row nests at most one level per 6 tokens and opens at most one outline
  * entry per 3, so a store of these per 1024-token segment of the batch holds
  * any row (up to DEEP_FRAMES and DEEP_ENTRY_BITS). */
-constexpr int64_t DEEP_FRAMES_PER_SEG = 1024 / 6 + 1;
-constexpr int64_t DEEP_BITS_PER_SEG = 1024 / 3 + 1;
+constexpr int64_t DEEP_FRAMES_PER_SEG = SEG_TOK / 6 + 1;
+constexpr int64_t DEEP_BITS_PER_SEG = SEG_TOK / 3 + 1;
 
 /* Token classes: 0 = Text, 1..12 = tags in tag_ids order. */
 enum : uint32_t {

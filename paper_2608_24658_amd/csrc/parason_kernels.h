@@ -1055,7 +1055,17 @@ __device__ __forceinline__ bool is_tag(const TagMatch &tm, int32_t t, int32_t ta
     return h;
 }
 
-__device__ __forceinline__ uint32_t lane_bit(uint64_t mask, int lane) { return (uint32_t)(mask >> lane) & 1u; }
+/* The class of a token known to be a tag: for contiguous ids one shift of
+ * the 64-bit nibble table (the id is base + o with o < 12). */
+template <int MODE>
+__device__ __forceinline__ uint32_t tag_class(const TagMatch &tm, int32_t t)
+{
+    if (MODE == TM_CONTIG) {
+        const uint64_t lut = (uint64_t)tm.lut_hi << 32 | tm.lut_lo;
+        return (uint32_t)(lut >> (4u * ((uint32_t)t - (uint32_t)tm.base))) & 15u;
+    }
+    return classify(tm, t, false);
+}
 
 /* Tags of the LOADS vectors x[i] (vector v0 + i*WAVE + lane of this lane) are
  * appended to dst[0 .. cap) in position order as (q + bias) << 4 | class, where
@@ -1080,28 +1090,26 @@ __device__ __forceinline__ void scan_vectors(const int4 (&x)[LOADS], int32_t q_l
         }
         const int32_t q0 = 4 * (i * WAVE + lane);
         uint64_t b[4];
+        uint32_t mine = 0; /* this lane's tags, bit j for token j */
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             bool hit = is_tag<MODE>(tm, t[j], tab);
             if (EDGE) hit = hit && q0 + j >= q_lo && q0 + j < q_hi;
             b[j] = __ballot(hit);
+            mine |= hit ? 1u << j : 0u;
         }
         if ((b[0] | b[1] | b[2] | b[3]) == 0) continue; /* wave-uniform: most vectors hold no tag */
         uint32_t pre = 0;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             pre = __builtin_amdgcn_mbcnt_hi((uint32_t)(b[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b[j], pre));
-        const uint32_t mine = lane_bit(b[0], lane) | lane_bit(b[1], lane) << 1 | lane_bit(b[2], lane) << 2 |
-                              lane_bit(b[3], lane) << 3;
-        if (mine) {
-            uint32_t idx = cnt + pre;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (mine & (1u << j)) {
-                    if (idx < cap) dst[idx] = ((uint32_t)(q0 + j + bias) << 4) | classify(tm, t[j], MODE == TM_CONTIG);
-                    ++idx;
-                }
-            }
+        /* the lane's tags in position order, one store each (a lane almost
+         * never holds more than one tag of a vector) */
+        for (uint32_t idx = cnt + pre; mine != 0; ++idx) {
+            const uint32_t j = (uint32_t)__builtin_ctz(mine);
+            mine &= mine - 1u;
+            const int32_t tj = j == 0 ? t[0] : j == 1 ? t[1] : j == 2 ? t[2] : t[3];
+            if (idx < cap) dst[idx] = ((uint32_t)(q0 + (int32_t)j + bias) << 4) | tag_class<MODE>(tm, tj);
         }
         cnt += (uint32_t)(__popcll(b[0]) + __popcll(b[1]) + __popcll(b[2]) + __popcll(b[3]));
     }
