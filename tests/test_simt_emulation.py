@@ -15,7 +15,8 @@ pattern and sized exactly, so reliance on its contents or reads past it fail.
 
 Planted mistakes in copies of the kernel sources (an off-by-one in a DPP
 segmented scan, a lost carry in the scan's compaction, a dropped row-edge
-mask, an unreserved pool part) must each be caught by these comparisons."""
+mask, an unreserved pool part, a tag class read from the wrong table nibble)
+must each be caught by these comparisons."""
 import os
 import shutil
 import subprocess
@@ -199,6 +200,9 @@ MUTANTS = {
                   "if (EDGE) hit = hit && q0 + j < q_hi;"),
     # a compact list's pool part is not reserved, so the next list overwrites it
     "pool-cursor": ("parason_kernels.h", "    rc.pc += need;\n}", "    rc.pc += 0 * need;\n}"),
+    # the class of a stored tag read from the neighbouring nibble of the table
+    "tag-class": ("parason_kernels.h", "(lut >> (4u * ((uint32_t)t - (uint32_t)tm.base)))",
+                  "(lut >> (4u * ((uint32_t)t - (uint32_t)tm.base + 1u)))"),
 }
 
 
