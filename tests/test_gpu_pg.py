@@ -147,6 +147,35 @@ def test_pg_layout_gaps_and_misalignment(dev):
         assert np.all(g[~inside] == 7.5)
 
 
+def test_pg_wide_log_ratio(dev):
+    """Log-ratios over [-70, 88]: rows of positive advantage keep the tokens
+    with d <= ln 1.28 (ratios down to 4e-31), rows of negative advantage those
+    with d >= ln 0.8 (ratios up to 1.6e38), so the kept gradients check the
+    kernel's exponential against the oracle's exp in double at the 2^-20 bound
+    over the range where the gradient -A rho / N stays a normal float (below
+    it a kept token's gradient could underflow to the zero that marks a
+    clipped one)."""
+    log("case pg wide log-ratio")
+    rng = np.random.default_rng(11)
+    n, row_len = 64, 16384
+    d = rng.permutation(np.linspace(-70.0, 88.0, n * row_len).astype(np.float32))
+    old_h = np.where(np.arange(d.size) % 2 == 0, np.float32(0.0), np.float32(-3.0)).astype(np.float32)
+    new_h = (old_h + d).astype(np.float32)
+    starts = (np.arange(n) * row_len).astype(np.int64)
+    lengths = np.full(n, row_len, np.int32)
+    reward = np.tile(np.array([1.0, 0.0], np.float32), n // 2)  # A = +1, -1 alternately
+    got = PX.pg_run(to_dev(reward, torch.float32, dev), to_dev(new_h, torch.float32, dev),
+                    to_dev(old_h, torch.float32, dev), to_dev(starts, torch.int64, dev),
+                    to_dev(lengths, torch.int32, dev), G, EPS_LO, EPS_HI)
+    torch.cuda.synchronize()
+    adv_exp = PG.advantages(reward, G)
+    assert set(np.unique(adv_exp).tolist()) == {-1.0, 1.0}
+    exp = PG.surrogate(new_h, old_h, starts, lengths, adv_exp.astype(np.float32), EPS_LO, EPS_HI)
+    g, _ = check(got, exp, adv_exp, starts, lengths, "wide log-ratio")
+    kept = g != 0
+    assert np.any(kept & (exp["d"] < -65)) and np.any(kept & (exp["d"] > 80))
+
+
 def test_pg_rejects_bad_arguments(dev):
     log("case pg args")
     t = torch.zeros(64, dtype=torch.float32, device=dev)
