@@ -198,18 +198,20 @@ void launch_rows(const pk::RowArgs &ra, const pk::GatherArgs &ga, int cus, uint8
                            deep_frames, deep_bits);
 }
 
+/* The scan's persistent grid: SCAN_BLOCKS_PER_CU blocks of SCAN_WAVES waves
+ * per CU, or the same waves in blocks of scan_waves<PLAN>(). */
 template <bool PLAN>
-void launch_scan(const pk::TagMatch &tm, const pk::ScanArgs &sa, unsigned scan_blocks, hipStream_t stream)
+void launch_scan(const pk::TagMatch &tm, const pk::ScanArgs &sa, int cus, hipStream_t stream)
 {
+    constexpr int NW = pk::scan_waves<PLAN>();
+    static_assert(SCAN_BLOCKS_PER_CU * pk::SCAN_WAVES % NW == 0, "whole blocks per CU");
+    const dim3 grid((unsigned)(cus * (SCAN_BLOCKS_PER_CU * pk::SCAN_WAVES / NW))), block(pk::WAVE * NW);
     if (tm.contiguous)
-        hipLaunchKernelGGL((pk::scan_rows<pk::TM_CONTIG, PLAN>), dim3(scan_blocks), dim3(pk::SCAN_THREADS), 0, stream,
-                           sa);
+        hipLaunchKernelGGL((pk::scan_rows<pk::TM_CONTIG, PLAN>), grid, block, 0, stream, sa);
     else if (tm.hashed)
-        hipLaunchKernelGGL((pk::scan_rows<pk::TM_HASH, PLAN>), dim3(scan_blocks), dim3(pk::SCAN_THREADS), 0, stream,
-                           sa);
+        hipLaunchKernelGGL((pk::scan_rows<pk::TM_HASH, PLAN>), grid, block, 0, stream, sa);
     else
-        hipLaunchKernelGGL((pk::scan_rows<pk::TM_LINEAR, PLAN>), dim3(scan_blocks), dim3(pk::SCAN_THREADS), 0, stream,
-                           sa);
+        hipLaunchKernelGGL((pk::scan_rows<pk::TM_LINEAR, PLAN>), grid, block, 0, stream, sa);
 }
 
 }  // namespace
@@ -376,12 +378,11 @@ int parason_run_timed(const parason_handle *h, const int32_t *tokens, const int6
     sa.split_count = counters + 2;
     sa.split_rows = split_rows;
     sa.counters = counters;
-    const unsigned scan_blocks = (unsigned)(cus * SCAN_BLOCKS_PER_CU);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[0], stream) != hipSuccess) return PARASON_ERR_HIP;
     if (plan_in_scan)
-        launch_scan<true>(h->tm, sa, scan_blocks, stream);
+        launch_scan<true>(h->tm, sa, cus, stream);
     else
-        launch_scan<false>(h->tm, sa, scan_blocks, stream);
+        launch_scan<false>(h->tm, sa, cus, stream);
     if (scan_events && hipEventRecord((hipEvent_t)scan_events[1], stream) != hipSuccess) return PARASON_ERR_HIP;
 
     pk::RowArgs ra;

@@ -14,8 +14,9 @@ the single-thread deep tier.  The workspace is handed over filled with a byte
 pattern and sized exactly, so reliance on its contents or reads past it fail.
 
 Planted mistakes in copies of the kernel sources (an off-by-one in a DPP
-segmented scan, a lost carry in the scan's compaction, a dropped row-edge
-mask, an unreserved pool part, a tag class read from the wrong table nibble)
+segmented scan, a carry lost inside a lane's events of rows_par's segmented
+scan, a lost carry in the scan's compaction, a dropped row-edge mask, an
+unreserved pool part, a tag class read from the wrong table nibble)
 must each be caught by these comparisons."""
 import os
 import shutil
@@ -194,6 +195,10 @@ MUTANTS = {
     "compaction-carry": ("parason_kernels.h",
                          "cnt += (uint32_t)(__popcll(b[0]) + __popcll(b[1])",
                          "cnt += (uint32_t)(0 + __popcll(b[1])"),
+    # the per-lane form of the segmented scan drops the carry into a lane's
+    # second to fourth events (rows_par, four events per lane)
+    "lane-carry": ("parason_kernels.h", "if (!seen) v[k] = Op::f(in, v[k]);",
+                   "if (!seen && k == 0) v[k] = Op::f(in, v[k]);"),
     # a row's edge segments keep tags of the neighbouring rows
     "edge-mask": ("parason_kernels.h",
                   "if (EDGE) hit = hit && q0 + j >= q_lo && q0 + j < q_hi;",
