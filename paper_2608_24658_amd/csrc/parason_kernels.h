@@ -884,7 +884,8 @@ __device__ __forceinline__ void par_seg_scan(int32_t (&v)[PAR_K], const bool (&h
  *     length less the saved tokens of its top-level blocks; a thread's own
  *     tokens (its tokens less those of the threads nested in it) take the
  *     type of the outline entry it pairs with.  Evaluated level by level,
- *     deepest first, with segmented scans (phase B).
+ *     deepest first, with segmented scans, one pass over the events per
+ *     level (phase B).
  * Rows holding more than PAR_EVENTS events, nested deeper than PAR_LEVELS,
  * or with a dense segment, run through the automaton on lane 0 (the single
  * automaton call site of this kernel).  Split rows are read from their
@@ -939,38 +940,66 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
             }
         }
     } else {
+        /* PAR_PASS segments at a time, four per lane: their records in one
+         * round of loads and an exclusive scan of their counts; then an LDS
+         * map from event to segment (each segment that holds events marks its
+         * first event, a running maximum spreads the marks) and the events'
+         * loads in one round per PAR_PASS events.  Until phase A, sD holds the
+         * map and sLAT, sOWN each segment's first slot and first event. */
         const int64_t vrow0 = row_first_vec(g);
-        for (int64_t c0 = s0; held && c0 < s1; c0 += WAVE) {
-            const int64_t s = c0 + lane;
-            const SegRec rec = s < s1 ? a.seg[s] : SegRec{0, 0u};
-            const int32_t cnt = rec.count;
-            const uint32_t list = rec.list; /* meaningless for a segment without events */
-            const int32_t incl = wave_incl_scan32(cnt, lane); /* DENSE counts cannot overflow it */
-            const int32_t excl = incl - cnt;
-            const int32_t total = lane63(incl);
+        for (int64_t c0 = s0; held && c0 < s1; c0 += PAR_PASS) {
+            const int32_t jb = PAR_K * lane; /* the chunk's segment of element 0 */
+            int32_t cnt[PAR_K], lst[PAR_K], incl[PAR_K];
+            bool dense = false;
+#pragma unroll
+            for (int k = 0; k < PAR_K; ++k) {
+                const int64_t s = c0 + jb + k;
+                const SegRec rec = s < s1 ? a.seg[s] : SegRec{0, 0u};
+                cnt[k] = rec.count;
+                lst[k] = (int32_t)rec.list; /* meaningless for a segment without events */
+                incl[k] = cnt[k];
+                dense = dense || cnt[k] == DENSE;
+            }
+            par_incl_scan<OpAdd>(incl, 0, lane); /* DENSE counts cannot overflow it */
+            const int32_t total = lane63(incl[PAR_K - 1]);
             /* a dense segment or too many events: the automaton below */
-            held = __ballot(cnt == DENSE) == 0 && m + total <= PAR_EVENTS;
-            for (int32_t f0 = 0; held && f0 < total; f0 += 2 * WAVE) { /* two loads per lane in flight */
-                int32_t j[2];
-                uint32_t w[2];
+            held = __ballot(dense) == 0 && m + total <= PAR_EVENTS;
+            if (!held || total == 0) continue;
+            for (int32_t f0 = 0; f0 < total; f0 += PAR_PASS) par_store(sD, f0 + jb, {-1, -1, -1, -1});
+            __syncthreads();
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    const int32_t f = f0 + u * WAVE + lane;
-                    j[u] = last_lane_at_most(excl, f);
-                    const int32_t first = __shfl(excl, j[u], WAVE);
-                    const uint32_t lj = __shfl(list, j[u], WAVE);
-                    w[u] = f < total ? a.slots[(int64_t)lj + (f - first)] : 0u;
-                }
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    const int32_t f = f0 + u * WAVE + lane;
-                    if (f < total) {
-                        const int64_t seg = c0 + j[u];
-                        sP[m + f] = (int32_t)(4 * (vrow0 + (seg - s0) * SEG_VEC) - g + (int64_t)(w[u] >> 4));
-                        sC[m + f] = (int32_t)(w[u] & 15u);
-                    }
+            for (int k = 0; k < PAR_K; ++k) {
+                if (cnt[k] > 0) {
+                    const int32_t e0 = incl[k] - cnt[k];
+                    sD[e0] = jb + k;
+                    sLAT[jb + k] = lst[k];
+                    sOWN[jb + k] = e0;
                 }
             }
+            __syncthreads();
+            int32_t carry = -1;
+            for (int32_t f0 = 0; f0 < total; f0 += PAR_PASS) {
+                int32_t j[PAR_K];
+                uint32_t w[PAR_K];
+                par_load(sD, f0 + jb, j);
+                par_incl_scan<OpMax>(j, carry, lane); /* every event's segment (position 0 is marked) */
+#pragma unroll
+                for (int k = 0; k < PAR_K; ++k) {
+                    const int32_t f = f0 + jb + k, jj = max(j[k], 0);
+                    w[k] = f < total ? a.slots[(int64_t)(uint32_t)sLAT[jj] + (f - sOWN[jj])] : 0u;
+                }
+#pragma unroll
+                for (int k = 0; k < PAR_K; ++k) {
+                    const int32_t f = f0 + jb + k;
+                    if (f < total) {
+                        const int64_t seg = c0 + j[k];
+                        sP[m + f] = (int32_t)(4 * (vrow0 + (seg - s0) * SEG_VEC) - g + (int64_t)(w[k] >> 4));
+                        sC[m + f] = (int32_t)(w[k] & 15u);
+                    }
+                }
+                carry = lane63(j[PAR_K - 1]);
+            }
+            __syncthreads(); /* the next chunk rewrites the map */
             m += total;
         }
     }
@@ -1077,8 +1106,11 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
     int32_t my_sub = 0, my_tri = 0, my_saved = 0;
     bool my_mismatch = false;
     for (int32_t lev = max_depth; lev >= 1; --lev) {
-        /* threads of level lev: tokens, latency, own tokens */
+        /* one pass per level: the threads of level lev (tokens, latency, own
+         * tokens), then, from those values still in registers, the blocks of
+         * level lev (saved tokens, thread types, count mismatch) */
         int32_t c_thr = -1, c_S = 0, c_CH = 0;
+        int32_t c_sum = 0, c_max = 0, c_n = 0, c_par = -1, c_eout = -1;
         for (int32_t i0 = 0; i0 < m; i0 += PAR_PASS) {
             const int32_t ib = i0 + PAR_K * lane;
             int32_t c[PAR_K], db[PAR_K], tb[PAR_K], sav[PAR_K], tk[PAR_K];
@@ -1087,8 +1119,8 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
             par_load(sT, ib, tb);
             par_load(sSAV, ib, sav);
             par_load(sTOK, ib, tk);
-            bool thr[PAR_K], ethr[PAR_K];
-            int32_t ti[PAR_K], S[PAR_K], CH[PAR_K];
+            bool thr[PAR_K], ethr[PAR_K], par[PAR_K], epar[PAR_K];
+            int32_t ti[PAR_K], S[PAR_K], CH[PAR_K], pi[PAR_K], oi[PAR_K];
 #pragma unroll
             for (int k = 0; k < PAR_K; ++k) {
                 const bool act = ib + k < m;
@@ -1096,59 +1128,33 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
                 ethr[k] = act & (c[k] == C_END_THR) & (tb[k] == lev);
                 const bool epar_in = act & (c[k] == C_END_PAR) & (db[k] == lev + 1);
                 const bool ethr_in = act & (c[k] == C_END_THR) & (tb[k] == lev + 1);
-                ti[k] = thr[k] ? ib + k : -1;
-                S[k] = epar_in ? sav[k] : 0;
-                CH[k] = ethr_in ? tk[k] : 0;
-            }
-            par_incl_scan<OpMax>(ti, c_thr, lane); /* the thread each event is in */
-            par_seg_scan<OpAdd>(S, thr, c_S, lane);
-            par_seg_scan<OpAdd>(CH, thr, c_CH, lane);
-#pragma unroll
-            for (int k = 0; k < PAR_K; ++k) {
-                if (ethr[k]) {
-                    const int32_t i = ib + k;
-                    const int32_t tok = sP[i] - sP[ti[k]] + 1;
-                    sTOK[i] = tok;
-                    sLAT[i] = tok - S[k];
-                    sOWN[i] = tok - CH[k];
-                }
-            }
-            c_thr = lane63(ti[PAR_K - 1]);
-            c_S = lane63(S[PAR_K - 1]);
-            c_CH = lane63(CH[PAR_K - 1]);
-        }
-        __syncthreads();
-        /* blocks of level lev: saved tokens, thread types, count mismatch */
-        int32_t c_sum = 0, c_max = 0, c_n = 0, c_par = -1, c_eout = -1;
-        for (int32_t i0 = 0; i0 < m; i0 += PAR_PASS) {
-            const int32_t ib = i0 + PAR_K * lane;
-            int32_t c[PAR_K], db[PAR_K], tb[PAR_K], tk[PAR_K], lt[PAR_K], own[PAR_K];
-            par_load(sC, ib, c);
-            par_load(sD, ib, db);
-            par_load(sT, ib, tb);
-            par_load(sTOK, ib, tk);
-            par_load(sLAT, ib, lt);
-            par_load(sOWN, ib, own);
-            bool par[PAR_K], epar[PAR_K], ethr[PAR_K];
-            int32_t sum[PAR_K], mx[PAR_K], nt[PAR_K], pi[PAR_K], oi[PAR_K];
-#pragma unroll
-            for (int k = 0; k < PAR_K; ++k) {
-                const bool act = ib + k < m;
                 par[k] = act & (c[k] == C_PAR) & (db[k] == lev - 1);
                 epar[k] = act & (c[k] == C_END_PAR) & (db[k] == lev);
                 const bool eout = act & (c[k] == C_END_OUT) & (db[k] == lev) & (tb[k] == lev - 1);
-                ethr[k] = act & (c[k] == C_END_THR) & (tb[k] == lev);
-                sum[k] = ethr[k] ? tk[k] : 0;
-                mx[k] = ethr[k] ? lt[k] : 0;
-                nt[k] = ethr[k] ? 1 : 0;
+                ti[k] = thr[k] ? ib + k : -1;
+                S[k] = epar_in ? sav[k] : 0;
+                CH[k] = ethr_in ? tk[k] : 0;
                 pi[k] = par[k] ? ib + k : -1;
                 oi[k] = eout ? ib + k : -1;
+            }
+            par_incl_scan<OpMax>(ti, c_thr, lane);  /* the thread each event is in */
+            par_seg_scan<OpAdd>(S, thr, c_S, lane);
+            par_seg_scan<OpAdd>(CH, thr, c_CH, lane);
+            par_incl_scan<OpMax>(pi, c_par, lane);  /* the block each event is in ... */
+            par_incl_scan<OpMax>(oi, c_eout, lane); /* ... and its outline's end */
+            int32_t sum[PAR_K], mx[PAR_K], nt[PAR_K], own[PAR_K];
+#pragma unroll
+            for (int k = 0; k < PAR_K; ++k) {
+                const int32_t tok = ethr[k] ? sP[ib + k] - sP[max(ti[k], 0)] + 1 : 0;
+                if (ethr[k]) sTOK[ib + k] = tok; /* read by the next level's threads */
+                sum[k] = tok;
+                mx[k] = ethr[k] ? tok - S[k] : 0; /* the thread's latency */
+                own[k] = tok - CH[k];
+                nt[k] = ethr[k] ? 1 : 0;
             }
             par_seg_scan<OpAdd>(sum, par, c_sum, lane);
             par_seg_scan<OpMax>(mx, par, c_max, lane);
             par_seg_scan<OpAdd>(nt, par, c_n, lane);
-            par_incl_scan<OpMax>(pi, c_par, lane);  /* the block each event is in ... */
-            par_incl_scan<OpMax>(oi, c_eout, lane); /* ... and its outline's end */
 #pragma unroll
             for (int k = 0; k < PAR_K; ++k) {
                 const int32_t n_e = (oi[k] - pi[k] - 2) / 2;
@@ -1167,6 +1173,9 @@ __global__ void __launch_bounds__(64) rows_par(RowArgs a, uint8_t *__restrict__ 
                     my_saved += lev == 1 ? saved : 0;
                 }
             }
+            c_thr = lane63(ti[PAR_K - 1]);
+            c_S = lane63(S[PAR_K - 1]);
+            c_CH = lane63(CH[PAR_K - 1]);
             c_sum = lane63(sum[PAR_K - 1]);
             c_max = lane63(mx[PAR_K - 1]);
             c_n = lane63(nt[PAR_K - 1]);

@@ -25,7 +25,8 @@ import subprocess
 import numpy as np
 import pytest
 
-from adversarial import adversarial_streams, pack
+import grammar_pins as GP
+from adversarial import adversarial_streams, deep_stream, fanout_stream, pack
 from gpu_util import DEFAULT_COEF, compare, insert_gaps, oracle_expect
 from oracle import oracle as O
 from paper_2608_24658_amd import parason as PX
@@ -128,6 +129,32 @@ def test_emulated_plan_boundary(emu, n):
     tokens, starts, lengths = pack(streams, TAGS)
     correct = (np.arange(n) % 3 != 0).astype(np.uint8)
     check(emu, tokens, starts, lengths, correct, cus=MANY, what="plan boundary %d" % n)
+
+
+def stretch(stream, total, rng):
+    """The stream with Text runs inserted after tags that Text may follow
+    (<think>, </Parallel>, <Thread>, entry openings), about `total` tokens in
+    all, so that its events spread over hundreds of segments."""
+    spots = [i for i, c in enumerate(stream) if c in (GP.THINK, GP.END_PAR, GP.THR, GP.SUB, GP.TRI)]
+    runs = rng.multinomial(total, np.ones(len(spots)) / len(spots))
+    out, last = [], 0
+    for i, r in zip(spots, runs):
+        out += stream[last: i + 1] + [GP.TEXT] * int(r)
+        last = i + 1
+    return out + stream[last:]
+
+
+def test_emulated_long_split_rows(emu):
+    """Rows of 270k-600k tokens whose events spread over more than 256 (and 512)
+    segments, so that rows_par gathers a split row in several chunks of
+    segments, some rows with more than 256 events (two event passes)."""
+    rng = np.random.default_rng(3)
+    streams = [stretch(fanout_stream(40), 300000, rng), stretch(deep_stream(4), 280000, rng),
+               stretch(fanout_stream(70), 600000, rng), stretch(fanout_stream(100, 90), 270000, rng),
+               stretch(deep_stream(12, GP.TRI), 330000, rng), stretch(fanout_stream(3), 520000, rng)]
+    tokens, starts, lengths = pack(streams, TAGS)
+    correct = (np.arange(lengths.size) % 2 == 0).astype(np.uint8)
+    check(emu, tokens, starts, lengths, correct, cus=MANY, what="long split rows")
 
 
 @pytest.mark.parametrize("tags", ["contiguous", "scattered", "scattered-compare", "low-ids"])
