@@ -7,8 +7,9 @@
  * fork
  *   fork_outline<false>  one wave per row: checks that the row ends with
  *                        </Outlines>, searches backwards for the outline's
- *                        <Outlines>, then walks the outline forwards in
- *                        256-token chunks, compacting its tags in order with
+ *                        <Outlines> (512 tokens a step), then walks the
+ *                        outline forwards in 256-token chunks (the next
+ *                        chunk's loads in flight), compacting its tags in order with
  *                        ballots and checking each against the one before it
  *                        (entries open, hold text, close, back to back).
  *                        Writes the row's worker and token counts.
@@ -58,6 +59,13 @@ constexpr int PACK_TILE = PACK_THREADS * PACK_ROWS_PER_THREAD;
 #endif
 constexpr int CHUNK_J = PARASON_OUTLINE_LOADS; /* loads per lane per step of the outline walk */
 constexpr int CHUNK = CHUNK_J * WAVE;          /* tokens per wave step of the outline walk */
+#ifndef PARASON_BACK_LOADS
+#define PARASON_BACK_LOADS 8
+#endif
+/* The backward search for the outline's start looks for two tags only, so its
+ * steps are longer: one round of loads covers most outlines. */
+constexpr int BACK_J = PARASON_BACK_LOADS; /* loads per lane per step of the backward search */
+constexpr int BACK = BACK_J * WAVE;
 constexpr int COPY_GROUP = 8;   /* worker contexts fork_copy writes from one read of a row tile */
 constexpr int SUMM_ENTRIES = 8; /* outline entries per row the first walk keeps for the second */
 #ifndef PARASON_OUTLINE_WAVES
@@ -283,22 +291,42 @@ __device__ __forceinline__ int64_t wave_incl_scan(int64_t v, int lane)
     return v;
 }
 
+/* Token p of the row at g for p < end, else 0 (end >= 1).  The load is
+ * unconditional, at min(p, end - 1), and the value selected after it: a load
+ * under a condition is a branch, and the wave waits for it before the next
+ * one, so J conditional loads cost J round trips instead of one. */
+__device__ __forceinline__ int32_t row_token(const ForkArgs &a, int64_t g, int64_t p, int64_t end)
+{
+    const int32_t t = a.tokens[g + min(p, end - 1)];
+    return p < end ? t : 0;
+}
+
 /* Position of the last tag before position o of the row at g (-1 if none);
  * called by a whole wave. */
 __device__ __forceinline__ int64_t last_tag_before(const ForkArgs &a, int64_t g, int64_t o, int lane, bool contig)
 {
     for (int64_t e = o; e > 0; e -= CHUNK) {
         const int64_t lo = e > CHUNK ? e - CHUNK : 0;
-        int32_t best = -1;
+        int32_t best = -1, tk[CHUNK_J];
+#pragma unroll
+        for (int j = 0; j < CHUNK_J; ++j) tk[j] = row_token(a, g, lo + lane + WAVE * j, e);
 #pragma unroll
         for (int j = 0; j < CHUNK_J; ++j) {
             const int64_t p = lo + lane + WAVE * j;
-            if (p < e && classify(a.tm, a.tokens[g + p], contig) != C_TEXT) best = (int32_t)p > best ? (int32_t)p : best;
+            if (p < e && classify(a.tm, tk[j], contig) != C_TEXT) best = (int32_t)p > best ? (int32_t)p : best;
         }
         best = wave_max_pos(best, lane);
         if (best >= 0) return best;
     }
     return -1;
+}
+
+/* Tokens lo + lane + WAVE * j of the row at g below end (0 beyond), end >= 1. */
+__device__ __forceinline__ void outline_tokens(const ForkArgs &a, int64_t g, int64_t lo, int64_t end,
+                                               int32_t (&tk)[CHUNK_J], int lane)
+{
+#pragma unroll
+    for (int j = 0; j < CHUNK_J; ++j) tk[j] = row_token(a, g, lo + lane + WAVE * j, end);
 }
 
 /* One row's outline, by one wave.  WRITE = false: status and counts (the
@@ -343,15 +371,18 @@ __device__ __forceinline__ void outline_row(const ForkArgs &a, int64_t i, int64_
          * before it, and the class of the token right before that when it
          * is in the same chunk (1: <Parallel>, 0: not, -1: not seen) */
         int32_t par_before = -1;
-        for (int64_t e = (int64_t)L; st == 0 && e > 0 && o < 0; e -= CHUNK) {
-            const int64_t lo = e > CHUNK ? e - CHUNK : 0;
-            uint32_t c[CHUNK_J];
+        for (int64_t e = (int64_t)L; st == 0 && e > 0 && o < 0; e -= BACK) {
+            const int64_t lo = e > BACK ? e - BACK : 0;
+            uint32_t c[BACK_J];
             int32_t best = -1;
             bool end_mine = false;
+            int32_t tk[BACK_J];
 #pragma unroll
-            for (int j = 0; j < CHUNK_J; ++j) {
+            for (int j = 0; j < BACK_J; ++j) tk[j] = row_token(a, g, lo + lane + WAVE * j, e);
+#pragma unroll
+            for (int j = 0; j < BACK_J; ++j) {
                 const int64_t p = lo + lane + WAVE * j;
-                c[j] = p < e ? classify(a.tm, a.tokens[g + p], contig) : C_TEXT;
+                c[j] = p < e ? classify(a.tm, tk[j], contig) : C_TEXT;
                 if (p < (int64_t)L - 1 && c[j] == C_OUT) best = (int32_t)p > best ? (int32_t)p : best;
                 end_mine = end_mine || (p == (int64_t)L - 1 && c[j] == C_END_OUT);
             }
@@ -363,7 +394,7 @@ __device__ __forceinline__ void outline_row(const ForkArgs &a, int64_t i, int64_
             if (o >= 1 && o - 1 >= lo) {
                 bool par_mine = false;
 #pragma unroll
-                for (int j = 0; j < CHUNK_J; ++j) par_mine = par_mine || (lo + lane + WAVE * j == o - 1 && c[j] == C_PAR);
+                for (int j = 0; j < BACK_J; ++j) par_mine = par_mine || (lo + lane + WAVE * j == o - 1 && c[j] == C_PAR);
                 par_before = __ballot(par_mine) != 0 ? 1 : 0;
             }
         }
@@ -398,14 +429,20 @@ __device__ __forceinline__ void outline_row(const ForkArgs &a, int64_t i, int64_
     uint32_t prev_cls = C_OUT;
     int64_t text = 0;                    /* entry text tokens so far (the same in every lane) */
     bool ok = true;
+    /* the next chunk's tokens are loaded while this one is walked */
+    int32_t tk[CHUNK_J];
+    outline_tokens(a, g, o + 1, end, tk, lane);
     for (int64_t lo = o + 1; lo < end; lo += CHUNK) {
+        int32_t tn[CHUNK_J];
+        outline_tokens(a, g, lo + CHUNK, end, tn, lane);
         uint64_t b[CHUNK_J];
         uint32_t c[CHUNK_J];
 #pragma unroll
         for (int j = 0; j < CHUNK_J; ++j) {
             const int64_t p = lo + lane + WAVE * j;
-            c[j] = p < end ? classify(a.tm, a.tokens[g + p], contig) : C_TEXT;
+            c[j] = p < end ? classify(a.tm, tk[j], contig) : C_TEXT;
             b[j] = __ballot(c[j] != C_TEXT);
+            tk[j] = tn[j];
         }
         uint32_t base = 0;
 #pragma unroll
@@ -825,21 +862,30 @@ __device__ __forceinline__ int64_t join_row(const JoinArgs &a, int64_t i)
         /* JOIN_UNROLL workers at a time: their records in one round of loads,
          * then the tokens after the row and at the end in one more */
         for (int64_t wb = w0; wb < w1; wb += JOIN_UNROLL) {
+            /* every load unconditional, from a valid address (the last
+             * worker of the row, or this row's own status word, in place of
+             * one not needed), and the value selected after it: a load under
+             * a condition waits for the one before it */
             int64_t wl[JOIN_UNROLL], ws[JOIN_UNROLL];
 #pragma unroll
             for (int u = 0; u < JOIN_UNROLL; ++u) {
                 const bool in = wb + u < w1;
-                wl[u] = in ? (int64_t)a.wlengths[wb + u] : 0;
-                ws[u] = in ? a.wstarts[wb + u] : 0;
+                const int64_t w = in ? wb + u : w1 - 1;
+                const int64_t l = a.wlengths[w], s = a.wstarts[w];
+                wl[u] = in ? l : 0;
+                ws[u] = in ? s : 0;
             }
             int32_t first[JOIN_UNROLL], last[JOIN_UNROLL];
             bool chk[JOIN_UNROLL];
+            const int32_t *safe = reinterpret_cast<const int32_t *>(a.status + i);
 #pragma unroll
             for (int u = 0; u < JOIN_UNROLL; ++u) {
                 const int64_t tail = wl[u] > L ? wl[u] - L : 0;
                 chk[u] = wb + u < w1 && wl[u] >= 0 && ws[u] >= 0 && tail >= 2;
-                first[u] = chk[u] ? a.wtokens[ws[u] + L] : 0;
-                last[u] = chk[u] ? a.wtokens[ws[u] + wl[u] - 1] : 0;
+                const int32_t f = *(chk[u] ? a.wtokens + ws[u] + L : safe);
+                const int32_t e = *(chk[u] ? a.wtokens + ws[u] + wl[u] - 1 : safe);
+                first[u] = chk[u] ? f : 0;
+                last[u] = chk[u] ? e : 0;
             }
 #pragma unroll
             for (int u = 0; u < JOIN_UNROLL; ++u) {
