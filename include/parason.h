@@ -235,13 +235,17 @@ int parason_run_noalloc(const parason_handle *h, const int32_t *tokens, const in
 void parason_destroy(parason_handle *h);
 
 /* Measurement aid, not an operation of the paper: a plain streaming read of
- * data[0 .. bytes) with the token scan's loads and grid and nothing else, the
- * ceiling that a read of every token once reaches on this GPU (the scan's
- * roofline is reported against it and against the HBM peak).  data: device
- * memory, 16-byte aligned, bytes a multiple of 4.  sink: device uint32[sink_len],
- * sink_len >= 1; each wave stores a checksum of what it read to
- * sink[wave % sink_len].  Asynchronous on `stream`; host-side argument errors
- * return a negative status before any launch. */
+ * data[0 .. bytes) with the token scan's loads, grid and work distribution
+ * (an equal share per wave, then the rest in chunks through a counter) and
+ * nothing else, the ceiling that a read of every token once reaches on this
+ * GPU (the scan's roofline is reported against it and against the HBM peak).
+ * data: device memory, 16-byte aligned, bytes a multiple of 4.  sink: device
+ * uint32[sink_len], sink_len >= 1; each wave stores a checksum of what it read
+ * to sink[wave % sink_len].  Asynchronous on `stream`; host-side argument
+ * errors return a negative status before any launch.  The chunk counter is a
+ * static variable of the library, one per GPU, cleared by a launch of its own
+ * before the read: probes that overlap on one GPU read only part of their
+ * data (never outside it).  Serialise them. */
 int parason_read_probe(const void *data, size_t bytes, uint32_t *sink, int64_t sink_len, void *stream);
 
 /* ---- policy-gradient step ------------------------------------------------

@@ -484,6 +484,23 @@ void *scratch_for_current_device()
     scratch_ptr[dev].store(p, std::memory_order_release);
     return p;
 }
+
+/* The chunk counter of parason_read_probe, one per GPU (probes on one GPU
+ * must not overlap); its address is had as the scratch's is. */
+static __device__ int32_t probe_next;
+std::atomic<int32_t *> probe_ptr[64];
+
+int32_t *probe_counter_for_current_device()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    int32_t *p = probe_ptr[dev].load(std::memory_order_acquire);
+    if (p) return p;
+    void *q = nullptr;
+    if (hipGetSymbolAddress(&q, HIP_SYMBOL(probe_next)) != hipSuccess || !q) return nullptr;
+    probe_ptr[dev].store((int32_t *)q, std::memory_order_release);
+    return (int32_t *)q;
+}
 }  // namespace
 
 int parason_run_noalloc(const parason_handle *h, const int32_t *tokens, const int64_t *starts, const int32_t *lengths,
@@ -518,8 +535,11 @@ int parason_read_probe(const void *data, size_t bytes, uint32_t *sink, int64_t s
     const int64_t n_vec = (int64_t)(bytes / 16);
     const int32_t n_tail = (int32_t)((bytes % 16) / 4);
     const int32_t *tail = (const int32_t *)((const char *)data + (size_t)n_vec * 16);
+    int32_t *next = probe_counter_for_current_device();
+    if (!next) return PARASON_ERR_HIP;
+    hipLaunchKernelGGL(pk::probe_reset, dim3(1), dim3(1), 0, (hipStream_t)stream_ptr, next);
     hipLaunchKernelGGL(pk::read_probe, dim3((unsigned)(cus * SCAN_BLOCKS_PER_CU)), dim3(pk::WAVE * pk::SCAN_WAVES), 0,
-                       (hipStream_t)stream_ptr, (const int4 *)data, n_vec, tail, n_tail, sink, sink_len);
+                       (hipStream_t)stream_ptr, (const int4 *)data, n_vec, tail, n_tail, sink, sink_len, next);
     return hipGetLastError() == hipSuccess ? PARASON_OK : PARASON_ERR_HIP;
 }
 

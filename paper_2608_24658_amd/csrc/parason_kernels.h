@@ -1417,10 +1417,6 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
     return w.s == w.last && !rc.global;
 }
 
-/* One wave per segment; waves take contiguous ranges of segment ids.  Two
- * register buffers alternate: the loads of segment s + 1 are issued before
- * segment s is compacted (and a finished row's events flushed), so a wave
- * always has a segment in flight. */
 /* The segment plan of a batch of at most SCAN_PLAN_ROWS rows, made by one
  * scan block in LDS (off[r] = first segment of row r, off[n] = the total):
  * the segment counts with coalesced loads (row t + SCAN_THREADS * j for thread
@@ -1477,29 +1473,81 @@ __device__ __forceinline__ void scan_plan(const ScanArgs &a, int64_t *off, int64
     }
 }
 
-template <int MODE, bool PLAN>
-__global__ void __launch_bounds__(WAVE * scan_waves<PLAN>(), PARASON_SCAN_WAVES_PER_SIMD) scan_rows(ScanArgs a)
-{
-    constexpr int NW = scan_waves<PLAN>();
-    __shared__ uint32_t lds_ev[NW][EVL];
-    __shared__ int64_t plan_off[PLAN ? SCAN_PLAN_ROWS + 1 : 1];
-    __shared__ int64_t plan_part[NW];
-    const int lane = threadIdx.x & (WAVE - 1);
-    const int wib = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
-    const int64_t wave = uniform64((int64_t)blockIdx.x * NW + wib);
-    const int64_t n_waves = (int64_t)gridDim.x * NW;
-    const int64_t *seg_off = a.seg_off;
-    if (PLAN) {
-        scan_plan<NW>(a, plan_off, plan_part);
-        seg_off = plan_off;
-    }
-    const int64_t S = uniform64(seg_off[a.n]);
-    if (S > a.seg_cap) return; /* the row kernel reports PARASON_FLAG_WS_OVERFLOW */
-    /* S < 2^40 and n_waves < 2^20 (checked on the host), so S * wave fits */
-    const int64_t s_begin = uniform64(S * wave / n_waves);
-    const int64_t s_end = uniform64(S * (wave + 1) / n_waves);
-    if (s_begin >= s_end) return;
+/* Work distribution of a large scan.  Compute units do not all stream at the
+ * same rate (on this GPU the waves of half of the dies finish an equal share
+ * about 9 % later than the others), so equal static shares leave part of the
+ * chip idle at the end.  A scan with at least DYN_MIN_PER_WAVE segments per
+ * wave therefore gives each wave an equal contiguous share of the first
+ * S1 = S - S * DYN_NUM / DYN_DEN segments, and hands out the rest in chunks,
+ * in segment order, through one counter: rounds of one chunk per wave whose
+ * size halves from c0 = (S - S1) / (2 W) down to DYN_KMIN, then chunks of
+ * DYN_KMIN to the end.  A wave that finishes early takes more chunks.  Rows cut
+ * by a chunk boundary are split rows, handled as those cut by a share's
+ * boundary.  Every range (share or chunk) has its own region of the slot pool:
+ * range q (shares 0 .. W-1, then chunk i as W + i) covering segments [b, e)
+ * owns slots [POOL_PER_SEG * b + x * q, POOL_PER_SEG * e + x * (q + 1)) past
+ * pool_base, x = (pool_slots - POOL_PER_SEG * S) / (W + chunks) rounded down
+ * to 4, so regions are disjoint and in segment order. */
+constexpr int64_t DYN_MIN_PER_WAVE = 256;
+constexpr int64_t DYN_NUM = 3, DYN_DEN = 16;
+constexpr int64_t DYN_KMIN = 32;
 
+struct ScanSched {
+    int64_t S, S1, c0, base_final, n_chunks, W;
+    int32_t rounds;
+    bool dyn;
+
+    /* all wave-uniform */
+    int64_t kmin;
+
+    /* S units (segments) over W waves; kmin: the smallest chunk; num / den of
+     * the units handed out in chunks (all wave-uniform) */
+    __device__ void init(int64_t S_, int64_t W_, bool allow, int64_t kmin_ = DYN_KMIN, int64_t num = DYN_NUM,
+                         int64_t den = DYN_DEN)
+    {
+        S = S_;
+        W = W_;
+        kmin = kmin_;
+        dyn = allow && S >= DYN_MIN_PER_WAVE * kmin / DYN_KMIN * W;
+        S1 = dyn ? S - S / den * num - S % den * num / den : S;
+        c0 = (S - S1) / (2 * W);
+        rounds = 0;
+        int64_t b = S1;
+        while ((c0 >> rounds) >= kmin) {
+            b += W * (c0 >> rounds);
+            ++rounds;
+        }
+        base_final = b;
+        n_chunks = dyn ? W * rounds + (S - b + kmin - 1) / kmin : 0;
+    }
+    /* units [b, e) of chunk i < n_chunks */
+    __device__ void chunk(int64_t i, int64_t &b, int64_t &e) const
+    {
+        if (i >= W * rounds) {
+            b = base_final + (i - W * rounds) * kmin;
+            e = min(b + kmin, S);
+            return;
+        }
+        int64_t base = S1;
+        int32_t r = 0;
+        while (i >= W) {
+            base += W * (c0 >> r);
+            i -= W;
+            ++r;
+        }
+        b = base + i * (c0 >> r);
+        e = b + (c0 >> r);
+    }
+};
+
+/* Scan segments [s_begin, s_end) (a share or a chunk), filling the pool region
+ * [pc, p_end).  Two register buffers: segment s + 1 is in flight while s is
+ * compacted (and a finished row's events flushed), so the wave always has a
+ * segment in flight. */
+template <int MODE, bool PLAN>
+__device__ __forceinline__ void scan_range(const ScanArgs &a, const int64_t *seg_off, int64_t s_begin, int64_t s_end,
+                                           uint32_t pc, uint32_t p_end, uint32_t *lev, int32_t tab, int lane)
+{
     const int4 *src = reinterpret_cast<const int4 *>(a.tok_base);
     SegCursor cur;
     cur.seg_off = seg_off;
@@ -1509,19 +1557,12 @@ __global__ void __launch_bounds__(WAVE * scan_waves<PLAN>(), PARASON_SCAN_WAVES_
     cur.s_begin = s_begin;
     cur.s_end = s_end;
     cur.seek(s_begin, a.n);
-    uint32_t *lev = lds_ev[wib];
-    const int32_t tab = MODE == TM_HASH ? a.tm.slot_id[lane] : 0;
 
     RowCollect rc;
     rc.lcnt = 0;
-    rc.global = true; /* a row already begun in the previous wave's range */
-    /* the slots the segments leave, shared equally (slot indices fit 32 bits,
-     * which the host checks) */
-    const uint32_t extra = ((a.pool_slots - POOL_PER_SEG * (uint32_t)S) / (uint32_t)n_waves) & ~3u;
-    rc.pc = __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)s_begin + extra * (uint32_t)wave);
-    rc.p_end =
-        __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)s_end + extra * (uint32_t)(wave + 1));
-    /* two register buffers: segment s + 1 is in flight while s is compacted */
+    rc.global = true; /* a row already begun in the previous range */
+    rc.pc = pc;
+    rc.p_end = p_end;
     SegView w = cur.view(s_begin);
     int4 xa[LOADS], xb[LOADS];
     issue_loads(xa, src, w.v0, w.v1, w.edge, lane);
@@ -1551,31 +1592,102 @@ __global__ void __launch_bounds__(WAVE * scan_waves<PLAN>(), PARASON_SCAN_WAVES_
     }
 }
 
+/* One wave per segment: each wave scans its share of the segments, then (a
+ * large scan) takes chunks of the rest until none is left. */
+template <int MODE, bool PLAN>
+__global__ void __launch_bounds__(WAVE * scan_waves<PLAN>(), PARASON_SCAN_WAVES_PER_SIMD) scan_rows(ScanArgs a)
+{
+    constexpr int NW = scan_waves<PLAN>();
+    __shared__ uint32_t lds_ev[NW][EVL];
+    __shared__ int64_t plan_off[PLAN ? SCAN_PLAN_ROWS + 1 : 1];
+    __shared__ int64_t plan_part[NW];
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int wib = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
+    const int64_t wave = uniform64((int64_t)blockIdx.x * NW + wib);
+    const int64_t n_waves = (int64_t)gridDim.x * NW;
+    const int64_t *seg_off = a.seg_off;
+    if (PLAN) {
+        scan_plan<NW>(a, plan_off, plan_part);
+        seg_off = plan_off;
+    }
+    const int64_t S = uniform64(seg_off[a.n]);
+    if (S > a.seg_cap) return; /* the row kernel reports PARASON_FLAG_WS_OVERFLOW */
+    ScanSched sch;
+    sch.init(S, n_waves, !PLAN); /* a batch the scan plans itself is small: static shares only */
+    uint32_t *lev = lds_ev[wib];
+    const int32_t tab = MODE == TM_HASH ? a.tm.slot_id[lane] : 0;
+    /* the slots the segments leave, shared equally by the ranges (slot
+     * indices fit 32 bits, which the host checks) */
+    const uint32_t extra =
+        ((a.pool_slots - POOL_PER_SEG * (uint32_t)S) / (uint32_t)(n_waves + sch.n_chunks)) & ~3u;
+    /* S1 < 2^40 and n_waves < 2^20 (checked on the host), so S1 * wave fits */
+    int64_t b = uniform64(sch.S1 * wave / n_waves), e = uniform64(sch.S1 * (wave + 1) / n_waves);
+    int64_t q = wave;
+    while (true) {
+        if (b < e) {
+            const uint32_t pc = __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)b + extra * (uint32_t)q);
+            const uint32_t p_end =
+                __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)e + extra * (uint32_t)(q + 1));
+            scan_range<MODE, PLAN>(a, seg_off, b, e, pc, p_end, lev, tab, lane);
+        }
+        if (!sch.dyn) break;
+        int32_t i = 0;
+        if (lane == 0) i = atomicAdd(&a.counters[3], 1);
+        i = __builtin_amdgcn_readfirstlane(i);
+        if ((int64_t)i >= sch.n_chunks) break;
+        sch.chunk(i, b, e);
+        b = uniform64(b);
+        e = uniform64(e);
+        q = n_waves + i;
+    }
+}
+
 /* The ceiling the token scan is measured against: a plain streaming read of
  * the same buffer with the scan's 16-byte nontemporal loads and persistent
- * grid, each wave over a contiguous range of 8 KB chunks whose eight loads per
- * lane are all issued before any is used, and no other work.  Each wave stores
- * the XOR of what it read to sink[wave % sink_len] (so the loads are kept). */
+ * grid, every unit handed out in chunks through a counter as ScanSched does
+ * (a chunk unit is one 8 KB step of eight loads per lane, all issued before
+ * any is used), and no other work.  Each wave stores the XOR of what it read to
+ * sink[wave % sink_len] (so the loads are kept).  *next must be zero at the
+ * launch (probe_reset clears it). */
 constexpr int PROBE_LOADS = 8;
 constexpr int PROBE_CHUNK = PROBE_LOADS * WAVE; /* 16-byte vectors per chunk */
+static_assert(PROBE_CHUNK == 2 * SEG_VEC, "a probe step reads two scan segments");
+
+__global__ void probe_reset(int32_t *next) { *next = 0; }
 
 __global__ void __launch_bounds__(WAVE * SCAN_WAVES) read_probe(const int4 *__restrict__ src, int64_t n_vec,
                                                                 const int32_t *__restrict__ tail, int32_t n_tail,
-                                                                uint32_t *__restrict__ sink, int64_t sink_len)
+                                                                uint32_t *__restrict__ sink, int64_t sink_len,
+                                                                int32_t *__restrict__ next)
 {
     const int lane = threadIdx.x & (WAVE - 1);
     const int64_t wave = uniform64((int64_t)blockIdx.x * SCAN_WAVES + threadIdx.x / WAVE);
     const int64_t n_waves = (int64_t)gridDim.x * SCAN_WAVES;
     const int64_t n_chunks = n_vec / PROBE_CHUNK;
-    const int64_t c0 = uniform64(n_chunks * wave / n_waves), c1 = uniform64(n_chunks * (wave + 1) / n_waves);
+    ScanSched sch;
+    /* units of two segments, all of them in chunks: the waves of a pure read
+     * stream at rates up to twice apart, more than the scan's equal shares
+     * leave room for */
+    sch.init(n_chunks, n_waves, true, DYN_KMIN / 2, 1, 1);
+    int64_t c0 = uniform64(sch.S1 * wave / n_waves), c1 = uniform64(sch.S1 * (wave + 1) / n_waves);
     uint32_t acc = 0;
-    for (int64_t c = c0; c < c1; ++c) {
-        int4 x[PROBE_LOADS];
-        const int4 *p = src + c * PROBE_CHUNK + lane;
+    while (true) {
+        for (int64_t c = c0; c < c1; ++c) {
+            int4 x[PROBE_LOADS];
+            const int4 *p = src + c * PROBE_CHUNK + lane;
 #pragma unroll
-        for (int i = 0; i < PROBE_LOADS; ++i) x[i] = load_vec(p + i * WAVE);
+            for (int i = 0; i < PROBE_LOADS; ++i) x[i] = load_vec(p + i * WAVE);
 #pragma unroll
-        for (int i = 0; i < PROBE_LOADS; ++i) acc ^= (uint32_t)(x[i].x ^ x[i].y ^ x[i].z ^ x[i].w);
+            for (int i = 0; i < PROBE_LOADS; ++i) acc ^= (uint32_t)(x[i].x ^ x[i].y ^ x[i].z ^ x[i].w);
+        }
+        if (!sch.dyn) break;
+        int32_t i = 0;
+        if (lane == 0) i = atomicAdd(next, 1);
+        i = __builtin_amdgcn_readfirstlane(i);
+        if ((int64_t)i >= sch.n_chunks) break;
+        sch.chunk(i, c0, c1);
+        c0 = uniform64(c0);
+        c1 = uniform64(c1);
     }
     if (wave == n_waves - 1) {
         /* the vectors after the last whole chunk, then the last 0-3 elements */

@@ -279,3 +279,27 @@ def test_read_probe_reads_every_word(dev, n_elem):
     want = np.bitwise_xor.reduce(buf[:n_elem].view(np.uint32)) if n_elem else np.uint32(0)
     got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
     assert got == want
+
+
+def test_read_probe_dynamic_chunks_read_every_word(dev):
+    """A buffer of at least 128 eight-kilobyte steps per wave takes the
+    probe's counter-driven chunks after the equal shares (the scan's
+    distribution): every word is still read exactly once.  The buffer holds
+    0 .. N-1, whose XOR has a closed form."""
+    waves = torch.cuda.get_device_properties(dev).multi_processor_count * 16
+    n_elem = 128 * waves * 2048 + 2048 * 333 + 7  # whole steps, a partial one, a tail of 3 words
+    log("case read probe dynamic %d" % n_elem)
+    assert n_elem < 2 ** 31
+    d = torch.arange(n_elem, dtype=torch.int32, device=dev)
+    sink = torch.zeros(waves, dtype=torch.int32, device=dev)
+    for _ in range(2):  # the counter is cleared for every call
+        sink.zero_()
+        rc = PX.read_probe_raw(d.data_ptr(), 4 * n_elem, sink.data_ptr(), waves,
+                               torch.cuda.current_stream(dev).cuda_stream)
+        assert rc == PX.OK
+        torch.cuda.synchronize()
+        m = n_elem - 1
+        want = [m, 1, m + 1, 0][m % 4]  # XOR of 0 .. m
+        got = int(np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32)))
+        assert got == want
+    del d

@@ -16,7 +16,8 @@ pattern and sized exactly, so reliance on its contents or reads past it fail.
 Planted mistakes in copies of the kernel sources (an off-by-one in a DPP
 segmented scan, a carry lost inside a lane's events of rows_par's segmented
 scan, a lost carry in the scan's compaction, a dropped row-edge mask, an
-unreserved pool part, a tag class read from the wrong table nibble)
+unreserved pool part, a tag class read from the wrong table nibble, a
+dynamic scan chunk that ends a segment early)
 must each be caught by these comparisons."""
 import os
 import shutil
@@ -157,6 +158,25 @@ def test_emulated_long_split_rows(emu):
     check(emu, tokens, starts, lengths, correct, cus=MANY, what="long split rows")
 
 
+def dynamic_batch():
+    """2,000 rows of 2,000-5,000 tokens (6.9e6 tokens): on one emulated unit
+    (16 scan waves) more than 256 segments per wave, so the scan takes 13/16
+    of an equal share per wave, then chunks of the rest in segment order: one
+    round of one chunk per wave (c0 = (S - S1) / 32 of about 50 segments), then
+    32-segment chunks.  Rows cut by chunk boundaries take the split-row path."""
+    P = S.make_params("small")
+    tok, st, ln, co = S.host_batch(P, 2000)
+    segs = int(np.sum((ln.astype(np.int64) + 1023) // 1024))  # a lower bound of the scan's segments
+    s_dyn = segs * 3 // 16
+    assert segs >= 256 * 16 and s_dyn // 32 >= 32, "the batch must reach the dynamic rounds"
+    return tok, st, ln, co
+
+
+def test_emulated_dynamic_scan(emu):
+    tok, st, ln, co = dynamic_batch()
+    check(emu, tok, st, ln, co, cus=FEW, what="dynamic scan")
+
+
 @pytest.mark.parametrize("tags", ["contiguous", "scattered", "scattered-compare", "low-ids"])
 @pytest.mark.parametrize("cus", [16, FEW])
 def test_emulated_adversarial(emu, tags, cus):
@@ -214,6 +234,8 @@ def test_emulated_bad_rows_and_workspace_overflow(emu):
 
 
 MUTANTS = {
+    # a dynamic chunk of the scan that ends one segment early (that segment is never scanned)
+    "dyn-chunk-gap": ("parason_kernels.h", "e = b + (c0 >> r);", "e = b + (c0 >> r) - 1;"),
     # a DPP segmented scan whose carry out of the first row of 16 lanes is read one lane early
     "seg-scan-off-by-one": ("device_common.h",
                             "const int32_t v0 = __builtin_amdgcn_readlane(v, 15), v1",
@@ -258,10 +280,13 @@ def test_planted_mistakes_are_caught(tmp_path):
     tok, st, ln, co = S.host_batch(P, 64)
     tokens, starts, lengths = pack(adversarial_streams(), TAGS)
     correct = (np.arange(lengths.size) % 3 != 0).astype(np.uint8)
+    dyn = dynamic_batch()
     for name, (_, binary) in sorted(procs.items()):
         caught = 0
-        for args, cus in (((tok, st, ln, co), MANY), ((tokens, starts, lengths, correct), 16),
-                          ((tok, st, ln, co), FEW)):
+        configs = [((tok, st, ln, co), MANY), ((tokens, starts, lengths, correct), 16), ((tok, st, ln, co), FEW)]
+        if name.startswith("dyn-"):
+            configs = [(dyn, FEW)]  # only a large batch takes the dynamic chunks
+        for args, cus in configs:
             try:
                 check(binary, *args, cus=cus, what=name)
             except (AssertionError, RuntimeError):
