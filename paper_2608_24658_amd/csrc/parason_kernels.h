@@ -1491,6 +1491,8 @@ __device__ __forceinline__ void scan_plan(const ScanArgs &a, int64_t *off, int64
 constexpr int64_t DYN_MIN_PER_WAVE = 256;
 constexpr int64_t DYN_NUM = 3, DYN_DEN = 16;
 constexpr int64_t DYN_KMIN = 32;
+constexpr int64_t BLK_CHUNK = 2; /* segments per chunk of a block's own pool ... */
+constexpr int64_t BLK_MIN = 64;  /* ... which a block has from this many segments on */
 
 struct ScanSched {
     int64_t S, S1, c0, base_final, n_chunks, W;
@@ -1606,29 +1608,70 @@ __global__ void __launch_bounds__(WAVE * scan_waves<PLAN>(), PARASON_SCAN_WAVES_
     const int64_t wave = uniform64((int64_t)blockIdx.x * NW + wib);
     const int64_t n_waves = (int64_t)gridDim.x * NW;
     const int64_t *seg_off = a.seg_off;
+    /* a batch the scan plans (a small one): block k scans segments
+     * [S k / nb, S (k + 1) / nb), its waves an equal share each of the first
+     * L1 = L - 3 L / 16 of them, then the rest in chunks of BLK_CHUNK handed
+     * out by an LDS counter, so that the block's waves end together (a block
+     * of fewer than BLK_MIN segments keeps equal shares of all of them: its
+     * waves are done before a counter would pay); ranges are numbered
+     * k Q + wave (shares), k Q + NW + j (chunks), Q above any block's share
+     * and chunk count. */
+    __shared__ uint32_t blk_next;
     if (PLAN) {
+        if (threadIdx.x == 0) blk_next = 0; /* before scan_plan's barriers */
         scan_plan<NW>(a, plan_off, plan_part);
         seg_off = plan_off;
     }
     const int64_t S = uniform64(seg_off[a.n]);
     if (S > a.seg_cap) return; /* the row kernel reports PARASON_FLAG_WS_OVERFLOW */
-    ScanSched sch;
-    sch.init(S, n_waves, !PLAN); /* a batch the scan plans itself is small: static shares only */
     uint32_t *lev = lds_ev[wib];
     const int32_t tab = MODE == TM_HASH ? a.tm.slot_id[lane] : 0;
-    /* the slots the segments leave, shared equally by the ranges (slot
-     * indices fit 32 bits, which the host checks) */
-    const uint32_t extra =
-        ((a.pool_slots - POOL_PER_SEG * (uint32_t)S) / (uint32_t)(n_waves + sch.n_chunks)) & ~3u;
-    /* S1 < 2^40 and n_waves < 2^20 (checked on the host), so S1 * wave fits */
-    int64_t b = uniform64(sch.S1 * wave / n_waves), e = uniform64(sch.S1 * (wave + 1) / n_waves);
-    int64_t q = wave;
+    int64_t b, e, q, Bk = 0, Ek = 0, L1 = 0, Q = 0;
+    bool blk_dyn = false;
+    uint32_t extra;
+    ScanSched sch;
+    if (PLAN) {
+        /* 64-bit divisions are long on the scalar unit: by shifts when the
+         * block count is a power of two (two blocks per compute unit) */
+        const uint32_t nb = gridDim.x;
+        const bool pow2 = (nb & (nb - 1)) == 0;
+        const int sh = __builtin_ctz(nb);
+        const int64_t k = blockIdx.x;
+        Bk = uniform64(pow2 ? (S * k) >> sh : S * k / nb);
+        Ek = uniform64(pow2 ? (S * (k + 1)) >> sh : S * (k + 1) / nb);
+        Q = uniform64(NW + ((pow2 ? S >> sh : S / nb) + 1) * DYN_NUM / DYN_DEN / BLK_CHUNK + 2);
+        /* slot indices fit 32 bits, which the host checks */
+        extra = ((a.pool_slots - POOL_PER_SEG * (uint32_t)S) / (uint32_t)(nb * Q)) & ~3u;
+        blk_dyn = Ek - Bk >= BLK_MIN;
+        L1 = blk_dyn ? (Ek - Bk) - (Ek - Bk) * DYN_NUM / DYN_DEN : Ek - Bk;
+        b = uniform64(Bk + L1 * wib / NW);
+        e = uniform64(Bk + L1 * (wib + 1) / NW);
+        q = k * Q + wib;
+    } else {
+        sch.init(S, n_waves, true);
+        /* S1 < 2^40 and n_waves < 2^20 (checked on the host), so S1 * wave fits */
+        b = uniform64(sch.S1 * wave / n_waves);
+        e = uniform64(sch.S1 * (wave + 1) / n_waves);
+        q = wave;
+        extra = ((a.pool_slots - POOL_PER_SEG * (uint32_t)S) / (uint32_t)(n_waves + sch.n_chunks)) & ~3u;
+    }
     while (true) {
         if (b < e) {
             const uint32_t pc = __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)b + extra * (uint32_t)q);
             const uint32_t p_end =
                 __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)e + extra * (uint32_t)(q + 1));
             scan_range<MODE, PLAN>(a, seg_off, b, e, pc, p_end, lev, tab, lane);
+        }
+        if (PLAN) {
+            if (!blk_dyn) break;
+            uint32_t j = 0;
+            if (lane == 0) j = atomicAdd(&blk_next, 1u);
+            j = __builtin_amdgcn_readfirstlane(j);
+            b = uniform64(Bk + L1 + (int64_t)j * BLK_CHUNK);
+            if (b >= Ek) break;
+            e = uniform64(min(b + BLK_CHUNK, Ek));
+            q = blockIdx.x * Q + NW + j;
+            continue;
         }
         if (!sch.dyn) break;
         int32_t i = 0;
@@ -1651,7 +1694,7 @@ __global__ void __launch_bounds__(WAVE * scan_waves<PLAN>(), PARASON_SCAN_WAVES_
  * launch (probe_reset clears it). */
 constexpr int PROBE_LOADS = 8;
 constexpr int PROBE_CHUNK = PROBE_LOADS * WAVE; /* 16-byte vectors per chunk */
-static_assert(PROBE_CHUNK == 2 * SEG_VEC, "a probe step reads two scan segments");
+constexpr int64_t PROBE_KMIN = 16;              /* the smallest chunk: 16 steps of 8 KB */
 
 __global__ void probe_reset(int32_t *next) { *next = 0; }
 
@@ -1665,10 +1708,10 @@ __global__ void __launch_bounds__(WAVE * SCAN_WAVES) read_probe(const int4 *__re
     const int64_t n_waves = (int64_t)gridDim.x * SCAN_WAVES;
     const int64_t n_chunks = n_vec / PROBE_CHUNK;
     ScanSched sch;
-    /* units of two segments, all of them in chunks: the waves of a pure read
-     * stream at rates up to twice apart, more than the scan's equal shares
-     * leave room for */
-    sch.init(n_chunks, n_waves, true, DYN_KMIN / 2, 1, 1);
+    /* units of 8 KB, all of them in chunks: the waves of a pure read
+     * stream at rates several times apart, more than the scan's equal
+     * shares leave room for */
+    sch.init(n_chunks, n_waves, true, PROBE_KMIN, 1, 1);
     int64_t c0 = uniform64(sch.S1 * wave / n_waves), c1 = uniform64(sch.S1 * (wave + 1) / n_waves);
     uint32_t acc = 0;
     while (true) {

@@ -17,7 +17,8 @@ Planted mistakes in copies of the kernel sources (an off-by-one in a DPP
 segmented scan, a carry lost inside a lane's events of rows_par's segmented
 scan, a lost carry in the scan's compaction, a dropped row-edge mask, an
 unreserved pool part, a tag class read from the wrong table nibble, a
-dynamic scan chunk that ends a segment early)
+dynamic scan chunk that ends a segment early, a block pool chunk that starts
+a segment late)
 must each be caught by these comparisons."""
 import os
 import shutil
@@ -177,6 +178,29 @@ def test_emulated_dynamic_scan(emu):
     check(emu, tok, st, ln, co, cus=FEW, what="dynamic scan")
 
 
+BLOCK_POOL_CUS = 16
+
+
+def block_pool_batch(n=632, cus=BLOCK_POOL_CUS):
+    """n rows of 2,000-5,000 tokens on `cus` emulated units take the scan that
+    plans the batch itself (2 cus blocks of 8 waves, rows_par after it) with
+    more than 64 segments per block, so each block's waves scan equal shares
+    of 13/16 of its segments and take the rest two at a time from the block's
+    LDS counter."""
+    assert n / 2 < cus * 20 and n <= 2048, "the batch must take rows_par and the planning scan"
+    P = S.make_params("small")
+    tok, st, ln, co = S.host_batch(P, n)
+    segs = int(np.sum((ln.astype(np.int64) + 1023) // 1024))  # a lower bound of the scan's segments
+    assert segs >= 64 * 2 * cus, "every block must reach its pool"
+    return tok, st, ln, co
+
+
+@pytest.mark.parametrize("n,cus", [(632, 16), (472, 12)])  # 32 blocks (shifts), 24 blocks (divisions)
+def test_emulated_block_pool(emu, n, cus):
+    tok, st, ln, co = block_pool_batch(n, cus)
+    check(emu, tok, st, ln, co, cus=cus, what="block pool %d rows, %d units" % (n, cus))
+
+
 @pytest.mark.parametrize("tags", ["contiguous", "scattered", "scattered-compare", "low-ids"])
 @pytest.mark.parametrize("cus", [16, FEW])
 def test_emulated_adversarial(emu, tags, cus):
@@ -236,6 +260,9 @@ def test_emulated_bad_rows_and_workspace_overflow(emu):
 MUTANTS = {
     # a dynamic chunk of the scan that ends one segment early (that segment is never scanned)
     "dyn-chunk-gap": ("parason_kernels.h", "e = b + (c0 >> r);", "e = b + (c0 >> r) - 1;"),
+    # a block's pool chunks that start one segment late (a segment of a small batch is never scanned)
+    "block-chunk-skip": ("parason_kernels.h", "b = uniform64(Bk + L1 + (int64_t)j * BLK_CHUNK);",
+                         "b = uniform64(Bk + L1 + 1 + (int64_t)j * BLK_CHUNK);"),
     # a DPP segmented scan whose carry out of the first row of 16 lanes is read one lane early
     "seg-scan-off-by-one": ("device_common.h",
                             "const int32_t v0 = __builtin_amdgcn_readlane(v, 15), v1",
@@ -281,11 +308,14 @@ def test_planted_mistakes_are_caught(tmp_path):
     tokens, starts, lengths = pack(adversarial_streams(), TAGS)
     correct = (np.arange(lengths.size) % 3 != 0).astype(np.uint8)
     dyn = dynamic_batch()
+    blk = block_pool_batch()
     for name, (_, binary) in sorted(procs.items()):
         caught = 0
         configs = [((tok, st, ln, co), MANY), ((tokens, starts, lengths, correct), 16), ((tok, st, ln, co), FEW)]
         if name.startswith("dyn-"):
             configs = [(dyn, FEW)]  # only a large batch takes the dynamic chunks
+        if name.startswith("block-"):
+            configs = [(blk, BLOCK_POOL_CUS)]  # a planned batch with blocks of at least 64 segments
         for args, cus in configs:
             try:
                 check(binary, *args, cus=cus, what=name)
