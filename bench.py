@@ -648,7 +648,27 @@ def bench_fork(args):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / args.steps
 
-    fork_ms = timed(lambda: px.fork(tokens, starts, lengths, seed=True, max_workers=W, ctx_capacity=T))
+    # outputs and workspace allocated once: the timed region holds the C-ABI calls only
+    i64, i32 = dict(dtype=torch.int64, device=dev), dict(dtype=torch.int32, device=dev)
+    fws = torch.empty(PX._ws_size("parason_fork_workspace_size", B), dtype=torch.uint8, device=dev)
+    fo = dict(ctx_tokens=torch.empty(T, **i32), ctx_starts=torch.empty(W, **i64), ctx_lengths=torch.empty(W, **i32),
+              ctx_row=torch.empty(W, **i32), ctx_entry=torch.empty(W, **i32), ctx_kind=torch.empty(W, **i32),
+              worker_off=torch.empty(B + 1, **i64), row_status=torch.empty(B, **i32), totals=torch.empty(3, **i64))
+    f_out = PX.ForkOutputs(W, T, *[fo[k].data_ptr() for k in (
+        "ctx_tokens", "ctx_starts", "ctx_lengths", "ctx_row", "ctx_entry", "ctx_kind", "worker_off", "row_status",
+        "totals")])
+    stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def fork_call():
+        rc = px.fork_raw(tokens.data_ptr(), starts.data_ptr(), lengths.data_ptr(), B, PX.FORK_SEED_ENTRY, f_out,
+                         fws.data_ptr(), fws.numel(), stream)
+        if rc != PX.OK:
+            raise PX.ParasonError(rc, "parason_fork")
+
+    fork_ms = timed(fork_call)
+    for k, v in fo.items():  # the timed calls wrote what the sizing call did
+        if not torch.equal(v, first[k]):
+            raise RuntimeError("timed fork calls differ from the first call in %s" % k)
     # workers: their context + 64 generated tokens + </Thread>, packed
     ctx_lens = first["ctx_lengths"].to(torch.int64)
     wlen = ctx_lens + 65
@@ -665,8 +685,22 @@ def bench_fork(args):
     jfirst = px.join(tokens, starts, lengths, first["worker_off"], wtokens, wstarts, wl32)
     JT = int(jfirst["totals"][0].item())
     assert not jfirst["row_status"].any().item()
-    join_ms = timed(lambda: px.join(tokens, starts, lengths, first["worker_off"], wtokens, wstarts, wl32,
-                                    capacity=JT))
+    jws = torch.empty(PX._ws_size("parason_join_workspace_size", B), dtype=torch.uint8, device=dev)
+    jo = dict(tokens=torch.empty(JT, **i32), starts=torch.empty(B + 1, **i64), lengths=torch.empty(B, **i32),
+              row_status=torch.empty(B, **i32), totals=torch.empty(2, **i64))
+    j_out = PX.JoinOutputs(JT, *[jo[k].data_ptr() for k in ("tokens", "starts", "lengths", "row_status", "totals")])
+
+    def join_call():
+        rc = px.join_raw(tokens.data_ptr(), starts.data_ptr(), lengths.data_ptr(), B, first["worker_off"].data_ptr(),
+                         wtokens.data_ptr(), wstarts.data_ptr(), wl32.data_ptr(), W, PX.JOIN_CLOSE_PARALLEL, j_out,
+                         jws.data_ptr(), jws.numel(), stream)
+        if rc != PX.OK:
+            raise PX.ParasonError(rc, "parason_join")
+
+    join_ms = timed(join_call)
+    for k, v in jo.items():
+        if not torch.equal(v, jfirst[k]):
+            raise RuntimeError("timed join calls differ from the first call in %s" % k)
     # references at the same sizes: torch's copy_ of T int32 (the contexts' bytes, read and written) and of
     # JT int32 (the joined rows' bytes)
     ref_src = torch.empty(T, dtype=torch.int32, device=dev)
@@ -693,7 +727,8 @@ def bench_fork(args):
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int32",
-        "data": "synthetic (typical-workload rollouts cut after an outline; generated thread text is filler)",
+        "data": "synthetic (typical-workload rollouts cut after an outline; generated thread text is filler); outputs "
+                "and workspace allocated before the timed calls, whose outputs are checked against the first call's",
         "config": {"workload": "fork %d rows (%d tokens) into %d workers (%d context tokens); join back with 64 "
                                "generated tokens per worker" % (B, rows_read, W, T),
                    "rows": B, "rows_forked": n_rows_forked, "workers": W, "context_tokens": T, "joined_tokens": JT},
@@ -751,6 +786,14 @@ def traffic_summary(d):
            "traffic_over_algorithmic": traffic / alg,
            "other_kernels_gb_per_launch": {k: [f[k] * 1024 / fetch_factor / 1e9, w.get(k, 0.0) * 1024 / write_factor / 1e9]
                                            for k in f if k.startswith("pk::") or "pk::" in k}}
+    # a second calibration point of known size from the same FETCH_SIZE run: the
+    # read probe reads each of the run's tokens exactly once (4 B per token)
+    probe = next((k for k in f if "read_probe" in k), None)
+    if probe is not None:
+        probe_bytes = 4.0 * run["config"]["tokens"]
+        rec["probe_check"] = {"kernel": probe, "bytes_read": probe_bytes, "fetch_kib": f[probe],
+                              "fetch_factor": f[probe] * 1024 / probe_bytes,
+                              "calibrated_over_read": f[probe] * 1024 / fetch_factor / probe_bytes}
     with open(PROFILE_TRAFFIC, "w") as fh:
         json.dump(rec, fh, indent=1)
     print(json.dumps(rec, indent=1))
