@@ -329,8 +329,9 @@ def main():
             "read_ceiling_gbs": 4.0 * n_tok / (probe_avg * 1e-3) / 1e9,
             "scan_over_ceiling": scan_avg / probe_avg,
             "read_ceiling": "parason_read_probe: plain streaming read of the same token buffer (the scan's "
-                            "16-byte nontemporal loads and grid, 8 loads per lane in flight, no work), timed "
-                            "with HIP events on the same stream in the same run",
+                            "16-byte nontemporal loads and grid, 8 loads per lane in flight, every 8 KB step "
+                            "handed out through a counter in shrinking chunks, no work), timed with HIP events "
+                            "on the same stream in the same run",
         },
     }
     if not args.no_cpu_baseline:
