@@ -1904,13 +1904,25 @@ __device__ __forceinline__ double zscore(double x, Moments m, bool all_equal)
     return (all_equal || m.sigma == 0.0) ? 0.0 : __ddiv_rn(__dsub_rn(x, m.mu), m.sigma);
 }
 
-__device__ __forceinline__ void write_reward(const RewardArgs &a, int64_t r, double zT, double zs, double zr, double xs,
-                                             double xr)
+/* A row's accounting outputs and correctness, loaded once. */
+struct RowVals {
+    uint32_t fl;
+    int32_t lat, tot, ns, nt;
+    uint8_t correct;
+};
+
+__device__ __forceinline__ RowVals row_vals(const RewardArgs &a, int64_t r)
 {
-    const int32_t tot = a.total[r];
-    const double e = tot > 0 ? __dsub_rn(1.0, __ddiv_rn((double)a.latency[r], (double)tot)) : 0.0;
-    const bool valid = (a.flags[r] & PARASON_FLAG_VALID) != 0;
-    const bool c = a.correct[r] != 0 && (valid || (a.cfg_flags & PARASON_CFG_INVALID_KEEPS_CORRECTNESS));
+    return RowVals{a.flags[r], a.latency[r], a.total[r], a.n_subtask[r], a.n_trial[r], a.correct[r]};
+}
+
+__device__ __forceinline__ void write_reward(const RewardArgs &a, int64_t r, const RowVals &v, double zT, double zs,
+                                             double zr, double xs, double xr)
+{
+    const int32_t tot = v.tot;
+    const double e = tot > 0 ? __dsub_rn(1.0, __ddiv_rn((double)v.lat, (double)tot)) : 0.0;
+    const bool valid = (v.fl & PARASON_FLAG_VALID) != 0;
+    const bool c = v.correct != 0 && (valid || (a.cfg_flags & PARASON_CFG_INVALID_KEEPS_CORRECTNESS));
     const double accel = __dmul_rn(a.rho, e);
     const double clipped = accel < a.rho_clip ? accel : a.rho_clip;
     double inner = __dsub_rn(1.0, __dmul_rn(a.alpha, zT));
@@ -1923,11 +1935,11 @@ __device__ __forceinline__ void write_reward(const RewardArgs &a, int64_t r, dou
     if (a.r_trial) a.r_trial[r] = (float)xr;
     if (a.eta) a.eta[r] = (float)e;
     /* a row with tokens has latency >= 1 (an invalid row's latency is its length) */
-    if (a.accel) a.accel[r] = tot > 0 ? (float)__ddiv_rn((double)tot, (double)a.latency[r]) : 1.0f;
-    if (a.saved) a.saved[r] = tot - a.latency[r];
+    if (a.accel) a.accel[r] = tot > 0 ? (float)__ddiv_rn((double)tot, (double)v.lat) : 1.0f;
+    if (a.saved) a.saved[r] = tot - v.lat;
 }
 
-__device__ __forceinline__ void write_nan(const RewardArgs &a, int64_t r)
+__device__ __forceinline__ void write_nan(const RewardArgs &a, int64_t r, const RowVals &v)
 {
     const float nan = __int_as_float(0x7fc00000);
     a.reward[r] = nan;
@@ -1935,21 +1947,25 @@ __device__ __forceinline__ void write_nan(const RewardArgs &a, int64_t r)
     if (a.r_trial) a.r_trial[r] = nan;
     if (a.eta) a.eta[r] = nan;
     if (a.accel) a.accel[r] = nan;
-    if (a.saved) a.saved[r] = (a.flags[r] & NOT_EVALUATED) ? 0 : a.total[r] - a.latency[r];
+    if (a.saved) a.saved[r] = (v.fl & NOT_EVALUATED) ? 0 : v.tot - v.lat;
 }
 
 /* A group of G rows (G a power of two up to 64) in G consecutive lanes of one
  * wave: each lane loads its own row once and reads the others' values with
- * shuffles, in the group's order. */
-__device__ __forceinline__ void group_reward_lanes(const RewardArgs &a, int64_t r, int32_t G)
+ * shuffles, in the group's order.  GC > 0 fixes G at compile time (the
+ * paper's G = 8), so that the group's shuffles are unrolled and issue
+ * together instead of one sum step after another. */
+template <int GC>
+__device__ __forceinline__ void group_reward_lanes(const RewardArgs &a, int64_t r, int32_t G_run, const RowVals &v)
 {
+    const int32_t G = GC > 0 ? GC : G_run;
     const int lane = threadIdx.x & (WAVE - 1);
     const int gl = lane & ~(G - 1); /* the group's first lane */
     const uint64_t gmask = (G == WAVE ? ~0ull : ((1ull << G) - 1ull)) << gl;
-    const uint32_t fl = a.flags[r];
-    const int32_t lat = a.latency[r], tot = a.total[r], ns = a.n_subtask[r], nt = a.n_trial[r];
+    const uint32_t fl = v.fl;
+    const int32_t lat = v.lat, tot = v.tot, ns = v.ns, nt = v.nt;
     if ((__ballot(!(fl & NOT_EVALUATED)) & gmask) != gmask) {
-        write_nan(a, r);
+        write_nan(a, r, v);
         return; /* the whole group returns here */
     }
     const bool lat_equal = (__ballot(lat == __shfl(lat, gl, WAVE)) & gmask) == gmask;
@@ -1963,7 +1979,7 @@ __device__ __forceinline__ void group_reward_lanes(const RewardArgs &a, int64_t 
     const Moments mT = moments([&](int32_t j) { return __shfl(xT, gl + j, WAVE); }, G);
     const Moments ms = moments([&](int32_t j) { return __shfl(xs, gl + j, WAVE); }, G);
     const Moments mr = moments([&](int32_t j) { return __shfl(xr, gl + j, WAVE); }, G);
-    write_reward(a, r, zscore(xT, mT, lat_equal), zscore(xs, ms, sub_equal), zscore(xr, mr, tri_equal), xs, xr);
+    write_reward(a, r, v, zscore(xT, mT, lat_equal), zscore(xs, ms, sub_equal), zscore(xr, mr, tri_equal), xs, xr);
 }
 
 /* Row r's reward from its group's values in memory, in the group's row order
@@ -1978,8 +1994,9 @@ __device__ __forceinline__ void group_reward_memory(const RewardArgs &a, int64_t
         evaluated = evaluated && !(a.flags[r0 + i] & NOT_EVALUATED);
         lat_equal = lat_equal && a.latency[r0 + i] == a.latency[r0];
     }
+    const RowVals v = row_vals(a, r);
     if (!evaluated) {
-        write_nan(a, r);
+        write_nan(a, r, v);
         return;
     }
     const bool sub_equal = same_ratio(a.n_subtask, a.total, r0, G);
@@ -1989,7 +2006,7 @@ __device__ __forceinline__ void group_reward_memory(const RewardArgs &a, int64_t
     auto xr = [&](int32_t i) { return ratio(a.n_trial[r0 + i], a.total[r0 + i]); };
     const Moments mT = moments(xT, G), ms = moments(xs, G), mr = moments(xr, G);
     const int32_t i = (int32_t)(r - r0);
-    write_reward(a, r, zscore(xT(i), mT, lat_equal), zscore(xs(i), ms, sub_equal), zscore(xr(i), mr, tri_equal),
+    write_reward(a, r, v, zscore(xT(i), mT, lat_equal), zscore(xs(i), ms, sub_equal), zscore(xr(i), mr, tri_equal),
                  xs(i), xr(i));
 }
 
@@ -2021,6 +2038,10 @@ template <bool LENIENT>
 __global__ void __launch_bounds__(256) group_reward(RewardArgs a, DeepArgs d)
 {
     const int32_t G = a.G;
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    /* the row's values in the same round of loads as the deep count (rows of
+     * groups the deep tier writes during this launch are not read from v) */
+    const RowVals v = row_vals(a, min(r, a.n - 1));
     const int32_t n_deep = d.counters[1]; /* the same for every thread */
     if (n_deep > 0 && blockIdx.x == 0) {
         if (threadIdx.x == 0) run_deep_rows<LENIENT>(d.rows, d.mode, n_deep, d.deep_rows, d.frames, d.bits);
@@ -2030,7 +2051,6 @@ __global__ void __launch_bounds__(256) group_reward(RewardArgs a, DeepArgs d)
             group_reward_memory(a, rd - rd % G + k % G);
         }
     }
-    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= a.n) return; /* n is a multiple of G: whole groups only */
     if (n_deep > 0) {
         const int64_t r0 = r - r % G;
@@ -2038,7 +2058,8 @@ __global__ void __launch_bounds__(256) group_reward(RewardArgs a, DeepArgs d)
         for (int32_t i = 0; i < G; ++i) deep = deep || (d.mode[r0 + i] & MODE_DEEP) != 0;
         if (deep) return; /* the whole group returns here */
     }
-    if (G <= WAVE && (G & (G - 1)) == 0) group_reward_lanes(a, r, G);
+    if (G == 8) group_reward_lanes<8>(a, r, G, v);
+    else if (G <= WAVE && (G & (G - 1)) == 0) group_reward_lanes<0>(a, r, G, v);
     else group_reward_memory(a, r);
 }
 
@@ -2048,12 +2069,13 @@ __global__ void __launch_bounds__(256) batch_reward(RewardArgs a)
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= a.n) return;
     const BatchStats &b = *a.batch;
+    const RowVals v = row_vals(a, r);
     if (b.not_evaluated) {
-        write_nan(a, r);
+        write_nan(a, r, v);
         return;
     }
-    const double xT = (double)a.latency[r], xs = ratio(a.n_subtask[r], a.total[r]), xr = ratio(a.n_trial[r], a.total[r]);
-    write_reward(a, r, zscore(xT, Moments{b.mu[0], b.sigma[0]}, b.all_equal[0] != 0),
+    const double xT = (double)v.lat, xs = ratio(v.ns, v.tot), xr = ratio(v.nt, v.tot);
+    write_reward(a, r, v, zscore(xT, Moments{b.mu[0], b.sigma[0]}, b.all_equal[0] != 0),
                  zscore(xs, Moments{b.mu[1], b.sigma[1]}, b.all_equal[1] != 0),
                  zscore(xr, Moments{b.mu[2], b.sigma[2]}, b.all_equal[2] != 0), xs, xr);
 }
