@@ -1425,9 +1425,10 @@ __device__ __forceinline__ bool collect_segment(const ScanArgs &a, const int4 (&
  * the row kernels, clears the mode of rows without segments (no scan wave
  * sees them; all rows when the batch overflows the workspace) and the
  * counters; every other row's mode is cleared by the wave holding its first
- * segment. */
+ * segment.  The rows' starts and lengths stay in LDS (st, ln) for the block's
+ * segment cursors. */
 template <int NW>
-__device__ __forceinline__ void scan_plan(const ScanArgs &a, int64_t *off, int64_t *part)
+__device__ __forceinline__ void scan_plan(const ScanArgs &a, int64_t *off, int64_t *part, int64_t *st, int32_t *ln)
 {
     constexpr int THREADS = WAVE * NW;
     constexpr int RPT = SCAN_PLAN_ROWS / THREADS;
@@ -1436,7 +1437,15 @@ __device__ __forceinline__ void scan_plan(const ScanArgs &a, int64_t *off, int64
 #pragma unroll
     for (int j = 0; j < RPT; ++j) {
         const int64_t r = t + (int64_t)THREADS * j;
-        off[r] = r < a.n ? row_segments(a.starts[r], a.lengths[r], a.mis) : 0;
+        if (r < a.n) {
+            const int64_t start = a.starts[r];
+            const int32_t len = a.lengths[r];
+            st[r] = start;
+            ln[r] = len;
+            off[r] = row_segments(start, len, a.mis);
+        } else {
+            off[r] = 0;
+        }
     }
     __syncthreads();
     int64_t c[RPT], sum = 0;
@@ -1547,14 +1556,15 @@ struct ScanSched {
  * compacted (and a finished row's events flushed), so the wave always has a
  * segment in flight. */
 template <int MODE, bool PLAN>
-__device__ __forceinline__ void scan_range(const ScanArgs &a, const int64_t *seg_off, int64_t s_begin, int64_t s_end,
+__device__ __forceinline__ void scan_range(const ScanArgs &a, const int64_t *seg_off, const int64_t *starts,
+                                           const int32_t *lengths, int64_t s_begin, int64_t s_end,
                                            uint32_t pc, uint32_t p_end, uint32_t *lev, int32_t tab, int lane)
 {
     const int4 *src = reinterpret_cast<const int4 *>(a.tok_base);
     SegCursor cur;
     cur.seg_off = seg_off;
-    cur.starts = a.starts;
-    cur.lengths = a.lengths;
+    cur.starts = starts;
+    cur.lengths = lengths;
     cur.mis = a.mis;
     cur.s_begin = s_begin;
     cur.s_end = s_end;
@@ -1602,6 +1612,8 @@ __global__ void __launch_bounds__(WAVE * scan_waves<PLAN>(), PARASON_SCAN_WAVES_
     constexpr int NW = scan_waves<PLAN>();
     __shared__ uint32_t lds_ev[NW][EVL];
     __shared__ int64_t plan_off[PLAN ? SCAN_PLAN_ROWS + 1 : 1];
+    __shared__ int64_t plan_st[PLAN ? SCAN_PLAN_ROWS : 1];
+    __shared__ int32_t plan_ln[PLAN ? SCAN_PLAN_ROWS : 1];
     __shared__ int64_t plan_part[NW];
     const int lane = threadIdx.x & (WAVE - 1);
     const int wib = __builtin_amdgcn_readfirstlane(threadIdx.x / WAVE);
@@ -1619,7 +1631,7 @@ __global__ void __launch_bounds__(WAVE * scan_waves<PLAN>(), PARASON_SCAN_WAVES_
     __shared__ uint32_t blk_next;
     if (PLAN) {
         if (threadIdx.x == 0) blk_next = 0; /* before scan_plan's barriers */
-        scan_plan<NW>(a, plan_off, plan_part);
+        scan_plan<NW>(a, plan_off, plan_part, plan_st, plan_ln);
         seg_off = plan_off;
     }
     const int64_t S = uniform64(seg_off[a.n]);
@@ -1660,7 +1672,8 @@ __global__ void __launch_bounds__(WAVE * scan_waves<PLAN>(), PARASON_SCAN_WAVES_
             const uint32_t pc = __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)b + extra * (uint32_t)q);
             const uint32_t p_end =
                 __builtin_amdgcn_readfirstlane(a.pool_base + POOL_PER_SEG * (uint32_t)e + extra * (uint32_t)(q + 1));
-            scan_range<MODE, PLAN>(a, seg_off, b, e, pc, p_end, lev, tab, lane);
+            scan_range<MODE, PLAN>(a, seg_off, PLAN ? plan_st : a.starts, PLAN ? plan_ln : a.lengths, b, e, pc, p_end,
+                                   lev, tab, lane);
         }
         if (PLAN) {
             if (!blk_dyn) break;
