@@ -1483,9 +1483,9 @@ __device__ __forceinline__ void scan_plan(const ScanArgs &a, int64_t *off, int64
 }
 
 /* Work distribution of a large scan.  Compute units do not all stream at the
- * same rate (on this GPU the waves of half of the dies finish an equal share
- * about 9 % later than the others), so equal static shares leave part of the
- * chip idle at the end.  A scan with at least DYN_MIN_PER_WAVE segments per
+ * same rate (on MI355X, with equal shares, the waves of four of the eight dies
+ * finished about 9 % later than the others), so equal static shares leave
+ * part of the chip idle at the end.  A scan with at least DYN_MIN_PER_WAVE segments per
  * wave therefore gives each wave an equal contiguous share of the first
  * S1 = S - S * DYN_NUM / DYN_DEN segments, and hands out the rest in chunks,
  * in segment order, through one counter: rounds of one chunk per wave whose
@@ -1507,9 +1507,7 @@ struct ScanSched {
     int64_t S, S1, c0, base_final, n_chunks, W;
     int32_t rounds;
     bool dyn;
-
-    /* all wave-uniform */
-    int64_t kmin;
+    int64_t kmin; /* every field is wave-uniform */
 
     /* S units (segments) over W waves; kmin: the smallest chunk; num / den of
      * the units handed out in chunks (all wave-uniform) */
