@@ -60,7 +60,10 @@ constexpr int FAST_DEPTH = PARASON_FAST_DEPTH; /* LDS frames per row (depth <= F
 constexpr int MID_DEPTH = 32;            /* LDS frames per row handed to the second tier */
 constexpr int FAST_ENTRIES = 64;         /* entries per open block on the fast path */
 constexpr int FRAME_WORDS = 8;
-constexpr int64_t DEEP_FRAMES = PARASON_MAX_DEPTH;
+/* frames hold the enclosing blocks (the innermost open block stays in
+ * registers), so PARASON_MAX_DEPTH - 1 of them evaluate a row nested
+ * PARASON_MAX_DEPTH deep and flag one nested deeper */
+constexpr int64_t DEEP_FRAMES = PARASON_MAX_DEPTH - 1;
 constexpr int64_t DEEP_ENTRY_BITS = PARASON_MAX_OPEN_ENTRIES;
 /* A row nests at most one level per 6 tokens and opens at most one outline
  * entry per 3, so a store of these per 1024-token segment of the batch holds
