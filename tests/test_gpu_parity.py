@@ -88,6 +88,28 @@ def test_adversarial_streams(dev, tags):
     log("adversarial: %d rows ok" % n)
 
 
+@pytest.mark.parametrize("reps", [4, 18])
+@pytest.mark.parametrize("tags", ["scattered", "scattered-compare", "low-ids"])
+def test_tag_lookups_on_the_larger_batch_paths(dev, tags, reps):
+    """The hashed and the twelve-compare tag tests in the scan instances and row
+    kernels of batches the scan does not plan itself: the adversarial rows
+    repeated 4 times (2,392 rows: the plan launch, then rows_par) and 18 times
+    (10,768 rows with the padding to whole groups: the per-lane row tiers,
+    their gather and the deep tier)."""
+    log("case tag lookups tags=%s reps=%d" % (tags, reps))
+    tag_ids = {"low-ids": LOW_IDS}.get(tags, S.SCATTERED_TAGS)
+    tokens, starts, lengths = pack(adversarial_streams() * reps, tag_ids)
+    n = lengths.size
+    assert (n > 2048) and ((n >= 10240) == (reps == 18))
+    correct = (np.arange(n) % 3 != 2).astype(np.uint8)
+    px, coef = px_for(tag_ids, flags=PX.CFG_TAG_COMPARE if tags == "scattered-compare" else 0)
+    got = run_gpu(px, to_dev(tokens, torch.int32, dev), to_dev(starts, torch.int64, dev),
+                  to_dev(lengths, torch.int32, dev), to_dev(correct, torch.uint8, dev))
+    compare(got, *oracle_expect(tokens, starts, lengths, correct, tag_ids, G, coef), what="tag lookups")
+    assert int(np.sum(got["max_depth"] == 1000)) == reps
+    log("tag lookups: %d rows ok" % n)
+
+
 @pytest.mark.parametrize("tags", ["contiguous", "scattered", "scattered-compare", "low-ids"])
 def test_text_ids_over_the_whole_int32_range(dev, tags):
     """Every id that is not one of the twelve tags is Text: negative ids, ids
