@@ -110,6 +110,25 @@ def test_tag_lookups_on_the_larger_batch_paths(dev, tags, reps):
     log("tag lookups: %d rows ok" % n)
 
 
+@pytest.mark.parametrize("n", [0, 8, 2056, 10240])
+def test_batches_without_tokens(dev, n):
+    """Degenerate batches: no rows, and rows that are all empty (not one token
+    in the batch) on each batch path: the scan's own plan (8 rows), the plan
+    launch with rows_par (2,056), the per-lane row tiers (10,240)."""
+    log("case batch without tokens n=%d" % n)
+    tokens = np.zeros(0, np.int32)
+    starts = np.zeros(n, np.int64)
+    lengths = np.zeros(n, np.int32)
+    correct = (np.arange(n) % 2).astype(np.uint8)
+    px, coef = px_for()
+    got = run_gpu(px, to_dev(tokens, torch.int32, dev), to_dev(starts, torch.int64, dev),
+                  to_dev(lengths, torch.int32, dev), to_dev(correct, torch.uint8, dev))
+    assert all(v.size == n for v in got.values())
+    if n:
+        compare(got, *oracle_expect(tokens, starts, lengths, correct, TAGS, G, coef), what="no tokens")
+        assert np.all(got["total"] == 0)
+
+
 @pytest.mark.parametrize("tags", ["contiguous", "scattered", "scattered-compare", "low-ids"])
 def test_text_ids_over_the_whole_int32_range(dev, tags):
     """Every id that is not one of the twelve tags is Text: negative ids, ids

@@ -146,6 +146,19 @@ def stretch(stream, total, rng):
     return out + stream[last:]
 
 
+@pytest.mark.parametrize("n,cus", [(8, MANY), (2056, MANY), (64, FEW)])
+def test_emulated_rows_without_tokens(emu, n, cus):
+    """Batches of empty rows only (not one token): the scan has no segment to
+    read, and each batch path (the scan's own plan, the plan launch with
+    rows_par, the per-lane row tiers) still writes every row's outputs."""
+    tokens = np.zeros(0, np.int32)
+    starts = np.zeros(n, np.int64)
+    lengths = np.zeros(n, np.int32)
+    correct = (np.arange(n) % 2).astype(np.uint8)
+    got = check(emu, tokens, starts, lengths, correct, cus=cus, what="empty rows n %d cus %d" % (n, cus))
+    assert np.all(got["total"] == 0)
+
+
 def test_emulated_long_split_rows(emu):
     """Rows of 270k-600k tokens whose events spread over more than 256 (and 512)
     segments, so that rows_par gathers a split row in several chunks of
