@@ -147,6 +147,29 @@ def test_pg_layout_gaps_and_misalignment(dev):
         assert np.all(g[~inside] == 7.5)
 
 
+def test_pg_rows_without_tokens(dev):
+    """Rows that are all empty: there is no token, so the loss, the token count
+    and the clip counts are 0, the advantages are still each group's, and the
+    gradient buffer is left as it was."""
+    log("case pg rows without tokens")
+    n = 16
+    starts = np.zeros(n, np.int64)
+    lengths = np.zeros(n, np.int32)
+    reward = np.random.default_rng(9).choice([-1.0, 0.5, 1.0], n).astype(np.float32)
+    logp = np.zeros(4, np.float32)
+    grad = to_dev(np.full(4, 7.5, np.float32), torch.float32, dev)
+    got = PX.pg_run(to_dev(reward, torch.float32, dev), to_dev(logp, torch.float32, dev),
+                    to_dev(logp, torch.float32, dev), to_dev(starts, torch.int64, dev),
+                    to_dev(lengths, torch.int32, dev), G, EPS_LO, EPS_HI, grad=grad)
+    torch.cuda.synchronize()
+    adv_exp = PG.advantages(reward, G)
+    exp = PG.surrogate(logp, logp, starts, lengths, adv_exp.astype(np.float32), EPS_LO, EPS_HI)
+    assert exp["tokens"] == 0 and exp["loss"] == 0.0
+    check(got, exp, adv_exp, starts, lengths, "no tokens")
+    assert np.all(got["grad"].cpu().numpy() == 7.5)
+    assert np.all(got["stats"].cpu().numpy() == 0.0)
+
+
 def test_pg_wide_log_ratio(dev):
     """Log-ratios over [-70, 88]: rows of positive advantage keep the tokens
     with d <= ln 1.28 (ratios down to 4e-31), rows of negative advantage those
